@@ -1,0 +1,163 @@
+"""fp64 reference ("oracle") of the co-batched multi-LoRA linear layer.
+
+TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the bench's
+CPU-baseline leg are the only callers.  The product path (the HIP library
+under ``paper_2607_28848_amd``) never imports this package, and this package
+imports nothing from it.
+
+The arithmetic lives in ``dsvo.c`` (plain fp64 loops, see ``dsvo.h`` for the
+definitions and the paper passages they follow).  This module builds that file
+with gcc and marshals numpy arrays through ctypes.
+
+Layouts (row-major, the paper's orientation of Sec. 2.2, i.e. the
+torch.nn.Linear / PEFT parameter layout):
+    X [T][K]   W [N][K]   A [n_ad][r_max][K]   B [n_ad][N][r_max]
+    dY, dX, H_save, G: compact training rows, ascending token row.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "dsvo.c")
+_LIB = os.path.join(_HERE, "libdsvo.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile dsvo.c into libdsvo.so next to it (gcc, -O2, OpenMP)."""
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + ".tmp%d" % os.getpid()
+        subprocess.check_call(
+            ["gcc", "-O2", "-fopenmp", "-shared", "-fPIC", "-std=c99", "-Wall",
+             "-o", tmp, _SRC, "-lm"], cwd=_HERE)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build(force=True)
+        lib = ctypes.CDLL(_LIB)
+        i32p = ctypes.POINTER(ctypes.c_int32)
+        f64p = ctypes.POINTER(ctypes.c_double)
+        ci = ctypes.c_int
+        lib.dsvo_rows.argtypes = [ci, ci, i32p, ci, i32p, i32p]
+        lib.dsvo_rows.restype = ci
+        lib.dsvo_forward.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, f64p, ci,
+                                     f64p, f64p, f64p, f64p, ci, i32p, f64p, f64p]
+        lib.dsvo_forward.restype = ci
+        lib.dsvo_backward.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, f64p, ci,
+                                      f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p,
+                                      ci, i32p, f64p]
+        lib.dsvo_backward.restype = ci
+        _lib = lib
+    return _lib
+
+
+def _i32(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.int32))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def _f64(a):
+    a = np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _seg_table(segments):
+    t = np.asarray(segments, dtype=np.int32).reshape(-1, 4)
+    return np.ascontiguousarray(t)
+
+
+def rows(segments, n_tokens: int, n_adapters: int):
+    """(row_adapter[T], train_rows[T_t]) of a segment table; raises on a bad table."""
+    seg, segp = _i32(_seg_table(segments))
+    ra, rap = _i32(np.zeros(max(n_tokens, 1), np.int32))
+    tr, trp = _i32(np.zeros(max(n_tokens, 1), np.int32))
+    tt = _load().dsvo_rows(n_tokens, seg.shape[0], segp, n_adapters, rap, trp)
+    if tt < 0:
+        raise ValueError("segment table does not tile [0, n_tokens) or names a bad adapter")
+    return ra[:n_tokens].copy(), tr[:tt].copy()
+
+
+def forward(segments, ranks, scales, r_max, X, W, A, B, rows_sel=None):
+    """fp64 forward.  Returns (Y[rows][N], H[rows][r_max]); rows default to all.
+
+    H entries at j >= r_a are NaN (never written by the definition)."""
+    X, Xp = _f64(X)
+    W, Wp = _f64(W)
+    A, Ap = _f64(A)
+    B, Bp = _f64(B)
+    T, K = X.shape
+    N = W.shape[0]
+    n_ad = A.shape[0]
+    assert W.shape == (N, K) and A.shape == (n_ad, r_max, K) and B.shape == (n_ad, N, r_max)
+    seg, segp = _i32(_seg_table(segments))
+    rk, rkp = _i32(ranks)
+    sc, scp = _f64(scales)
+    if rows_sel is None:
+        rows_sel = np.arange(T, dtype=np.int32)
+    rs, rsp = _i32(rows_sel)
+    Y = np.empty((rs.shape[0], N), np.float64)
+    H = np.full((rs.shape[0], r_max), np.nan, np.float64)
+    rc = _load().dsvo_forward(T, K, N, seg.shape[0], segp, n_ad, rkp, scp, r_max,
+                              Xp, Wp, Ap, Bp, rs.shape[0], rsp,
+                              Y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                              H.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    if rc != 0:
+        raise ValueError("oracle forward rejected its arguments")
+    return Y, H
+
+
+def backward(segments, ranks, scales, r_max, X, W, A, B, dY, dA=None, dB=None, dx_rows=None):
+    """fp64 backward.  Returns (G, dA, dB, dX).
+
+    dA/dB are copies of the given arrays (NaN-filled when None) with the slices
+    of adapters that own training rows overwritten.  dX covers the compact
+    training rows in dx_rows (default: all)."""
+    X, Xp = _f64(X)
+    W, Wp = _f64(W)
+    A, Ap = _f64(A)
+    B, Bp = _f64(B)
+    dY, dYp = _f64(dY)
+    T, K = X.shape
+    N = W.shape[0]
+    n_ad = A.shape[0]
+    seg, segp = _i32(_seg_table(segments))
+    rk, rkp = _i32(ranks)
+    sc, scp = _f64(scales)
+    tt = dY.shape[0]
+    dA = np.full((n_ad, r_max, K), np.nan) if dA is None else np.array(dA, np.float64, copy=True)
+    dB = np.full((n_ad, N, r_max), np.nan) if dB is None else np.array(dB, np.float64, copy=True)
+    G = np.full((max(tt, 1), r_max), np.nan)
+    if dx_rows is None:
+        dx_rows = np.arange(tt, dtype=np.int32)
+    dr, drp = _i32(dx_rows)
+    dX = np.empty((dr.shape[0], K), np.float64)
+    f64p = ctypes.POINTER(ctypes.c_double)
+    rc = _load().dsvo_backward(T, K, N, seg.shape[0], segp, n_ad, rkp, scp, r_max,
+                               Xp, Wp, Ap, Bp, dYp, G.ctypes.data_as(f64p),
+                               dA.ctypes.data_as(f64p), dB.ctypes.data_as(f64p),
+                               dr.shape[0], drp, dX.ctypes.data_as(f64p))
+    if rc != 0:
+        raise ValueError("oracle backward rejected its arguments")
+    return G[:tt], dA, dB, dX
+
+
+def rel_err(got, ref) -> float:
+    """max|got - ref| / max|ref| over the finite reference entries, in fp64."""
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    m = np.isfinite(ref)
+    den = np.max(np.abs(ref[m])) if m.any() else 0.0
+    num = np.max(np.abs(got[m] - ref[m])) if m.any() else 0.0
+    if den == 0.0:
+        return float(num)
+    return float(num / den)

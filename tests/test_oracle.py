@@ -1,0 +1,274 @@
+"""Pins of the fp64 reference against facts the paper and the mathematics fix.
+
+The paper prints no numeric example of the layer, so the reference is pinned
+by: a worked example computed by hand from the LoRA definition (Sec. 2.2), the
+merged-weight identity W_eff = W + s B A evaluated with a library matmul, the
+B = 0 special case, invariance under permutation of the segment table and under
+moving token blocks, central finite differences of L = <dY, Y_train> (exact up
+to rounding because L is linear in each of X, A and B), a pure-Python brute
+force on a tiny case, and the single-segment closed forms of the gradients.
+Shapes are non-square (K != N, r >= 2) so that a transposed operand or a
+swapped index cannot pass.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_28848_amd import workloads as wl
+
+GOLD = os.path.join(os.path.dirname(__file__), "golden", "lora_hand_example.txt")
+
+
+def _parse_golden(path):
+    out = {}
+    for line in open(path):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        key, rest = line.split(None, 1)
+        rows = [[float(v) for v in part.split()] for part in rest.split(";")]
+        out[key] = np.array(rows, np.float64)
+    return out
+
+
+def _small(segments, ranks, K=40, N=24, r_max=None, seed=3, pad=np.nan, scales=None):
+    w = wl.custom(segments, ranks, K, N, dtype="f32", r_max=r_max, seed=seed, scales=scales)
+    t = w.tensors(0, pad=pad)
+    return w, t
+
+
+def _fwd(w, t, rows=None):
+    return oracle.forward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B, rows)
+
+
+def _bwd(w, t, dY=None, **kw):
+    return oracle.backward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B,
+                           t.dY if dY is None else dY, **kw)
+
+
+SEGS = [(0, 7, 1, 0), (7, 5, 0, 1), (12, 9, 2, 0), (21, 6, 0, 1), (27, 4, 1, 1), (31, 3, 2, 0)]
+RANKS = [3, 2, 4]
+
+
+def test_golden_hand_example():
+    g = _parse_golden(GOLD)
+    segs = [tuple(int(v) for v in row) for row in g["segments"]]
+    ranks = g["ranks"][0].astype(np.int32)
+    scales = g["scales"][0]
+    A = np.stack([g["A0"], g["A1"]])           # [2][1][3]
+    B = np.stack([g["B0"], g["B1"]])           # [2][2][1]
+    Y, H = oracle.forward(segs, ranks, scales, 1, g["X"], g["W"], A, B)
+    np.testing.assert_array_equal(Y, g["Y"])
+    np.testing.assert_array_equal(H, g["H"].reshape(2, 1))
+    G, dA, dB, dX = oracle.backward(segs, ranks, scales, 1, g["X"], g["W"], A, B, g["dY"])
+    np.testing.assert_array_equal(G, g["G"])
+    np.testing.assert_array_equal(dA[1], g["dA1"])
+    np.testing.assert_array_equal(dB[1], g["dB1"])
+    np.testing.assert_array_equal(dX, g["dX"])
+    assert np.isnan(dA[0]).all() and np.isnan(dB[0]).all()   # no training rows on adapter 0
+
+
+def test_merged_weight_identity():
+    """y = x (W + s_a B_a A_a)^T for every row, with the merged weight formed densely."""
+    w, t = _small(SEGS, RANKS)
+    Y, H = _fwd(w, t)
+    for (st, ln, a, _) in w.segments:
+        r = int(w.ranks[a])
+        Weff = t.W + float(w.scales[a]) * (t.B[a, :, :r] @ t.A[a, :r, :])
+        ref = t.X[st:st + ln] @ Weff.T
+        assert oracle.rel_err(Y[st:st + ln], ref) < 1e-13
+        np.testing.assert_allclose(H[st:st + ln, :r], t.X[st:st + ln] @ t.A[a, :r, :].T, rtol=1e-12, atol=1e-14)
+        assert np.isnan(H[st:st + ln, r:]).all()
+
+
+def test_zero_B_gives_base_exactly():
+    w, t = _small(SEGS, RANKS)
+    t.B[np.isfinite(t.B)] = 0.0
+    Y, _ = _fwd(w, t)
+    w0 = wl.custom(w.segments, w.ranks, 40, 24, dtype="f32", scales=np.zeros(3))
+    Y0, _ = _fwd(w0, t)
+    np.testing.assert_array_equal(Y, Y0)                     # LoRA term exactly zero
+    assert oracle.rel_err(Y, t.X @ t.W.T) < 1e-14            # and it is X W^T
+    G, dA, dB, dX = _bwd(w, t)
+    assert (G[np.isfinite(G)] == 0).all() and np.isfinite(G[:, :2]).all()
+    for a in (0, 1):                                         # adapters with training rows
+        r = int(w.ranks[a])
+        assert (dA[a, :r] == 0).all()
+    assert oracle.rel_err(dX, t.dY @ t.W) < 1e-14
+
+
+def test_single_segment_is_plain_matmul():
+    w, t = _small([(0, 13, 0, 1)], [3], K=36, N=20)
+    Y, H = _fwd(w, t)
+    s = float(w.scales[0])
+    Hr = t.X @ t.A[0, :3].T
+    assert oracle.rel_err(Y, t.X @ t.W.T + s * Hr @ t.B[0, :, :3].T) < 1e-13
+    G, dA, dB, dX = _bwd(w, t)
+    Gr = s * t.dY @ t.B[0, :, :3]
+    assert oracle.rel_err(G[:, :3], Gr) < 1e-13
+    assert oracle.rel_err(dB[0, :, :3], s * t.dY.T @ Hr) < 1e-13
+    assert oracle.rel_err(dA[0, :3], Gr.T @ t.X) < 1e-13
+    assert oracle.rel_err(dX, t.dY @ t.W + Gr @ t.A[0, :3]) < 1e-13
+
+
+def _loss(w, t, X, A, B, tr):
+    Y, _ = oracle.forward(w.segments, w.ranks, w.scales, w.r_max, X, t.W, A, B, tr)
+    return float(np.sum(t.dY * Y))
+
+
+def test_finite_differences():
+    """Central differences of L = sum_i <dY_i, y_{t_i}> over training rows; L is linear in
+    each of X, A, B, so the difference quotient equals the derivative up to rounding."""
+    w, t = _small(SEGS, RANKS, pad=0.0)
+    _, tr = oracle.rows(w.segments, w.n_tokens, 3)
+    G, dA, dB, dX = _bwd(w, t)
+    rng = np.random.default_rng(7)
+    h = 0.5
+    # dA and dB: both adapters that own training rows (0 and 1), sampled coordinates
+    for a in (0, 1):
+        r = int(w.ranks[a])
+        for _ in range(6):
+            j, k = int(rng.integers(r)), int(rng.integers(40))
+            Ap, Am = t.A.copy(), t.A.copy()
+            Ap[a, j, k] += h
+            Am[a, j, k] -= h
+            fd = (_loss(w, t, t.X, Ap, t.B, tr) - _loss(w, t, t.X, Am, t.B, tr)) / (2 * h)
+            assert abs(fd - dA[a, j, k]) <= 1e-9 * max(1.0, abs(fd))
+            n = int(rng.integers(24))
+            Bp, Bm = t.B.copy(), t.B.copy()
+            Bp[a, n, j] += h
+            Bm[a, n, j] -= h
+            fd = (_loss(w, t, t.X, t.A, Bp, tr) - _loss(w, t, t.X, t.A, Bm, tr)) / (2 * h)
+            assert abs(fd - dB[a, n, j]) <= 1e-9 * max(1.0, abs(fd))
+    # adapter 2 has no training rows: L does not depend on it, its slices stay untouched
+    assert np.isnan(dA[2]).all() and np.isnan(dB[2]).all()
+    Ap = t.A.copy()
+    Ap[2, 0, 0] += h
+    assert _loss(w, t, t.X, Ap, t.B, tr) == _loss(w, t, t.X, t.A, t.B, tr)
+    # dX: every training row, sampled columns
+    for i, row in enumerate(tr):
+        k = int(rng.integers(40))
+        Xp, Xm = t.X.copy(), t.X.copy()
+        Xp[row, k] += h
+        Xm[row, k] -= h
+        fd = (_loss(w, t, Xp, t.A, t.B, tr) - _loss(w, t, Xm, t.A, t.B, tr)) / (2 * h)
+        assert abs(fd - dX[i, k]) <= 1e-9 * max(1.0, abs(fd))
+
+
+def test_table_permutation_invariance():
+    w, t = _small(SEGS, RANKS)
+    Y, H = _fwd(w, t)
+    G, dA, dB, dX = _bwd(w, t)
+    rng = np.random.default_rng(11)
+    for _ in range(3):
+        perm = [w.segments[i] for i in rng.permutation(len(w.segments))]
+        w2 = wl.custom(perm, w.ranks, 40, 24, dtype="f32")
+        Y2, H2 = _fwd(w2, t)
+        np.testing.assert_array_equal(Y, Y2)
+        np.testing.assert_array_equal(H, H2)
+        G2, dA2, dB2, dX2 = _bwd(w2, t)
+        for u, v in ((G, G2), (dA, dA2), (dB, dB2), (dX, dX2)):
+            np.testing.assert_array_equal(u, v)
+
+
+def test_moving_token_blocks():
+    """Relocating whole segments inside the batch moves their outputs with them."""
+    w, t = _small(SEGS, RANKS)
+    Y, H = _fwd(w, t)
+    order = [3, 0, 5, 2, 1, 4]
+    X2 = np.empty_like(t.X)
+    segs2, start, rowmap = [], 0, []
+    for i in order:
+        st, ln, a, tr = w.segments[i]
+        X2[start:start + ln] = t.X[st:st + ln]
+        segs2.append((start, ln, a, tr))
+        rowmap += list(range(st, st + ln))
+        start += ln
+    w2 = wl.custom(segs2, w.ranks, 40, 24, dtype="f32")
+    Y2, H2 = oracle.forward(segs2, w.ranks, w.scales, w.r_max, X2, t.W, t.A, t.B)
+    np.testing.assert_array_equal(Y2, Y[rowmap])
+    np.testing.assert_array_equal(H2, H[rowmap])
+
+
+def test_bwd_linear_in_dY():
+    w, t = _small(SEGS, RANKS)
+    G, dA, dB, dX = _bwd(w, t)
+    G3, dA3, dB3, dX3 = _bwd(w, t, dY=-3.0 * t.dY)
+    for u, v in ((G, G3), (dA, dA3), (dB, dB3), (dX, dX3)):
+        m = np.isfinite(u)
+        np.testing.assert_allclose(v[m], -3.0 * u[m], rtol=1e-12, atol=1e-13)
+
+
+def test_nan_padding_never_read():
+    w, t = _small(SEGS, [1, 2, 3], r_max=5, pad=np.nan)
+    Y, H = _fwd(w, t)
+    assert np.isfinite(Y).all()
+    G, dA, dB, dX = _bwd(w, t, dA=np.full((3, 5, 40), 7.0), dB=np.full((3, 24, 5), 7.0))
+    assert np.isfinite(dX).all()
+    for a in range(3):
+        r = int(w.ranks[a])
+        assert np.isfinite(G[:, :1]).all()
+        if a in (0, 1):
+            assert np.isfinite(dA[a, :r]).all() and (dA[a, r:] == 7.0).all()
+            assert np.isfinite(dB[a, :, :r]).all() and (dB[a, :, r:] == 7.0).all()
+        else:
+            assert (dA[a] == 7.0).all() and (dB[a] == 7.0).all()
+
+
+def test_brute_force_python_loops():
+    """Tiny case evaluated with plain Python loops in the merged-weight form."""
+    segs = [(0, 2, 1, 1), (2, 1, 0, 0), (3, 2, 1, 0)]
+    w, t = _small(segs, [2, 3], K=5, N=4, seed=5)
+    Y, _ = _fwd(w, t)
+    for (st, ln, a, _) in segs:
+        r, s = int(w.ranks[a]), float(w.scales[a])
+        for row in range(st, st + ln):
+            for n in range(4):
+                acc = 0.0
+                for k in range(5):
+                    weff = t.W[n][k]
+                    for j in range(r):
+                        weff += s * t.B[a][n][j] * t.A[a][j][k]
+                    acc += t.X[row][k] * weff
+                assert abs(acc - Y[row][n]) <= 1e-12 * max(1.0, abs(acc))
+
+
+@pytest.mark.parametrize("segs", [
+    [(0, 4, 0, 0), (5, 3, 0, 0)],                 # gap at row 4
+    [(0, 5, 0, 0), (4, 4, 0, 0)],                 # overlap
+    [(0, 8, 3, 0)],                               # adapter out of range
+    [(0, 9, 0, 0)],                               # runs past T
+])
+def test_bad_tables_rejected(segs):
+    X = np.zeros((8, 8))
+    with pytest.raises(ValueError):
+        oracle.forward(segs, [2, 2], [2.0, 2.0], 2, X, np.zeros((4, 8)), np.zeros((2, 2, 8)),
+                       np.zeros((2, 4, 2)))
+
+
+def test_zero_length_segments_and_train_order():
+    segs = [(3, 2, 0, 1), (0, 0, 1, 1), (0, 3, 1, 1), (5, 0, 0, 0), (5, 1, 0, 0)]
+    ra, tr = oracle.rows(segs, 6, 2)
+    np.testing.assert_array_equal(tr, [0, 1, 2, 3, 4])
+    np.testing.assert_array_equal(ra, [1, 1, 1, 0, 0, 0])
+
+
+def test_bf16_rounding_is_nearest_even():
+    # exact halfway cases between bf16 neighbours round to the even mantissa
+    one = 1.0
+    ulp = 2.0 ** -7
+    v, bits = wl.round_bf16(np.array([one + ulp / 2, one + 3 * ulp / 2, -(one + ulp / 2),
+                                      one + ulp / 2 + 2.0 ** -30, 3.0, 0.0]))
+    np.testing.assert_array_equal(v, [1.0, one + 2 * ulp, -1.0, one + ulp, 3.0, 0.0])
+    np.testing.assert_array_equal(wl.bf16_bits_to_f64(bits), v)
+    # against brute force: nearest of all bf16 values around x
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal(2000) * 3
+    v, _ = wl.round_bf16(x)
+    for xi, vi in zip(x, v):
+        m, e = np.frexp(xi)
+        cands = np.array([np.floor(m * 256), np.ceil(m * 256)]) * 2.0 ** (e - 8)
+        d = np.abs(cands - xi)
+        assert vi in cands and abs(vi - xi) == d.min()
