@@ -1,0 +1,306 @@
+#!/usr/bin/env python3
+"""Throughput of the co-batched multi-LoRA layer (forward + LoRA backward) on one MI355X.
+
+One step = one pass of the whole path over one synthetic batch: pack the segment
+table (dsv_segments_build, host + one copy to the device), then for every
+projection of the workload the co-batched forward (shrink, gathered low-rank
+terms, base GEMM with the low-rank prologue, training-row h saved) and the LoRA
+backward of the training rows (g, dB, dA, dX).  Inputs are resident in HBM
+before the timed region starts.
+
+Default workload: the Llama-3-8B layer set (q, k, v, o 4096x4096/1024, gate/up
+4096x14336, down 14336x4096) in bf16, 8 prefill segments of 512 tokens on
+adapters drawn from 32 rank-16 adapters plus 2 fine-tuning sequences of 1024
+tokens on adapter 0 (T = 6144, T_t = 2048).
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ProcessPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+from paper_2607_28848_amd import workloads as wl  # noqa: E402
+
+METRIC = "co-batched multi-LoRA fwd+bwd TFLOP/s and % of bf16 MFMA peak, 1 GPU"
+PEAK_BF16_TFLOPS = 2516.6   # 256 CUs x 2.4 GHz x 4096 dense bf16 FLOP/clk/CU
+WORKLOADS = {
+    "llama8b": wl.llama8b_mixed,
+    "decode": wl.decode_heavy,
+    "llama70b": wl.llama70b,
+    "sweep0": lambda: wl.load_sweep(0.0),
+    "sweep25": lambda: wl.load_sweep(0.25),
+    "sweep50": lambda: wl.load_sweep(0.5),
+    "sweep75": lambda: wl.load_sweep(0.75),
+    "sweep100": lambda: wl.load_sweep(1.0),
+}
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algo_flops(w, proj):
+    """(fwd, bwd) algorithmic FLOPs of one projection, true ranks only:
+    fwd 2 T K N + sum_seg 2 len r_a (K + N); bwd 2 T_t K N + sum_train 4 len r_a (K + N)."""
+    K, N = proj.K, proj.N
+    fwd = 2.0 * w.n_tokens * K * N
+    bwd = 2.0 * w.train_tokens * K * N
+    for (_, l, a, t) in w.segments:
+        r = int(w.ranks[a])
+        fwd += 2.0 * l * r * (K + N)
+        if t:
+            bwd += 4.0 * l * r * (K + N)
+    return fwd, bwd
+
+
+def gemm_fwd_flops(w, proj, gathered_rows):
+    """Algorithmic FLOPs of the forward GEMM launch: the base product plus the
+    low-rank expand of the rows whose term rides the tile (not the gathered ones)."""
+    row_rank = np.zeros(w.n_tokens, np.int64)
+    for (s, l, a, _) in w.segments:
+        row_rank[s:s + l] = int(w.ranks[a])
+    expand = 2.0 * proj.N * float(row_rank.sum() - row_rank[gathered_rows].sum())
+    return 2.0 * w.n_tokens * proj.K * proj.N + expand
+
+
+def gemm_bwd_flops(w, proj):
+    """dX GEMM: 2 T_t N K + 2 sum_train len r_a K."""
+    f = 2.0 * w.train_tokens * proj.K * proj.N
+    for (_, l, a, t) in w.segments:
+        if t:
+            f += 2.0 * l * int(w.ranks[a]) * proj.K
+    return f
+
+
+def _gen(args):
+    name, p = args
+    w = WORKLOADS[name]()
+    t = w.tensors(p, pad=0.0)
+    return t.store
+
+
+def cpu_baseline(w, stores, n_fwd_rows, n_dx_rows, seed=0):
+    """The fp64 reference timed on the host cores over a bounded sample of the same
+    workload: every projection's forward on n_fwd_rows sampled rows and its backward
+    (g, dA, dB in full, dX on n_dx_rows sampled training rows)."""
+    import oracle
+    rng = np.random.default_rng(seed)
+    rows = np.sort(rng.choice(w.n_tokens, n_fwd_rows, replace=False)).astype(np.int32)
+    Tt = w.train_tokens
+    dxr = np.sort(rng.choice(Tt, min(n_dx_rows, Tt), replace=False)).astype(np.int32) if Tt else None
+    flops, secs = 0.0, 0.0
+    row_rank = np.zeros(w.n_tokens, np.int64)
+    for (s, l, a, _) in w.segments:
+        row_rank[s:s + l] = int(w.ranks[a])
+    tr_rank = row_rank[[t for (s, l, a, tt) in w.segments if tt for t in range(s, s + l)]]
+    for p, proj in enumerate(w.projections):
+        st = stores[p]
+        cvt = (lambda b: wl.bf16_bits_to_f64(b)) if w.dtype == "bf16" else (lambda b: b.astype(np.float64))
+        X, W, A, B, dY = (cvt(st[k]) for k in ("X", "W", "A", "B", "dY"))
+        K, N = proj.K, proj.N
+        t0 = time.perf_counter()
+        oracle.forward(w.segments, w.ranks, w.scales, w.r_max, X, W, A, B, rows)
+        if Tt:
+            oracle.backward(w.segments, w.ranks, w.scales, w.r_max, X, W, A, B, dY, dx_rows=dxr)
+        secs += time.perf_counter() - t0
+        flops += float(sum(2.0 * K * N + 2.0 * row_rank[r] * (K + N) for r in rows))
+        if Tt:
+            rsum = float(tr_rank.sum())
+            flops += 2.0 * rsum * N * 2 + 2.0 * rsum * K          # g, dB, dA
+            flops += len(dxr) * 2.0 * N * K + 2.0 * K * float(tr_rank[dxr].sum())  # dX rows
+        log("  cpu baseline %s: %.1f s so far" % (proj.name, secs))
+    return flops, secs
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="llama8b", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-rows", type=int, default=48, help="forward rows per projection in the CPU sample")
+    ap.add_argument("--cpu-dx-rows", type=int, default=24)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    w = WORKLOADS[args.workload]()
+    log("workload %s: T=%d T_t=%d projections=%s" % (
+        w.name, w.n_tokens, w.train_tokens, [(p.name, p.K, p.N) for p in w.projections]))
+    t0 = time.time()
+    with ProcessPoolExecutor(max_workers=min(8, len(w.projections))) as ex:
+        stores = list(ex.map(_gen, [(args.workload, p) for p in range(len(w.projections))]))
+    log("inputs drawn in %.1f s" % (time.time() - t0))
+
+    import torch
+    from paper_2607_28848_amd import dsv
+
+    dev = torch.device("cuda", 0)
+    stream = torch.cuda.current_stream(dev)
+    bf = w.dtype == "bf16"
+
+    def up(a):
+        if bf:
+            return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    tdt = torch.bfloat16 if bf else torch.float32
+    code = dsv.BF16 if bf else dsv.F32
+    probe = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max)
+    Tt = probe.train_tokens
+    P = []
+    for p, proj in enumerate(w.projections):
+        st = stores[p]
+        d = dict(X=up(st["X"]), W=up(st["W"]), A=up(st["A"]), B=up(st["B"]), dY=up(st["dY"]))
+        K, N = proj.K, proj.N
+        d["Y"] = torch.empty((w.n_tokens, N), dtype=tdt, device=dev)
+        d["H"] = torch.empty((max(Tt, 1), w.r_max), dtype=tdt, device=dev)
+        d["dX"] = torch.empty((max(Tt, 1), K), dtype=tdt, device=dev)
+        d["dA"] = torch.zeros((w.n_adapters, w.r_max, K), dtype=torch.float32, device=dev)
+        d["dB"] = torch.zeros((w.n_adapters, N, w.r_max), dtype=torch.float32, device=dev)
+        d["wsf"] = torch.empty(max(dsv.fwd_workspace_bytes(probe, code, K, N), 256), dtype=torch.uint8, device=dev)
+        d["wsb"] = torch.empty(max(dsv.bwd_workspace_bytes(probe, code, K, N), 256), dtype=torch.uint8, device=dev)
+        P.append(d)
+    torch.cuda.synchronize()
+    log("inputs resident on %s" % torch.cuda.get_device_name(dev))
+
+    lib = dsv.lib_handle()
+    seg = np.ascontiguousarray(np.asarray(w.segments, np.int32).reshape(-1, 4))
+    ranks = np.ascontiguousarray(w.ranks, np.int32)
+    scales = np.ascontiguousarray(w.scales, np.float32)
+    import ctypes
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    f32p = ctypes.POINTER(ctypes.c_float)
+    meta_bytes = ctypes.c_size_t(probe.meta_bytes)
+    metas = [torch.empty(max(probe.meta_bytes, 256), dtype=torch.uint8, device=dev) for _ in range(2)]
+    sh = ctypes.c_void_p(int(stream.cuda_stream))
+    ptr = lambda t: ctypes.c_void_p(int(t.data_ptr()))  # noqa: E731
+    plan_ms = []
+
+    def step(i):
+        h = ctypes.c_void_p()
+        tp = time.perf_counter()
+        rc = lib.dsv_segments_build(seg.ctypes.data_as(i32p), seg.shape[0], w.n_tokens,
+                                    ranks.ctypes.data_as(i32p), scales.ctypes.data_as(f32p),
+                                    ranks.shape[0], w.r_max, ptr(metas[i & 1]), ctypes.byref(meta_bytes),
+                                    sh, ctypes.byref(h))
+        plan_ms.append((time.perf_counter() - tp) * 1e3)
+        if rc != 0:
+            raise RuntimeError("dsv_segments_build failed: %d" % rc)
+        for p, proj in enumerate(w.projections):
+            d = P[p]
+            K, N = proj.K, proj.N
+            rc = lib.dsv_cobatch_fwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                     ptr(d["Y"]), ptr(d["H"]), ptr(d["wsf"]), d["wsf"].numel(), sh)
+            if rc != 0:
+                raise RuntimeError("dsv_cobatch_fwd failed: %d" % rc)
+            rc = lib.dsv_lora_bwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                  ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
+                                  0, ptr(d["wsb"]), d["wsb"].numel(), sh)
+            if rc != 0:
+                raise RuntimeError("dsv_lora_bwd failed: %d" % rc)
+        lib.dsv_plan_free(h)  # the blob's copy was issued; the device metadata stays valid
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    log("warmup done (%d steps)" % args.warmup)
+    plan_ms.clear()
+    dsv.timing_enable(True)
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    ev0.record(stream)
+    for i in range(args.steps):
+        step(i)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    dsv.timing_enable(False)
+    fwd_ms, fwd_n, bwd_ms, bwd_n = dsv.timing_read()
+    gpu_ms = ev0.elapsed_time(ev1)
+    elapsed_s = max(wall, gpu_ms / 1e3)
+    ms_per_step = elapsed_s * 1e3 / args.steps
+
+    step_flops = sum(sum(algo_flops(w, proj)) for proj in w.projections)
+    value = step_flops * args.steps / elapsed_s / 1e12
+    gathered = probe.gathered_rows().astype(np.int64)
+    fwd_gemm_flops = sum(gemm_fwd_flops(w, proj, gathered) for proj in w.projections)
+    bwd_gemm_flops = sum(gemm_bwd_flops(w, proj) for proj in w.projections)
+    fwd_avg_ms = fwd_ms / max(fwd_n, 1)
+    achieved = fwd_gemm_flops * (fwd_n / len(w.projections)) / (fwd_ms / 1e3) / 1e12 if fwd_ms > 0 else None
+    bwd_achieved = bwd_gemm_flops * (bwd_n / len(w.projections)) / (bwd_ms / 1e3) / 1e12 if bwd_ms > 0 else None
+    log("timed %d steps: %.3f ms/step, %.1f TFLOP/s; fwd GEMM %.1f TFLOP/s avg %.1f us; dX GEMM %s TFLOP/s"
+        % (args.steps, ms_per_step, value, achieved or 0, fwd_avg_ms * 1e3,
+           "%.1f" % bwd_achieved if bwd_achieved else "n/a"))
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log("cpu baseline: fp64 reference on a sample (%d rows/projection fwd, %d dX rows)"
+            % (args.cpu_rows, args.cpu_dx_rows))
+        fl, secs = cpu_baseline(w, stores, args.cpu_rows, args.cpu_dx_rows)
+        cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+        cpu = {"value": fl / secs / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+               "sample": "every projection: forward of %d sampled rows, backward g/dA/dB over all %d "
+                         "training rows and dX of %d sampled training rows; %.2f GFLOP in %.1f s"
+                         % (args.cpu_rows, w.train_tokens, args.cpu_dx_rows, fl / 1e9, secs)}
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if bf else "f32",
+        "data": "synthetic",
+        "pct_of_bf16_peak": round(100.0 * value / PEAK_BF16_TFLOPS, 2),
+        "config": {
+            "workload": w.name,
+            "tokens": w.n_tokens,
+            "train_tokens": w.train_tokens,
+            "projections_KxN": [[p.name, p.K, p.N] for p in w.projections],
+            "adapters": w.n_adapters,
+            "ranks": sorted(set(int(r) for r in w.ranks)),
+            "algorithmic_gflop_per_step": round(step_flops / 1e9, 2),
+            "plan_build_ms": round(float(np.median(plan_ms)), 4) if plan_ms else None,
+        },
+        "roofline": {
+            "kernel": "gemm_lora_kernel<NT> (forward base GEMM + low-rank prologue)",
+            "bound": "mfma",
+            "achieved": round(achieved, 2) if achieved else None,
+            "peak": PEAK_BF16_TFLOPS,
+            "unit": "TFLOP/s",
+            "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
+            "traffic": None,
+            "avg_launch_us": round(fwd_avg_ms * 1e3, 2),
+            "launches": fwd_n,
+            "dx_gemm_tflops": round(bwd_achieved, 2) if bwd_achieved else None,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

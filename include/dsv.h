@@ -1,0 +1,210 @@
+/*
+ * dsv.h -- C ABI of the co-batched multi-LoRA linear layer for AMD MI355X (gfx950).
+ *
+ * One linear layer runs a mixed batch of inference tokens (prefill or decode)
+ * and LoRA fine-tuning tokens in a single pass, as in DeltaServe
+ * (arXiv 2607.28848):
+ *   - Sec. 2.2 ("Parameter-Efficient Fine-Tuning"): a frozen weight W of shape
+ *     d x k receives the low-rank update B A, A of shape r x k, B of shape d x r;
+ *     multi-LoRA batching lets tokens of different adapters share one pass of
+ *     the frozen base while each applies its own adapter.
+ *   - Sec. 3.2 ("Co-Serving Model", "Mixed forward batch"): each fine-tuning
+ *     sample is one more batch entry bound to a reserved training adapter; only
+ *     its rows keep activations for the backward.
+ *   - Sec. 3.2 ("Backward subprocess"): the backward computes the LoRA
+ *     gradients of the training rows; the base weight stays frozen.
+ *   - Sec. 4.1 ("Fine-tuning Workload"): rank 16 with alpha 32; each adapter
+ *     here carries its own scale s_a (alpha / r for the paper's adapter).
+ *
+ * For a token row x bound to adapter a (row-vector form):
+ *     h = x A_a^T                  (rank r_a; kept for training rows)
+ *     y = x W^T + s_a h B_a^T      (one rounding of the fp32 sum)
+ * and, for training rows with upstream gradient dy:
+ *     g   = s_a dy B_a             (gradient reaching h)
+ *     dB_a += s_a dy^T h,  dA_a += g^T x,  dx = dy W + g A_a.
+ *
+ * LAYOUTS.  Every matrix is dense row-major in the paper's orientation, which
+ * is also the torch.nn.Linear / PEFT parameter layout (K = in features,
+ * N = out features, T = tokens in the batch, T_t = training tokens):
+ *     X      [T][K]                 input rows of the whole batch
+ *     W      [N][K]                 frozen base weight
+ *     A      [n_ad][r_max][K]       stacked adapter down-projections
+ *     B      [n_ad][N][r_max]       stacked adapter up-projections
+ *     Y      [T][N]                 output
+ *     H_save [T_t][r_max]           h of the training rows (pre-scale)
+ *     dY     [T_t][N]               upstream gradient of the training rows
+ *     dX     [T_t][K]               input gradient of the training rows
+ *     dA     [n_ad][r_max][K] fp32, dB [n_ad][N][r_max] fp32
+ * Training rows are numbered in ascending token-row order ("compact order");
+ * H_save, dY and dX use it.  Rank-padding entries (index j >= r_a) are never
+ * read or written.  Element type: bf16 (DSV_BF16) or fp32 (DSV_F32) for every
+ * tensor except dA / dB, which are fp32 in both modes.  bf16 arithmetic
+ * accumulates in fp32; h is rounded to bf16 once and that same value feeds
+ * both the output and H_save.
+ *
+ * OWNERSHIP.  The caller owns every device buffer (metadata blob, inputs,
+ * outputs, workspaces).  The library allocates no device memory; it owns only
+ * the host-side plan.  Every launch is asynchronous on the caller's HIP stream
+ * (NULL = default stream); a plan is immutable once built and may serve any
+ * number of projections and streams.
+ *
+ * ERRORS.  Every check runs on the host before any launch; a call that
+ * returns an error has launched nothing and written nothing.  Launch failures
+ * are reported as DSV_ERR_DEVICE.  No C++ exception crosses this interface.
+ */
+#ifndef DSV_H
+#define DSV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* One batch entry: tokens [start, start + len) of the batch, bound to
+ * `adapter`; is_train = 1 marks a fine-tuning sample (Sec. 3.2). */
+typedef struct {
+  int32_t start;
+  int32_t len;
+  int32_t adapter;
+  int32_t is_train;
+} dsv_segment;
+
+typedef enum { DSV_BF16 = 0, DSV_F32 = 1 } dsv_dtype;
+
+enum {
+  DSV_OK = 0,
+  DSV_ERR_ARG = -1,    /* null / misaligned pointer, negative count, plan not on device */
+  DSV_ERR_RANGE = -2,  /* adapter id, rank, r_max, scale or flag out of range */
+  DSV_ERR_LAYOUT = -3, /* segments do not tile [0, n_tokens) exactly */
+  DSV_ERR_SIZE = -4,   /* buffer too small, K / N not a positive multiple of 8, too large */
+  DSV_ERR_DEVICE = -5  /* a HIP call or kernel launch failed */
+};
+
+typedef struct dsv_plan dsv_plan;
+
+/* Largest supported adapter rank stride. */
+#define DSV_MAX_RANK 64
+
+/*
+ * dsv_segments_build -- validate and pack the batch's segment table.
+ *
+ * segs[n_segs]: the batch entries, in any order.  They must tile
+ * [0, n_tokens) exactly; zero-length entries are no-ops (0 <= start <=
+ * n_tokens) and are otherwise ignored.  adapter_rank[n_adapters] in
+ * [1, r_max], adapter_scale[n_adapters] finite, 1 <= r_max <= DSV_MAX_RANK.
+ *
+ * The plan records the per-row adapter map, the compact training-row order,
+ * the rows of each adapter for the rank-r shrink, the split between rows
+ * whose low-rank term rides the GEMM tile and rows grouped by adapter for the
+ * gathered path (many short segments, e.g. decode), the GEMM tile list and
+ * the per-adapter chunks of the backward reductions.
+ *
+ * d_meta == NULL: validation and size query only.  *meta_bytes receives the
+ *   device blob size; if out_plan is not NULL a host-only plan is returned
+ *   that the dsv_plan_* queries accept but fwd / bwd reject (DSV_ERR_ARG).
+ * d_meta != NULL: a 256-byte aligned device buffer of at least *meta_bytes
+ *   bytes; the packed metadata is copied into it with one asynchronous copy
+ *   on hip_stream, and the returned plan refers to it.  d_meta must stay
+ *   allocated while the plan is used.
+ * On error *out_plan is set to NULL (when out_plan is not NULL).
+ */
+int dsv_segments_build(const dsv_segment* segs, int32_t n_segs, int32_t n_tokens,
+                       const int32_t* adapter_rank, const float* adapter_scale,
+                       int32_t n_adapters, int32_t r_max, void* d_meta,
+                       size_t* meta_bytes, void* hip_stream, dsv_plan** out_plan);
+
+/* Number of training tokens T_t (rows of H_save, dY and dX); -1 if plan is NULL. */
+int32_t dsv_plan_train_rows(const dsv_plan* plan);
+
+/* Copies the compact training-row order (T_t token rows, ascending) into
+ * host_out.  Returns T_t or a negative status. */
+int32_t dsv_plan_train_row_index(const dsv_plan* plan, int32_t* host_out);
+
+/* Copies the token rows served by the gathered low-rank path (slot order:
+ * by adapter, then row) into host_out.  Returns their count or a negative
+ * status. */
+int32_t dsv_plan_gathered_rows(const dsv_plan* plan, int32_t* host_out);
+
+/* Copies the host image of the packed metadata (meta_bytes bytes) into
+ * host_out, for inspection.  Returns DSV_OK or a negative status. */
+int dsv_plan_meta_copy(const dsv_plan* plan, void* host_out, size_t bytes);
+
+/* Counts of the plan's work lists, in this order: fwd GEMM row tiles,
+ * shrink items, gathered rows, gathered items, bwd GEMM row tiles, bwd
+ * chunks, adapters owning training rows, bwd rank-r items.  Returns DSV_OK
+ * or DSV_ERR_ARG. */
+int dsv_plan_counts(const dsv_plan* plan, int32_t out[8]);
+
+/* Releases the host plan (NULL is a no-op).  If the plan was uploaded, first
+ * waits until its asynchronous metadata copy has completed.  Does not touch
+ * d_meta; kernels already queued keep reading it from there. */
+void dsv_plan_free(dsv_plan* plan);
+
+/*
+ * dsv_cobatch_fwd_workspace -- bytes of device workspace dsv_cobatch_fwd
+ * needs for this plan, dtype and shape (h of every row, plus the fp32
+ * low-rank terms of the gathered rows).
+ */
+int dsv_cobatch_fwd_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                              size_t* bytes);
+
+/*
+ * dsv_cobatch_fwd -- Y = X W^T + s_a (X A_a^T) B_a^T for every row, and
+ * H_save = X A_a^T for the training rows (Sec. 2.2, Sec. 3.2).
+ * H_save may be NULL only when the plan has no training rows.  K and N must
+ * be positive multiples of 8; every pointer 16-byte aligned; workspace of at
+ * least dsv_cobatch_fwd_workspace bytes, 256-byte aligned.
+ */
+int dsv_cobatch_fwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                    const void* X, const void* W, const void* A, const void* B, void* Y,
+                    void* H_save, void* workspace, size_t workspace_bytes, void* hip_stream);
+
+/*
+ * dsv_lora_bwd_workspace -- bytes of device workspace dsv_lora_bwd needs
+ * (transposed copies of the small operands, g, and the fp32 partial sums of
+ * the deterministic reductions over training tokens).
+ */
+int dsv_lora_bwd_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                           size_t* bytes);
+
+/*
+ * dsv_lora_bwd -- LoRA backward of the training rows (Sec. 3.2, "Backward
+ * subprocess"): with g = s_a dY B_a,
+ *     dB_a  (+)=  s_a dY^T H_save      dA_a  (+)=  g^T X_train
+ *     dX     =   dY W + g A_a          (skipped when dX is NULL)
+ * where the sums run over the training rows of adapter a.  accumulate = 0
+ * overwrites, accumulate = 1 adds to, the dA / dB slices of adapters that own
+ * training rows; other slices are untouched.  The reductions over tokens are
+ * deterministic (fixed-order fp32 partial sums, no atomics): repeated calls
+ * give bit-identical results.  With no training rows the call is a no-op.
+ */
+int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                 const void* X, const void* W, const void* A, const void* B,
+                 const void* H_save, const void* dY, float* dA, float* dB, void* dX,
+                 int32_t accumulate, void* workspace, size_t workspace_bytes,
+                 void* hip_stream);
+
+/*
+ * Kernel timing for benchmarks.  While enabled (on = 1), every
+ * dsv_cobatch_fwd / dsv_lora_bwd call records a HIP event pair on its own
+ * stream immediately around its matrix-core GEMM launch (forward: the base
+ * GEMM with its low-rank prologue; backward: the dX GEMM).  Up to 4096 pairs
+ * are kept; further launches are not timed.  dsv_timing_read waits for the
+ * recorded events, returns the summed milliseconds and launch counts of the
+ * forward and backward GEMMs, and releases the pairs.  Not thread-safe:
+ * enable it only in a single-threaded benchmark.  Returns DSV_OK, or
+ * DSV_ERR_DEVICE if a HIP event call failed.
+ */
+int dsv_timing_enable(int32_t on);
+int dsv_timing_read(double* fwd_ms, int32_t* fwd_launches, double* bwd_ms,
+                    int32_t* bwd_launches);
+
+/* Static description of a status code. */
+const char* dsv_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DSV_H */

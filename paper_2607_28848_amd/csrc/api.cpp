@@ -1,0 +1,415 @@
+// api.cpp -- the C entry points: argument checks on the host, workspace
+// carving, and the launch sequence of the forward and backward passes.
+#include <hip/hip_runtime.h>
+
+#include <cstring>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace {
+
+using namespace dsv;
+
+constexpr int64_t kMaxDim = 1 << 20;
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+int64_t ld_rank(int32_t r_max) { return (r_max + 7) & ~7; }  // 16-byte rows of rank entries
+
+struct FwdWs {
+  size_t h_all, delta, total;
+};
+struct BwdWs {
+  size_t bt, ht, g, gt, part_b, part_a, total;
+  int64_t ldt;
+};
+
+FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N) {
+  FwdWs w{};
+  size_t off = 0;
+  if (dt == DSV_BF16) {
+    w.h_all = off;
+    off = align256(off + (size_t)p.T * ld_rank(p.r_max) * 2);
+    w.delta = off;
+    off = align256(off + (size_t)p.n_gather * N * 4);
+  } else {
+    w.h_all = off;
+    off = align256(off + (size_t)p.T * p.r_max * 4);
+    w.delta = off;
+  }
+  w.total = off;
+  return w;
+}
+
+BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
+  BwdWs w{};
+  size_t off = 0;
+  w.ldt = (p.T_t + 7) & ~7;
+  if (dt == DSV_BF16) {
+    w.bt = off;
+    off = align256(off + (size_t)p.n_tads * p.r_max * N * 2);
+    w.ht = off;
+    off = align256(off + (size_t)p.r_max * w.ldt * 2);
+    w.g = off;
+    off = align256(off + (size_t)p.T_t * ld_rank(p.r_max) * 2);
+    w.gt = off;
+    off = align256(off + (size_t)p.r_max * w.ldt * 2);
+    w.part_b = off;
+    off = align256(off + (size_t)p.n_chunks * N * p.r_max * 4);
+    w.part_a = off;
+    off = align256(off + (size_t)p.n_chunks * K * p.r_max * 4);
+  } else {
+    w.g = off;
+    off = align256(off + (size_t)p.T_t * p.r_max * 4);
+  }
+  w.total = off;
+  return w;
+}
+
+int check_common(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N) {
+  if (!p) return DSV_ERR_ARG;
+  if (dt != DSV_BF16 && dt != DSV_F32) return DSV_ERR_RANGE;
+  if (K <= 0 || N <= 0 || (K & 7) || (N & 7) || K > kMaxDim || N > kMaxDim) return DSV_ERR_SIZE;
+  return DSV_OK;
+}
+
+int ptr_ok(const void* p) { return p && aligned16(p); }
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+// Benchmark timing of the GEMM launches (dsv_timing_enable / dsv_timing_read).
+struct Timing {
+  static constexpr int kMaxPairs = 4096;
+  bool on = false;
+  int n = 0;
+  hipEvent_t ev[kMaxPairs][2] = {};
+  int kind[kMaxPairs] = {};  // 0 forward GEMM, 1 dX GEMM
+};
+Timing g_timing;
+
+// Records the start event of a timed launch; returns the pair index or -1.
+int timing_begin(int kind, hipStream_t s) {
+  Timing& t = g_timing;
+  if (!t.on || t.n >= Timing::kMaxPairs) return -1;
+  const int i = t.n;
+  for (int k = 0; k < 2; ++k)
+    if (!t.ev[i][k] && hipEventCreate(&t.ev[i][k]) != hipSuccess) return -1;
+  if (hipEventRecord(t.ev[i][0], s) != hipSuccess) return -1;
+  t.kind[i] = kind;
+  t.n = i + 1;
+  return i;
+}
+
+void timing_end(int i, hipStream_t s) {
+  if (i >= 0) (void)hipEventRecord(g_timing.ev[i][1], s);
+}
+
+}  // namespace
+
+extern "C" int dsv_timing_enable(int32_t on) {
+  g_timing.on = on != 0;
+  return DSV_OK;
+}
+
+extern "C" int dsv_timing_read(double* fwd_ms, int32_t* fwd_n, double* bwd_ms, int32_t* bwd_n) {
+  double ms[2] = {0.0, 0.0};
+  int32_t cnt[2] = {0, 0};
+  int rc = DSV_OK;
+  for (int i = 0; i < g_timing.n; ++i) {
+    float e = 0.f;
+    if (hipEventSynchronize(g_timing.ev[i][1]) != hipSuccess ||
+        hipEventElapsedTime(&e, g_timing.ev[i][0], g_timing.ev[i][1]) != hipSuccess) {
+      rc = DSV_ERR_DEVICE;
+      continue;
+    }
+    ms[g_timing.kind[i]] += e;
+    cnt[g_timing.kind[i]] += 1;
+  }
+  g_timing.n = 0;
+  if (fwd_ms) *fwd_ms = ms[0];
+  if (fwd_n) *fwd_n = cnt[0];
+  if (bwd_ms) *bwd_ms = ms[1];
+  if (bwd_n) *bwd_n = cnt[1];
+  return rc;
+}
+
+extern "C" int dsv_cobatch_fwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N,
+                                         size_t* bytes) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  if (!bytes) return DSV_ERR_ARG;
+  *bytes = fwd_ws(*p, dt, N).total;
+  return DSV_OK;
+}
+
+extern "C" int dsv_lora_bwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N,
+                                      size_t* bytes) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  if (!bytes) return DSV_ERR_ARG;
+  *bytes = bwd_ws(*p, dt, K, N).total;
+  return DSV_OK;
+}
+
+extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                               const void* W, const void* A, const void* B, void* Y, void* H_save,
+                               void* workspace, size_t workspace_bytes, void* hip_stream) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  if (!p->d_meta) return DSV_ERR_ARG;
+  if (p->T == 0) return DSV_OK;  // empty batch: nothing to read or write
+  if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(Y)) return DSV_ERR_ARG;
+  if (p->T_t > 0 && !ptr_ok(H_save)) return DSV_ERR_ARG;
+  const FwdWs ws = fwd_ws(*p, dt, N);
+  if (ws.total > 0) {
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
+    if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const MetaLayout& L = p->lay;
+  const int32_t* ranks = p->dptr(L.ranks);
+  const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
+  hipError_t e = hipSuccess;
+
+  if (dt == DSV_F32) {
+    F32Args a{};
+    a.T = p->T;
+    a.Tt = p->T_t;
+    a.K = K;
+    a.N = N;
+    a.r_max = p->r_max;
+    a.row_adapter = p->dptr(L.row_adapter);
+    a.row_train = p->dptr(L.row_train);
+    a.ranks = ranks;
+    a.scales = scales;
+    a.X = static_cast<const float*>(X);
+    a.W = static_cast<const float*>(W);
+    a.A = static_cast<const float*>(A);
+    a.B = static_cast<const float*>(B);
+    a.Y = static_cast<float*>(Y);
+    a.Hsave = static_cast<float*>(H_save);
+    a.Hall = at<float>(workspace, ws.h_all);
+    e = launch_f32_fwd(a, s);
+    return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
+  }
+
+  const int64_t ldh = ld_rank(p->r_max);
+  uint16_t* h_all = at<uint16_t>(workspace, ws.h_all);
+  float* delta = p->n_gather > 0 ? at<float>(workspace, ws.delta) : nullptr;
+
+  // 1. shrink: h of every row, grouped by adapter.
+  SkinnyArgs sk{};
+  sk.P = static_cast<const uint16_t*>(X);
+  sk.ldp = K;
+  sk.rows = p->dptr(L.shrink_rows);
+  sk.items = p->dptr(L.shrink_items);
+  sk.Q = static_cast<const uint16_t*>(A);
+  sk.q_ad = (int64_t)p->r_max * K;
+  sk.ldq = K;
+  sk.qsel = nullptr;
+  sk.ranks = ranks;
+  sk.scales = nullptr;
+  sk.C = K;
+  sk.out1 = h_all;
+  sk.ld1 = ldh;
+  sk.out2 = static_cast<uint16_t*>(H_save);
+  sk.ld2 = p->r_max;
+  sk.row_train = p->dptr(L.row_train);
+  if ((e = launch_shrink(sk, p->n_shrink, s)) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 2. gathered rows: fp32 low-rank term, each touched adapter read once.
+  if (p->n_gather > 0) {
+    e = launch_gather_expand(h_all, ldh, static_cast<const uint16_t*>(B), N, p->r_max,
+                             p->dptr(L.gather_items), p->n_gitems, p->dptr(L.gather_rows), ranks,
+                             scales, delta, s);
+    if (e != hipSuccess) return DSV_ERR_DEVICE;
+  }
+
+  // 3. base GEMM with the low-rank prologue, one rounding.
+  GemmArgs g{};
+  g.P = static_cast<const uint16_t*>(X);
+  g.ldp = K;
+  g.Q = static_cast<const uint16_t*>(W);
+  g.ldq = K;
+  g.out = static_cast<uint16_t*>(Y);
+  g.ldo = N;
+  g.Nout = N;
+  g.C = K;
+  g.tiles = p->dptr(L.fwd_tiles);
+  g.n_mtiles = p->n_ftiles;
+  g.n_ntiles = (N + 255) / 256;
+  g.Lp = h_all;
+  g.ldl = ldh;
+  g.Lq = static_cast<const uint16_t*>(B);
+  g.lq_ad = (int64_t)N * p->r_max;
+  g.lq_j = 1;
+  g.lq_col = p->r_max;
+  g.ranks = ranks;
+  g.scales = scales;
+  g.delta = delta;
+  g.gslot = p->dptr(L.gslot);
+  const int tk = timing_begin(0, s);
+  e = launch_gemm_nt(g, s);
+  timing_end(tk, s);
+  if (e != hipSuccess) return DSV_ERR_DEVICE;
+  return DSV_OK;
+}
+
+extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                            const void* W, const void* A, const void* B, const void* H_save,
+                            const void* dY, float* dA, float* dB, void* dX, int32_t accumulate,
+                            void* workspace, size_t workspace_bytes, void* hip_stream) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  if (accumulate != 0 && accumulate != 1) return DSV_ERR_RANGE;
+  if (!p->d_meta) return DSV_ERR_ARG;
+  if (p->T_t == 0) return DSV_OK;  // no training rows: nothing to read or write
+  if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(dA) || !ptr_ok(dB))
+    return DSV_ERR_ARG;
+  if (dX && !aligned16(dX)) return DSV_ERR_ARG;
+  if (p->T_t > 0 && (!ptr_ok(H_save) || !ptr_ok(dY))) return DSV_ERR_ARG;
+  const BwdWs ws = bwd_ws(*p, dt, K, N);
+  if (ws.total > 0) {
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
+    if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const MetaLayout& L = p->lay;
+  const int32_t* ranks = p->dptr(L.ranks);
+  const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
+  hipError_t e = hipSuccess;
+
+  if (dt == DSV_F32) {
+    F32Args a{};
+    a.T = p->T;
+    a.Tt = p->T_t;
+    a.K = K;
+    a.N = N;
+    a.r_max = p->r_max;
+    a.train_rows = p->dptr(L.train_rows);
+    a.train_adapter = p->dptr(L.train_adapter);
+    a.train_ads = p->dptr(L.train_ads);
+    a.n_tads = p->n_tads;
+    a.tad_ptr = p->dptr(L.tad_chunk_ptr);
+    a.tad_chunks = p->dptr(L.tad_chunks);
+    a.chunks = p->dptr(L.chunks);
+    a.ranks = ranks;
+    a.scales = scales;
+    a.X = static_cast<const float*>(X);
+    a.W = static_cast<const float*>(W);
+    a.A = static_cast<const float*>(A);
+    a.B = static_cast<const float*>(B);
+    a.Hs = static_cast<const float*>(H_save);
+    a.dY = static_cast<const float*>(dY);
+    a.G = at<float>(workspace, ws.g);
+    a.dA = dA;
+    a.dB = dB;
+    a.dX = static_cast<float*>(dX);
+    a.accumulate = accumulate;
+    e = launch_f32_bwd(a, s);
+    return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
+  }
+
+  const int64_t ldh = ld_rank(p->r_max);
+  uint16_t* bt = at<uint16_t>(workspace, ws.bt);
+  uint16_t* ht = at<uint16_t>(workspace, ws.ht);
+  uint16_t* gm = at<uint16_t>(workspace, ws.g);
+  uint16_t* gt = at<uint16_t>(workspace, ws.gt);
+  float* part_b = at<float>(workspace, ws.part_b);
+  float* part_a = at<float>(workspace, ws.part_a);
+  const int32_t* train_ads = p->dptr(L.train_ads);
+
+  // 1. transposed copies of the training adapters' B and of H_save.
+  if ((e = launch_transpose_b(static_cast<const uint16_t*>(B), N, p->r_max, train_ads, p->n_tads, ranks,
+                              bt, s)) != hipSuccess)
+    return DSV_ERR_DEVICE;
+  if ((e = launch_transpose_h(static_cast<const uint16_t*>(H_save), p->T_t, p->r_max,
+                              p->dptr(L.train_adapter), ranks, ht, ws.ldt, s)) != hipSuccess)
+    return DSV_ERR_DEVICE;
+
+  // 2. g = s_a dy B_a (contraction over N) -> G [T_t][ldh] and G^T [r_max][ldt].
+  SkinnyArgs sk{};
+  sk.P = static_cast<const uint16_t*>(dY);
+  sk.ldp = N;
+  sk.rows = nullptr;
+  sk.items = p->dptr(L.train_items);
+  sk.Q = bt;
+  sk.q_ad = (int64_t)p->r_max * N;
+  sk.ldq = N;
+  sk.qsel = p->dptr(L.ad_slot);
+  sk.ranks = ranks;
+  sk.scales = scales;
+  sk.C = N;
+  sk.out1 = gm;
+  sk.ld1 = ldh;
+  sk.out2 = gt;
+  sk.ld2 = ws.ldt;
+  if ((e = launch_gmat(sk, p->n_titems, s)) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 3. per-chunk fp32 partials of dy^T h (-> dB) and x^T g (-> dA).
+  TokenReduceArgs tb{};
+  tb.P = static_cast<const uint16_t*>(dY);
+  tb.ldp = N;
+  tb.prow = nullptr;
+  tb.Qt = ht;
+  tb.ldqt = ws.ldt;
+  tb.chunks = p->dptr(L.chunks);
+  tb.ranks = ranks;
+  tb.C = N;
+  tb.r_max = p->r_max;
+  tb.part = part_b;
+  if ((e = launch_token_reduce(tb, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  TokenReduceArgs ta = tb;
+  ta.P = static_cast<const uint16_t*>(X);
+  ta.ldp = K;
+  ta.prow = p->dptr(L.train_rows);
+  ta.Qt = gt;
+  ta.C = K;
+  ta.part = part_a;
+  if ((e = launch_token_reduce(ta, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 4. fixed-order sums into dB (scaled by s_a) and dA.
+  const int32_t* tad_ptr = p->dptr(L.tad_chunk_ptr);
+  const int32_t* tad_chunks = p->dptr(L.tad_chunks);
+  if ((e = launch_reduce_out(part_b, N, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks,
+                             scales, false, accumulate, dB, s)) != hipSuccess)
+    return DSV_ERR_DEVICE;
+  if ((e = launch_reduce_out(part_a, K, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks,
+                             nullptr, true, accumulate, dA, s)) != hipSuccess)
+    return DSV_ERR_DEVICE;
+
+  // 5. dx = dy W + g A_a on the matrix cores (W read with a transposing load).
+  if (dX) {
+    GemmArgs g{};
+    g.P = static_cast<const uint16_t*>(dY);
+    g.ldp = N;
+    g.Q = static_cast<const uint16_t*>(W);
+    g.ldq = K;
+    g.out = static_cast<uint16_t*>(dX);
+    g.ldo = K;
+    g.Nout = K;
+    g.C = N;
+    g.tiles = p->dptr(L.bwd_tiles);
+    g.n_mtiles = p->n_btiles;
+    g.n_ntiles = (K + 255) / 256;
+    g.Lp = gm;
+    g.ldl = ldh;
+    g.Lq = static_cast<const uint16_t*>(A);
+    g.lq_ad = (int64_t)p->r_max * K;
+    g.lq_j = K;
+    g.lq_col = 1;
+    g.ranks = ranks;
+    g.scales = nullptr;
+    g.delta = nullptr;
+    g.gslot = nullptr;
+    const int tk = timing_begin(1, s);
+    e = launch_gemm_nn(g, s);
+    timing_end(tk, s);
+    if (e != hipSuccess) return DSV_ERR_DEVICE;
+  }
+  return DSV_OK;
+}

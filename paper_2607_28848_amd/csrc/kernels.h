@@ -1,0 +1,113 @@
+// kernels.h -- argument blocks and host launchers of the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dsv {
+
+// GEMM with a low-rank prologue:  out = P Q' + (low-rank term) rounded once.
+//   NT (forward):  out[m][n] = sum_c P[m][c] Q[n][c]        Q is [Nout][C]
+//   NN (dX):       out[m][n] = sum_c P[m][c] Q[c][n]        Q is [C][Nout]
+// Low-rank term of a row m in tile group (a, lo, hi):
+//   scale(a) * sum_j Lp[m][j] Lq(a, j, n),  j < rank(a),
+//   Lq(a, j, n) = Lq[a * lq_ad + j * lq_j + n * lq_col]
+// Rows gathered elsewhere add delta[gslot[m]][n] (fp32, already scaled).
+struct GemmArgs {
+  const uint16_t* P;
+  int64_t ldp;
+  const uint16_t* Q;
+  int64_t ldq;
+  uint16_t* out;
+  int64_t ldo;
+  int32_t Nout, C;
+  const int32_t* tiles;  // row tiles, kTileWords words each
+  int32_t n_mtiles, n_ntiles;
+  const uint16_t* Lp;
+  int64_t ldl;
+  const uint16_t* Lq;
+  int64_t lq_ad, lq_j, lq_col;
+  const int32_t* ranks;
+  const float* scales;   // nullptr: scale 1
+  const float* delta;    // nullptr: no gathered rows
+  const int32_t* gslot;
+};
+
+// Rank-r contraction of a few rows of one adapter (shrink h = x A^T, and
+// g = s dy B in the backward).
+struct SkinnyArgs {
+  const uint16_t* P;
+  int64_t ldp;
+  const int32_t* rows;   // item element -> P row
+  const int32_t* items;  // {adapter, begin, count, aux}
+  const uint16_t* Q;     // per adapter slot: [r][C], row stride ldq
+  int64_t q_ad, ldq;
+  const int32_t* qsel;   // adapter -> Q slot (nullptr: the adapter id)
+  const int32_t* ranks;
+  const float* scales;   // nullptr: scale 1
+  int32_t C;
+  // outputs (mode-dependent)
+  uint16_t* out1;        // [rows][ld1]
+  int64_t ld1;
+  uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train; g: transposed [r][ld2]
+  int64_t ld2;
+  const int32_t* row_train;
+};
+
+// Per-chunk fp32 partial sums over training tokens:
+//   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Qt[j][t]
+struct TokenReduceArgs {
+  const uint16_t* P;
+  int64_t ldp;
+  const int32_t* prow;   // compact row -> P row (nullptr: identity)
+  const uint16_t* Qt;    // [r_max][ldqt]
+  int64_t ldqt;
+  const int32_t* chunks;
+  const int32_t* ranks;
+  int32_t C, r_max;
+  float* part;
+};
+
+// Launchers (bf16).  Each returns hipSuccess or the launch error.
+hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
+hipError_t launch_gemm_nn(const GemmArgs& a, hipStream_t s);
+hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, hipStream_t s);
+hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, hipStream_t s);
+hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
+                                int32_t r_max, const int32_t* items, int32_t n_items,
+                                const int32_t* gather_rows, const int32_t* ranks,
+                                const float* scales, float* delta, hipStream_t s);
+hipError_t launch_token_reduce(const TokenReduceArgs& a, int32_t n_chunks, hipStream_t s);
+hipError_t launch_reduce_out(const float* part, int32_t C, int32_t r_max, const int32_t* train_ads,
+                             int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
+                             const int32_t* ranks, const float* scales, bool a_layout,
+                             int32_t accumulate, float* out, hipStream_t s);
+hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
+                              int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
+hipError_t launch_transpose_h(const uint16_t* Hs, int32_t Tt, int32_t r_max,
+                              const int32_t* train_adapter, const int32_t* ranks, uint16_t* Ht,
+                              int64_t ldt, hipStream_t s);
+
+// Launchers (fp32 mode: plain FMA kernels, same semantics).
+struct F32Args {
+  int32_t T, Tt, K, N, r_max;
+  const int32_t* row_adapter;
+  const int32_t* row_train;
+  const int32_t* train_rows;
+  const int32_t* train_adapter;
+  const int32_t* train_ads;
+  int32_t n_tads;
+  const int32_t* tad_ptr;
+  const int32_t* tad_chunks;
+  const int32_t* chunks;
+  const int32_t* ranks;
+  const float* scales;
+  const float *X, *W, *A, *B, *Hs, *dY;
+  float *Y, *Hsave, *Hall, *G, *dA, *dB, *dX;
+  int32_t accumulate;
+};
+hipError_t launch_f32_fwd(const F32Args& a, hipStream_t s);
+hipError_t launch_f32_bwd(const F32Args& a, hipStream_t s);
+
+}  // namespace dsv

@@ -1,0 +1,142 @@
+// kernels_f32.hip -- fp32 mode of the co-batched multi-LoRA layer: plain
+// fp32 FMA kernels, one thread per output element, with the same semantics,
+// layouts and fixed summation orders as the bf16 path (no matrix cores: this
+// mode exists for tight-tolerance checks, not for throughput).
+#include <hip/hip_runtime.h>
+
+#include "kernels.h"
+#include "plan.h"
+
+namespace dsv {
+namespace {
+
+// h = x A_a^T for every row (j < r_a); training rows also into H_save.
+__global__ void f32_shrink(F32Args g) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int t = (int)(idx / g.r_max), j = (int)(idx % g.r_max);
+  if (t >= g.T) return;
+  const int a = g.row_adapter[t];
+  if (j >= g.ranks[a]) return;
+  const float* x = g.X + (int64_t)t * g.K;
+  const float* Aj = g.A + ((int64_t)a * g.r_max + j) * g.K;
+  float acc = 0.f;
+  for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], Aj[k], acc);
+  g.Hall[(int64_t)t * g.r_max + j] = acc;
+  const int tr = g.row_train[t];
+  if (tr >= 0) g.Hsave[(int64_t)tr * g.r_max + j] = acc;
+}
+
+// y = x W^T + s_a h B_a^T, fp32 sum, one store.
+__global__ void f32_out(F32Args g) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int t = (int)(idx / g.N), n = (int)(idx % g.N);
+  if (t >= g.T) return;
+  const int a = g.row_adapter[t], r = g.ranks[a];
+  const float* x = g.X + (int64_t)t * g.K;
+  const float* w = g.W + (int64_t)n * g.K;
+  float low = 0.f;
+  const float* h = g.Hall + (int64_t)t * g.r_max;
+  const float* b = g.B + ((int64_t)a * g.N + n) * g.r_max;
+  for (int j = 0; j < r; ++j) low = fmaf(h[j], b[j], low);
+  float acc = g.scales[a] * low;
+  for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], w[k], acc);
+  g.Y[(int64_t)t * g.N + n] = acc;
+}
+
+// g = s_a dy B_a for every training row.
+__global__ void f32_gmat(F32Args g) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int i = (int)(idx / g.r_max), j = (int)(idx % g.r_max);
+  if (i >= g.Tt) return;
+  const int a = g.train_adapter[i];
+  if (j >= g.ranks[a]) return;
+  const float* dy = g.dY + (int64_t)i * g.N;
+  const float* b = g.B + (int64_t)a * g.N * g.r_max + j;
+  float acc = 0.f;
+  for (int n = 0; n < g.N; ++n) acc = fmaf(dy[n], b[(int64_t)n * g.r_max], acc);
+  g.G[(int64_t)i * g.r_max + j] = g.scales[a] * acc;
+}
+
+// dB[a][n][j] (+)= s_a sum_i H_save[i][j] dy[i][n]; training rows of a in
+// compact order (chunk list), fixed order.
+__global__ void f32_db(F32Args g) {
+  const int slot = blockIdx.y;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int n = (int)(idx / g.r_max), j = (int)(idx % g.r_max);
+  if (n >= g.N) return;
+  const int a = g.train_ads[slot];
+  if (j >= g.ranks[a]) return;
+  float acc = 0.f;
+  for (int p = g.tad_ptr[slot]; p < g.tad_ptr[slot + 1]; ++p) {
+    const int32_t* ck = g.chunks + (int64_t)g.tad_chunks[p] * kItemWords;
+    for (int i = ck[1]; i < ck[1] + ck[2]; ++i)
+      acc = fmaf(g.Hs[(int64_t)i * g.r_max + j], g.dY[(int64_t)i * g.N + n], acc);
+  }
+  float* o = g.dB + ((int64_t)a * g.N + n) * g.r_max + j;
+  const float v = g.scales[a] * acc;
+  *o = g.accumulate ? *o + v : v;
+}
+
+// dA[a][j][k] (+)= sum_i g[i][j] x[t_i][k].
+__global__ void f32_da(F32Args g) {
+  const int slot = blockIdx.y;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int j = (int)(idx / g.K), k = (int)(idx % g.K);
+  if (j >= g.r_max) return;
+  const int a = g.train_ads[slot];
+  if (j >= g.ranks[a]) return;
+  float acc = 0.f;
+  for (int p = g.tad_ptr[slot]; p < g.tad_ptr[slot + 1]; ++p) {
+    const int32_t* ck = g.chunks + (int64_t)g.tad_chunks[p] * kItemWords;
+    for (int i = ck[1]; i < ck[1] + ck[2]; ++i)
+      acc = fmaf(g.G[(int64_t)i * g.r_max + j], g.X[(int64_t)g.train_rows[i] * g.K + k], acc);
+  }
+  float* o = g.dA + ((int64_t)a * g.r_max + j) * g.K + k;
+  *o = g.accumulate ? *o + acc : acc;
+}
+
+// dx = dy W + g A_a.
+__global__ void f32_dx(F32Args g) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int i = (int)(idx / g.K), k = (int)(idx % g.K);
+  if (i >= g.Tt) return;
+  const int a = g.train_adapter[i], r = g.ranks[a];
+  float acc = 0.f;
+  const float* gi = g.G + (int64_t)i * g.r_max;
+  const float* Aa = g.A + (int64_t)a * g.r_max * g.K + k;
+  for (int j = 0; j < r; ++j) acc = fmaf(gi[j], Aa[(int64_t)j * g.K], acc);
+  const float* dy = g.dY + (int64_t)i * g.N;
+  for (int n = 0; n < g.N; ++n) acc = fmaf(dy[n], g.W[(int64_t)n * g.K + k], acc);
+  g.dX[(int64_t)i * g.K + k] = acc;
+}
+
+unsigned blocks(int64_t n) { return (unsigned)((n + 255) / 256); }
+
+}  // namespace
+
+hipError_t launch_f32_fwd(const F32Args& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  hipLaunchKernelGGL(f32_shrink, dim3(blocks((int64_t)a.T * a.r_max)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(f32_out, dim3(blocks((int64_t)a.T * a.N)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_f32_bwd(const F32Args& a, hipStream_t s) {
+  if (a.Tt <= 0) return hipSuccess;
+  hipLaunchKernelGGL(f32_gmat, dim3(blocks((int64_t)a.Tt * a.r_max)), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(f32_db, dim3(blocks((int64_t)a.N * a.r_max), a.n_tads), dim3(256), 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  hipLaunchKernelGGL(f32_da, dim3(blocks((int64_t)a.r_max * a.K), a.n_tads), dim3(256), 0, s, a);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (a.dX) {
+    hipLaunchKernelGGL(f32_dx, dim3(blocks((int64_t)a.Tt * a.K)), dim3(256), 0, s, a);
+    e = hipGetLastError();
+  }
+  return e;
+}
+
+}  // namespace dsv

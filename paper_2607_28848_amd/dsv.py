@@ -1,0 +1,259 @@
+"""ctypes binding of libdsv.so (include/dsv.h): argument marshalling only.
+
+Every step of the layer runs in the HIP library; torch supplies device memory
+and the current HIP stream.  Importing this module fails loudly when the
+library has not been built (``python -m paper_2607_28848_amd.build``).
+
+Layouts (the paper's orientation, = torch.nn.Linear / PEFT parameters):
+    X [T][K], W [N][K], A [n_ad][r_max][K], B [n_ad][N][r_max],
+    Y [T][N], H_save / dY / dX over the compact training rows,
+    dA [n_ad][r_max][K] fp32, dB [n_ad][N][r_max] fp32.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdsv.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError("libdsv.so is not built: run `python -m paper_2607_28848_amd.build` "
+                      "(there is no fallback implementation)")
+
+# torch ships its own HIP runtime (same SONAME as /opt/rocm's).  Load it first so
+# that libdsv.so binds to that one runtime: device pointers and streams handed
+# over from torch are only valid in the runtime that created them.
+import torch  # noqa: E402,F401
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+OK, ERR_ARG, ERR_RANGE, ERR_LAYOUT, ERR_SIZE, ERR_DEVICE = 0, -1, -2, -3, -4, -5
+BF16, F32 = 0, 1
+MAX_RANK = 64
+
+_vp = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_sz = ctypes.c_size_t
+_i32p = ctypes.POINTER(ctypes.c_int32)
+_f32p = ctypes.POINTER(ctypes.c_float)
+
+_lib.dsv_segments_build.argtypes = [_i32p, _i32, _i32, _i32p, _f32p, _i32, _i32, _vp,
+                                    ctypes.POINTER(_sz), _vp, ctypes.POINTER(_vp)]
+_lib.dsv_segments_build.restype = ctypes.c_int
+_lib.dsv_plan_train_rows.argtypes = [_vp]
+_lib.dsv_plan_train_rows.restype = _i32
+_lib.dsv_plan_train_row_index.argtypes = [_vp, _i32p]
+_lib.dsv_plan_train_row_index.restype = _i32
+_lib.dsv_plan_gathered_rows.argtypes = [_vp, _i32p]
+_lib.dsv_plan_gathered_rows.restype = _i32
+_lib.dsv_plan_meta_copy.argtypes = [_vp, _vp, _sz]
+_lib.dsv_plan_meta_copy.restype = ctypes.c_int
+_lib.dsv_plan_counts.argtypes = [_vp, _i32p]
+_lib.dsv_plan_counts.restype = ctypes.c_int
+_lib.dsv_plan_free.argtypes = [_vp]
+_lib.dsv_plan_free.restype = None
+_lib.dsv_cobatch_fwd_workspace.argtypes = [_vp, ctypes.c_int, _i32, _i32, ctypes.POINTER(_sz)]
+_lib.dsv_cobatch_fwd_workspace.restype = ctypes.c_int
+_lib.dsv_cobatch_fwd.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                 _vp, _sz, _vp]
+_lib.dsv_cobatch_fwd.restype = ctypes.c_int
+_lib.dsv_lora_bwd_workspace.argtypes = [_vp, ctypes.c_int, _i32, _i32, ctypes.POINTER(_sz)]
+_lib.dsv_lora_bwd_workspace.restype = ctypes.c_int
+_lib.dsv_lora_bwd.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                              _vp, _vp, _i32, _vp, _sz, _vp]
+_lib.dsv_lora_bwd.restype = ctypes.c_int
+_lib.dsv_timing_enable.argtypes = [_i32]
+_lib.dsv_timing_enable.restype = ctypes.c_int
+_lib.dsv_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), _i32p,
+                                 ctypes.POINTER(ctypes.c_double), _i32p]
+_lib.dsv_timing_read.restype = ctypes.c_int
+_lib.dsv_status_string.argtypes = [ctypes.c_int]
+_lib.dsv_status_string.restype = ctypes.c_char_p
+
+COUNT_NAMES = ("fwd_tiles", "shrink_items", "gathered_rows", "gather_items", "bwd_tiles",
+               "chunks", "train_adapters", "train_items")
+
+
+class DsvError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__("%s: %s" % (what, _lib.dsv_status_string(status).decode()))
+
+
+def _check(rc: int, what: str):
+    if rc != OK:
+        raise DsvError(rc, what)
+
+
+def lib_handle() -> ctypes.CDLL:
+    return _lib
+
+
+def _stream_handle(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(int(stream.cuda_stream))
+
+
+def _ptr(t) -> ctypes.c_void_p:
+    return ctypes.c_void_p(0 if t is None else int(t.data_ptr()))
+
+
+class Plan:
+    """A packed segment table.  device=None builds a host-only plan (inspection only)."""
+
+    def __init__(self, segments: Sequence[Sequence[int]], n_tokens: int, ranks, scales, r_max: int,
+                 device=None, stream=None):
+        seg = np.ascontiguousarray(np.asarray(segments, np.int32).reshape(-1, 4))
+        self.segments = seg
+        self.n_tokens = int(n_tokens)
+        self.ranks = np.ascontiguousarray(np.asarray(ranks, np.int32))
+        self.scales = np.ascontiguousarray(np.asarray(scales, np.float32))
+        self.r_max = int(r_max)
+        self._h = ctypes.c_void_p()
+        self.meta = None
+        nbytes = _sz(0)
+        args = (seg.ctypes.data_as(_i32p), seg.shape[0], self.n_tokens,
+                self.ranks.ctypes.data_as(_i32p), self.scales.ctypes.data_as(_f32p),
+                self.ranks.shape[0], self.r_max)
+        if device is None:
+            _check(_lib.dsv_segments_build(*args, None, ctypes.byref(nbytes), None,
+                                           ctypes.byref(self._h)), "dsv_segments_build")
+        else:
+            import torch
+            _check(_lib.dsv_segments_build(*args, None, ctypes.byref(nbytes), None, None),
+                   "dsv_segments_build (size query)")
+            self.meta = torch.empty(max(int(nbytes.value), 256), dtype=torch.uint8, device=device)
+            _check(_lib.dsv_segments_build(*args, _ptr(self.meta), ctypes.byref(nbytes),
+                                           _stream_handle(stream), ctypes.byref(self._h)),
+                   "dsv_segments_build")
+        self.meta_bytes = int(nbytes.value)
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h is not None and h.value:
+            _lib.dsv_plan_free(h)
+            self._h = ctypes.c_void_p()
+
+    @property
+    def handle(self):
+        return self._h
+
+    @property
+    def train_tokens(self) -> int:
+        return int(_lib.dsv_plan_train_rows(self._h))
+
+    def train_rows(self) -> np.ndarray:
+        out = np.zeros(max(self.train_tokens, 1), np.int32)
+        n = _lib.dsv_plan_train_row_index(self._h, out.ctypes.data_as(_i32p))
+        if n < 0:
+            raise DsvError(n, "dsv_plan_train_row_index")
+        return out[:n]
+
+    def gathered_rows(self) -> np.ndarray:
+        out = np.zeros(max(self.n_tokens, 1), np.int32)
+        n = _lib.dsv_plan_gathered_rows(self._h, out.ctypes.data_as(_i32p))
+        if n < 0:
+            raise DsvError(n, "dsv_plan_gathered_rows")
+        return out[:n]
+
+    def meta_words(self) -> np.ndarray:
+        out = np.zeros(self.meta_bytes // 4, np.int32)
+        _check(_lib.dsv_plan_meta_copy(self._h, out.ctypes.data, self.meta_bytes), "dsv_plan_meta_copy")
+        return out
+
+    def counts(self) -> dict:
+        out = np.zeros(8, np.int32)
+        _check(_lib.dsv_plan_counts(self._h, out.ctypes.data_as(_i32p)), "dsv_plan_counts")
+        return dict(zip(COUNT_NAMES, (int(v) for v in out)))
+
+
+def segments_build(segments, n_tokens, ranks, scales, r_max, device=None, stream=None) -> Plan:
+    return Plan(segments, n_tokens, ranks, scales, r_max, device=device, stream=stream)
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise TypeError("dsv supports bfloat16 and float32 tensors, got %s" % t.dtype)
+
+
+def fwd_workspace_bytes(plan: Plan, dtype_code: int, K: int, N: int) -> int:
+    n = _sz(0)
+    _check(_lib.dsv_cobatch_fwd_workspace(plan.handle, dtype_code, K, N, ctypes.byref(n)),
+           "dsv_cobatch_fwd_workspace")
+    return int(n.value)
+
+
+def bwd_workspace_bytes(plan: Plan, dtype_code: int, K: int, N: int) -> int:
+    n = _sz(0)
+    _check(_lib.dsv_lora_bwd_workspace(plan.handle, dtype_code, K, N, ctypes.byref(n)),
+           "dsv_lora_bwd_workspace")
+    return int(n.value)
+
+
+def _workspace(nbytes, device, given):
+    import torch
+    if given is not None:
+        return given
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+
+
+def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, stream=None):
+    """Y = X W^T + s_a (X A_a^T) B_a^T per row; H_save = X A_a^T of the training rows."""
+    import torch
+    dt = _dtype_code(X)
+    T, K = X.shape
+    N = W.shape[0]
+    if Y is None:
+        Y = torch.empty((T, N), dtype=X.dtype, device=X.device)
+    if H_save is None and plan.train_tokens > 0:
+        H_save = torch.empty((plan.train_tokens, plan.r_max), dtype=X.dtype, device=X.device)
+    ws = _workspace(fwd_workspace_bytes(plan, dt, K, N), X.device, workspace)
+    _check(_lib.dsv_cobatch_fwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y),
+                                _ptr(H_save), _ptr(ws), ws.numel() * ws.element_size(),
+                                _stream_handle(stream)), "dsv_cobatch_fwd")
+    return Y, H_save
+
+
+def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want_dx=True,
+             accumulate: bool = False, workspace=None, stream=None):
+    """LoRA gradients of the training rows: dA, dB (fp32) and dX."""
+    import torch
+    dt = _dtype_code(X)
+    T, K = X.shape
+    N = W.shape[0]
+    n_ad = A.shape[0]
+    if dA is None:
+        dA = torch.zeros((n_ad, plan.r_max, K), dtype=torch.float32, device=X.device)
+    if dB is None:
+        dB = torch.zeros((n_ad, N, plan.r_max), dtype=torch.float32, device=X.device)
+    if dX is None and want_dx and plan.train_tokens > 0:
+        dX = torch.empty((plan.train_tokens, K), dtype=X.dtype, device=X.device)
+    ws = _workspace(bwd_workspace_bytes(plan, dt, K, N), X.device, workspace)
+    _check(_lib.dsv_lora_bwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H_save),
+                             _ptr(dY), _ptr(dA), _ptr(dB), _ptr(dX if want_dx else None),
+                             1 if accumulate else 0, _ptr(ws), ws.numel() * ws.element_size(),
+                             _stream_handle(stream)), "dsv_lora_bwd")
+    return dA, dB, dX
+
+
+def timing_enable(on: bool = True):
+    _check(_lib.dsv_timing_enable(1 if on else 0), "dsv_timing_enable")
+
+
+def timing_read():
+    """(fwd GEMM ms, fwd launches, dX GEMM ms, dX launches) since the last read."""
+    fm, bm = ctypes.c_double(0), ctypes.c_double(0)
+    fn, bn = ctypes.c_int32(0), ctypes.c_int32(0)
+    _check(_lib.dsv_timing_read(ctypes.byref(fm), ctypes.byref(fn), ctypes.byref(bm),
+                                ctypes.byref(bn)), "dsv_timing_read")
+    return fm.value, fn.value, bm.value, bn.value

@@ -36,16 +36,23 @@ def round_bf16(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 
     Returns (values as float64, storage bits as uint16).  NaN stays NaN.
     Finite inputs must lie in the normal bf16 range (true for every draw here).
+    The rounding works on the float64 bit pattern: the 45 low mantissa bits
+    are dropped with round-half-to-even (a carry ripples into the exponent).
     """
-    x = np.asarray(x, np.float64)
+    x = np.ascontiguousarray(x, np.float64)
+    u = x.view(np.uint64)
+    r = u >> np.uint64(45)
+    r &= np.uint64(1)
+    r += np.uint64((1 << 44) - 1)
+    r += u
+    r &= np.uint64(~((1 << 45) - 1) & 0xFFFFFFFFFFFFFFFF)
+    v = r.view(np.float64)
     nan = np.isnan(x)
-    xs = np.where(nan, 0.0, x)
-    m, e = np.frexp(xs)                 # xs = m * 2**e, 0.5 <= |m| < 1
-    q = np.rint(m * 256.0)              # 8 significant bits, ties to even
-    v = np.ldexp(q, e - 8)
-    v = np.where(nan, np.nan, v)
-    bits = (v.astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
-    return v, bits
+    if nan.any():
+        v[nan] = np.nan
+    bits = v.astype(np.float32).view(np.uint32)
+    bits >>= np.uint32(16)
+    return v, bits.astype(np.uint16)
 
 
 def round_f32(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
@@ -54,7 +61,9 @@ def round_f32(x: np.ndarray) -> Tuple[np.ndarray, np.ndarray]:
 
 
 def bf16_bits_to_f64(bits: np.ndarray) -> np.ndarray:
-    return (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    f32 = (np.asarray(bits, np.uint16).astype(np.uint32) << 16).view(np.float32)
+    with np.errstate(invalid="ignore"):
+        return f32.astype(np.float64)
 
 
 @dataclasses.dataclass

@@ -1,0 +1,246 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 reference.
+
+Bar: max|gpu - ref| / max|ref| per output tensor <= 2e-2 for bf16 inputs and
+<= 1e-5 for fp32 inputs; indexing (H_save placement, untouched slices and
+padding) bit-exact; permuting the segment table and repeating a call give
+bit-identical results.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_28848_amd import workloads as wl
+from gpu_util import (TOL_BF16, TOL_F32, Run, oracle_bwd, oracle_fwd, to_host,
+                      train_mask_slices)
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _check_all(w, run, Y, H, dA, dB, dX, tol, rows=None, dx_rows=None):
+    t = run.t
+    Yr, Hr = oracle_fwd(w, t, rows)
+    Yg = to_host(Y) if rows is None else to_host(Y)[rows]
+    errs = {"Y": oracle.rel_err(Yg, Yr)}
+    tr = run.plan.train_rows()
+    if len(tr):
+        Hg = to_host(H)
+        # H_save row i is the h of token row tr[i]
+        Hfull, _ = None, None
+        Hr_t = oracle_fwd(w, t, tr)[1]
+        errs["H_save"] = oracle.rel_err(Hg, Hr_t)
+        G, dAr, dBr, dXr = oracle_bwd(w, t, dx_rows=dx_rows)
+        dAg, dBg = to_host(dA), to_host(dB)
+        for a, r in train_mask_slices(w):
+            errs["dA%d" % a] = oracle.rel_err(dAg[a, :r], dAr[a, :r])
+            errs["dB%d" % a] = oracle.rel_err(dBg[a, :, :r], dBr[a, :, :r])
+        dXg = to_host(dX) if dx_rows is None else to_host(dX)[dx_rows]
+        errs["dX"] = oracle.rel_err(dXg, dXr)
+    _say("  rel errors: " + ", ".join("%s=%.2e" % kv for kv in errs.items()))
+    for k, v in errs.items():
+        assert v <= tol, (k, v)
+    return errs
+
+
+def _full(w, pad=np.nan, tol=TOL_BF16):
+    _say("case %s T=%d Tt=%d K=%d N=%d" % (w.name, w.n_tokens, w.train_tokens,
+                                          w.projections[0].K, w.projections[0].N))
+    run = Run(w, pad=pad)
+    Y, H = run.fwd()
+    dA, dB, dX = run.bwd(H)
+    import torch
+    torch.cuda.synchronize()
+    return run, _check_all(w, run, Y, H, dA, dB, dX, tol)
+
+
+def test_tiny_f32():
+    """Tiny fp32 layer: K = N = 512, 2 adapters of rank 8, 3 segments."""
+    _full(wl.tiny(), tol=TOL_F32)
+
+
+MIXED = [(0, 100, 3, 0), (100, 1, 1, 0), (101, 1, 2, 0), (102, 300, 0, 1), (402, 1, 3, 0),
+         (403, 57, 2, 0), (460, 2, 1, 0), (462, 129, 1, 1), (591, 3, 0, 0), (594, 111, 4, 0)]
+MIXED_RANKS = [16, 8, 64, 32, 5]
+
+
+def test_mixed_bf16_ragged():
+    """Several row tiles with a ragged tail, K not a multiple of 64, N not of 256, mixed
+    ranks (one of them not a multiple of 8), decode singles among prefill and two
+    training segments on two adapters; rank padding is NaN."""
+    w = wl.custom(MIXED, MIXED_RANKS, K=520, N=776, r_max=64, name="mixed_ragged")
+    _full(w)
+
+
+def test_mixed_f32_ragged():
+    w = wl.custom(MIXED, MIXED_RANKS, K=136, N=200, dtype="f32", r_max=64, name="mixed_f32")
+    _full(w, tol=TOL_F32)
+
+
+def test_decode_heavy_small():
+    rng = np.random.default_rng(5)
+    pieces = [(1, int(a), 0) for a in rng.integers(0, 16, size=300)] + [(200, 1, 1)]
+    order = rng.permutation(len(pieces))
+    segs, s = [], 0
+    for i in order:
+        l, a, t = pieces[i]
+        segs.append((s, l, a, t))
+        s += l
+    ranks = [(8, 16, 32, 64)[a % 4] for a in range(16)]
+    w = wl.custom(segs, ranks, K=256, N=512, r_max=64, name="decode_small")
+    run, _ = _full(w)
+    assert run.plan.counts()["gathered_rows"] >= 290
+
+
+def test_inference_only_and_training_only():
+    w = wl.custom([(0, 300, 0, 0), (300, 33, 1, 0)], [8, 16], K=128, N=264, r_max=16, name="inf_only")
+    run = Run(w)
+    Y, H = run.fwd()
+    assert H is None and run.plan.train_tokens == 0
+    dA, dB, dX = run.bwd(None)                   # no training rows: a no-op
+    Yr, _ = oracle_fwd(w, run.t)
+    assert oracle.rel_err(to_host(Y), Yr) <= TOL_BF16
+    assert (to_host(dA) == 0).all() and (to_host(dB) == 0).all() and dX is None
+    w2 = wl.custom([(0, 70, 1, 1), (70, 200, 0, 1)], [8, 16], K=128, N=264, r_max=16, name="train_only")
+    _full(w2)
+
+
+def test_empty_batch():
+    import torch
+    from paper_2607_28848_amd import dsv
+    plan = dsv.segments_build([], 0, [4], [2.0], 4, device="cuda")
+    X = torch.empty((0, 64), dtype=torch.bfloat16, device="cuda")
+    W = torch.zeros((32, 64), dtype=torch.bfloat16, device="cuda")
+    A = torch.zeros((1, 4, 64), dtype=torch.bfloat16, device="cuda")
+    B = torch.zeros((1, 32, 4), dtype=torch.bfloat16, device="cuda")
+    Y, H = dsv.cobatch_fwd(plan, X, W, A, B)
+    assert Y.shape == (0, 32) and H is None
+
+
+def test_zero_B_is_exactly_base():
+    """B = 0: the low-rank term enters the fp32 accumulator as an exact zero, so Y is
+    bit-identical however the rows are grouped (tile groups or gathered path)."""
+    import torch
+    w1 = wl.custom(MIXED, MIXED_RANKS, K=520, N=776, r_max=64, name="zeroB")
+    run1 = Run(w1)
+    run1.B.zero_()
+    Y1, _ = run1.fwd()
+    # same tokens, every row its own single-token segment on a rotating adapter
+    segs = [(t, 1, t % 5, 0) for t in range(w1.n_tokens)]
+    w2 = wl.custom(segs, MIXED_RANKS, K=520, N=776, r_max=64, name="zeroB_singles")
+    run2 = Run(w2, tensors=run1.t)
+    run2.B.zero_()
+    Y2, _ = run2.fwd()
+    torch.cuda.synchronize()
+    assert run2.plan.counts()["gathered_rows"] == w2.n_tokens
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    t = run1.t
+    assert oracle.rel_err(to_host(Y1), t.X @ t.W.T) <= TOL_BF16
+
+
+def test_table_permutation_bit_exact_and_deterministic():
+    import torch
+    w = wl.custom(MIXED, MIXED_RANKS, K=520, N=776, r_max=64, name="perm")
+    run = Run(w)
+    Tt = run.plan.train_tokens
+    nan_h = lambda: torch.full((Tt, 64), float("nan"), dtype=torch.bfloat16, device="cuda")  # noqa: E731
+    Y, H = run.fwd(H_save=nan_h())   # rank padding of H_save is never written: same sentinel
+    dA, dB, dX = run.bwd(H)
+    rng = np.random.default_rng(3)
+    perm = [MIXED[i] for i in rng.permutation(len(MIXED))]
+    w2 = wl.custom(perm, MIXED_RANKS, K=520, N=776, r_max=64, name="perm2")
+    run2 = Run(w2, tensors=run.t)
+    for _ in range(2):  # permuted table, then a repeat of it
+        Y2, H2 = run2.fwd(H_save=nan_h())
+        dA2, dB2, dX2 = run2.bwd(H2)
+        torch.cuda.synchronize()
+        for name, u, v in (("Y", Y, Y2), ("H_save", H, H2), ("dX", dX, dX2)):
+            assert torch.equal(u.view(torch.int16), v.view(torch.int16)), name
+        for name, u, v in (("dA", dA, dA2), ("dB", dB, dB2)):
+            assert torch.equal(u.view(torch.int32), v.view(torch.int32)), name
+
+
+def test_accumulate_and_untouched_slices():
+    """accumulate=1 adds to the training adapters' slices; other adapters' slices and
+    the rank padding of every slice keep their sentinel bits; H_save padding columns
+    are never written."""
+    import torch
+    w = wl.custom(MIXED, MIXED_RANKS, K=520, N=776, r_max=64, name="accum")
+    run = Run(w)
+    Tt = run.plan.train_tokens
+    H = torch.full((Tt, 64), float("nan"), dtype=torch.bfloat16, device="cuda")
+    Y, H = run.fwd(H_save=H)
+    dA0 = torch.randn((5, 64, 520), device="cuda")
+    dB0 = torch.randn((5, 776, 64), device="cuda")
+    dA, dB = dA0.clone(), dB0.clone()
+    run.bwd(H, dA=dA, dB=dB, accumulate=True)
+    torch.cuda.synchronize()
+    Hh = to_host(H)
+    ra = np.array([w.ranks[a] for a in oracle.rows(w.segments, w.n_tokens, 5)[0][run.plan.train_rows()]])
+    for i, r in enumerate(ra):
+        assert np.isnan(Hh[i, r:]).all() and np.isfinite(Hh[i, :r]).all()
+    G, dAr, dBr, _ = oracle_bwd(w, run.t)
+    dA_h, dB_h, dA0_h, dB0_h = (x.cpu().numpy().astype(np.float64) for x in (dA, dB, dA0, dB0))
+    owners = dict(train_mask_slices(w))
+    for a in range(5):
+        r = int(w.ranks[a])
+        if a in owners:
+            assert oracle.rel_err(dA_h[a, :r] - dA0_h[a, :r], dAr[a, :r]) <= TOL_BF16
+            assert oracle.rel_err(dB_h[a, :, :r] - dB0_h[a, :, :r], dBr[a, :, :r]) <= TOL_BF16
+            assert (dA_h[a, r:] == dA0_h[a, r:]).all() and (dB_h[a, :, r:] == dB0_h[a, :, r:]).all()
+        else:
+            assert (dA_h[a] == dA0_h[a]).all() and (dB_h[a] == dB0_h[a]).all()
+
+
+def _sampled(w, p, n_rows=24, seed=0):
+    """Full-size projection: every output of the HIP path against the reference on
+    sampled rows (Y, dX) and in full (H_save, dA, dB)."""
+    import torch
+    K, N = w.projections[p].K, w.projections[p].N
+    _say("case %s/%s T=%d Tt=%d K=%d N=%d" % (w.name, w.projections[p].name, w.n_tokens,
+                                             w.train_tokens, K, N))
+    run = Run(w, p=p, pad=np.nan)
+    Y, H = run.fwd()
+    dA, dB, dX = run.bwd(H)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(seed + p)
+    # segment boundaries and random rows
+    firsts = [s for (s, l, _, _) in w.segments if l] + [s + l - 1 for (s, l, _, _) in w.segments if l]
+    rows = np.unique(np.concatenate([rng.choice(w.n_tokens, n_rows, replace=False),
+                                     rng.choice(firsts, min(n_rows, len(firsts)), replace=False)]))
+    Tt = w.train_tokens
+    dx_rows = np.unique(np.concatenate([rng.choice(Tt, n_rows, replace=False), [0, Tt - 1]])) if Tt else None
+    return _check_all(w, run, Y, H, dA, dB, dX, TOL_BF16, rows=rows.astype(np.int32),
+                      dx_rows=None if dx_rows is None else dx_rows.astype(np.int32))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("p", range(7))
+def test_llama8b_layer_set_full_size(p):
+    """Llama-3-8B layer set (q, k, v, o, gate, up, down) at full size, bf16."""
+    _sampled(wl.llama8b_mixed(), p)
+
+
+@pytest.mark.timeout(600)
+def test_decode_heavy_full_size():
+    """256 single-token decode segments over 64 adapters of ranks 8..64 + 2048 training
+    tokens on the 4096 x 14336 gate projection."""
+    w = wl.decode_heavy()
+    _sampled(w, 0)
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("p", range(2))
+def test_llama70b_full_size(p):
+    _sampled(wl.llama70b(), p, n_rows=12)
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("frac", [0.0, 0.5, 1.0])
+def test_load_sweep_full_size(frac):
+    _sampled(wl.load_sweep(frac), 0, n_rows=12)
