@@ -131,11 +131,11 @@ int32_t dsv_plan_gathered_rows(const dsv_plan* plan, int32_t* host_out);
  * host_out, for inspection.  Returns DSV_OK or a negative status. */
 int dsv_plan_meta_copy(const dsv_plan* plan, void* host_out, size_t bytes);
 
-/* Counts of the plan's work lists, in this order: fwd GEMM row tiles,
- * shrink items, gathered rows, gathered items, bwd GEMM row tiles, bwd
- * chunks, adapters owning training rows, bwd rank-r items.  Returns DSV_OK
- * or DSV_ERR_ARG. */
-int dsv_plan_counts(const dsv_plan* plan, int32_t out[8]);
+/* Counts of the plan's work lists, in this order: fwd 256-row GEMM tiles,
+ * shrink items, gathered rows, gathered items, bwd 256-row GEMM tiles, bwd
+ * chunks, adapters owning training rows, bwd rank-r items, fwd 128-row GEMM
+ * tiles, bwd 128-row GEMM tiles.  Returns DSV_OK or DSV_ERR_ARG. */
+int dsv_plan_counts(const dsv_plan* plan, int32_t out[10]);
 
 /* Releases the host plan (NULL is a no-op).  If the plan was uploaded, first
  * waits until its asynchronous metadata copy has completed.  Does not touch

@@ -76,6 +76,34 @@ int check_common(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N) {
 
 int ptr_ok(const void* p) { return p && aligned16(p); }
 
+// GEMM tile shape for an output of (row tiles of 256 / of 128) x n_out: the
+// shape whose launch finishes soonest on 256 compute units, counting whole
+// waves of workgroups (1 resident workgroup per CU for 256-row tiles, 2 for
+// 128 x 128) and a relative matrix-core efficiency per shape (smaller tiles
+// re-read more operand bytes per FLOP from L2 and LDS).
+struct TileChoice {
+  int tm, tn;
+};
+TileChoice choose_tiles(int32_t m256, int32_t m128, int32_t n_out) {
+  struct Cand {
+    int tm, tn, bpc;
+    double eff;
+  } cands[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.9}, {128, 128, 2, 0.75}};
+  TileChoice best{256, 256};
+  double best_cost = 1e300;
+  for (const Cand& c : cands) {
+    const int64_t mt = c.tm == 256 ? m256 : m128;
+    const int64_t tiles = mt * ((n_out + c.tn - 1) / c.tn);
+    const int64_t slots = 256LL * c.bpc;
+    const double cost = (double)((tiles + slots - 1) / slots) * c.bpc * (c.tm * c.tn / 65536.0) / c.eff;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best = {c.tm, c.tn};
+    }
+  }
+  return best;
+}
+
 template <typename T>
 T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(base) + off);
@@ -237,11 +265,13 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   g.ldq = K;
   g.out = static_cast<uint16_t*>(Y);
   g.ldo = N;
+  g.M = p->T;
   g.Nout = N;
   g.C = K;
-  g.tiles = p->dptr(L.fwd_tiles);
-  g.n_mtiles = p->n_ftiles;
-  g.n_ntiles = (N + 255) / 256;
+  const TileChoice tc = choose_tiles(p->n_ftiles, p->n_ftiles128, N);
+  g.tiles = p->dptr(tc.tm == 256 ? L.fwd_tiles : L.fwd_tiles128);
+  g.n_mtiles = tc.tm == 256 ? p->n_ftiles : p->n_ftiles128;
+  g.n_ntiles = (N + tc.tn - 1) / tc.tn;
   g.Lp = h_all;
   g.ldl = ldh;
   g.Lq = static_cast<const uint16_t*>(B);
@@ -253,7 +283,7 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   g.delta = delta;
   g.gslot = p->dptr(L.gslot);
   const int tk = timing_begin(0, s);
-  e = launch_gemm_nt(g, s);
+  e = launch_gemm_nt(g, tc.tm, tc.tn, s);
   timing_end(tk, s);
   if (e != hipSuccess) return DSV_ERR_DEVICE;
   return DSV_OK;
@@ -391,11 +421,13 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     g.ldq = K;
     g.out = static_cast<uint16_t*>(dX);
     g.ldo = K;
+    g.M = p->T_t;
     g.Nout = K;
     g.C = N;
-    g.tiles = p->dptr(L.bwd_tiles);
-    g.n_mtiles = p->n_btiles;
-    g.n_ntiles = (K + 255) / 256;
+    const TileChoice tc = choose_tiles(p->n_btiles, p->n_btiles128, K);
+    g.tiles = p->dptr(tc.tm == 256 ? L.bwd_tiles : L.bwd_tiles128);
+    g.n_mtiles = tc.tm == 256 ? p->n_btiles : p->n_btiles128;
+    g.n_ntiles = (K + tc.tn - 1) / tc.tn;
     g.Lp = gm;
     g.ldl = ldh;
     g.Lq = static_cast<const uint16_t*>(A);
@@ -407,7 +439,7 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     g.delta = nullptr;
     g.gslot = nullptr;
     const int tk = timing_begin(1, s);
-    e = launch_gemm_nn(g, s);
+    e = launch_gemm_nn(g, tc.tm, tc.tn, s);
     timing_end(tk, s);
     if (e != hipSuccess) return DSV_ERR_DEVICE;
   }

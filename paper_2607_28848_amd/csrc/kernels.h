@@ -21,6 +21,7 @@ struct GemmArgs {
   int64_t ldq;
   uint16_t* out;
   int64_t ldo;
+  int32_t M;             // rows of P (bounds of the operand loads)
   int32_t Nout, C;
   const int32_t* tiles;  // row tiles, kTileWords words each
   int32_t n_mtiles, n_ntiles;
@@ -70,8 +71,10 @@ struct TokenReduceArgs {
 };
 
 // Launchers (bf16).  Each returns hipSuccess or the launch error.
-hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s);
-hipError_t launch_gemm_nn(const GemmArgs& a, hipStream_t s);
+// Tile shapes (tm x tn): 256x256, 256x128 or 128x128; `tiles` must be the
+// plan's row-tile list of height tm.
+hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);
+hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, hipStream_t s);
 hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, hipStream_t s);
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,

@@ -74,26 +74,64 @@ __device__ __forceinline__ void transpose8x8(const u32x4 in[8], u32x4 out[8]) {
 }
 
 // ---------------------------------------------------------------------------
-// GEMM: 256 x 256 output tile per workgroup, 4 waves in a 2 x 2 grid, each
-// wave 128 x 128 = 4 x 4 tiles of v_mfma_f32_32x32x16_bf16.  K-steps of 64,
-// double-buffered LDS tiles of [256][64] bf16 for each operand, 16-byte
-// chunks XOR-swizzled so that both the staging stores and the fragment reads
-// are free of bank conflicts.
+// GEMM with a low-rank prologue.  TM x TN output tile per workgroup (256x256,
+// 256x128 or 128x128), 4 waves in a 2 x 2 grid, each wave (TM/2) x (TN/2) =
+// FM x FN tiles of v_mfma_f32_32x32x16_bf16.  K-steps of 64.
+//
+// Operand tiles go from global memory straight into LDS (buffer loads with
+// the LDS destination, 16 bytes per lane, one contiguous KiB per wave
+// instruction), double-buffered, one barrier per K-step.  Lanes are assigned
+// global chunks so that the LDS image is swizzled:
+//   K-contiguous tiles ([rows][64] bf16, 128-byte rows): 16-byte chunk c of
+//   row r sits in slot c ^ swz(r); MFMA fragments are 16-byte reads.
+//   N-contiguous weight tile of the dX GEMM ([64][TN] bf16): chunk c of row n
+//   sits in slot c ^ 2(n & 3); fragments are read with ds_read_b64_tr_b16,
+//   which hands each lane 4 contraction values of one output column.
+// Both read patterns are free of bank conflicts.  Out-of-range lanes point
+// past the buffer descriptor's range and receive zeros.
 // ---------------------------------------------------------------------------
-constexpr int TN = 256, TK = 64;
-constexpr int kStageLd = TN + 8;  // epilogue staging row stride (elements)
-constexpr int kLdsElems = (2 * 2 * kTileM * TK > kTileM * kStageLd) ? 2 * 2 * kTileM * TK
-                                                                     : kTileM * kStageLd;
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+extern "C" __device__ void llvm_amdgcn_raw_buffer_load_lds(i32x4 rsrc, lds_u32* lds, int size,
+                                                           int voffset, int soffset, int offset,
+                                                           int aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
 
-__device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * TK + ((chunk ^ swz(row)) << 3);
+// Buffer descriptor: 64-bit base, byte range, CDNA data-format word.
+__device__ __forceinline__ i32x4 make_rsrc(const void* base, uint64_t range) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  const uint32_t rg = range > 0xFFFFFFF0ull ? 0xFFFFFFF0u : (uint32_t)range;
+  i32x4 r;
+  r.x = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r.y = __builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  r.z = __builtin_amdgcn_readfirstlane((int)rg);
+  r.w = 0x00020000;
+  return r;
 }
 
-template <bool NN>
+__device__ __forceinline__ void vmem_wait_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+constexpr int TK = 64;
+
+__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+__device__ __forceinline__ int nn_swz(int n) { return 2 * (n & 3); }
+
+template <int TM, int TN>
+struct GemmShape {
+  static constexpr int WM = TM / 2, WN = TN / 2, FM = WM / 32, FN = WN / 32;
+  static constexpr int A_BYTES = TM * TK * 2, B_BYTES = TN * TK * 2;
+  static constexpr int STAGE = A_BYTES + B_BYTES;
+  static constexpr int STG_LD = TN + 8;  // epilogue staging row stride (elements)
+  static constexpr int LDS = (2 * STAGE > TM * STG_LD * 2) ? 2 * STAGE : TM * STG_LD * 2;
+};
+
+template <bool NN, int TM, int TN>
 __global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) uint16_t smem[kLdsElems];
+  using S = GemmShape<TM, TN>;
+  constexpr int WM = S::WM, WN = S::WN, FM = S::FM, FN = S::FN;
+  __shared__ __attribute__((aligned(1024))) char smem[S::LDS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave >> 1, wn = wave & 1;
 
@@ -115,187 +153,240 @@ __global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
   const int m0 = td[0], ngroups = td[1], has_gather = td[2], nrows = td[3];
   const int n0 = nt * TN;
 
-  f32x16 acc[4][4];
+  f32x16 acc[FM][FN];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
   // ---- low-rank prologue: tile groups on the matrix cores -----------------
+  // acc += (s_a h) B_a for the rows of each group.  s_a h is formed in fp32
+  // and split into bf16 hi + lo (|lo| <= 2^-9 |hi|), so the product carries
+  // the scale to about 2^-16 relative with no VALU work on the accumulators;
+  // with scale 1 (or a power of two) lo is exactly zero and is skipped.
   for (int gi = 0; gi < ngroups; ++gi) {
     const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
+    if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
     const int r = g.ranks[a];
+    const float sc = g.scales ? g.scales[a] : 1.f;
     const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
     for (int j0 = 0; j0 < r; j0 += 16) {
       const int jb = j0 + 8 * (lane >> 5);
       const int nv = min(8, r - jb);
-      bf16x8 af[4], bq[4];
+      bf16x8 af_hi[FM], af_lo[FM], bq[FN];
+      bool any_lo = false;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm * 128 + 32 * i + (lane & 31);
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * WM + 32 * i + (lane & 31);
         u32x4 v = zero4();
         if (row >= lo && row < hi && nv > 0) {
           const uint16_t* p = g.Lp + (int64_t)(m0 + row) * g.ldl + jb;
           v = (nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
         }
-        af[i] = as_bf(v);
+        uint32_t wh[4], wl[4];
+#pragma unroll
+        for (int d = 0; d < 4; ++d) {
+          const float x0 = sc * __uint_as_float(v[d] << 16);
+          const float x1 = sc * __uint_as_float(v[d] & 0xffff0000u);
+          const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+          const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+          wh[d] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          wl[d] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+          any_lo |= (wl[d] & 0x7fff7fffu) != 0u;
+        }
+        af_hi[i] = as_bf(u32x4{wh[0], wh[1], wh[2], wh[3]});
+        af_lo[i] = as_bf(u32x4{wl[0], wl[1], wl[2], wl[3]});
       }
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int col = n0 + wn * 128 + 32 * j + (lane & 31);
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + wn * WN + 32 * j + (lane & 31);
         u32x4 v = zero4();
-        if (col < g.Nout && nv > 0) v = ld8_masked(lq + (int64_t)jb * g.lq_j + (int64_t)col * g.lq_col, g.lq_j, nv);
+        if (col < g.Nout && nv > 0)
+          v = ld8_masked(lq + (int64_t)jb * g.lq_j + (int64_t)col * g.lq_col, g.lq_j, nv);
         bq[j] = as_bf(v);
       }
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bq[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af_hi[i], bq[j], acc[i][j], 0, 0, 0);
+      if (__builtin_amdgcn_ballot_w64(any_lo) != 0) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af_lo[i], bq[j], acc[i][j], 0, 0, 0);
+      }
     }
   }
-  if (g.scales != nullptr && ngroups > 0) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * 128 + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        float s = 1.f;
-        for (int gi = 0; gi < ngroups; ++gi)
-          if (row >= td[5 + 3 * gi] && row < td[6 + 3 * gi]) s = g.scales[td[4 + 3 * gi]];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j][v] *= s;
-      }
-  }
-  if (has_gather && g.delta != nullptr) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * 128 + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        if (row < nrows) {
-          const int gs = g.gslot[m0 + row];
-          if (gs >= 0) {
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int col = n0 + wn * 128 + 32 * j + (lane & 31);
-              if (col < g.Nout) acc[i][j][v] += g.delta[(int64_t)gs * g.Nout + col];
-            }
-          }
-        }
-      }
-  }
 
-  // ---- main loop -----------------------------------------------------------
-  // buffer b: A-operand tile at smem + b * 2 * kTileM * TK, B-operand tile right after it
-  auto sA = [&](int b) { return smem + b * (2 * kTileM * TK); };
-  auto sB = [&](int b) { return smem + b * (2 * kTileM * TK) + kTileM * TK; };
-  const int nk = (g.C + TK - 1) / TK;
-  u32x4 ra[8], rb[8];
+  // ---- main loop: direct-to-LDS operand tiles, double-buffered ----------
+  constexpr int A_LOADS = TM / 32, B_LOADS = TN / 32;  // 1-KiB wave loads per wave per K-step
+  int a_off[A_LOADS], a_kc[A_LOADS];
+#pragma unroll
+  for (int i = 0; i < A_LOADS; ++i) {
+    const int q = wave * A_LOADS + i;
+    const int row = 8 * q + (lane >> 3);
+    const int c = (lane & 7) ^ swz(row);
+    a_off[i] = (int)(((int64_t)row * g.ldp + 8 * c) * 2);
+    a_kc[i] = 8 * c;
+  }
+  int b_off[B_LOADS], b_kc[B_LOADS];
+#pragma unroll
+  for (int i = 0; i < B_LOADS; ++i) {
+    const int q = wave * B_LOADS + i;
+    if constexpr (!NN) {
+      const int col = 8 * q + (lane >> 3);
+      const int c = (lane & 7) ^ swz(col);
+      b_off[i] = (int)(((int64_t)col * g.ldq + 8 * c) * 2);
+      b_kc[i] = 8 * c;
+    } else {
+      const int byte = q * 1024 + 16 * lane;
+      const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
+      b_off[i] = (int)(((int64_t)n * g.ldq + 8 * (slot ^ nn_swz(n))) * 2);
+      b_kc[i] = n;
+    }
+  }
+  const uint16_t* a_base = g.P + (int64_t)m0 * g.ldp;
+  const int64_t a_rows = min((int64_t)TM, (int64_t)g.M - m0);
+  const uint16_t* b_base = NN ? g.Q + n0 : g.Q + (int64_t)n0 * g.ldq;
+  const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
 
-  auto load_tile = [&](int kt) {
+  auto issue = [&](int kt, int stage) {
     const int k0 = kt * TK;
-    const int ch = tid & 7;
-    const int kk = k0 + ch * 8;
+    char* sa = smem + stage * S::STAGE;
+    char* sb = sa + S::A_BYTES;
+    // descriptors rebased on the K-step keep every offset well inside 32 bits
+    const i32x4 ra = make_rsrc(a_base + k0, (uint64_t)(a_rows * g.ldp - k0) * 2);
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = (tid >> 3) + 32 * i;
-      ra[i] = (row < nrows && kk < g.C) ? ld16(g.P + (int64_t)(m0 + row) * g.ldp + kk) : zero4();
+    for (int i = 0; i < A_LOADS; ++i) {
+      const int q = wave * A_LOADS + i;
+      const int vo = (k0 + a_kc[i] < g.C) ? a_off[i] : (int)0x7FFFFFF0;
+      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
     }
     if constexpr (!NN) {
+      const i32x4 rb = make_rsrc(b_base + k0, (uint64_t)(b_cols * g.ldq - k0) * 2);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int col = (tid >> 3) + 32 * i;
-        rb[i] = (n0 + col < g.Nout && kk < g.C) ? ld16(g.Q + (int64_t)(n0 + col) * g.ldq + kk) : zero4();
+      for (int i = 0; i < B_LOADS; ++i) {
+        const int q = wave * B_LOADS + i;
+        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
+        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
       }
     } else {
-      const int cb = tid >> 5, ob = tid & 31;
-      const int ncol = n0 + 8 * ob;
+      // the 64 contraction rows of this K-step (fewer at the tail)
+      const i32x4 rb = make_rsrc(b_base + (int64_t)k0 * g.ldq,
+                                 (uint64_t)((int64_t)min(TK, g.C - k0) * g.ldq - n0) * 2);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int crow = k0 + 8 * cb + e;
-        rb[e] = (crow < g.C && ncol < g.Nout) ? ld16(g.Q + (int64_t)crow * g.ldq + ncol) : zero4();
+      for (int i = 0; i < B_LOADS; ++i) {
+        const int q = wave * B_LOADS + i;
+        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
+        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
       }
-    }
-  };
-  auto store_tile = [&](int buf) {
-    const int ch = tid & 7;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int row = (tid >> 3) + 32 * i;
-      *reinterpret_cast<u32x4*>(sA(buf) + lds_off(row, ch)) = ra[i];
-    }
-    if constexpr (!NN) {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int col = (tid >> 3) + 32 * i;
-        *reinterpret_cast<u32x4*>(sB(buf) + lds_off(col, ch)) = rb[i];
-      }
-    } else {
-      const int cb = tid >> 5, ob = tid & 31;
-      u32x4 tb[8];
-      transpose8x8(rb, tb);
-#pragma unroll
-      for (int c = 0; c < 8; ++c)
-        *reinterpret_cast<u32x4*>(sB(buf) + lds_off(8 * ob + c, cb)) = tb[c];
     }
   };
 
-  if (nk > 0) {
-    load_tile(0);
-    store_tile(0);
-  }
-  __syncthreads();
+  auto load_frags = [&](const char* sa, const char* sb, int s, bf16x8* af, bf16x8* bq) {
+    const int ch = 2 * s + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 32 * i + (lane & 31);
+      af[i] = as_bf(*reinterpret_cast<const u32x4*>(sa + row * 128 + 16 * (ch ^ swz(row))));
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      if constexpr (!NN) {
+        const int col = wn * WN + 32 * j + (lane & 31);
+        bq[j] = as_bf(*reinterpret_cast<const u32x4*>(sb + col * 128 + 16 * (ch ^ swz(col))));
+      } else {
+        const int gq = lane >> 4, lam = lane & 15;
+        const int c = wn * WN + 32 * j + 16 * (gq & 1) + 4 * (lam & 3);
+        s16x4 h[2];
+#pragma unroll
+        for (int hh = 0; hh < 2; ++hh) {
+          const int n = 16 * s + 8 * (gq >> 1) + 4 * hh + (lam >> 2);
+          const char* p = sb + n * (TN * 2) + 16 * ((c >> 3) ^ nn_swz(n)) + 2 * (c & 7);
+          h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+        }
+        u32x4 v;
+        v[0] = (uint32_t)(uint16_t)h[0][0] | ((uint32_t)(uint16_t)h[0][1] << 16);
+        v[1] = (uint32_t)(uint16_t)h[0][2] | ((uint32_t)(uint16_t)h[0][3] << 16);
+        v[2] = (uint32_t)(uint16_t)h[1][0] | ((uint32_t)(uint16_t)h[1][1] << 16);
+        v[3] = (uint32_t)(uint16_t)h[1][2] | ((uint32_t)(uint16_t)h[1][3] << 16);
+        bq[j] = as_bf(v);
+      }
+    }
+  };
+
+  const int nk = (g.C + TK - 1) / TK;
+  issue(0, 0);
   for (int kt = 0; kt < nk; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < nk) load_tile(kt + 1);
+    vmem_wait_all();
+    __syncthreads();
+    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
+    const char* sa = smem + (kt & 1) * S::STAGE;
+    const char* sb = sa + S::A_BYTES;
+    bf16x8 af[2][FM], bq[2][FN];
+    load_frags(sa, sb, 0, af[0], bq[0]);
 #pragma unroll
     for (int s = 0; s < TK / 16; ++s) {
-      const int ch = 2 * s + (lane >> 5);
-      bf16x8 af[4], bq[4];
+      if (s + 1 < TK / 16) load_frags(sa, sb, s + 1, af[(s + 1) & 1], bq[(s + 1) & 1]);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = wm * 128 + 32 * i + (lane & 31);
-        af[i] = as_bf(*reinterpret_cast<const u32x4*>(sA(buf) + lds_off(row, ch)));
-      }
+      for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int col = wn * 128 + 32 * j + (lane & 31);
-        bq[j] = as_bf(*reinterpret_cast<const u32x4*>(sB(buf) + lds_off(col, ch)));
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bq[j], acc[i][j], 0, 0, 0);
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bq[s & 1][j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) store_tile(buf ^ 1);
-    __syncthreads();
+    // Schedule of the K-step: the operand loads of the next K-step first,
+    // then the fragments of step 0, then each step's MFMAs with the next
+    // step's fragment reads spread between them.
+    constexpr int kReads = FM + (NN ? 2 : 1) * FN;  // LDS reads per 16-wide step
+    constexpr int kMfma = FM * FN;
+    __builtin_amdgcn_sched_group_barrier(0x020, A_LOADS + B_LOADS, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
+#pragma unroll
+    for (int s = 0; s < TK / 16 - 1; ++s) {
+#pragma unroll
+      for (int t = 0; t < kReads; ++t) {
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfma / kReads > 0 ? kMfma / kReads : 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      }
+      if (kMfma > kReads * (kMfma / kReads))
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads * (kMfma / kReads), 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
   }
 
   // ---- epilogue: one rounding, staged through LDS for 16-byte stores ------
-  uint16_t* st = smem;
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * 128 + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        const int col = wn * 128 + 32 * j + (lane & 31);
-        st[row * kStageLd + col] = f2bf(acc[i][j][v]);
-      }
   __syncthreads();
+  uint16_t* st = reinterpret_cast<uint16_t*>(smem);
+  const bool gather_tile = has_gather && g.delta != nullptr;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      // rows of the gathered path add their fp32 low-rank term before the rounding
+      const int gs = (gather_tile && row < nrows) ? g.gslot[m0 + row] : -1;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = wn * WN + 32 * j + (lane & 31);
+        float x = acc[i][j][v];
+        if (gs >= 0 && n0 + col < g.Nout) x += g.delta[(int64_t)gs * g.Nout + n0 + col];
+        st[row * S::STG_LD + col] = f2bf(x);
+      }
+    }
+  __syncthreads();
+  constexpr int CH = TN / 8;  // 16-byte chunks per staged row
 #pragma unroll 4
-  for (int it = 0; it < (kTileM * TN / 8) / 256; ++it) {
+  for (int it = 0; it < (TM * CH) / 256; ++it) {
     const int idx = tid + 256 * it;
-    const int row = idx >> 5, ch = idx & 31;
+    const int row = idx / CH, ch = idx % CH;
     const int col = n0 + ch * 8;
     if (row < nrows && col < g.Nout)
       *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + row) * g.ldo + col) =
-          *reinterpret_cast<const u32x4*>(st + row * kStageLd + ch * 8);
+          *reinterpret_cast<const u32x4*>(st + row * S::STG_LD + ch * 8);
   }
 }
 
@@ -521,16 +612,29 @@ __global__ __launch_bounds__(256) void transpose_h_kernel(const uint16_t* __rest
 
 }  // namespace
 
-hipError_t launch_gemm_nt(const GemmArgs& a, hipStream_t s) {
+namespace {
+template <bool NN>
+hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   if (a.n_mtiles <= 0 || a.n_ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemm_lora_kernel<false>, dim3(a.n_mtiles * a.n_ntiles), dim3(256), 0, s, a);
+  const dim3 grid(a.n_mtiles * a.n_ntiles), block(256);
+  if (tm == 256 && tn == 256)
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256>), grid, block, 0, s, a);
+  else if (tm == 256 && tn == 128)
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 128>), grid, block, 0, s, a);
+  else if (tm == 128 && tn == 128)
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 128, 128>), grid, block, 0, s, a);
+  else
+    return hipErrorInvalidValue;
   return hipGetLastError();
 }
+}  // namespace
 
-hipError_t launch_gemm_nn(const GemmArgs& a, hipStream_t s) {
-  if (a.n_mtiles <= 0 || a.n_ntiles <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gemm_lora_kernel<true>, dim3(a.n_mtiles * a.n_ntiles), dim3(256), 0, s, a);
-  return hipGetLastError();
+hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s) {
+  return launch_gemm_tiled<false>(a, tm, tn, s);
+}
+
+hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
+  return launch_gemm_tiled<true>(a, tm, tn, s);
 }
 
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, hipStream_t s) {

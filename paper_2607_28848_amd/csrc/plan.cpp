@@ -23,6 +23,8 @@ using dsv::kItemRows;
 using dsv::kItemWords;
 using dsv::kMaxGroups;
 using dsv::kMinGroupRows;
+using dsv::kBlockGroups;
+using dsv::kBlockM;
 using dsv::kTileM;
 using dsv::kTileWords;
 
@@ -112,15 +114,15 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
     i = j;
   }
 
-  // Forward GEMM row tiles.  Inside a tile, the longest same-adapter runs of
-  // at least kMinGroupRows rows (up to kMaxGroups of them) get their low-rank
-  // term from matrix-core products inside the tile; every other row (short
-  // segments such as single-token decode entries) is gathered by adapter and
-  // its fp32 low-rank term is computed beforehand, reading each adapter once.
-  std::vector<int32_t> fwd_tiles;
+  // Forward GEMM row tiles.  Per 128-row block, the longest same-adapter runs
+  // of at least kMinGroupRows rows (up to kBlockGroups of them) ride the tile;
+  // every other row is gathered by adapter and its fp32 low-rank term is
+  // computed beforehand, reading each adapter once.
+  std::vector<std::vector<Run>> block_groups;
+  std::vector<int32_t> block_gather;
   std::vector<char> gathered(T, 0);
-  for (int32_t r0 = 0; r0 < T; r0 += kTileM) {
-    const int32_t r1 = std::min(T, r0 + kTileM);
+  for (int32_t r0 = 0; r0 < T; r0 += kBlockM) {
+    const int32_t r1 = std::min(T, r0 + kBlockM);
     std::vector<Run> runs = runs_of(row_adapter.data(), r0, r1);
     std::vector<int32_t> idx(runs.size());
     std::iota(idx.begin(), idx.end(), 0);
@@ -129,7 +131,7 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
     });
     std::vector<Run> groups;
     for (int32_t k : idx)
-      if ((int32_t)groups.size() < kMaxGroups && runs[k].hi - runs[k].lo >= kMinGroupRows)
+      if ((int32_t)groups.size() < kBlockGroups && runs[k].hi - runs[k].lo >= kMinGroupRows)
         groups.push_back(runs[k]);
     std::sort(groups.begin(), groups.end(), [](const Run& x, const Run& y) { return x.lo < y.lo; });
     int32_t has_gather = 0;
@@ -141,14 +143,39 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
         for (int32_t t = r.lo; t < r.hi; ++t) gathered[t] = 1;
       }
     }
-    int32_t w[kTileWords] = {r0, (int32_t)groups.size(), has_gather, r1 - r0};
-    for (size_t g = 0; g < groups.size(); ++g) {
-      w[4 + 3 * g] = groups[g].adapter;
-      w[5 + 3 * g] = groups[g].lo - r0;
-      w[6 + 3 * g] = groups[g].hi - r0;
-    }
-    fwd_tiles.insert(fwd_tiles.end(), w, w + kTileWords);
+    block_groups.push_back(groups);
+    block_gather.push_back(has_gather);
   }
+  // Tiles of `tm` rows (a multiple of kBlockM): the groups of their blocks,
+  // adjacent groups of one adapter merged.
+  auto fwd_tiles_of = [&](int32_t tm) {
+    std::vector<int32_t> out;
+    const int32_t per = tm / kBlockM;
+    for (int32_t b0 = 0; b0 < (int32_t)block_groups.size(); b0 += per) {
+      const int32_t r0 = b0 * kBlockM, r1 = std::min(T, r0 + tm);
+      std::vector<Run> groups;
+      int32_t has_gather = 0;
+      for (int32_t b = b0; b < std::min<int32_t>(b0 + per, (int32_t)block_groups.size()); ++b) {
+        has_gather |= block_gather[b];
+        for (const Run& g : block_groups[b]) {
+          if (!groups.empty() && groups.back().hi == g.lo && groups.back().adapter == g.adapter)
+            groups.back().hi = g.hi;
+          else
+            groups.push_back(g);
+        }
+      }
+      int32_t w[kTileWords] = {r0, (int32_t)groups.size(), has_gather, r1 - r0};
+      for (size_t g = 0; g < groups.size(); ++g) {
+        w[4 + 3 * g] = groups[g].adapter;
+        w[5 + 3 * g] = groups[g].lo - r0;
+        w[6 + 3 * g] = groups[g].hi - r0;
+      }
+      out.insert(out.end(), w, w + kTileWords);
+    }
+    return out;
+  };
+  std::vector<int32_t> fwd_tiles = fwd_tiles_of(kTileM);
+  std::vector<int32_t> fwd_tiles128 = fwd_tiles_of(kBlockM);
   // Gathered rows: slots ordered by (adapter, row); items of kItemRows slots.
   std::vector<int32_t> gather_rows, gslot(T, -1), gather_items;
   for (int32_t i = 0; i < T; ++i)
@@ -162,16 +189,16 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
     i = j;
   }
 
-  // Backward GEMM row tiles over compact training rows: at most kTileM rows
+  // Backward GEMM row tiles over compact training rows: at most `tm` rows
   // and at most kMaxGroups adapter runs each (a tile ends early otherwise),
   // so every training row's low-rank term rides its tile.
-  std::vector<int32_t> bwd_tiles;
-  {
+  auto bwd_tiles_of = [&](int32_t tm) {
+    std::vector<int32_t> out;
     std::vector<Run> runs = runs_of(train_adapter.data(), 0, Tt);
     size_t k = 0;  // run containing row `cur`
     int32_t r0 = 0;
     while (r0 < Tt) {
-      const int32_t limit = std::min(Tt, r0 + kTileM);
+      const int32_t limit = std::min(Tt, r0 + tm);
       int32_t w[kTileWords] = {r0, 0, 0, 0};
       int32_t cur = r0, ng = 0;
       while (cur < limit && ng < kMaxGroups) {
@@ -185,10 +212,13 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
       }
       w[1] = ng;
       w[3] = cur - r0;
-      bwd_tiles.insert(bwd_tiles.end(), w, w + kTileWords);
+      out.insert(out.end(), w, w + kTileWords);
       r0 = cur;
     }
-  }
+    return out;
+  };
+  std::vector<int32_t> bwd_tiles = bwd_tiles_of(kTileM);
+  std::vector<int32_t> bwd_tiles128 = bwd_tiles_of(kBlockM);
 
   // Adapters owning training rows, and single-adapter chunks of the compact
   // rows for the deterministic reductions over tokens.
@@ -241,7 +271,9 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
   L.gather_rows = put(gather_rows.data(), gather_rows.size());
   L.gather_items = put(gather_items.data(), gather_items.size());
   L.fwd_tiles = put(fwd_tiles.data(), fwd_tiles.size());
+  L.fwd_tiles128 = put(fwd_tiles128.data(), fwd_tiles128.size());
   L.bwd_tiles = put(bwd_tiles.data(), bwd_tiles.size());
+  L.bwd_tiles128 = put(bwd_tiles128.data(), bwd_tiles128.size());
   L.chunks = put(chunks.data(), chunks.size());
   L.train_items = put(train_items.data(), train_items.size());
   L.train_ads = put(train_ads.data(), train_ads.size());
@@ -258,6 +290,8 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
   p.n_gather = (int32_t)gather_rows.size();
   p.n_gitems = (int32_t)(gather_items.size() / kItemWords);
   p.n_btiles = (int32_t)(bwd_tiles.size() / kTileWords);
+  p.n_ftiles128 = (int32_t)(fwd_tiles128.size() / kTileWords);
+  p.n_btiles128 = (int32_t)(bwd_tiles128.size() / kTileWords);
   p.n_chunks = n_chunks;
   p.n_tads = n_tads;
   p.n_titems = (int32_t)(train_items.size() / kItemWords);
@@ -343,7 +377,7 @@ extern "C" int dsv_plan_meta_copy(const dsv_plan* p, void* host_out, size_t byte
   return DSV_OK;
 }
 
-extern "C" int dsv_plan_counts(const dsv_plan* p, int32_t out[8]) {
+extern "C" int dsv_plan_counts(const dsv_plan* p, int32_t out[10]) {
   if (!p || !out) return DSV_ERR_ARG;
   out[0] = p->n_ftiles;
   out[1] = p->n_shrink;
@@ -353,6 +387,8 @@ extern "C" int dsv_plan_counts(const dsv_plan* p, int32_t out[8]) {
   out[5] = p->n_chunks;
   out[6] = p->n_tads;
   out[7] = p->n_titems;
+  out[8] = p->n_ftiles128;
+  out[9] = p->n_btiles128;
   return DSV_OK;
 }
 

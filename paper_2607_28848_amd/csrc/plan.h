@@ -13,12 +13,17 @@
 
 namespace dsv {
 
-// GEMM row tile (output rows per workgroup) and the number of adapter groups
-// whose low-rank term a tile adds with matrix-core instructions itself.
+// GEMM row tiles come in two heights (256 and 128 output rows per
+// workgroup).  The low-rank term of a row either rides its tile (the tile adds
+// it with matrix-core instructions for each "group" = run of rows of one
+// adapter) or comes from the gathered path.  That choice is made per 128-row
+// block: its up to kBlockGroups longest runs of at least kMinGroupRows rows
+// ride the tile, every other row (short segments such as single-token decode
+// entries) is gathered.  A 256-row tile carries the groups of its two blocks.
 constexpr int kTileM = 256;
-constexpr int kMaxGroups = 4;
-// A run of same-adapter rows shorter than this inside a tile takes the
-// gathered path instead of a tile group.
+constexpr int kBlockM = 128;
+constexpr int kBlockGroups = 4;
+constexpr int kMaxGroups = 8;
 constexpr int kMinGroupRows = 4;
 // Rows per shrink / gathered work item (one 16-row matrix-core tile).
 constexpr int kItemRows = 16;
@@ -41,8 +46,10 @@ struct MetaLayout {
   int64_t gslot;         // [T]   slot of a gathered row or -1
   int64_t gather_rows;   // [T_g] token row of each gathered slot
   int64_t gather_items;  // [n_gitems][4] {adapter, slot_begin, count, 0}
-  int64_t fwd_tiles;     // [n_ftiles][kTileWords] over token rows
-  int64_t bwd_tiles;     // [n_btiles][kTileWords] over compact training rows
+  int64_t fwd_tiles;     // [n_ftiles][kTileWords] 256-row tiles over token rows
+  int64_t fwd_tiles128;  // [n_ftiles128][kTileWords] 128-row tiles over token rows
+  int64_t bwd_tiles;     // [n_btiles][kTileWords] <= 256-row tiles over compact training rows
+  int64_t bwd_tiles128;  // [n_btiles128][kTileWords] <= 128-row tiles
   int64_t chunks;        // [n_chunks][4] {adapter, begin, count, train_adapter_slot}
   int64_t train_items;   // [n_titems][4] {adapter, begin, count, 0}: <= 16 compact rows
   int64_t train_ads;     // [n_tads] adapters owning training rows (ascending)
@@ -59,7 +66,7 @@ struct MetaLayout {
 struct dsv_plan {
   int32_t T = 0, n_ad = 0, r_max = 0, T_t = 0;
   int32_t n_ftiles = 0, n_shrink = 0, n_gather = 0, n_gitems = 0, n_btiles = 0,
-          n_chunks = 0, n_tads = 0, n_titems = 0;
+          n_chunks = 0, n_tads = 0, n_titems = 0, n_ftiles128 = 0, n_btiles128 = 0;
   std::vector<int32_t> ranks;
   std::vector<float> scales;
   std::vector<int32_t> train_rows;     // host copy, compact order

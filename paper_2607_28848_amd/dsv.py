@@ -75,7 +75,7 @@ _lib.dsv_status_string.argtypes = [ctypes.c_int]
 _lib.dsv_status_string.restype = ctypes.c_char_p
 
 COUNT_NAMES = ("fwd_tiles", "shrink_items", "gathered_rows", "gather_items", "bwd_tiles",
-               "chunks", "train_adapters", "train_items")
+               "chunks", "train_adapters", "train_items", "fwd_tiles128", "bwd_tiles128")
 
 
 class DsvError(RuntimeError):
@@ -168,7 +168,7 @@ class Plan:
         return out
 
     def counts(self) -> dict:
-        out = np.zeros(8, np.int32)
+        out = np.zeros(len(COUNT_NAMES), np.int32)
         _check(_lib.dsv_plan_counts(self._h, out.ctypes.data_as(_i32p)), "dsv_plan_counts")
         return dict(zip(COUNT_NAMES, (int(v) for v in out)))
 
