@@ -78,9 +78,9 @@ int ptr_ok(const void* p) { return p && aligned16(p); }
 
 // GEMM tile shape for an output of (row tiles of 256 / of 128) x n_out: the
 // shape whose launch finishes soonest on 256 compute units, counting whole
-// waves of workgroups (1 resident workgroup per CU for 256-row tiles, 2 for
-// 128 x 128) and a relative matrix-core efficiency per shape (smaller tiles
-// re-read more operand bytes per FLOP from L2 and LDS).
+// waves of workgroups (one 256-row workgroup or two 128 x 128 workgroups
+// resident per CU) and a relative matrix-core efficiency per shape measured
+// on MI355X (the 256 x 256 tile re-reads fewer operand bytes per FLOP).
 struct TileChoice {
   int tm, tn;
 };
@@ -88,14 +88,14 @@ TileChoice choose_tiles(int32_t m256, int32_t m128, int32_t n_out) {
   struct Cand {
     int tm, tn, bpc;
     double eff;
-  } cands[3] = {{256, 256, 1, 1.0}, {256, 128, 1, 0.9}, {128, 128, 2, 0.75}};
-  TileChoice best{256, 256};
+  } cands[3] = {{128, 128, 2, 1.0}, {256, 256, 1, 1.05}, {256, 128, 1, 0.9}};
+  TileChoice best{128, 128};
   double best_cost = 1e300;
   for (const Cand& c : cands) {
     const int64_t mt = c.tm == 256 ? m256 : m128;
     const int64_t tiles = mt * ((n_out + c.tn - 1) / c.tn);
     const int64_t slots = 256LL * c.bpc;
-    const double cost = (double)((tiles + slots - 1) / slots) * c.bpc * (c.tm * c.tn / 65536.0) / c.eff;
+    const double cost = (double)((tiles + slots - 1) / slots) * c.bpc * (c.tm * c.tn / 16384.0) / c.eff;
     if (cost < best_cost) {
       best_cost = cost;
       best = {c.tm, c.tn};

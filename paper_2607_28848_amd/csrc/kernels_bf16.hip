@@ -113,27 +113,42 @@ __device__ __forceinline__ i32x4 make_rsrc(const void* base, uint64_t range) {
 
 __device__ __forceinline__ void vmem_wait_all() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-constexpr int TK = 64;
-
-__device__ __forceinline__ int swz(int row) { return (row ^ (row >> 3)) & 7; }
+// K-contiguous tiles hold rows of TK bf16 (TK / 8 chunks of 16 bytes); the
+// chunk slot is XOR-swizzled with a function of the row so that the 16 lanes
+// of one LDS access phase (16 consecutive rows, same logical chunk) hit
+// distinct banks.
+template <int TK>
+__device__ __forceinline__ int swz(int row) {
+  if constexpr (TK == 64) return (row ^ (row >> 3)) & 7;
+  else return (row >> 2) & 3;
+}
 __device__ __forceinline__ int nn_swz(int n) { return 2 * (n & 3); }
 
-template <int TM, int TN>
+template <int TM, int TN, int WGM, int WGN, int TK, int NS>
 struct GemmShape {
-  static constexpr int WM = TM / 2, WN = TN / 2, FM = WM / 32, FN = WN / 32;
+  static constexpr int NW = WGM * WGN, THREADS = 64 * NW;
+  static constexpr int WM = TM / WGM, WN = TN / WGN, FM = WM / 32, FN = WN / 32;
   static constexpr int A_BYTES = TM * TK * 2, B_BYTES = TN * TK * 2;
   static constexpr int STAGE = A_BYTES + B_BYTES;
   static constexpr int STG_LD = TN + 8;  // epilogue staging row stride (elements)
-  static constexpr int LDS = (2 * STAGE > TM * STG_LD * 2) ? 2 * STAGE : TM * STG_LD * 2;
+  static constexpr int LDS = (NS * STAGE > TM * STG_LD * 2) ? NS * STAGE : TM * STG_LD * 2;
 };
 
-template <bool NN, int TM, int TN>
-__global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
-  using S = GemmShape<TM, TN>;
-  constexpr int WM = S::WM, WN = S::WN, FM = S::FM, FN = S::FN;
+// s_waitcnt immediate (gfx9 encoding): wait until at most n vector-memory
+// operations of this wave are outstanding; lgkm and exp counters untouched.
+constexpr int vmcnt_imm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+template <bool NN, int TM, int TN, int WGM, int WGN, int TK, int NS>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
+  using S = GemmShape<TM, TN, WGM, WGN, TK, NS>;
+  constexpr int WM = S::WM, WN = S::WN, FM = S::FM, FN = S::FN, NW = S::NW;
+  constexpr int ROWB = TK * 2;          // bytes per row of a K-contiguous tile
+  constexpr int CPR = TK / 8;           // 16-byte chunks per row
+  static_assert(FM >= 1 && FN >= 1 && NS >= 2, "tile shape");
+  static_assert((TM * ROWB) % (1024 * NW) == 0 && (TN * ROWB) % (1024 * NW) == 0, "loads per wave");
   __shared__ __attribute__((aligned(1024))) char smem[S::LDS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WGN, wn = wave % WGN;
 
   // Workgroup -> tile.  Consecutive workgroup ids land on different XCDs
   // (round robin over 8); renumber so that each XCD owns a contiguous range
@@ -152,6 +167,77 @@ __global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
   const int32_t* td = g.tiles + (int64_t)mt * kTileWords;
   const int m0 = td[0], ngroups = td[1], has_gather = td[2], nrows = td[3];
   const int n0 = nt * TN;
+
+  // ---- operand tiles: per-lane global offsets of the direct-to-LDS loads ----
+  constexpr int A_LOADS = TM * ROWB / 1024 / NW, B_LOADS = TN * ROWB / 1024 / NW;
+  int a_off[A_LOADS], a_kc[A_LOADS];
+#pragma unroll
+  for (int i = 0; i < A_LOADS; ++i) {
+    const int q = wave * A_LOADS + i;
+    const int row = q * (1024 / ROWB) + lane / CPR;
+    const int c = (lane % CPR) ^ swz<TK>(row);
+    a_off[i] = (int)(((int64_t)row * g.ldp + 8 * c) * 2);
+    a_kc[i] = 8 * c;
+  }
+  int b_off[B_LOADS], b_kc[B_LOADS];
+#pragma unroll
+  for (int i = 0; i < B_LOADS; ++i) {
+    const int q = wave * B_LOADS + i;
+    if constexpr (!NN) {
+      const int col = q * (1024 / ROWB) + lane / CPR;
+      const int c = (lane % CPR) ^ swz<TK>(col);
+      b_off[i] = (int)(((int64_t)col * g.ldq + 8 * c) * 2);
+      b_kc[i] = 8 * c;
+    } else {
+      const int byte = q * 1024 + 16 * lane;
+      const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
+      b_off[i] = (int)(((int64_t)n * g.ldq + 8 * (slot ^ nn_swz(n))) * 2);
+      b_kc[i] = n;
+    }
+  }
+  const uint16_t* a_base = g.P + (int64_t)m0 * g.ldp;
+  const int64_t a_rows = min((int64_t)TM, (int64_t)g.M - m0);
+  const uint16_t* b_base = NN ? g.Q + n0 : g.Q + (int64_t)n0 * g.ldq;
+  const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
+
+  auto issue = [&](int kt, int stage) {
+    const int k0 = kt * TK;
+    char* sa = smem + stage * S::STAGE;
+    char* sb = sa + S::A_BYTES;
+    // descriptors rebased on the K-step keep every offset well inside 32 bits
+    const i32x4 ra = make_rsrc(a_base + k0, (uint64_t)(a_rows * g.ldp - k0) * 2);
+#pragma unroll
+    for (int i = 0; i < A_LOADS; ++i) {
+      const int q = wave * A_LOADS + i;
+      const int vo = (k0 + a_kc[i] < g.C) ? a_off[i] : (int)0x7FFFFFF0;
+      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
+    }
+    if constexpr (!NN) {
+      const i32x4 rb = make_rsrc(b_base + k0, (uint64_t)(b_cols * g.ldq - k0) * 2);
+#pragma unroll
+      for (int i = 0; i < B_LOADS; ++i) {
+        const int q = wave * B_LOADS + i;
+        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
+        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
+      }
+    } else {
+      // the TK contraction rows of this K-step (fewer at the tail)
+      const i32x4 rb = make_rsrc(b_base + (int64_t)k0 * g.ldq,
+                                 (uint64_t)((int64_t)min(TK, g.C - k0) * g.ldq - n0) * 2);
+#pragma unroll
+      for (int i = 0; i < B_LOADS; ++i) {
+        const int q = wave * B_LOADS + i;
+        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
+        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
+      }
+    }
+  };
+
+  // The first NS K-steps are in flight while the low-rank prologue runs.
+  const int nk = (g.C + TK - 1) / TK;
+#pragma unroll
+  for (int p = 0; p < NS; ++p)
+    if (p < nk) issue(p, p);
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -222,83 +308,19 @@ __global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
     }
   }
 
-  // ---- main loop: direct-to-LDS operand tiles, double-buffered ----------
-  constexpr int A_LOADS = TM / 32, B_LOADS = TN / 32;  // 1-KiB wave loads per wave per K-step
-  int a_off[A_LOADS], a_kc[A_LOADS];
-#pragma unroll
-  for (int i = 0; i < A_LOADS; ++i) {
-    const int q = wave * A_LOADS + i;
-    const int row = 8 * q + (lane >> 3);
-    const int c = (lane & 7) ^ swz(row);
-    a_off[i] = (int)(((int64_t)row * g.ldp + 8 * c) * 2);
-    a_kc[i] = 8 * c;
-  }
-  int b_off[B_LOADS], b_kc[B_LOADS];
-#pragma unroll
-  for (int i = 0; i < B_LOADS; ++i) {
-    const int q = wave * B_LOADS + i;
-    if constexpr (!NN) {
-      const int col = 8 * q + (lane >> 3);
-      const int c = (lane & 7) ^ swz(col);
-      b_off[i] = (int)(((int64_t)col * g.ldq + 8 * c) * 2);
-      b_kc[i] = 8 * c;
-    } else {
-      const int byte = q * 1024 + 16 * lane;
-      const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
-      b_off[i] = (int)(((int64_t)n * g.ldq + 8 * (slot ^ nn_swz(n))) * 2);
-      b_kc[i] = n;
-    }
-  }
-  const uint16_t* a_base = g.P + (int64_t)m0 * g.ldp;
-  const int64_t a_rows = min((int64_t)TM, (int64_t)g.M - m0);
-  const uint16_t* b_base = NN ? g.Q + n0 : g.Q + (int64_t)n0 * g.ldq;
-  const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
-
-  auto issue = [&](int kt, int stage) {
-    const int k0 = kt * TK;
-    char* sa = smem + stage * S::STAGE;
-    char* sb = sa + S::A_BYTES;
-    // descriptors rebased on the K-step keep every offset well inside 32 bits
-    const i32x4 ra = make_rsrc(a_base + k0, (uint64_t)(a_rows * g.ldp - k0) * 2);
-#pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-      const int q = wave * A_LOADS + i;
-      const int vo = (k0 + a_kc[i] < g.C) ? a_off[i] : (int)0x7FFFFFF0;
-      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
-    }
-    if constexpr (!NN) {
-      const i32x4 rb = make_rsrc(b_base + k0, (uint64_t)(b_cols * g.ldq - k0) * 2);
-#pragma unroll
-      for (int i = 0; i < B_LOADS; ++i) {
-        const int q = wave * B_LOADS + i;
-        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
-        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
-      }
-    } else {
-      // the 64 contraction rows of this K-step (fewer at the tail)
-      const i32x4 rb = make_rsrc(b_base + (int64_t)k0 * g.ldq,
-                                 (uint64_t)((int64_t)min(TK, g.C - k0) * g.ldq - n0) * 2);
-#pragma unroll
-      for (int i = 0; i < B_LOADS; ++i) {
-        const int q = wave * B_LOADS + i;
-        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
-        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
-      }
-    }
-  };
-
+  // ---- main loop ------------------------------------------------------------
   auto load_frags = [&](const char* sa, const char* sb, int s, bf16x8* af, bf16x8* bq) {
     const int ch = 2 * s + (lane >> 5);
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * WM + 32 * i + (lane & 31);
-      af[i] = as_bf(*reinterpret_cast<const u32x4*>(sa + row * 128 + 16 * (ch ^ swz(row))));
+      af[i] = as_bf(*reinterpret_cast<const u32x4*>(sa + row * ROWB + 16 * (ch ^ swz<TK>(row))));
     }
 #pragma unroll
     for (int j = 0; j < FN; ++j) {
       if constexpr (!NN) {
         const int col = wn * WN + 32 * j + (lane & 31);
-        bq[j] = as_bf(*reinterpret_cast<const u32x4*>(sb + col * 128 + 16 * (ch ^ swz(col))));
+        bq[j] = as_bf(*reinterpret_cast<const u32x4*>(sb + col * ROWB + 16 * (ch ^ swz<TK>(col))));
       } else {
         const int gq = lane >> 4, lam = lane & 15;
         const int c = wn * WN + 32 * j + 16 * (gq & 1) + 4 * (lam & 3);
@@ -319,43 +341,60 @@ __global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
     }
   };
 
-  const int nk = (g.C + TK - 1) / TK;
-  issue(0, 0);
+  // Pipeline: NS K-steps in flight.  In iteration kt the barrier that
+  // publishes step kt+1 sits before the last 16-wide MFMA step of kt (whose
+  // fragments are already in registers).  After it the buffer of kt is free
+  // and receives step kt+NS, and the first fragments of kt+1 are read while
+  // the last MFMAs of kt issue.
+  constexpr int kLoads = A_LOADS + B_LOADS;          // direct loads per wave per K-step
+  constexpr int kReads = FM + (NN ? 2 : 1) * FN;     // LDS reads per 16-wide step
+  constexpr int kMfma = FM * FN;                     // MFMAs per 16-wide step
+  constexpr int kSteps = TK / 16;
+  constexpr int L = (kSteps - 1) & 1;  // fragment buffer of the last step
+  static_assert(L == 1, "an even number of 16-wide steps per K-step");
+  if (nk >= NS) __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * kLoads));  // step 0 landed
+  else vmem_wait_all();
+  __syncthreads();
+  bf16x8 af[2][FM], bq[2][FN];
+  load_frags(smem, smem + S::A_BYTES, 0, af[0], bq[0]);
+  int stage = 0;
   for (int kt = 0; kt < nk; ++kt) {
-    vmem_wait_all();
-    __syncthreads();
-    if (kt + 1 < nk) issue(kt + 1, (kt + 1) & 1);
-    const char* sa = smem + (kt & 1) * S::STAGE;
-    const char* sb = sa + S::A_BYTES;
-    bf16x8 af[2][FM], bq[2][FN];
-    load_frags(sa, sb, 0, af[0], bq[0]);
+    char* sa = smem + stage * S::STAGE;
+    char* sb = sa + S::A_BYTES;
 #pragma unroll
-    for (int s = 0; s < TK / 16; ++s) {
-      if (s + 1 < TK / 16) load_frags(sa, sb, s + 1, af[(s + 1) & 1], bq[(s + 1) & 1]);
+    for (int s = 0; s < kSteps - 1; ++s) {
+      load_frags(sa, sb, s + 1, af[(s + 1) & 1], bq[(s + 1) & 1]);
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bq[s & 1][j], acc[i][j], 0, 0, 0);
     }
-    // Schedule of the K-step: the operand loads of the next K-step first,
-    // then the fragments of step 0, then each step's MFMAs with the next
-    // step's fragment reads spread between them.
-    constexpr int kReads = FM + (NN ? 2 : 1) * FN;  // LDS reads per 16-wide step
-    constexpr int kMfma = FM * FN;
-    __builtin_amdgcn_sched_group_barrier(0x020, A_LOADS + B_LOADS, 0);
-    __builtin_amdgcn_sched_group_barrier(0x100, kReads, 0);
 #pragma unroll
-    for (int s = 0; s < TK / 16 - 1; ++s) {
+    for (int s = 0; s < kSteps - 1; ++s) {
 #pragma unroll
       for (int t = 0; t < kReads; ++t) {
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfma / kReads > 0 ? kMfma / kReads : 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
-      if (kMfma > kReads * (kMfma / kReads))
-        __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads * (kMfma / kReads), 0);
+      if (kMfma > kReads) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, kMfma, 0);
+    const int next = (stage + 1 == NS) ? 0 : stage + 1;
+    if (kt + 1 < nk) {
+      // step kt+1 has landed once at most (steps issued after it) loads remain
+      if (kt + NS <= nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * kLoads));
+      else vmem_wait_all();
+      __syncthreads();  // everyone's part of kt+1 is in; buffer `stage` is free
+      if (kt + NS < nk) issue(kt + NS, stage);
+      char* na = smem + next * S::STAGE;
+      load_frags(na, na + S::A_BYTES, 0, af[L ^ 1], bq[L ^ 1]);
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[L][i], bq[L][j], acc[i][j], 0, 0, 0);
+    stage = next;
   }
 
   // ---- epilogue: one rounding, staged through LDS for 16-byte stores ------
@@ -380,8 +419,8 @@ __global__ __launch_bounds__(256) void gemm_lora_kernel(GemmArgs g) {
   __syncthreads();
   constexpr int CH = TN / 8;  // 16-byte chunks per staged row
 #pragma unroll 4
-  for (int it = 0; it < (TM * CH) / 256; ++it) {
-    const int idx = tid + 256 * it;
+  for (int it = 0; it < (TM * CH) / S::THREADS; ++it) {
+    const int idx = tid + S::THREADS * it;
     const int row = idx / CH, ch = idx % CH;
     const int col = n0 + ch * 8;
     if (row < nrows && col < g.Nout)
@@ -613,16 +652,19 @@ __global__ __launch_bounds__(256) void transpose_h_kernel(const uint16_t* __rest
 }  // namespace
 
 namespace {
+// Tile configurations: (TM, TN, wave grid, K-step, pipeline stages); two
+// waves per SIMD in each (8 waves per 256-row workgroup, or two 4-wave
+// 128 x 128 workgroups per CU).
 template <bool NN>
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   if (a.n_mtiles <= 0 || a.n_ntiles <= 0) return hipSuccess;
-  const dim3 grid(a.n_mtiles * a.n_ntiles), block(256);
+  const dim3 grid(a.n_mtiles * a.n_ntiles);
   if (tm == 256 && tn == 256)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2>), grid, dim3(512), 0, s, a);
   else if (tm == 256 && tn == 128)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 128>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 128, 4, 2, 64, 2>), grid, dim3(512), 0, s, a);
   else if (tm == 128 && tn == 128)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 128, 128>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2>), grid, dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();

@@ -9,7 +9,7 @@
 #include <cstdint>
 #include <vector>
 
-#include "../../include/dsv.h"
+#include "dsv.h"
 
 namespace dsv {
 

@@ -136,7 +136,7 @@ class Plan:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h is not None and h.value:
+        if h is not None and h.value and _lib is not None:  # _lib is None at interpreter exit
             _lib.dsv_plan_free(h)
             self._h = ctypes.c_void_p()
 
