@@ -21,8 +21,7 @@ struct FwdWs {
   size_t h_all, delta, total;
 };
 struct BwdWs {
-  size_t bt, ht, g, gt, part_b, part_a, total;
-  int64_t ldt;
+  size_t bt, g, part_b, part_a, total;
 };
 
 FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N) {
@@ -45,16 +44,11 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N) {
 BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
   BwdWs w{};
   size_t off = 0;
-  w.ldt = (p.T_t + 7) & ~7;
   if (dt == DSV_BF16) {
     w.bt = off;
     off = align256(off + (size_t)p.n_tads * p.r_max * N * 2);
-    w.ht = off;
-    off = align256(off + (size_t)p.r_max * w.ldt * 2);
     w.g = off;
     off = align256(off + (size_t)p.T_t * ld_rank(p.r_max) * 2);
-    w.gt = off;
-    off = align256(off + (size_t)p.r_max * w.ldt * 2);
     w.part_b = off;
     off = align256(off + (size_t)p.n_chunks * N * p.r_max * 4);
     w.part_a = off;
@@ -247,7 +241,7 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   sk.out2 = static_cast<uint16_t*>(H_save);
   sk.ld2 = p->r_max;
   sk.row_train = p->dptr(L.row_train);
-  if ((e = launch_shrink(sk, p->n_shrink, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  if ((e = launch_shrink(sk, p->n_shrink, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2. gathered rows: fp32 low-rank term, each touched adapter read once.
   if (p->n_gather > 0) {
@@ -346,22 +340,17 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
 
   const int64_t ldh = ld_rank(p->r_max);
   uint16_t* bt = at<uint16_t>(workspace, ws.bt);
-  uint16_t* ht = at<uint16_t>(workspace, ws.ht);
   uint16_t* gm = at<uint16_t>(workspace, ws.g);
-  uint16_t* gt = at<uint16_t>(workspace, ws.gt);
   float* part_b = at<float>(workspace, ws.part_b);
   float* part_a = at<float>(workspace, ws.part_a);
   const int32_t* train_ads = p->dptr(L.train_ads);
 
-  // 1. transposed copies of the training adapters' B and of H_save.
+  // 1. transposed copies of the training adapters' B ([r_max][N] per adapter).
   if ((e = launch_transpose_b(static_cast<const uint16_t*>(B), N, p->r_max, train_ads, p->n_tads, ranks,
                               bt, s)) != hipSuccess)
     return DSV_ERR_DEVICE;
-  if ((e = launch_transpose_h(static_cast<const uint16_t*>(H_save), p->T_t, p->r_max,
-                              p->dptr(L.train_adapter), ranks, ht, ws.ldt, s)) != hipSuccess)
-    return DSV_ERR_DEVICE;
 
-  // 2. g = s_a dy B_a (contraction over N) -> G [T_t][ldh] and G^T [r_max][ldt].
+  // 2. g = s_a dy B_a (contraction over N) -> G [T_t][ldh].
   SkinnyArgs sk{};
   sk.P = static_cast<const uint16_t*>(dY);
   sk.ldp = N;
@@ -376,17 +365,16 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   sk.C = N;
   sk.out1 = gm;
   sk.ld1 = ldh;
-  sk.out2 = gt;
-  sk.ld2 = ws.ldt;
-  if ((e = launch_gmat(sk, p->n_titems, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  sk.out2 = nullptr;
+  if ((e = launch_gmat(sk, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 3. per-chunk fp32 partials of dy^T h (-> dB) and x^T g (-> dA).
   TokenReduceArgs tb{};
   tb.P = static_cast<const uint16_t*>(dY);
   tb.ldp = N;
   tb.prow = nullptr;
-  tb.Qt = ht;
-  tb.ldqt = ws.ldt;
+  tb.Q = static_cast<const uint16_t*>(H_save);
+  tb.ldq = p->r_max;
   tb.chunks = p->dptr(L.chunks);
   tb.ranks = ranks;
   tb.C = N;
@@ -397,7 +385,8 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   ta.P = static_cast<const uint16_t*>(X);
   ta.ldp = K;
   ta.prow = p->dptr(L.train_rows);
-  ta.Qt = gt;
+  ta.Q = gm;
+  ta.ldq = ldh;
   ta.C = K;
   ta.part = part_a;
   if ((e = launch_token_reduce(ta, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;

@@ -51,19 +51,19 @@ struct SkinnyArgs {
   // outputs (mode-dependent)
   uint16_t* out1;        // [rows][ld1]
   int64_t ld1;
-  uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train; g: transposed [r][ld2]
+  uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train (nullptr: none)
   int64_t ld2;
   const int32_t* row_train;
 };
 
 // Per-chunk fp32 partial sums over training tokens:
-//   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Qt[j][t]
+//   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Q[t][j]
 struct TokenReduceArgs {
   const uint16_t* P;
   int64_t ldp;
   const int32_t* prow;   // compact row -> P row (nullptr: identity)
-  const uint16_t* Qt;    // [r_max][ldqt]
-  int64_t ldqt;
+  const uint16_t* Q;     // [T_t][ldq], compact rows
+  int64_t ldq;
   const int32_t* chunks;
   const int32_t* ranks;
   int32_t C, r_max;
@@ -75,8 +75,8 @@ struct TokenReduceArgs {
 // plan's row-tile list of height tm.
 hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
-hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, hipStream_t s);
-hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, hipStream_t s);
+hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
+hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
                                 int32_t r_max, const int32_t* items, int32_t n_items,
                                 const int32_t* gather_rows, const int32_t* ranks,
@@ -88,9 +88,6 @@ hipError_t launch_reduce_out(const float* part, int32_t C, int32_t r_max, const 
                              int32_t accumulate, float* out, hipStream_t s);
 hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
                               int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
-hipError_t launch_transpose_h(const uint16_t* Hs, int32_t Tt, int32_t r_max,
-                              const int32_t* train_adapter, const int32_t* ranks, uint16_t* Ht,
-                              int64_t ldt, hipStream_t s);
 
 // Launchers (fp32 mode: plain FMA kernels, same semantics).
 struct F32Args {

@@ -430,50 +430,83 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Skinny rank-r contraction: one workgroup per item of <= 16 rows of one
-// adapter; the 4 waves take interleaved 32-wide slices of the contraction
-// with v_mfma_f32_16x16x32_bf16 and combine them in LDS in a fixed order.
+// Skinny rank-r contraction: one workgroup per item of <= 32 rows of one
+// adapter (two 16-row tiles sharing each fragment of the adapter operand);
+// the SW waves take interleaved 32-wide slices of the contraction with
+// v_mfma_f32_16x16x32_bf16 (NJ = ceil(r/16) output tiles), U slices in flight
+// per wave, and combine their sums in LDS in a fixed order.
 // ---------------------------------------------------------------------------
-template <int MODE>  // 0: shrink (h -> H_all, H_save), 1: g (-> G, G^T)
-__global__ __launch_bounds__(256) void skinny_kernel(SkinnyArgs g) {
-  __shared__ float red[4][16][DSV_MAX_RANK + 1];
+constexpr int SW = 8;  // waves per rank-contraction workgroup
+
+template <int MODE, int NJ, int ROWS>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
+__global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
+  constexpr int U = NJ <= 2 ? 4 : 2;
+  constexpr int RT = ROWS / 16;  // 16-row tiles per item
+  __shared__ float red[SW][ROWS][DSV_MAX_RANK + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
   const int a = it[0], begin = it[1], cnt = it[2];
   const int r = g.ranks[a];
   const int slot = g.qsel ? g.qsel[a] : a;
   const uint16_t* Qa = g.Q + (int64_t)slot * g.q_ad;
-  const int i = lane & 15;
-  const int prow = (i < cnt) ? (g.rows ? g.rows[begin + i] : begin + i) : -1;
-  f32x4 acc[4];
+  int prow[RT];
+  const uint16_t* pp[RT];
 #pragma unroll
-  for (int jt = 0; jt < 4; ++jt) acc[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int nsteps = (g.C + 31) / 32;
-  for (int step = wave; step < nsteps; step += 4) {
-    const int k = step * 32 + 8 * (lane >> 4);
-    const bool kin = k < g.C;
-    const u32x4 av = (prow >= 0 && kin) ? ld16(g.P + (int64_t)prow * g.ldp + k) : zero4();
+  for (int t = 0; t < RT; ++t) {
+    const int i = 16 * t + (lane & 15);
+    prow[t] = (i < cnt) ? (g.rows ? g.rows[begin + i] : begin + i) : -1;
+    pp[t] = g.P + (int64_t)max(prow[t], 0) * g.ldp;
+  }
+  f32x4 acc[RT][NJ];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
-      if (16 * jt < r) {
-        const int j = 16 * jt + (lane & 15);
-        const u32x4 bv = (j < r && kin) ? ld16(Qa + (int64_t)j * g.ldq + k) : zero4();
-        acc[jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av), as_bf(bv), acc[jt], 0, 0, 0);
+  for (int t = 0; t < RT; ++t)
+#pragma unroll
+    for (int jt = 0; jt < NJ; ++jt) acc[t][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // a wave takes 64-wide slices (two 32-wide MFMA steps), so each row is read
+  // in whole 128-byte lines
+  const int nslices = (g.C + 63) / 64;
+  for (int s0 = wave; s0 < nslices; s0 += SW * U) {
+    u32x4 av[U][2][RT], bv[U][2][NJ];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int k = (s0 + SW * u) * 64 + 32 * h + 8 * (lane >> 4);
+        const bool kin = k < g.C;
+#pragma unroll
+        for (int t = 0; t < RT; ++t) av[u][h][t] = (prow[t] >= 0 && kin) ? ld16(pp[t] + k) : zero4();
+#pragma unroll
+        for (int jt = 0; jt < NJ; ++jt) {
+          const int j = 16 * jt + (lane & 15);
+          bv[u][h][jt] = (j < r && kin) ? ld16(Qa + (int64_t)j * g.ldq + k) : zero4();
+        }
       }
-    }
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int t = 0; t < RT; ++t)
+#pragma unroll
+          for (int jt = 0; jt < NJ; ++jt)
+            acc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av[u][h][t]), as_bf(bv[u][h][jt]), acc[t][jt], 0, 0, 0);
   }
 #pragma unroll
-  for (int jt = 0; jt < 4; ++jt)
+  for (int t = 0; t < RT; ++t)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) red[wave][4 * (lane >> 4) + v][16 * jt + (lane & 15)] = acc[jt][v];
+    for (int jt = 0; jt < NJ; ++jt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) red[wave][16 * t + 4 * (lane >> 4) + v][16 * jt + (lane & 15)] = acc[t][jt][v];
   __syncthreads();
   const float s = g.scales ? g.scales[a] : 1.f;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int idx = tid + 256 * q;
+  for (int q = 0; q < (ROWS * 64 + 64 * SW - 1) / (64 * SW); ++q) {
+    const int idx = tid + 64 * SW * q;
     const int row = idx >> 6, j = idx & 63;
-    if (row < cnt && j < r) {
-      const float sum = ((red[0][row][j] + red[1][row][j]) + red[2][row][j]) + red[3][row][j];
+    if (row < ROWS && row < cnt && j < r) {
+      float sum = 0.f;
+#pragma unroll
+      for (int w = 0; w < SW; ++w) sum += red[w][row][j];
       const int pr = g.rows ? g.rows[begin + row] : begin + row;
       if (MODE == 0) {
         const uint16_t hb = f2bf(sum);
@@ -483,9 +516,7 @@ __global__ __launch_bounds__(256) void skinny_kernel(SkinnyArgs g) {
           if (tr >= 0) g.out2[(int64_t)tr * g.ld2 + j] = hb;
         }
       } else {
-        const uint16_t gb = f2bf(s * sum);
-        g.out1[(int64_t)pr * g.ld1 + j] = gb;
-        g.out2[(int64_t)j * g.ld2 + pr] = gb;
+        g.out1[(int64_t)pr * g.ld1 + j] = f2bf(s * sum);
       }
     }
   }
@@ -539,56 +570,87 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
 
 // ---------------------------------------------------------------------------
 // Reduction over training tokens, per single-adapter chunk:
-//   part[chunk][c][j] = sum_t P[prow(t)][c] Qt[j][t]
-// A lane loads an 8 (tokens) x 8 (columns) block, transposes it in registers
-// and feeds the 8 columns as A-operands of 8 v_mfma_f32_16x16x32_bf16 tiles
-// (tile m, row rho <-> column c = base + 8 rho + m).  Each wave covers 128
-// columns, a workgroup 512.
+//   part[chunk][c][j] = sum_t P[prow(t)][c] Q[t][j]
+// One workgroup per (chunk, 128 columns); its 4 waves take consecutive
+// quarters of the chunk's tokens and their sums are added in LDS in wave
+// order.  A lane loads an 8 (tokens) x 8 (columns) block, transposes it in
+// registers and feeds the 8 columns as A-operands of 8
+// v_mfma_f32_16x16x32_bf16 tiles (tile m, row rho <-> column
+// c = base + 8 rho + m); the rank side Q[t][j] (h or g, row layout) is read
+// with 8 strided loads per fragment.
 // ---------------------------------------------------------------------------
+template <int NJ>
 __global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g) {
+  constexpr int TQ = kChunkRows / 4;  // tokens per wave
+  __shared__ f32x4 red[3][8 * NJ][64];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
   const int a = ck[0], begin = ck[1], cnt = ck[2];
   const int r = g.ranks[a];
   const int q = lane >> 4, rho = lane & 15;
-  const int cbase = blockIdx.y * 512 + wave * 128;
+  const int cbase = blockIdx.y * 128;
   const int c0 = cbase + 8 * rho;
-  f32x4 acc[8][4];
+  const bool cin = c0 < g.C;
+  f32x4 acc[8][NJ];
 #pragma unroll
   for (int m = 0; m < 8; ++m)
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) acc[m][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int t0 = 0; t0 < cnt; t0 += 32) {
-    const int tb = t0 + 8 * q;
-    u32x4 v[8], V[8];
+    for (int jt = 0; jt < NJ; ++jt) acc[m][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int tlo = wave * TQ, thi = min(cnt, tlo + TQ);
+  constexpr int U = 2;
+  for (int t0 = tlo; t0 < thi; t0 += 32 * U) {
+    u32x4 v[U][8], bv[U][NJ];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int t = tb + e;
-      v[e] = zero4();
-      if (t < cnt && c0 < g.C) {
-        const int pr = g.prow ? g.prow[begin + t] : begin + t;
-        v[e] = ld16(g.P + (int64_t)pr * g.ldp + c0);
+    for (int u = 0; u < U; ++u) {
+      const int tb = t0 + 32 * u + 8 * q;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int t = tb + e;
+        v[u][e] = zero4();
+        if (t < thi && cin) {
+          const int pr = g.prow ? g.prow[begin + t] : begin + t;
+          v[u][e] = ld16(g.P + (int64_t)pr * g.ldp + c0);
+        }
+      }
+      const int nt = min(8, thi - tb);
+#pragma unroll
+      for (int jt = 0; jt < NJ; ++jt) {
+        const int j = 16 * jt + rho;
+        bv[u][jt] = (j < r && nt > 0) ? ld8_masked(g.Q + (int64_t)(begin + tb) * g.ldq + j, g.ldq, nt)
+                                      : zero4();
       }
     }
-    transpose8x8(v, V);
-    const int nt = min(8, cnt - tb);
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) {
-      if (16 * jt < r) {
-        const int j = 16 * jt + rho;
-        u32x4 bv = zero4();
-        if (j < r && nt > 0) bv = ld8_masked(g.Qt + (int64_t)j * g.ldqt + begin + tb, 1, nt);
+    for (int u = 0; u < U; ++u) {
+      u32x4 V[8];
+      transpose8x8(v[u], V);
+#pragma unroll
+      for (int jt = 0; jt < NJ; ++jt)
 #pragma unroll
         for (int m = 0; m < 8; ++m)
-          acc[m][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(V[m]), as_bf(bv), acc[m][jt], 0, 0, 0);
-      }
+          acc[m][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(V[m]), as_bf(bv[u][jt]), acc[m][jt], 0, 0, 0);
     }
   }
+  // waves 1..3 hand their sums to wave 0, which adds them in wave order
+  if (wave > 0) {
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+#pragma unroll
+      for (int jt = 0; jt < NJ; ++jt) red[wave - 1][m * NJ + jt][lane] = acc[m][jt];
+  }
+  __syncthreads();
+  if (wave != 0) return;
+#pragma unroll
+  for (int w = 0; w < 3; ++w)
+#pragma unroll
+    for (int m = 0; m < 8; ++m)
+#pragma unroll
+      for (int jt = 0; jt < NJ; ++jt) acc[m][jt] += red[w][m * NJ + jt][lane];
   float* out = g.part + (int64_t)blockIdx.x * g.C * g.r_max;
 #pragma unroll
   for (int m = 0; m < 8; ++m)
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
+    for (int jt = 0; jt < NJ; ++jt)
 #pragma unroll
       for (int vv = 0; vv < 4; ++vv) {
         const int rr = 4 * q + vv;
@@ -637,18 +699,6 @@ __global__ __launch_bounds__(256) void transpose_b_kernel(const uint16_t* __rest
   Bt[((int64_t)slot * r_max + j) * N + n] = v;
 }
 
-// Ht[j][t] = H_save[t][j]  (j < rank of row t; other entries zero).
-__global__ __launch_bounds__(256) void transpose_h_kernel(const uint16_t* __restrict__ Hs, int32_t Tt,
-                                                          int32_t r_max, const int32_t* __restrict__ train_adapter,
-                                                          const int32_t* __restrict__ ranks,
-                                                          uint16_t* __restrict__ Ht, int64_t ldt) {
-  const int j = blockIdx.y;
-  const int t = blockIdx.x * 256 + threadIdx.x;
-  if (t >= Tt) return;
-  const uint16_t v = (j < ranks[train_adapter[t]]) ? Hs[(int64_t)t * r_max + j] : (uint16_t)0;
-  Ht[(int64_t)j * ldt + t] = v;
-}
-
 }  // namespace
 
 namespace {
@@ -679,16 +729,26 @@ hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   return launch_gemm_tiled<true>(a, tm, tn, s);
 }
 
-hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, hipStream_t s) {
+namespace {
+template <int MODE, int ROWS>
+hipError_t launch_skinny(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(skinny_kernel<0>, dim3(n_items), dim3(256), 0, s, a);
+  if (r_max <= 16)
+    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
+  else if (r_max <= 32)
+    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
+  else
+    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
   return hipGetLastError();
 }
+}  // namespace
 
-hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(skinny_kernel<1>, dim3(n_items), dim3(256), 0, s, a);
-  return hipGetLastError();
+hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
+  return launch_skinny<0, kRankItemRows>(a, n_items, r_max, s);
+}
+
+hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
+  return launch_skinny<1, kItemRows>(a, n_items, r_max, s);
 }
 
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
@@ -703,7 +763,13 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
 
 hipError_t launch_token_reduce(const TokenReduceArgs& a, int32_t n_chunks, hipStream_t s) {
   if (n_chunks <= 0) return hipSuccess;
-  hipLaunchKernelGGL(token_reduce_kernel, dim3(n_chunks, (a.C + 511) / 512), dim3(256), 0, s, a);
+  const dim3 grid(n_chunks, (a.C + 127) / 128);
+  if (a.r_max <= 16)
+    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(256), 0, s, a);
+  else if (a.r_max <= 32)
+    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -724,15 +790,6 @@ hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const
   if (n_tads <= 0) return hipSuccess;
   hipLaunchKernelGGL(transpose_b_kernel, dim3((N + 255) / 256, r_max, n_tads), dim3(256), 0, s, B, N,
                      r_max, train_ads, ranks, Bt);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_h(const uint16_t* Hs, int32_t Tt, int32_t r_max,
-                              const int32_t* train_adapter, const int32_t* ranks, uint16_t* Ht,
-                              int64_t ldt, hipStream_t s) {
-  if (Tt <= 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_h_kernel, dim3((Tt + 255) / 256, r_max), dim3(256), 0, s, Hs, Tt, r_max,
-                     train_adapter, ranks, Ht, ldt);
   return hipGetLastError();
 }
 

@@ -20,6 +20,7 @@ namespace {
 
 using dsv::kChunkRows;
 using dsv::kItemRows;
+using dsv::kRankItemRows;
 using dsv::kItemWords;
 using dsv::kMaxGroups;
 using dsv::kMinGroupRows;
@@ -101,7 +102,7 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
   p.train_rows = train_rows;
 
   // Shrink work list: rows grouped by adapter (ascending row inside), split
-  // into items of kItemRows rows; each item reads its adapter's A once.
+  // into items of kRankItemRows rows; each item reads its adapter's A once.
   std::vector<int32_t> shrink_rows(T);
   std::iota(shrink_rows.begin(), shrink_rows.end(), 0);
   std::stable_sort(shrink_rows.begin(), shrink_rows.end(),
@@ -109,7 +110,7 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
   std::vector<int32_t> shrink_items;
   for (int32_t i = 0; i < T;) {
     int32_t a = row_adapter[shrink_rows[i]], j = i;
-    while (j < T && row_adapter[shrink_rows[j]] == a && j - i < kItemRows) ++j;
+    while (j < T && row_adapter[shrink_rows[j]] == a && j - i < kRankItemRows) ++j;
     shrink_items.insert(shrink_items.end(), {a, i, j - i, 0});
     i = j;
   }

@@ -25,8 +25,10 @@ constexpr int kBlockM = 128;
 constexpr int kBlockGroups = 4;
 constexpr int kMaxGroups = 8;
 constexpr int kMinGroupRows = 4;
-// Rows per shrink / gathered work item (one 16-row matrix-core tile).
+// Rows per gathered / g work item (one 16-row matrix-core tile) and per
+// shrink item (two 16-row tiles sharing the adapter operand).
 constexpr int kItemRows = 16;
+constexpr int kRankItemRows = 32;
 // Training rows per chunk of the backward reductions over tokens.
 constexpr int kChunkRows = 256;
 
@@ -42,7 +44,7 @@ struct MetaLayout {
   int64_t train_rows;    // [T_t] token row of each compact training index
   int64_t train_adapter; // [T_t] adapter of each compact training index
   int64_t shrink_rows;   // [T]   token rows sorted by (adapter, row)
-  int64_t shrink_items;  // [n_shrink][4] {adapter, begin, count, 0} into shrink_rows
+  int64_t shrink_items;  // [n_shrink][4] {adapter, begin, count <= 32, 0} into shrink_rows
   int64_t gslot;         // [T]   slot of a gathered row or -1
   int64_t gather_rows;   // [T_g] token row of each gathered slot
   int64_t gather_items;  // [n_gitems][4] {adapter, slot_begin, count, 0}
