@@ -83,6 +83,21 @@ def gemm_bwd_flops(w, proj):
     return f
 
 
+def measured_traffic():
+    """HBM bytes per forward-GEMM launch from the committed counter summary, if it was
+    taken with the kernel source as it is now (else None)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic_fwd_gemm_llama8b_mixed.json")
+    try:
+        doc = json.load(open(path))
+        src = open(os.path.join(ROOT, doc["kernel_source"]), "rb").read()
+    except (OSError, ValueError, KeyError):
+        return None
+    if hashlib.sha256(src).hexdigest() != doc.get("kernel_source_sha256"):
+        return None
+    return float(doc["traffic_bytes_per_launch"])
+
+
 def _gen(args):
     name, p = args
     w = WORKLOADS[name]()
@@ -132,6 +147,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=48, help="forward rows per projection in the CPU sample")
     ap.add_argument("--cpu-dx-rows", type=int, default=24)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first run 3 plain device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -158,6 +175,17 @@ def main():
         if bf:
             return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)
         return torch.from_numpy(np.ascontiguousarray(a, np.float32)).to(dev)
+
+    if args.calibrate_copy > 0:
+        n = args.calibrate_copy << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log("calibration: 3 copies of %d MiB" % args.calibrate_copy)
+        del src, dst
 
     tdt = torch.bfloat16 if bf else torch.float32
     code = dsv.BF16 if bf else dsv.F32
@@ -292,7 +320,9 @@ def main():
             "peak": PEAK_BF16_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(achieved / PEAK_BF16_TFLOPS, 4) if achieved else None,
-            "traffic": None,
+            "traffic": (round(measured_traffic()) if measured_traffic() and args.workload == "llama8b"
+                        else None),
+            "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_us": round(fwd_avg_ms * 1e3, 2),
             "launches": fwd_n,
             "dx_gemm_tflops": round(bwd_achieved, 2) if bwd_achieved else None,
