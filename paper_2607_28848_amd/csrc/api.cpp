@@ -2,6 +2,7 @@
 // carving, and the launch sequence of the forward and backward passes.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstring>
 
 #include "kernels.h"
@@ -17,14 +18,88 @@ size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 int64_t ld_rank(int32_t r_max) { return (r_max + 7) & ~7; }  // 16-byte rows of rank entries
 
+// Compute units of the current device (0 if the query fails).
+int device_cus() {
+  static int cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return 0;
+  if (dev < 64 && cached[dev] > 0) return cached[dev];
+  int n = 0;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (dev < 64) cached[dev] = n;
+  return n;
+}
+
+// GEMM launch plan: tile shape and work split.  Candidates, costed in
+// CU-time (one 128 x 128 x C tile on one CU = 1):
+//   128 x 128, two workgroups per CU, whole tiles in whole waves of 2 * CUs;
+//   256 x 256 (4 units, at a relative matrix-core efficiency kEff256), one
+//     workgroup per CU, whole tiles in whole waves of CUs;
+//   the same with the r tiles of a last, partial wave split into
+//     s = CUs / r equal K ranges (one workgroup per piece, at least
+//     kMinSkIters K-steps each), so that wave takes 1/s of a tile's time,
+//     plus kSplitCost64 for the pieces' fp32 partials and the kernel that sums
+//     them (relative to a tile of 64 K-steps, so smaller for longer tiles).
+// The constants were fitted to timings of the Llama-3-8B projections
+// (forward and dX) on MI355X.
+struct GemmPlan {
+  int tm = 128, tn = 128;
+  int32_t n_mtiles = 0, n_ntiles = 0;
+  int32_t dp_tiles = 0, sk_tiles = 0, sk_split = 0;
+};
+constexpr int kMinSkIters = 8;
+constexpr double kEff256 = 1.12;
+constexpr double kSplitCost64 = 0.4;
+
+GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C) {
+  GemmPlan best;
+  best.n_mtiles = m128;
+  best.n_ntiles = (n_out + 127) / 128;
+  best.dp_tiles = best.n_mtiles * best.n_ntiles;
+  const int cus = device_cus();
+  if (cus <= 0) return best;
+  const int64_t t128 = (int64_t)m128 * best.n_ntiles;
+  const double cost128 = (double)((t128 + 2 * cus - 1) / (2 * cus)) * 2.0;
+
+  const int64_t n256 = (n_out + 255) / 256, t256 = (int64_t)m256 * n256;
+  const int64_t nk = (C + 63) / 64;
+  if (t256 <= 0) return best;
+  GemmPlan p;
+  p.tm = p.tn = 256;
+  p.n_mtiles = m256;
+  p.n_ntiles = (int32_t)n256;
+  p.dp_tiles = (int32_t)t256;
+  const int64_t full = t256 / cus, r = t256 % cus;
+  double cost256 = (double)(full + (r > 0)) * 4.0 / kEff256;
+  const int64_t split = r > 0 ? std::min<int64_t>(cus / r, nk / kMinSkIters) : 0;
+  if (split >= 2 && ((full * cus) & 7) == 0) {
+    const double cost_split =
+        ((double)full + 1.0 / (double)split) * 4.0 / kEff256 + kSplitCost64 * 64.0 / (double)nk;
+    if (cost_split < cost256) {
+      cost256 = cost_split;
+      p.dp_tiles = (int32_t)(full * cus);
+      p.sk_tiles = (int32_t)r;
+      p.sk_split = (int32_t)split;
+    }
+  }
+  return cost256 < cost128 ? p : best;
+}
+
 struct FwdWs {
-  size_t h_all, delta, total;
+  size_t h_all, delta, sk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, part_b, part_a, total;
+  size_t bt, g, part_b, part_a, sk_part, total;
 };
 
-FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N) {
+// Split-tile scratch of a GEMM plan: one fp32 partial tile per piece.
+size_t carve_sk(const GemmPlan& gp, size_t off, size_t* part) {
+  *part = off;
+  if (gp.sk_tiles <= 0) return off;
+  return align256(off + (size_t)gp.sk_tiles * gp.sk_split * gp.tm * gp.tn * 4);
+}
+
+FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N, const GemmPlan& gp) {
   FwdWs w{};
   size_t off = 0;
   if (dt == DSV_BF16) {
@@ -32,6 +107,7 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N) {
     off = align256(off + (size_t)p.T * ld_rank(p.r_max) * 2);
     w.delta = off;
     off = align256(off + (size_t)p.n_gather * N * 4);
+    off = carve_sk(gp, off, &w.sk_part);
   } else {
     w.h_all = off;
     off = align256(off + (size_t)p.T * p.r_max * 4);
@@ -41,7 +117,7 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N) {
   return w;
 }
 
-BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
+BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPlan& gp) {
   BwdWs w{};
   size_t off = 0;
   if (dt == DSV_BF16) {
@@ -53,12 +129,22 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
     off = align256(off + (size_t)p.n_chunks * N * p.r_max * 4);
     w.part_a = off;
     off = align256(off + (size_t)p.n_chunks * K * p.r_max * 4);
+    off = carve_sk(gp, off, &w.sk_part);
   } else {
     w.g = off;
     off = align256(off + (size_t)p.T_t * p.r_max * 4);
   }
   w.total = off;
   return w;
+}
+
+GemmPlan fwd_gemm_plan(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
+  if (dt != DSV_BF16 || p.T == 0) return GemmPlan{};
+  return plan_gemm(p.n_ftiles, p.n_ftiles128, N, K);
+}
+GemmPlan bwd_gemm_plan(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
+  if (dt != DSV_BF16 || p.T_t == 0) return GemmPlan{};
+  return plan_gemm(p.n_btiles, p.n_btiles128, K, N);
 }
 
 int check_common(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N) {
@@ -70,37 +156,18 @@ int check_common(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N) {
 
 int ptr_ok(const void* p) { return p && aligned16(p); }
 
-// GEMM tile shape for an output of (row tiles of 256 / of 128) x n_out: the
-// shape whose launch finishes soonest on 256 compute units, counting whole
-// waves of workgroups (one 256-row workgroup or two 128 x 128 workgroups
-// resident per CU) and a relative matrix-core efficiency per shape measured
-// on MI355X (the 256 x 256 tile re-reads fewer operand bytes per FLOP).
-struct TileChoice {
-  int tm, tn;
-};
-TileChoice choose_tiles(int32_t m256, int32_t m128, int32_t n_out) {
-  struct Cand {
-    int tm, tn, bpc;
-    double eff;
-  } cands[3] = {{128, 128, 2, 1.0}, {256, 256, 1, 1.05}, {256, 128, 1, 0.9}};
-  TileChoice best{128, 128};
-  double best_cost = 1e300;
-  for (const Cand& c : cands) {
-    const int64_t mt = c.tm == 256 ? m256 : m128;
-    const int64_t tiles = mt * ((n_out + c.tn - 1) / c.tn);
-    const int64_t slots = 256LL * c.bpc;
-    const double cost = (double)((tiles + slots - 1) / slots) * c.bpc * (c.tm * c.tn / 16384.0) / c.eff;
-    if (cost < best_cost) {
-      best_cost = cost;
-      best = {c.tm, c.tn};
-    }
-  }
-  return best;
-}
-
 template <typename T>
 T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+void set_split(GemmArgs& g, const GemmPlan& gp, void* ws, size_t part_off) {
+  g.n_mtiles = gp.n_mtiles;
+  g.n_ntiles = gp.n_ntiles;
+  g.dp_tiles = gp.dp_tiles;
+  g.sk_tiles = gp.sk_tiles;
+  g.sk_split = gp.sk_split;
+  g.sk_part = gp.sk_tiles > 0 ? at<float>(ws, part_off) : nullptr;
 }
 
 // Benchmark timing of the GEMM launches (dsv_timing_enable / dsv_timing_read).
@@ -164,7 +231,7 @@ extern "C" int dsv_cobatch_fwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   if (!bytes) return DSV_ERR_ARG;
-  *bytes = fwd_ws(*p, dt, N).total;
+  *bytes = fwd_ws(*p, dt, N, fwd_gemm_plan(*p, dt, K, N)).total;
   return DSV_OK;
 }
 
@@ -173,7 +240,7 @@ extern "C" int dsv_lora_bwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   if (!bytes) return DSV_ERR_ARG;
-  *bytes = bwd_ws(*p, dt, K, N).total;
+  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N)).total;
   return DSV_OK;
 }
 
@@ -186,7 +253,8 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   if (p->T == 0) return DSV_OK;  // empty batch: nothing to read or write
   if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(Y)) return DSV_ERR_ARG;
   if (p->T_t > 0 && !ptr_ok(H_save)) return DSV_ERR_ARG;
-  const FwdWs ws = fwd_ws(*p, dt, N);
+  const GemmPlan gp = fwd_gemm_plan(*p, dt, K, N);
+  const FwdWs ws = fwd_ws(*p, dt, N, gp);
   if (ws.total > 0) {
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
     if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
@@ -262,10 +330,8 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   g.M = p->T;
   g.Nout = N;
   g.C = K;
-  const TileChoice tc = choose_tiles(p->n_ftiles, p->n_ftiles128, N);
-  g.tiles = p->dptr(tc.tm == 256 ? L.fwd_tiles : L.fwd_tiles128);
-  g.n_mtiles = tc.tm == 256 ? p->n_ftiles : p->n_ftiles128;
-  g.n_ntiles = (N + tc.tn - 1) / tc.tn;
+  g.tiles = p->dptr(gp.tm == 256 ? L.fwd_tiles : L.fwd_tiles128);
+  set_split(g, gp, workspace, ws.sk_part);
   g.Lp = h_all;
   g.ldl = ldh;
   g.Lq = static_cast<const uint16_t*>(B);
@@ -277,7 +343,7 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   g.delta = delta;
   g.gslot = p->dptr(L.gslot);
   const int tk = timing_begin(0, s);
-  e = launch_gemm_nt(g, tc.tm, tc.tn, s);
+  e = launch_gemm_nt(g, gp.tm, gp.tn, s);
   timing_end(tk, s);
   if (e != hipSuccess) return DSV_ERR_DEVICE;
   return DSV_OK;
@@ -296,7 +362,8 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     return DSV_ERR_ARG;
   if (dX && !aligned16(dX)) return DSV_ERR_ARG;
   if (p->T_t > 0 && (!ptr_ok(H_save) || !ptr_ok(dY))) return DSV_ERR_ARG;
-  const BwdWs ws = bwd_ws(*p, dt, K, N);
+  const GemmPlan gp = bwd_gemm_plan(*p, dt, K, N);
+  const BwdWs ws = bwd_ws(*p, dt, K, N, gp);
   if (ws.total > 0) {
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
     if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
@@ -413,10 +480,8 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     g.M = p->T_t;
     g.Nout = K;
     g.C = N;
-    const TileChoice tc = choose_tiles(p->n_btiles, p->n_btiles128, K);
-    g.tiles = p->dptr(tc.tm == 256 ? L.bwd_tiles : L.bwd_tiles128);
-    g.n_mtiles = tc.tm == 256 ? p->n_btiles : p->n_btiles128;
-    g.n_ntiles = (K + tc.tn - 1) / tc.tn;
+    g.tiles = p->dptr(gp.tm == 256 ? L.bwd_tiles : L.bwd_tiles128);
+    set_split(g, gp, workspace, ws.sk_part);
     g.Lp = gm;
     g.ldl = ldh;
     g.Lq = static_cast<const uint16_t*>(A);
@@ -428,7 +493,7 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     g.delta = nullptr;
     g.gslot = nullptr;
     const int tk = timing_begin(1, s);
-    e = launch_gemm_nn(g, tc.tm, tc.tn, s);
+    e = launch_gemm_nn(g, gp.tm, gp.tn, s);
     timing_end(tk, s);
     if (e != hipSuccess) return DSV_ERR_DEVICE;
   }

@@ -33,6 +33,14 @@ struct GemmArgs {
   const float* scales;   // nullptr: scale 1
   const float* delta;    // nullptr: no gathered rows
   const int32_t* gslot;
+  // Work split over n_mtiles * n_ntiles tiles (tile order: groups of 8 row
+  // tiles walked column by column).  Workgroups [0, dp_tiles) take tiles
+  // [0, dp_tiles) whole; tiles [dp_tiles, tiles) (sk_tiles of them) are each
+  // split into sk_split equal K ranges, one workgroup per piece, dispatched
+  // after the whole tiles.  Pieces write fp32 partials to sk_part (one tm * tn
+  // slot per piece); a second kernel sums them and writes those tiles.
+  int32_t dp_tiles, sk_tiles, sk_split;
+  float* sk_part;
 };
 
 // Rank-r contraction of a few rows of one adapter (shrink h = x A^T, and
@@ -72,7 +80,8 @@ struct TokenReduceArgs {
 
 // Launchers (bf16).  Each returns hipSuccess or the launch error.
 // Tile shapes (tm x tn): 256x256, 256x128 or 128x128; `tiles` must be the
-// plan's row-tile list of height tm.
+// plan's row-tile list of height tm.  Split tiles (sk_tiles > 0) are
+// supported for 256x256 only.
 hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);

@@ -37,12 +37,14 @@ __device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
 
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
-// fp32 -> bf16, round to nearest even (NaN kept quiet).
+// fp32 -> bf16, round to nearest even (NaN kept quiet).  Written as a select,
+// not a branch: a branch per element makes the compiler spill accumulators
+// around every conversion of an epilogue.
 __device__ __forceinline__ uint16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
+  const uint32_t u = __float_as_uint(f);
+  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t quiet = (u >> 16) | 0x40u;
+  return (uint16_t)(((u & 0x7fffffffu) > 0x7f800000u) ? quiet : rounded);
 }
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
@@ -138,69 +140,60 @@ struct GemmShape {
 // operations of this wave are outstanding; lgkm and exp counters untouched.
 constexpr int vmcnt_imm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
-template <bool NN, int TM, int TN, int WGM, int WGN, int TK, int NS>
-__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
+// Workgroup id -> logical index.  Consecutive workgroup ids land on different
+// XCDs (round robin over 8); the renumbering gives each XCD a contiguous
+// range of logical indices, so work that runs together on one XCD is
+// adjacent in the tile order and shares operand panels in that XCD's L2.
+__device__ __forceinline__ int xcd_major(int bid, int n) {
+  const int per = n >> 3, rem = n & 7, xcd = bid & 7;
+  return xcd * per + min(xcd, rem) + (bid >> 3);
+}
+
+// Tile -> (row tile, column tile): groups of 8 row tiles are walked column by
+// column, so tiles in flight together share row and column panels.
+__device__ __forceinline__ void tile_coords(const GemmArgs& g, int lin, int& mt, int& nt) {
+  const int GM = 8;
+  const int span = GM * g.n_ntiles;
+  const int grp = lin / span, first_m = grp * GM;
+  const int gsz = min(g.n_mtiles - first_m, GM);
+  mt = first_m + (lin % span) % gsz;
+  nt = (lin % span) / gsz;
+}
+
+// One piece of a tile: K-steps [kb, ke) of tile `lin`.  A piece that covers
+// the whole K range writes the tile; a piece of a split tile (t_sk: its index
+// among the split tiles) writes its fp32 partial to slot t_sk * split + piece.
+template <bool NN, int TM, int TN, int WGM, int WGN, int TK, int NS, bool SK>
+__device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int tid, int lin,
+                                           int t_sk, int piece, int kb, int ke, int nk) {
   using S = GemmShape<TM, TN, WGM, WGN, TK, NS>;
   constexpr int WM = S::WM, WN = S::WN, FM = S::FM, FN = S::FN, NW = S::NW;
   constexpr int ROWB = TK * 2;          // bytes per row of a K-contiguous tile
   constexpr int CPR = TK / 8;           // 16-byte chunks per row
-  static_assert(FM >= 1 && FN >= 1 && NS >= 2, "tile shape");
-  static_assert((TM * ROWB) % (1024 * NW) == 0 && (TN * ROWB) % (1024 * NW) == 0, "loads per wave");
-  __shared__ __attribute__((aligned(1024))) char smem[S::LDS];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int A_LOADS = TM * ROWB / 1024 / NW, B_LOADS = TN * ROWB / 1024 / NW;
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
 
-  // Workgroup -> tile.  Consecutive workgroup ids land on different XCDs
-  // (round robin over 8); renumber so that each XCD owns a contiguous range
-  // of tiles, then walk that range in groups of 8 row tiles so the tiles
-  // running together on one XCD share row and column panels in its L2.
-  const int nblk = gridDim.x, bid = blockIdx.x;
-  const int per = nblk >> 3, rem = nblk & 7, xcd = bid & 7;
-  const int logical = xcd * per + min(xcd, rem) + (bid >> 3);
-  const int GM = 8;
-  const int span = GM * g.n_ntiles;
-  const int grp = logical / span, first_m = grp * GM;
-  const int gsz = min(g.n_mtiles - first_m, GM);
-  const int mt = first_m + (logical % span) % gsz;
-  const int nt = (logical % span) / gsz;
+  int mt, nt;
+  tile_coords(g, lin, mt, nt);
 
   const int32_t* td = g.tiles + (int64_t)mt * kTileWords;
   const int m0 = td[0], ngroups = td[1], has_gather = td[2], nrows = td[3];
   const int n0 = nt * TN;
-
-  // ---- operand tiles: per-lane global offsets of the direct-to-LDS loads ----
-  constexpr int A_LOADS = TM * ROWB / 1024 / NW, B_LOADS = TN * ROWB / 1024 / NW;
-  int a_off[A_LOADS], a_kc[A_LOADS];
-#pragma unroll
-  for (int i = 0; i < A_LOADS; ++i) {
-    const int q = wave * A_LOADS + i;
-    const int row = q * (1024 / ROWB) + lane / CPR;
-    const int c = (lane % CPR) ^ swz<TK>(row);
-    a_off[i] = (int)(((int64_t)row * g.ldp + 8 * c) * 2);
-    a_kc[i] = 8 * c;
-  }
-  int b_off[B_LOADS], b_kc[B_LOADS];
-#pragma unroll
-  for (int i = 0; i < B_LOADS; ++i) {
-    const int q = wave * B_LOADS + i;
-    if constexpr (!NN) {
-      const int col = q * (1024 / ROWB) + lane / CPR;
-      const int c = (lane % CPR) ^ swz<TK>(col);
-      b_off[i] = (int)(((int64_t)col * g.ldq + 8 * c) * 2);
-      b_kc[i] = 8 * c;
-    } else {
-      const int byte = q * 1024 + 16 * lane;
-      const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
-      b_off[i] = (int)(((int64_t)n * g.ldq + 8 * (slot ^ nn_swz(n))) * 2);
-      b_kc[i] = n;
-    }
-  }
   const uint16_t* a_base = g.P + (int64_t)m0 * g.ldp;
   const int64_t a_rows = min((int64_t)TM, (int64_t)g.M - m0);
   const uint16_t* b_base = NN ? g.Q + n0 : g.Q + (int64_t)n0 * g.ldq;
   const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
 
+  // Direct-to-LDS loads of K-step kt into stage `stage`.  With 8 or more
+  // accumulator tiles per wave the per-lane offsets are recomputed here from
+  // the lane id, read afresh so that the compiler cannot hoist them: held in
+  // registers across the main loop they would be spilled.  Smaller tiles keep
+  // them in registers.
   auto issue = [&](int kt, int stage) {
+    int ln = lane;
+    if constexpr (FM * FN >= 8)
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
     const int k0 = kt * TK;
     char* sa = smem + stage * S::STAGE;
     char* sb = sa + S::A_BYTES;
@@ -209,7 +202,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 #pragma unroll
     for (int i = 0; i < A_LOADS; ++i) {
       const int q = wave * A_LOADS + i;
-      const int vo = (k0 + a_kc[i] < g.C) ? a_off[i] : (int)0x7FFFFFF0;
+      const int row = q * (1024 / ROWB) + ln / CPR;
+      const int c = (ln % CPR) ^ swz<TK>(row);
+      const int vo = (k0 + 8 * c < g.C) ? (row * (int)g.ldp + 8 * c) * 2 : (int)0x7FFFFFF0;
       llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
     }
     if constexpr (!NN) {
@@ -217,7 +212,9 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 #pragma unroll
       for (int i = 0; i < B_LOADS; ++i) {
         const int q = wave * B_LOADS + i;
-        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
+        const int col = q * (1024 / ROWB) + ln / CPR;
+        const int c = (ln % CPR) ^ swz<TK>(col);
+        const int vo = (k0 + 8 * c < g.C) ? (col * (int)g.ldq + 8 * c) * 2 : (int)0x7FFFFFF0;
         llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
       }
     } else {
@@ -227,17 +224,18 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 #pragma unroll
       for (int i = 0; i < B_LOADS; ++i) {
         const int q = wave * B_LOADS + i;
-        const int vo = (k0 + b_kc[i] < g.C) ? b_off[i] : (int)0x7FFFFFF0;
+        const int byte = q * 1024 + 16 * ln;
+        const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
+        const int vo = (k0 + n < g.C) ? (n * (int)g.ldq + 8 * (slot ^ nn_swz(n))) * 2 : (int)0x7FFFFFF0;
         llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
       }
     }
   };
 
   // The first NS K-steps are in flight while the low-rank prologue runs.
-  const int nk = (g.C + TK - 1) / TK;
 #pragma unroll
   for (int p = 0; p < NS; ++p)
-    if (p < nk) issue(p, p);
+    if (kb + p < ke) issue(kb + p, p);
 
   f32x16 acc[FM][FN];
 #pragma unroll
@@ -247,12 +245,12 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-  // ---- low-rank prologue: tile groups on the matrix cores -----------------
+  // ---- low-rank prologue (the piece that starts the tile's K range) -----
   // acc += (s_a h) B_a for the rows of each group.  s_a h is formed in fp32
   // and split into bf16 hi + lo (|lo| <= 2^-9 |hi|), so the product carries
   // the scale to about 2^-16 relative with no VALU work on the accumulators;
   // with scale 1 (or a power of two) lo is exactly zero and is skipped.
-  for (int gi = 0; gi < ngroups; ++gi) {
+  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
     const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
     if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
     const int r = g.ranks[a];
@@ -308,7 +306,7 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
     }
   }
 
-  // ---- main loop ------------------------------------------------------------
+  // ---- main loop ----------------------------------------------------------
   auto load_frags = [&](const char* sa, const char* sb, int s, bf16x8* af, bf16x8* bq) {
     const int ch = 2 * s + (lane >> 5);
 #pragma unroll
@@ -352,13 +350,13 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
   constexpr int kSteps = TK / 16;
   constexpr int L = (kSteps - 1) & 1;  // fragment buffer of the last step
   static_assert(L == 1, "an even number of 16-wide steps per K-step");
-  if (nk >= NS) __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * kLoads));  // step 0 landed
+  if (ke - kb >= NS) __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 1) * kLoads));  // first step landed
   else vmem_wait_all();
   __syncthreads();
   bf16x8 af[2][FM], bq[2][FN];
   load_frags(smem, smem + S::A_BYTES, 0, af[0], bq[0]);
   int stage = 0;
-  for (int kt = 0; kt < nk; ++kt) {
+  for (int kt = kb; kt < ke; ++kt) {
     char* sa = smem + stage * S::STAGE;
     char* sb = sa + S::A_BYTES;
 #pragma unroll
@@ -373,19 +371,19 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 #pragma unroll
     for (int s = 0; s < kSteps - 1; ++s) {
 #pragma unroll
-      for (int t = 0; t < kReads; ++t) {
+      for (int q = 0; q < kReads; ++q) {
         __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       }
       if (kMfma > kReads) __builtin_amdgcn_sched_group_barrier(0x008, kMfma - kReads, 0);
     }
     const int next = (stage + 1 == NS) ? 0 : stage + 1;
-    if (kt + 1 < nk) {
+    if (kt + 1 < ke) {
       // step kt+1 has landed once at most (steps issued after it) loads remain
-      if (kt + NS <= nk) __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * kLoads));
+      if (kt + NS <= ke) __builtin_amdgcn_s_waitcnt(vmcnt_imm((NS - 2) * kLoads));
       else vmem_wait_all();
       __syncthreads();  // everyone's part of kt+1 is in; buffer `stage` is free
-      if (kt + NS < nk) issue(kt + NS, stage);
+      if (kt + NS < ke) issue(kt + NS, stage);
       char* na = smem + next * S::STAGE;
       load_frags(na, na + S::A_BYTES, 0, af[L ^ 1], bq[L ^ 1]);
     }
@@ -397,7 +395,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
     stage = next;
   }
 
-  // ---- epilogue: one rounding, staged through LDS for 16-byte stores ------
+  // ---- a piece of a split tile: its fp32 partial goes to its slot (in the
+  // MFMA result layout); a follow-up kernel sums the pieces and writes ----
+  if (SK && !(kb == 0 && ke == nk)) {
+    f32x4* part = reinterpret_cast<f32x4*>(g.sk_part) +
+                  (int64_t)(t_sk * g.sk_split + piece) * (TM * TN / 4) + wave * (FM * FN * 4 * 64);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          part[((i * FN + j) * 4 + q) * 64 + lane] =
+              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+    return;
+  }
+
+  // ---- epilogue: one rounding, staged through LDS for 16-byte stores ----
   __syncthreads();
   uint16_t* st = reinterpret_cast<uint16_t*>(smem);
   const bool gather_tile = has_gather && g.delta != nullptr;
@@ -419,13 +433,113 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
   __syncthreads();
   constexpr int CH = TN / 8;  // 16-byte chunks per staged row
 #pragma unroll 4
-  for (int it = 0; it < (TM * CH) / S::THREADS; ++it) {
-    const int idx = tid + S::THREADS * it;
+  for (int q = 0; q < (TM * CH) / S::THREADS; ++q) {
+    const int idx = tid + S::THREADS * q;
     const int row = idx / CH, ch = idx % CH;
     const int col = n0 + ch * 8;
     if (row < nrows && col < g.Nout)
       *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + row) * g.ldo + col) =
           *reinterpret_cast<const u32x4*>(st + row * S::STG_LD + ch * 8);
+  }
+}
+
+template <bool NN, int TM, int TN, int WGM, int WGN, int TK, int NS, bool SK>
+__global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
+  using S = GemmShape<TM, TN, WGM, WGN, TK, NS>;
+  static_assert(S::FM >= 1 && S::FN >= 1 && NS >= 2, "tile shape");
+  static_assert((TM * TK * 2) % (1024 * S::NW) == 0 && (TN * TK * 2) % (1024 * S::NW) == 0, "loads per wave");
+  __shared__ __attribute__((aligned(1024))) char smem[S::LDS];
+  const int tid0 = threadIdx.x;
+  const int nk = (g.C + TK - 1) / TK;
+
+  // Whole tiles first (XCD-major over the tile order), then the pieces of
+  // the split tiles, numbered piece-major so that the pieces running together
+  // on one XCD sit at the same K offset of neighbouring tiles.
+  int lin, t_sk = -1, piece = 0, kb = 0, ke = nk;
+  if (!SK || (int)blockIdx.x < g.dp_tiles) {
+    lin = xcd_major(blockIdx.x, SK ? g.dp_tiles : gridDim.x);
+  } else {
+    const int q = xcd_major(blockIdx.x - g.dp_tiles, gridDim.x - g.dp_tiles);
+    piece = q / g.sk_tiles;
+    t_sk = q - piece * g.sk_tiles;
+    lin = g.dp_tiles + t_sk;
+    kb = (int)(((int64_t)piece * nk) / g.sk_split);
+    ke = (int)(((int64_t)(piece + 1) * nk) / g.sk_split);
+  }
+  gemm_piece<NN, TM, TN, WGM, WGN, TK, NS, SK>(g, smem, tid0, lin, t_sk, piece, kb, ke, nk);
+}
+
+// ---------------------------------------------------------------------------
+// Split tiles: sum the fp32 partials of a tile's pieces in K order, add the
+// gathered rows' term, round once to bf16 and store -- the GEMM epilogue for
+// the tiles the GEMM left in pieces.  One workgroup per (split tile, pair of
+// waves of the GEMM workgroup), i.e. a WM x 2WN region of the tile, read in
+// the GEMM's MFMA result layout (16-byte loads, one contiguous KiB per wave).
+// ---------------------------------------------------------------------------
+template <int TM, int TN, int WGM, int WGN>
+__global__ __launch_bounds__(128) void split_fixup_kernel(GemmArgs g) {
+  constexpr int NW = WGM * WGN, WM = TM / WGM, WN = TN / WGN, FM = WM / 32, FN = WN / 32;
+  static_assert(WGN % 2 == 0, "the two waves of a pair share their rows");
+  constexpr int RW = 2 * WN, LD = RW + 8;  // region width, staging row stride
+  __shared__ __attribute__((aligned(16))) uint16_t st[WM * LD];
+  const int t_sk = blockIdx.x / (NW / 2), pair = blockIdx.x % (NW / 2);
+  const int tid = threadIdx.x, lane = tid & 63, wave = 2 * pair + (tid >> 6);
+  const int wm = wave / WGN, wn = wave % WGN, wn0 = wn & ~1;
+  int mt, nt;
+  tile_coords(g, g.dp_tiles + t_sk, mt, nt);
+  const int32_t* td = g.tiles + (int64_t)mt * kTileWords;
+  const int m0 = td[0], has_gather = td[2], nrows = td[3];
+  const int n0 = nt * TN;
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+  const f32x4* src = reinterpret_cast<const f32x4*>(g.sk_part) + (int64_t)t_sk * g.sk_split * (TM * TN / 4) +
+                     wave * (FM * FN * 4 * 64);
+  for (int p = 0; p < g.sk_split; ++p, src += TM * TN / 4) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const f32x4 v = src[((i * FN + j) * 4 + q) * 64 + lane];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
+        }
+  }
+
+  const bool gather_tile = has_gather && g.delta != nullptr;
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int row = 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);  // within the region
+      const int trow = wm * WM + row;                                     // within the tile
+      const int gs = (gather_tile && trow < nrows) ? g.gslot[m0 + trow] : -1;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = (wn - wn0) * WN + 32 * j + (lane & 31);
+        const int gcol = n0 + wn0 * WN + col;
+        float x = acc[i][j][v];
+        if (gs >= 0 && gcol < g.Nout) x += g.delta[(int64_t)gs * g.Nout + gcol];
+        st[row * LD + col] = f2bf(x);
+      }
+    }
+  __syncthreads();
+  constexpr int CH = RW / 8;  // 16-byte chunks per staged row
+#pragma unroll 4
+  for (int q = 0; q < (WM * CH) / 128; ++q) {
+    const int idx = tid + 128 * q;
+    const int row = idx / CH, ch = idx % CH;
+    const int trow = wm * WM + row, gcol = n0 + wn0 * WN + ch * 8;
+    if (trow < nrows && gcol < g.Nout)
+      *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + trow) * g.ldo + gcol) =
+          *reinterpret_cast<const u32x4*>(st + row * LD + ch * 8);
   }
 }
 
@@ -708,13 +822,27 @@ namespace {
 template <bool NN>
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   if (a.n_mtiles <= 0 || a.n_ntiles <= 0) return hipSuccess;
-  const dim3 grid(a.n_mtiles * a.n_ntiles);
-  if (tm == 256 && tn == 256)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2>), grid, dim3(512), 0, s, a);
+  const int64_t tiles = (int64_t)a.n_mtiles * a.n_ntiles;
+  if (a.dp_tiles < 0 || a.sk_tiles < 0 || a.dp_tiles + (int64_t)a.sk_tiles != tiles) return hipErrorInvalidValue;
+  if (a.sk_tiles > 0) {
+    // split tiles: 256x256 only, whole tiles a multiple of 8 (the pieces keep
+    // the hardware's XCD round robin), and at least one K-step per piece
+    const int64_t nk = (a.C + 63) / 64;
+    if (tm != 256 || tn != 256 || (a.dp_tiles & 7) || a.sk_split < 2 || a.sk_split > nk || !a.sk_part)
+      return hipErrorInvalidValue;
+  }
+  const dim3 grid((unsigned)(a.dp_tiles + (int64_t)a.sk_tiles * (a.sk_tiles > 0 ? a.sk_split : 0)));
+  if (tm == 256 && tn == 256 && a.sk_tiles > 0) {
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>), grid, dim3(512), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL((split_fixup_kernel<256, 256, 2, 4>), dim3((unsigned)a.sk_tiles * 4), dim3(128), 0, s, a);
+  } else if (tm == 256 && tn == 256)
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>), grid, dim3(512), 0, s, a);
   else if (tm == 256 && tn == 128)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 128, 4, 2, 64, 2>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 128, 4, 2, 64, 2, false>), grid, dim3(512), 0, s, a);
   else if (tm == 128 && tn == 128)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2, false>), grid, dim3(256), 0, s, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
