@@ -190,7 +190,8 @@ int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
  * Kernel timing for benchmarks.  While enabled (on = 1), every
  * dsv_cobatch_fwd / dsv_lora_bwd call records a HIP event pair on its own
  * stream immediately around its matrix-core GEMM launch (forward: the base
- * GEMM with its low-rank prologue; backward: the dX GEMM).  Up to 4096 pairs
+ * GEMM with its low-rank prologue; backward: the dX GEMM; in both, when tiles
+ * are split along the contraction, also the kernel that sums their pieces).  Up to 4096 pairs
  * are kept; further launches are not timed.  dsv_timing_read waits for the
  * recorded events, returns the summed milliseconds and launch counts of the
  * forward and backward GEMMs, and releases the pairs.  Not thread-safe:
@@ -200,6 +201,18 @@ int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
 int dsv_timing_enable(int32_t on);
 int dsv_timing_read(double* fwd_ms, int32_t* fwd_launches, double* bwd_ms,
                     int32_t* bwd_launches);
+
+/* GEMM launch configuration that dsv_cobatch_fwd (pass 0) or dsv_lora_bwd
+ * (pass 1, the dX GEMM) uses for this plan, dtype and K x N on the current
+ * device, for benchmarks and tests.  out[6] receives: tile rows, tile
+ * columns, row tiles, column tiles, the number of tiles split along the
+ * contraction and the number of pieces each of them is split into (0 and 0
+ * when none is split).  The bf16 path picks, per launch, the tile shape and
+ * split with the smallest estimated time; fp32 and empty passes report zeros.
+ * Returns DSV_OK, DSV_ERR_ARG (NULL plan or out, pass not 0 or 1) or the
+ * dsv_cobatch_fwd size and dtype errors. */
+int dsv_gemm_config(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N, int32_t pass,
+                    int32_t out[6]);
 
 /* Static description of a status code. */
 const char* dsv_status_string(int status);

@@ -226,6 +226,23 @@ extern "C" int dsv_timing_read(double* fwd_ms, int32_t* fwd_n, double* bwd_ms, i
   return rc;
 }
 
+extern "C" int dsv_gemm_config(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, int32_t pass,
+                               int32_t out[6]) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  if (!out || (pass != 0 && pass != 1)) return DSV_ERR_ARG;
+  for (int i = 0; i < 6; ++i) out[i] = 0;
+  if (dt != DSV_BF16 || (pass == 0 ? p->T : p->T_t) == 0) return DSV_OK;
+  const GemmPlan gp = pass == 0 ? fwd_gemm_plan(*p, dt, K, N) : bwd_gemm_plan(*p, dt, K, N);
+  out[0] = gp.tm;
+  out[1] = gp.tn;
+  out[2] = gp.n_mtiles;
+  out[3] = gp.n_ntiles;
+  out[4] = gp.sk_tiles;
+  out[5] = gp.sk_split;
+  return DSV_OK;
+}
+
 extern "C" int dsv_cobatch_fwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N,
                                          size_t* bytes) {
   int rc = check_common(p, dt, K, N);

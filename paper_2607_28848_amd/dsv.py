@@ -71,6 +71,8 @@ _lib.dsv_timing_enable.restype = ctypes.c_int
 _lib.dsv_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), _i32p,
                                  ctypes.POINTER(ctypes.c_double), _i32p]
 _lib.dsv_timing_read.restype = ctypes.c_int
+_lib.dsv_gemm_config.argtypes = [_vp, ctypes.c_int, _i32, _i32, _i32, _i32p]
+_lib.dsv_gemm_config.restype = ctypes.c_int
 _lib.dsv_status_string.argtypes = [ctypes.c_int]
 _lib.dsv_status_string.restype = ctypes.c_char_p
 
@@ -244,6 +246,16 @@ def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want
                              1 if accumulate else 0, _ptr(ws), ws.numel() * ws.element_size(),
                              _stream_handle(stream)), "dsv_lora_bwd")
     return dA, dB, dX
+
+
+GEMM_CONFIG_NAMES = ("tile_m", "tile_n", "row_tiles", "col_tiles", "split_tiles", "split_ways")
+
+
+def gemm_config(plan: Plan, dtype_code: int, K: int, N: int, pass_: int) -> dict:
+    """Tile shape and contraction split of the forward (pass_ 0) or dX (pass_ 1) GEMM."""
+    out = (ctypes.c_int32 * 6)()
+    _check(_lib.dsv_gemm_config(plan.handle, dtype_code, K, N, pass_, out), "dsv_gemm_config")
+    return dict(zip(GEMM_CONFIG_NAMES, list(out)))
 
 
 def timing_enable(on: bool = True):

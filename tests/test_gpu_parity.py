@@ -77,6 +77,39 @@ def test_mixed_bf16_ragged():
     _full(w)
 
 
+SPLIT = ([(0, 180, 1, 0)] + [(180 + i, 1, 2 + i % 3, 0) for i in range(20)] +
+         [(200, 300, 0, 1), (500, 200, 3, 0)])
+SPLIT_RANKS = [16, 8, 32, 64, 5]
+
+
+def test_split_tiles_ragged():
+    """256 x 256 tiles whose last partial wave is split along the contraction, in both
+    GEMMs: ragged rows (T = 700, T_t = 300), columns (N = 2000) and contraction (the dX
+    GEMM's 2000 = 31 * 64 + 16), decode singles on the gathered path inside split tiles.
+    Y and dX on sampled rows, H_save, dA and dB in full; a repeat is bit-identical."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    w = wl.custom(SPLIT, SPLIT_RANKS, K=4096, N=2000, r_max=64, name="split_ragged")
+    run = Run(w, pad=np.nan)
+    fc = dsv.gemm_config(run.plan, dsv.BF16, 4096, 2000, 0)
+    bc = dsv.gemm_config(run.plan, dsv.BF16, 4096, 2000, 1)
+    _say("  gemm configs: fwd %s dX %s" % (fc, bc))
+    if fc["split_tiles"] == 0 or bc["split_tiles"] == 0:
+        pytest.skip("this device's compute-unit count gives no split for these shapes")
+    assert run.plan.counts()["gathered_rows"] >= 20
+    Y, H = run.fwd()
+    dA, dB, dX = run.bwd(H)
+    Y2, _ = run.fwd()
+    _, _, dX2 = run.bwd(H)
+    torch.cuda.synchronize()
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+    assert torch.equal(dX.view(torch.int16), dX2.view(torch.int16))
+    rows = np.unique(np.concatenate([np.arange(0, 700, 7), [179, 180, 199, 200, 499, 500, 699]]))
+    dx_rows = np.unique(np.concatenate([np.arange(0, 300, 5), [255, 256, 299]]))
+    _check_all(w, run, Y, H, dA, dB, dX, TOL_BF16, rows=rows.astype(np.int32),
+               dx_rows=dx_rows.astype(np.int32))
+
+
 def test_mixed_f32_ragged():
     w = wl.custom(MIXED, MIXED_RANKS, K=136, N=200, dtype="f32", r_max=64, name="mixed_f32")
     _full(w, tol=TOL_F32)
