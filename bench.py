@@ -278,6 +278,17 @@ def main():
         % (args.steps, ms_per_step, value, achieved or 0, fwd_avg_ms * 1e3,
            "%.1f" % bwd_achieved if bwd_achieved else "n/a"))
 
+    def cfg_str(c):
+        if not c["tile_m"]:
+            return None
+        s = "%dx%d tiles, %dx%d" % (c["tile_m"], c["tile_n"], c["row_tiles"], c["col_tiles"])
+        if c["split_tiles"]:
+            s += ", %d split %d ways" % (c["split_tiles"], c["split_ways"])
+        return s
+    gemm_launches = {proj.name: {"fwd": cfg_str(dsv.gemm_config(probe, code, proj.K, proj.N, 0)),
+                                 "dx": cfg_str(dsv.gemm_config(probe, code, proj.K, proj.N, 1))}
+                     for proj in w.projections}
+
     cpu = None
     if not args.no_cpu_baseline:
         log("cpu baseline: fp64 reference on a sample (%d rows/projection fwd, %d dX rows)"
@@ -314,7 +325,8 @@ def main():
             "plan_build_ms": round(float(np.median(plan_ms)), 4) if plan_ms else None,
         },
         "roofline": {
-            "kernel": "gemm_lora_kernel<NT> (forward base GEMM + low-rank prologue)",
+            "kernel": "gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the "
+                      "low-rank prologue; the fixup sums contraction-split tiles)",
             "bound": "mfma",
             "achieved": round(achieved, 2) if achieved else None,
             "peak": PEAK_BF16_TFLOPS,
@@ -326,6 +338,7 @@ def main():
             "avg_launch_us": round(fwd_avg_ms * 1e3, 2),
             "launches": fwd_n,
             "dx_gemm_tflops": round(bwd_achieved, 2) if bwd_achieved else None,
+            "gemm_launches": gemm_launches,
         },
         "cpu_baseline": cpu,
     }

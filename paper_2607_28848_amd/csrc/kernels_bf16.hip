@@ -170,7 +170,13 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   constexpr int WM = S::WM, WN = S::WN, FM = S::FM, FN = S::FN, NW = S::NW;
   constexpr int ROWB = TK * 2;          // bytes per row of a K-contiguous tile
   constexpr int CPR = TK / 8;           // 16-byte chunks per row
-  constexpr int A_LOADS = TM * ROWB / 1024 / NW, B_LOADS = TN * ROWB / 1024 / NW;
+  // With 8 waves (two per SIMD) the operand loads of a K-step are all issued
+  // by waves 0-3, one per SIMD: a wave whose load issue stalls on the
+  // texture-address queue holds back its own later MFMAs, and the other wave
+  // of its SIMD, which issues no loads, keeps the matrix core busy meanwhile.
+  constexpr int LW = NW >= 8 ? NW / 2 : NW;  // loading waves
+  constexpr int A_LOADS = TM * ROWB / 1024 / LW, B_LOADS = TN * ROWB / 1024 / LW;
+  static_assert(A_LOADS * 1024 * LW == TM * ROWB && B_LOADS * 1024 * LW == TN * ROWB, "loads per wave");
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WGN, wn = wave % WGN;
 
@@ -191,6 +197,7 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // registers across the main loop they would be spilled.  Smaller tiles keep
   // them in registers.
   auto issue = [&](int kt, int stage) {
+    if (LW < NW && wave >= LW) return;
     int ln = lane;
     if constexpr (FM * FN >= 8)
       asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
@@ -395,19 +402,18 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
     stage = next;
   }
 
-  // ---- a piece of a split tile: its fp32 partial goes to its slot (in the
-  // MFMA result layout); a follow-up kernel sums the pieces and writes ----
+  // ---- a piece of a split tile: its fp32 partial goes to its slot (row-major
+  // tm x tn); a follow-up kernel sums the pieces and writes the tile ----
   if (SK && !(kb == 0 && ke == nk)) {
-    f32x4* part = reinterpret_cast<f32x4*>(g.sk_part) +
-                  (int64_t)(t_sk * g.sk_split + piece) * (TM * TN / 4) + wave * (FM * FN * 4 * 64);
+    float* part = g.sk_part + (int64_t)(t_sk * g.sk_split + piece) * (TM * TN);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int v = 0; v < 16; ++v) {
+        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          part[((i * FN + j) * 4 + q) * 64 + lane] =
-              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        for (int j = 0; j < FN; ++j) part[row * TN + wn * WN + 32 * j + (lane & 31)] = acc[i][j][v];
+      }
     return;
   }
 
@@ -472,75 +478,32 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
 // ---------------------------------------------------------------------------
 // Split tiles: sum the fp32 partials of a tile's pieces in K order, add the
 // gathered rows' term, round once to bf16 and store -- the GEMM epilogue for
-// the tiles the GEMM left in pieces.  One workgroup per (split tile, pair of
-// waves of the GEMM workgroup), i.e. a WM x 2WN region of the tile, read in
-// the GEMM's MFMA result layout (16-byte loads, one contiguous KiB per wave).
+// the tiles the GEMM left in pieces.  Elementwise: one thread per 4 columns
+// of a row, (TM * TN / 4) / 256 workgroups per split tile.
 // ---------------------------------------------------------------------------
-template <int TM, int TN, int WGM, int WGN>
-__global__ __launch_bounds__(128) void split_fixup_kernel(GemmArgs g) {
-  constexpr int NW = WGM * WGN, WM = TM / WGM, WN = TN / WGN, FM = WM / 32, FN = WN / 32;
-  static_assert(WGN % 2 == 0, "the two waves of a pair share their rows");
-  constexpr int RW = 2 * WN, LD = RW + 8;  // region width, staging row stride
-  __shared__ __attribute__((aligned(16))) uint16_t st[WM * LD];
-  const int t_sk = blockIdx.x / (NW / 2), pair = blockIdx.x % (NW / 2);
-  const int tid = threadIdx.x, lane = tid & 63, wave = 2 * pair + (tid >> 6);
-  const int wm = wave / WGN, wn = wave % WGN, wn0 = wn & ~1;
+template <bool NN, int TM, int TN>  // NN: the dX GEMM's tiles (the layout is the same)
+__global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs g) {
+  constexpr int PER_TILE = TM * TN / 4 / 256;
+  const int t_sk = blockIdx.x / PER_TILE;
+  const int idx = (blockIdx.x % PER_TILE) * 256 + threadIdx.x;
+  const int row = idx / (TN / 4), c4 = idx % (TN / 4);
   int mt, nt;
   tile_coords(g, g.dp_tiles + t_sk, mt, nt);
   const int32_t* td = g.tiles + (int64_t)mt * kTileWords;
   const int m0 = td[0], has_gather = td[2], nrows = td[3];
-  const int n0 = nt * TN;
-
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-  const f32x4* src = reinterpret_cast<const f32x4*>(g.sk_part) + (int64_t)t_sk * g.sk_split * (TM * TN / 4) +
-                     wave * (FM * FN * 4 * 64);
-  for (int p = 0; p < g.sk_split; ++p, src += TM * TN / 4) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const f32x4 v = src[((i * FN + j) * 4 + q) * 64 + lane];
-#pragma unroll
-          for (int e = 0; e < 4; ++e) acc[i][j][4 * q + e] += v[e];
-        }
+  const int col = nt * TN + 4 * c4;
+  if (row >= nrows || col >= g.Nout) return;  // Nout % 8 == 0: all 4 columns or none
+  const f32x4* src = reinterpret_cast<const f32x4*>(g.sk_part + (int64_t)t_sk * g.sk_split * (TM * TN)) + idx;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int p = 0; p < g.sk_split; ++p) acc += src[(int64_t)p * (TM * TN / 4)];
+  if (has_gather && g.delta != nullptr) {
+    // rows of the gathered path add their fp32 low-rank term before the rounding
+    const int gs = g.gslot[m0 + row];
+    if (gs >= 0) acc += *reinterpret_cast<const f32x4*>(g.delta + (int64_t)gs * g.Nout + col);
   }
-
-  const bool gather_tile = has_gather && g.delta != nullptr;
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);  // within the region
-      const int trow = wm * WM + row;                                     // within the tile
-      const int gs = (gather_tile && trow < nrows) ? g.gslot[m0 + trow] : -1;
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = (wn - wn0) * WN + 32 * j + (lane & 31);
-        const int gcol = n0 + wn0 * WN + col;
-        float x = acc[i][j][v];
-        if (gs >= 0 && gcol < g.Nout) x += g.delta[(int64_t)gs * g.Nout + gcol];
-        st[row * LD + col] = f2bf(x);
-      }
-    }
-  __syncthreads();
-  constexpr int CH = RW / 8;  // 16-byte chunks per staged row
-#pragma unroll 4
-  for (int q = 0; q < (WM * CH) / 128; ++q) {
-    const int idx = tid + 128 * q;
-    const int row = idx / CH, ch = idx % CH;
-    const int trow = wm * WM + row, gcol = n0 + wn0 * WN + ch * 8;
-    if (trow < nrows && gcol < g.Nout)
-      *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + trow) * g.ldo + gcol) =
-          *reinterpret_cast<const u32x4*>(st + row * LD + ch * 8);
-  }
+  const uint32_t lo = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
+  const uint32_t hi = (uint32_t)f2bf(acc[2]) | ((uint32_t)f2bf(acc[3]) << 16);
+  *reinterpret_cast<uint2*>(g.out + (int64_t)(m0 + row) * g.ldo + col) = make_uint2(lo, hi);
 }
 
 // ---------------------------------------------------------------------------
@@ -836,7 +799,8 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
     hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>), grid, dim3(512), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((split_fixup_kernel<256, 256, 2, 4>), dim3((unsigned)a.sk_tiles * 4), dim3(128), 0, s, a);
+    hipLaunchKernelGGL((split_fixup_kernel<NN, 256, 256>), dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)),
+                       dim3(256), 0, s, a);
   } else if (tm == 256 && tn == 256)
     hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>), grid, dim3(512), 0, s, a);
   else if (tm == 256 && tn == 128)
