@@ -147,6 +147,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-rows", type=int, default=48, help="forward rows per projection in the CPU sample")
     ap.add_argument("--cpu-dx-rows", type=int, default=24)
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the timing of the steps that follow the layer (the AdamW update)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 3 plain device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -278,6 +280,71 @@ def main():
         % (args.steps, ms_per_step, value, achieved or 0, fwd_avg_ms * 1e3,
            "%.1f" % bwd_achieved if bwd_achieved else "n/a"))
 
+    # The step after the backward: one fused AdamW update of the training adapter of
+    # every projection (not part of `value`).  HBM bytes per updated element: gradient,
+    # master, m and v read (16), master, m and v written (12), bf16 copy written (2).
+    extras = None
+    if not args.no_extras and bf:
+        hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
+        opt = []
+        for p, proj in enumerate(w.projections):
+            d = P[p]
+            st = [d["A"].float(), d["B"].float()]
+            opt.append(st + [torch.zeros_like(st[0]), torch.zeros_like(st[0]),
+                             torch.zeros_like(st[1]), torch.zeros_like(st[1])])
+        torch.cuda.synchronize()
+
+        def opt_step(t):
+            for p, proj in enumerate(w.projections):
+                d, o = P[p], opt[p]
+                dsv.adamw_step(probe_dev, t, d["dA"], d["dB"], o[0], o[1], o[2], o[3], o[4], o[5],
+                               A=d["A"], B=d["B"], stream=stream, **hp)
+        probe_dev = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device=dev)
+        for t in range(1, 6):
+            opt_step(t)
+        torch.cuda.synchronize()
+        n_opt = 50
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for t in range(6, 6 + n_opt):
+            opt_step(t)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / n_opt
+        tr = [a for a in range(w.n_adapters) if any(s[2] == a and s[3] and s[1] for s in w.segments)]
+        elems = sum(int(w.ranks[a]) * (proj.K + proj.N) for a in tr for proj in w.projections)
+        nbytes = 30 * elems
+        extras = {"adamw": {"kernel": "adamw_kernel (fused AdamW of the training adapters' A and B)",
+                            "launches_per_step": len(w.projections), "us_per_step": round(us, 2),
+                            "bytes_per_step": nbytes, "achieved_GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                            "peak_GBps": 8000.0, "frac": round(nbytes / (us * 1e-6) / 8e12, 4),
+                            "bound": "hbm (at these sizes: launch latency)"}}
+        log("adamw: %.2f us per step (%d launches), %.1f GB/s" % (us, len(w.projections),
+                                                                  nbytes / (us * 1e-6) / 1e9))
+
+        # Residual-only retention: the backward of every projection with h recomputed
+        # from X (H_save not kept) against the backward that reads the kept H_save.
+        def bwd_all(keep):
+            for p, proj in enumerate(w.projections):
+                d = P[p]
+                dsv.lora_bwd(probe_dev, d["X"], d["W"], d["A"], d["B"], d["H"] if keep else None, d["dY"],
+                             dA=d["dA"], dB=d["dB"], dX=d["dX"], workspace=d["wsb"], stream=stream)
+        bt = {}
+        for keep in (True, False, True, False):
+            bwd_all(keep)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(10):
+                bwd_all(keep)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            bt[keep] = e0.elapsed_time(e1) * 1e3 / 10
+        extras["recompute_h"] = {"bwd_us_per_step_kept_h": round(bt[True], 2),
+                                 "bwd_us_per_step_recomputed_h": round(bt[False], 2),
+                                 "h_bytes_not_kept_per_step": int(sum(w.train_tokens * w.r_max * 2
+                                                                      for _ in w.projections))}
+        log("backward with kept h %.1f us, with recomputed h %.1f us per step" % (bt[True], bt[False]))
+
     def cfg_str(c):
         if not c["tile_m"]:
             return None
@@ -341,6 +408,7 @@ def main():
             "gemm_launches": gemm_launches,
         },
         "cpu_baseline": cpu,
+        "extras": extras,
     }
     print(json.dumps(out), flush=True)
 

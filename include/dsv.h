@@ -153,9 +153,11 @@ int dsv_cobatch_fwd_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, 
 /*
  * dsv_cobatch_fwd -- Y = X W^T + s_a (X A_a^T) B_a^T for every row, and
  * H_save = X A_a^T for the training rows (Sec. 2.2, Sec. 3.2).
- * H_save may be NULL only when the plan has no training rows.  K and N must
- * be positive multiples of 8; every pointer 16-byte aligned; workspace of at
- * least dsv_cobatch_fwd_workspace bytes, 256-byte aligned.
+ * H_save == NULL keeps nothing for the backward (residual-only retention,
+ * Sec. 3.2 "Mixed forward batch": the caller keeps X and dsv_lora_bwd
+ * recomputes h).  K and N must be positive multiples of 8; every pointer
+ * 16-byte aligned; workspace of at least dsv_cobatch_fwd_workspace bytes,
+ * 256-byte aligned.
  */
 int dsv_cobatch_fwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
                     const void* X, const void* W, const void* A, const void* B, void* Y,
@@ -178,7 +180,10 @@ int dsv_lora_bwd_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int
  * overwrites, accumulate = 1 adds to, the dA / dB slices of adapters that own
  * training rows; other slices are untouched.  The reductions over tokens are
  * deterministic (fixed-order fp32 partial sums, no atomics): repeated calls
- * give bit-identical results.  With no training rows the call is a no-op.
+ * give bit-identical results.  H_save == NULL recomputes h of the training
+ * rows from X and A first (the forward's own shrink, so the same values bit
+ * for bit; 2 T_t K r FLOP and one read of X's training rows), for a forward
+ * that kept no H_save.  With no training rows the call is a no-op.
  */
 int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
                  const void* X, const void* W, const void* A, const void* B,
@@ -201,6 +206,40 @@ int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
 int dsv_timing_enable(int32_t on);
 int dsv_timing_read(double* fwd_ms, int32_t* fwd_launches, double* bwd_ms,
                     int32_t* bwd_launches);
+
+/*
+ * dsv_adamw_step -- one fused AdamW step of the plan's training adapters
+ * (the optimizer update that follows the LoRA backward, Sec. 3.2 "Backward
+ * subprocess"; AdamW with decoupled weight decay, Sec. 4.1: lr 1e-3, weight
+ * decay 0.01).  For every adapter with training rows in the plan and every
+ * element of its A slice (rows j < r_a) and B slice (columns j < r_a):
+ *     p <- p (1 - lr wd)
+ *     m <- beta1 m + (1 - beta1) g,      v <- beta2 v + (1 - beta2) g^2
+ *     p <- p - lr m_hat / (sqrt(v_hat) + eps),
+ *          m_hat = m / (1 - beta1^step), v_hat = v / (1 - beta2^step)
+ * with g from dA / dB (as dsv_lora_bwd leaves them), then writes p rounded
+ * once (bf16: to nearest even; fp32: copied) into the parameter stacks A / B
+ * that dsv_cobatch_fwd reads.  A_master / B_master, A_m, A_v, B_m, B_v are
+ * fp32 in the dA / dB layouts ([n_ad][r_max][K], [n_ad][N][r_max]), owned by
+ * the caller (moments start at zero, masters at the fp32 value of A / B).
+ * A or B may be NULL to skip that copy.  step >= 1 is the 1-based step
+ * count.  Other adapters and rank-padding entries are neither read nor
+ * written.  Returns DSV_OK, DSV_ERR_ARG (NULL / misaligned pointer, plan not
+ * on device), DSV_ERR_RANGE (step < 1, lr or wd < 0 or not finite, beta not
+ * in [0, 1), eps <= 0), DSV_ERR_SIZE or DSV_ERR_DEVICE.
+ */
+typedef struct {
+  double lr;
+  double beta1;
+  double beta2;
+  double eps;
+  double weight_decay;
+} dsv_adamw_hparams;  /* double: 1 - beta is formed on the host before rounding to fp32 */
+
+int dsv_adamw_step(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N, int32_t step,
+                   const dsv_adamw_hparams* hp, const float* dA, const float* dB, float* A_master,
+                   float* B_master, float* A_m, float* A_v, float* B_m, float* B_v, void* A,
+                   void* B, void* hip_stream);
 
 /* GEMM launch configuration that dsv_cobatch_fwd (pass 0) or dsv_lora_bwd
  * (pass 1, the dX GEMM) uses for this plan, dtype and K x N on the current

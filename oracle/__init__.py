@@ -161,3 +161,23 @@ def rel_err(got, ref) -> float:
     if den == 0.0:
         return float(num)
     return float(num / den)
+
+
+def adamw(p, g, m, v, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01):
+    """One AdamW step in fp64 (Sec. 4.1 training configuration: AdamW, learning
+    rate 1e-3, weight decay 0.01; Sec. 3.2: the update is applied to the adapter
+    weights after the backward).  Decoupled weight decay as in Loshchilov & Hutter
+    (ICLR 2019) with the schedule multiplier equal to the learning rate:
+
+        m_t = beta1 m + (1 - beta1) g           v_t = beta2 v + (1 - beta2) g^2
+        m^  = m_t / (1 - beta1^t)                v^  = v_t / (1 - beta2^t)
+        p_t = p - lr (m^ / (sqrt(v^) + eps) + weight_decay p)
+
+    Returns (p_t, m_t, v_t) as new fp64 arrays; the inputs are not modified."""
+    p, g, m, v = (np.asarray(x, np.float64) for x in (p, g, m, v))
+    m_t = beta1 * m + (1.0 - beta1) * g
+    v_t = beta2 * v + (1.0 - beta2) * g * g
+    m_hat = m_t / (1.0 - beta1 ** step)
+    v_hat = v_t / (1.0 - beta2 ** step)
+    p_t = p - lr * (m_hat / (np.sqrt(v_hat) + eps) + weight_decay * p)
+    return p_t, m_t, v_t

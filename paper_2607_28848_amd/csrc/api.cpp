@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstring>
 
 #include "kernels.h"
@@ -89,7 +90,7 @@ struct FwdWs {
   size_t h_all, delta, sk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, part_b, part_a, sk_part, total;
+  size_t bt, g, hrec, part_b, part_a, sk_part, total;
 };
 
 // Split-tile scratch of a GEMM plan: one fp32 partial tile per piece.
@@ -125,6 +126,8 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     off = align256(off + (size_t)p.n_tads * p.r_max * N * 2);
     w.g = off;
     off = align256(off + (size_t)p.T_t * ld_rank(p.r_max) * 2);
+    w.hrec = off;  // h of the training rows, recomputed when H_save is not kept
+    off = align256(off + (size_t)p.T_t * ld_rank(p.r_max) * 2);
     w.part_b = off;
     off = align256(off + (size_t)p.n_chunks * N * p.r_max * 4);
     w.part_a = off;
@@ -132,6 +135,8 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     off = carve_sk(gp, off, &w.sk_part);
   } else {
     w.g = off;
+    off = align256(off + (size_t)p.T_t * p.r_max * 4);
+    w.hrec = off;
     off = align256(off + (size_t)p.T_t * p.r_max * 4);
   }
   w.total = off;
@@ -226,6 +231,53 @@ extern "C" int dsv_timing_read(double* fwd_ms, int32_t* fwd_n, double* bwd_ms, i
   return rc;
 }
 
+extern "C" int dsv_adamw_step(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, int32_t step,
+                              const dsv_adamw_hparams* hp, const float* dA, const float* dB, float* A_master,
+                              float* B_master, float* A_m, float* A_v, float* B_m, float* B_v, void* A,
+                              void* B, void* hip_stream) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  if (!p->d_meta || !hp) return DSV_ERR_ARG;
+  if (step < 1 || !std::isfinite(hp->lr) || hp->lr < 0.0 || !std::isfinite(hp->weight_decay) ||
+      hp->weight_decay < 0.0 || !(hp->beta1 >= 0.0 && hp->beta1 < 1.0) ||
+      !(hp->beta2 >= 0.0 && hp->beta2 < 1.0) || !(hp->eps > 0.0) || !std::isfinite(hp->eps))
+    return DSV_ERR_RANGE;
+  if (!ptr_ok(dA) || !ptr_ok(dB) || !ptr_ok(A_master) || !ptr_ok(B_master) || !ptr_ok(A_m) ||
+      !ptr_ok(A_v) || !ptr_ok(B_m) || !ptr_ok(B_v) || (A && !aligned16(A)) || (B && !aligned16(B)))
+    return DSV_ERR_ARG;
+  if (p->n_tads == 0) return DSV_OK;
+  AdamWArgs a{};
+  a.K = K;
+  a.N = N;
+  a.r_max = p->r_max;
+  a.train_ads = p->dptr(p->lay.train_ads);
+  a.ranks = p->dptr(p->lay.ranks);
+  // factors formed in double on the host, rounded once to fp32
+  const double bc1 = 1.0 - std::pow(hp->beta1, (double)step);
+  const double bc2 = 1.0 - std::pow(hp->beta2, (double)step);
+  a.decay = (float)(1.0 - hp->lr * hp->weight_decay);
+  a.b1 = (float)hp->beta1;
+  a.b2 = (float)hp->beta2;
+  a.c1 = (float)(1.0 - hp->beta1);
+  a.c2 = (float)(1.0 - hp->beta2);
+  a.eps = (float)hp->eps;
+  a.step_size = (float)(hp->lr / bc1);
+  a.sqrt_bc2 = (float)std::sqrt(bc2);
+  a.dA = dA;
+  a.dB = dB;
+  a.pA = A_master;
+  a.pB = B_master;
+  a.mA = A_m;
+  a.vA = A_v;
+  a.mB = B_m;
+  a.vB = B_v;
+  a.A = A;
+  a.B = B;
+  a.bf16 = dt == DSV_BF16;
+  return launch_adamw(a, p->n_tads, static_cast<hipStream_t>(hip_stream)) == hipSuccess ? DSV_OK
+                                                                                       : DSV_ERR_DEVICE;
+}
+
 extern "C" int dsv_gemm_config(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, int32_t pass,
                                int32_t out[6]) {
   int rc = check_common(p, dt, K, N);
@@ -269,7 +321,7 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   if (!p->d_meta) return DSV_ERR_ARG;
   if (p->T == 0) return DSV_OK;  // empty batch: nothing to read or write
   if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(Y)) return DSV_ERR_ARG;
-  if (p->T_t > 0 && !ptr_ok(H_save)) return DSV_ERR_ARG;
+  if (H_save && !aligned16(H_save)) return DSV_ERR_ARG;
   const GemmPlan gp = fwd_gemm_plan(*p, dt, K, N);
   const FwdWs ws = fwd_ws(*p, dt, N, gp);
   if (ws.total > 0) {
@@ -298,7 +350,7 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
     a.A = static_cast<const float*>(A);
     a.B = static_cast<const float*>(B);
     a.Y = static_cast<float*>(Y);
-    a.Hsave = static_cast<float*>(H_save);
+    a.Hsave = p->T_t > 0 ? static_cast<float*>(H_save) : nullptr;
     a.Hall = at<float>(workspace, ws.h_all);
     e = launch_f32_fwd(a, s);
     return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
@@ -323,7 +375,7 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   sk.C = K;
   sk.out1 = h_all;
   sk.ld1 = ldh;
-  sk.out2 = static_cast<uint16_t*>(H_save);
+  sk.out2 = p->T_t > 0 ? static_cast<uint16_t*>(H_save) : nullptr;
   sk.ld2 = p->r_max;
   sk.row_train = p->dptr(L.row_train);
   if ((e = launch_shrink(sk, p->n_shrink, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
@@ -378,7 +430,7 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(dA) || !ptr_ok(dB))
     return DSV_ERR_ARG;
   if (dX && !aligned16(dX)) return DSV_ERR_ARG;
-  if (p->T_t > 0 && (!ptr_ok(H_save) || !ptr_ok(dY))) return DSV_ERR_ARG;
+  if (!ptr_ok(dY) || (H_save && !aligned16(H_save))) return DSV_ERR_ARG;
   const GemmPlan gp = bwd_gemm_plan(*p, dt, K, N);
   const BwdWs ws = bwd_ws(*p, dt, K, N, gp);
   if (ws.total > 0) {
@@ -412,6 +464,7 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     a.A = static_cast<const float*>(A);
     a.B = static_cast<const float*>(B);
     a.Hs = static_cast<const float*>(H_save);
+    a.Hrec = at<float>(workspace, ws.hrec);
     a.dY = static_cast<const float*>(dY);
     a.G = at<float>(workspace, ws.g);
     a.dA = dA;
@@ -452,13 +505,40 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   sk.out2 = nullptr;
   if ((e = launch_gmat(sk, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
+  // 2b. H_save not kept (residual-only retention): recompute h of the training
+  //     rows from X with the forward's shrink (same values, bit for bit).
+  const uint16_t* hs = static_cast<const uint16_t*>(H_save);
+  int64_t ldhs = p->r_max;
+  if (!hs) {
+    uint16_t* hrec = at<uint16_t>(workspace, ws.hrec);
+    SkinnyArgs sh{};
+    sh.P = static_cast<const uint16_t*>(X);
+    sh.ldp = K;
+    sh.rows = p->dptr(L.train_rows);
+    sh.items = p->dptr(L.train_items);
+    sh.Q = static_cast<const uint16_t*>(A);
+    sh.q_ad = (int64_t)p->r_max * K;
+    sh.ldq = K;
+    sh.qsel = nullptr;
+    sh.ranks = ranks;
+    sh.scales = nullptr;
+    sh.C = K;
+    sh.out1 = nullptr;
+    sh.out2 = hrec;
+    sh.ld2 = ldh;
+    sh.row_train = p->dptr(L.row_train);
+    if ((e = launch_shrink_train(sh, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
+    hs = hrec;
+    ldhs = ldh;
+  }
+
   // 3. per-chunk fp32 partials of dy^T h (-> dB) and x^T g (-> dA).
   TokenReduceArgs tb{};
   tb.P = static_cast<const uint16_t*>(dY);
   tb.ldp = N;
   tb.prow = nullptr;
-  tb.Q = static_cast<const uint16_t*>(H_save);
-  tb.ldq = p->r_max;
+  tb.Q = hs;
+  tb.ldq = ldhs;
   tb.chunks = p->dptr(L.chunks);
   tb.ranks = ranks;
   tb.C = N;

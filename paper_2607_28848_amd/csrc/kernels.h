@@ -57,7 +57,7 @@ struct SkinnyArgs {
   const float* scales;   // nullptr: scale 1
   int32_t C;
   // outputs (mode-dependent)
-  uint16_t* out1;        // [rows][ld1]
+  uint16_t* out1;        // [rows][ld1] (shrink: nullptr = not written)
   int64_t ld1;
   uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train (nullptr: none)
   int64_t ld2;
@@ -86,6 +86,8 @@ hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
 hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
+// shrink over items of <= 16 rows (the training items): recomputes h for the backward
+hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
                                 int32_t r_max, const int32_t* items, int32_t n_items,
                                 const int32_t* gather_rows, const int32_t* ranks,
@@ -97,6 +99,24 @@ hipError_t launch_reduce_out(const float* part, int32_t C, int32_t r_max, const 
                              int32_t accumulate, float* out, hipStream_t s);
 hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
                               int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
+
+// Fused AdamW step of the training adapters' A and B slices (fp32 master
+// weights and moments in the A / B layouts; the parameter copy A / B is bf16
+// when bf16 != 0, fp32 otherwise, or not written when nullptr).
+struct AdamWArgs {
+  int32_t K, N, r_max;
+  const int32_t* train_ads;  // training adapters (device)
+  const int32_t* ranks;
+  float decay;               // 1 - lr * wd
+  float b1, b2, c1, c2, eps; // beta1, beta2, 1 - beta1, 1 - beta2
+  float step_size;           // lr / (1 - b1^t)
+  float sqrt_bc2;            // sqrt(1 - b2^t)
+  const float *dA, *dB;
+  float *pA, *pB, *mA, *vA, *mB, *vB;
+  void *A, *B;
+  int32_t bf16;
+};
+hipError_t launch_adamw(const AdamWArgs& a, int32_t n_tads, hipStream_t s);
 
 // Launchers (fp32 mode: plain FMA kernels, same semantics).
 struct F32Args {
@@ -114,6 +134,7 @@ struct F32Args {
   const float* scales;
   const float *X, *W, *A, *B, *Hs, *dY;
   float *Y, *Hsave, *Hall, *G, *dA, *dB, *dX;
+  float* Hrec;   // backward with Hs == nullptr: h of the training rows recomputed here
   int32_t accumulate;
 };
 hipError_t launch_f32_fwd(const F32Args& a, hipStream_t s);

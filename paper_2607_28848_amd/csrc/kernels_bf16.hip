@@ -587,7 +587,7 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
       const int pr = g.rows ? g.rows[begin + row] : begin + row;
       if (MODE == 0) {
         const uint16_t hb = f2bf(sum);
-        g.out1[(int64_t)pr * g.ld1 + j] = hb;
+        if (g.out1) g.out1[(int64_t)pr * g.ld1 + j] = hb;
         if (g.out2) {
           const int tr = g.row_train[pr];
           if (tr >= 0) g.out2[(int64_t)tr * g.ld2 + j] = hb;
@@ -841,6 +841,10 @@ hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hi
 
 hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   return launch_skinny<1, kItemRows>(a, n_items, r_max, s);
+}
+
+hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
+  return launch_skinny<0, kItemRows>(a, n_items, r_max, s);
 }
 
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,

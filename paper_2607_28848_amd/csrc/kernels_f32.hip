@@ -23,7 +23,22 @@ __global__ void f32_shrink(F32Args g) {
   for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], Aj[k], acc);
   g.Hall[(int64_t)t * g.r_max + j] = acc;
   const int tr = g.row_train[t];
-  if (tr >= 0) g.Hsave[(int64_t)tr * g.r_max + j] = acc;
+  if (tr >= 0 && g.Hsave) g.Hsave[(int64_t)tr * g.r_max + j] = acc;
+}
+
+// Backward without a kept H_save: h of the training rows again, in the same
+// order of operations as f32_shrink (so the same values).
+__global__ void f32_hrec(F32Args g) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int i = (int)(idx / g.r_max), j = (int)(idx % g.r_max);
+  if (i >= g.Tt) return;
+  const int a = g.train_adapter[i];
+  if (j >= g.ranks[a]) return;
+  const float* x = g.X + (int64_t)g.train_rows[i] * g.K;
+  const float* Aj = g.A + ((int64_t)a * g.r_max + j) * g.K;
+  float acc = 0.f;
+  for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], Aj[k], acc);
+  g.Hrec[(int64_t)i * g.r_max + j] = acc;
 }
 
 // y = x W^T + s_a h B_a^T, fp32 sum, one store.
@@ -123,10 +138,17 @@ hipError_t launch_f32_fwd(const F32Args& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_f32_bwd(const F32Args& a, hipStream_t s) {
-  if (a.Tt <= 0) return hipSuccess;
+hipError_t launch_f32_bwd(const F32Args& a0, hipStream_t s) {
+  if (a0.Tt <= 0) return hipSuccess;
+  F32Args a = a0;
+  hipError_t e;
+  if (!a.Hs) {
+    hipLaunchKernelGGL(f32_hrec, dim3(blocks((int64_t)a.Tt * a.r_max)), dim3(256), 0, s, a);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+    a.Hs = a.Hrec;
+  }
   hipLaunchKernelGGL(f32_gmat, dim3(blocks((int64_t)a.Tt * a.r_max)), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(f32_db, dim3(blocks((int64_t)a.N * a.r_max), a.n_tads), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;

@@ -71,6 +71,13 @@ _lib.dsv_timing_enable.restype = ctypes.c_int
 _lib.dsv_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), _i32p,
                                  ctypes.POINTER(ctypes.c_double), _i32p]
 _lib.dsv_timing_read.restype = ctypes.c_int
+class AdamWHparams(ctypes.Structure):
+    _fields_ = [("lr", ctypes.c_double), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("weight_decay", ctypes.c_double)]
+
+
+_lib.dsv_adamw_step.argtypes = [_vp, ctypes.c_int, _i32, _i32, _i32, ctypes.POINTER(AdamWHparams)] + [_vp] * 11
+_lib.dsv_adamw_step.restype = ctypes.c_int
 _lib.dsv_gemm_config.argtypes = [_vp, ctypes.c_int, _i32, _i32, _i32, _i32p]
 _lib.dsv_gemm_config.restype = ctypes.c_int
 _lib.dsv_status_string.argtypes = [ctypes.c_int]
@@ -209,15 +216,17 @@ def _workspace(nbytes, device, given):
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
 
 
-def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, stream=None):
-    """Y = X W^T + s_a (X A_a^T) B_a^T per row; H_save = X A_a^T of the training rows."""
+def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, stream=None,
+                keep_h: bool = True):
+    """Y = X W^T + s_a (X A_a^T) B_a^T per row; H_save = X A_a^T of the training rows
+    (keep_h=False keeps none: lora_bwd with H_save=None recomputes it from X)."""
     import torch
     dt = _dtype_code(X)
     T, K = X.shape
     N = W.shape[0]
     if Y is None:
         Y = torch.empty((T, N), dtype=X.dtype, device=X.device)
-    if H_save is None and plan.train_tokens > 0:
+    if H_save is None and plan.train_tokens > 0 and keep_h:
         H_save = torch.empty((plan.train_tokens, plan.r_max), dtype=X.dtype, device=X.device)
     ws = _workspace(fwd_workspace_bytes(plan, dt, K, N), X.device, workspace)
     _check(_lib.dsv_cobatch_fwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y),
@@ -246,6 +255,23 @@ def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want
                              1 if accumulate else 0, _ptr(ws), ws.numel() * ws.element_size(),
                              _stream_handle(stream)), "dsv_lora_bwd")
     return dA, dB, dX
+
+
+def adamw_step(plan: Plan, step: int, dA, dB, A_master, B_master, A_m, A_v, B_m, B_v, A=None, B=None,
+               lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01, stream=None):
+    """One fused AdamW step of the plan's training adapters (dsv_adamw_step); updates
+    the fp32 masters and moments in place and writes the rounded copy into A / B."""
+    import torch
+    K = A_master.shape[2]
+    N = B_master.shape[1]
+    ref = A if A is not None else A_master
+    code = BF16 if ref.dtype == torch.bfloat16 else F32
+    hp = AdamWHparams(lr, beta1, beta2, eps, weight_decay)
+    ptr = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    _check(_lib.dsv_adamw_step(plan.handle, code, K, N, step, ctypes.byref(hp), ptr(dA), ptr(dB),
+                               ptr(A_master), ptr(B_master), ptr(A_m), ptr(A_v), ptr(B_m), ptr(B_v),
+                               ptr(A), ptr(B), _stream_handle(stream)),
+           "dsv_adamw_step")
 
 
 GEMM_CONFIG_NAMES = ("tile_m", "tile_n", "row_tiles", "col_tiles", "split_tiles", "split_ways")

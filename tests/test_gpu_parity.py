@@ -110,6 +110,25 @@ def test_split_tiles_ragged():
                dx_rows=dx_rows.astype(np.int32))
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_residual_only_retention_recomputes_h_bit_exact(dtype):
+    """A forward that keeps no H_save (the caller keeps X) and a backward that
+    recomputes h from X and A give bit-identical Y, dA, dB and dX to keeping H_save
+    (the recompute is the forward's own shrink over the training rows)."""
+    import torch
+    w = wl.custom(MIXED, MIXED_RANKS, K=520, N=776, dtype=dtype, r_max=64, name="recompute")
+    run = Run(w)
+    Y1, H = run.fwd()
+    dA1, dB1, dX1 = run.bwd(H)
+    Y2, H2 = run.dsv.cobatch_fwd(run.plan, run.X, run.W, run.A, run.B, keep_h=False)
+    assert H2 is None
+    dA2, dB2, dX2 = run.bwd(None)
+    torch.cuda.synchronize()
+    bits = lambda t: t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)  # noqa: E731
+    for a, b in ((Y1, Y2), (dA1, dA2), (dB1, dB2), (dX1, dX2)):
+        assert torch.equal(bits(a), bits(b))
+
+
 def test_mixed_f32_ragged():
     w = wl.custom(MIXED, MIXED_RANKS, K=136, N=200, dtype="f32", r_max=64, name="mixed_f32")
     _full(w, tol=TOL_F32)

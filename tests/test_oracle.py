@@ -272,3 +272,64 @@ def test_bf16_rounding_is_nearest_even():
         cands = np.array([np.floor(m * 256), np.ceil(m * 256)]) * 2.0 ** (e - 8)
         d = np.abs(cands - xi)
         assert vi in cands and abs(vi - xi) == d.min()
+
+
+# ---------------------------------------------------------------------------
+# AdamW step of the training adapter (Sec. 4.1 training configuration)
+# ---------------------------------------------------------------------------
+HP = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
+
+
+def test_adamw_first_step_closed_form():
+    """From zero moments the bias-corrected moments of step 1 are g and g^2, so the
+    step is p (1 - lr wd) - lr g / (|g| + eps): nearly lr * sign(g) off the decay."""
+    rng = np.random.default_rng(11)
+    p, g = rng.normal(size=1000), rng.normal(size=1000) * 1e-2
+    z = np.zeros(1000)
+    p1, m1, v1 = oracle.adamw(p, g, z, z, 1, **HP)
+    lr, wd, eps = HP["lr"], HP["weight_decay"], HP["eps"]
+    np.testing.assert_allclose(p1, p * (1 - lr * wd) - lr * g / (np.abs(g) + eps), rtol=0, atol=1e-15)
+    np.testing.assert_allclose(m1, (1 - HP["beta1"]) * g, rtol=1e-15)
+    np.testing.assert_allclose(v1, (1 - HP["beta2"]) * g * g, rtol=1e-15)
+
+
+def test_adamw_constant_gradient_bias_correction():
+    """For a constant gradient the bias-corrected moments equal g and g^2 at every
+    step (m_t = (1 - b1^t) g), so each step moves p by the same lr g / (|g| + eps)
+    on top of the decay."""
+    rng = np.random.default_rng(12)
+    p0, g = rng.normal(size=500), rng.normal(size=500)
+    p, m, v = p0.copy(), np.zeros(500), np.zeros(500)
+    expect = p0.copy()
+    lr, wd, eps = HP["lr"], HP["weight_decay"], HP["eps"]
+    for t in range(1, 21):
+        p, m, v = oracle.adamw(p, g, m, v, t, **HP)
+        expect = expect * (1 - lr * wd) - lr * g / (np.abs(g) + eps)
+    np.testing.assert_allclose(p, expect, rtol=0, atol=1e-13)
+
+
+def test_adamw_zero_gradient_is_pure_decay():
+    p0 = np.linspace(-1, 1, 101)
+    p, m, v = p0.copy(), np.zeros(101), np.zeros(101)
+    for t in range(1, 8):
+        p, m, v = oracle.adamw(p, np.zeros(101), m, v, t, **HP)
+    np.testing.assert_allclose(p, p0 * (1 - HP["lr"] * HP["weight_decay"]) ** 7, rtol=1e-15, atol=0)
+    assert not m.any() and not v.any()
+
+
+def test_adamw_matches_torch_optimizer_fp64():
+    """Five steps with varying gradients against torch.optim.AdamW (decoupled weight
+    decay) in float64 on the CPU, an implementation independent of the oracle."""
+    import torch
+    rng = np.random.default_rng(13)
+    p0 = rng.normal(size=(16, 64))
+    grads = [rng.normal(size=(16, 64)) * 10.0 ** rng.uniform(-4, 0) for _ in range(5)]
+    t = torch.tensor(p0, dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.AdamW([t], lr=HP["lr"], betas=(HP["beta1"], HP["beta2"]), eps=HP["eps"],
+                            weight_decay=HP["weight_decay"])
+    p, m, v = p0.copy(), np.zeros_like(p0), np.zeros_like(p0)
+    for k, g in enumerate(grads, start=1):
+        t.grad = torch.tensor(g, dtype=torch.float64)
+        opt.step()
+        p, m, v = oracle.adamw(p, g, m, v, k, **HP)
+    np.testing.assert_allclose(p, t.detach().numpy(), rtol=1e-13, atol=1e-16)
