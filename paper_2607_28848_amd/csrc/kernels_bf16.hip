@@ -191,50 +191,96 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   const uint16_t* b_base = NN ? g.Q + n0 : g.Q + (int64_t)n0 * g.ldq;
   const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
 
-  // Direct-to-LDS loads of K-step kt into stage `stage`.  With 8 or more
-  // accumulator tiles per wave the per-lane offsets are recomputed here from
-  // the lane id, read afresh so that the compiler cannot hoist them: held in
-  // registers across the main loop they would be spilled.  Smaller tiles keep
-  // them in registers.
+  // Direct-to-LDS loads of K-step kt into stage `stage`.
+  //
+  // Large tiles (8+ accumulator tiles per wave, all loads issued by waves
+  // 0..LW-1, 8+ loads of each operand per wave): the per-lane offsets are
+  // recomputed here from a freshly read lane id -- held in registers across
+  // the main loop they would be spilled -- in a form that costs a few VALU
+  // operations per load.  With q = wave * LOADS + i, LOADS a multiple of 8:
+  //   K-contiguous tile (8 rows of 64 per 1 KiB load): row = 8q + ln/8 and the
+  //     chunk swizzle is (ln%8) ^ (ln/8) ^ (i%8), so the lane part is fixed
+  //     and i only selects a constant XOR;
+  //   N-contiguous dX weight tile (2 rows of 256 per load): n = 2q + ln/32 and
+  //     the slot swizzle is (ln%32) ^ 2(ln/32) ^ 4(i%2).
+  // Only the last, partial K-step checks the contraction bound per lane.
+  // Other tiles keep the offsets in registers.
   auto issue = [&](int kt, int stage) {
     if (LW < NW && wave >= LW) return;
-    int ln = lane;
-    if constexpr (FM * FN >= 8)
-      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
     const int k0 = kt * TK;
     char* sa = smem + stage * S::STAGE;
     char* sb = sa + S::A_BYTES;
     // descriptors rebased on the K-step keep every offset well inside 32 bits
     const i32x4 ra = make_rsrc(a_base + k0, (uint64_t)(a_rows * g.ldp - k0) * 2);
+    constexpr bool kFast = FM * FN >= 8 && TK == 64 && A_LOADS % 8 == 0 && B_LOADS % 8 == 0 && (!NN || TN == 256);
+    if (kFast && k0 + TK <= g.C) {  // every K-step but a partial last one
+      int ln;
+      asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+      const int lr = ln >> 3, x16 = ((ln & 7) ^ lr) << 4;
+      const int lpa = lr * (int)g.ldp * 2;
 #pragma unroll
-    for (int i = 0; i < A_LOADS; ++i) {
-      const int q = wave * A_LOADS + i;
-      const int row = q * (1024 / ROWB) + ln / CPR;
-      const int c = (ln % CPR) ^ swz<TK>(row);
-      const int vo = (k0 + 8 * c < g.C) ? (row * (int)g.ldp + 8 * c) * 2 : (int)0x7FFFFFF0;
-      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
-    }
-    if constexpr (!NN) {
-      const i32x4 rb = make_rsrc(b_base + k0, (uint64_t)(b_cols * g.ldq - k0) * 2);
+      for (int i = 0; i < A_LOADS; ++i) {
+        const int q = wave * A_LOADS + i;
+        const int sq = __builtin_amdgcn_readfirstlane(q * 16 * (int)g.ldp);  // row block: scalar
+        llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, (x16 ^ ((i & 7) << 4)) + lpa + sq,
+                                        0, 0, 0);
+      }
+      if constexpr (!NN) {
+        const i32x4 rb = make_rsrc(b_base + k0, (uint64_t)(b_cols * g.ldq - k0) * 2);
+        const int lpb = lr * (int)g.ldq * 2;
 #pragma unroll
-      for (int i = 0; i < B_LOADS; ++i) {
-        const int q = wave * B_LOADS + i;
-        const int col = q * (1024 / ROWB) + ln / CPR;
-        const int c = (ln % CPR) ^ swz<TK>(col);
-        const int vo = (k0 + 8 * c < g.C) ? (col * (int)g.ldq + 8 * c) * 2 : (int)0x7FFFFFF0;
-        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
+        for (int i = 0; i < B_LOADS; ++i) {
+          const int q = wave * B_LOADS + i;
+          const int sq = __builtin_amdgcn_readfirstlane(q * 16 * (int)g.ldq);
+          llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, (x16 ^ ((i & 7) << 4)) + lpb + sq,
+                                          0, 0, 0);
+        }
+      } else {
+        const i32x4 rb = make_rsrc(b_base + (int64_t)k0 * g.ldq, (uint64_t)((int64_t)TK * g.ldq - n0) * 2);
+        const int h = ln >> 5, y16 = ((ln & 31) ^ (2 * h)) << 4;
+        const int lpb = h * (int)g.ldq * 2;
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+          const int q = wave * B_LOADS + i;
+          const int sq = __builtin_amdgcn_readfirstlane(q * 4 * (int)g.ldq);
+          llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, (y16 ^ ((i & 1) << 6)) + lpb + sq,
+                                          0, 0, 0);
+        }
       }
     } else {
-      // the TK contraction rows of this K-step (fewer at the tail)
-      const i32x4 rb = make_rsrc(b_base + (int64_t)k0 * g.ldq,
-                                 (uint64_t)((int64_t)min(TK, g.C - k0) * g.ldq - n0) * 2);
+      int ln = lane;
+      if constexpr (kFast)
+        asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
 #pragma unroll
-      for (int i = 0; i < B_LOADS; ++i) {
-        const int q = wave * B_LOADS + i;
-        const int byte = q * 1024 + 16 * ln;
-        const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
-        const int vo = (k0 + n < g.C) ? (n * (int)g.ldq + 8 * (slot ^ nn_swz(n))) * 2 : (int)0x7FFFFFF0;
-        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
+      for (int i = 0; i < A_LOADS; ++i) {
+        const int q = wave * A_LOADS + i;
+        const int row = q * (1024 / ROWB) + ln / CPR;
+        const int c = (ln % CPR) ^ swz<TK>(row);
+        const int vo = (k0 + 8 * c < g.C) ? (row * (int)g.ldp + 8 * c) * 2 : (int)0x7FFFFFF0;
+        llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
+      }
+      if constexpr (!NN) {
+        const i32x4 rb = make_rsrc(b_base + k0, (uint64_t)(b_cols * g.ldq - k0) * 2);
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+          const int q = wave * B_LOADS + i;
+          const int col = q * (1024 / ROWB) + ln / CPR;
+          const int c = (ln % CPR) ^ swz<TK>(col);
+          const int vo = (k0 + 8 * c < g.C) ? (col * (int)g.ldq + 8 * c) * 2 : (int)0x7FFFFFF0;
+          llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
+        }
+      } else {
+        // the TK contraction rows of this K-step (fewer at the tail)
+        const i32x4 rb = make_rsrc(b_base + (int64_t)k0 * g.ldq,
+                                   (uint64_t)((int64_t)min(TK, g.C - k0) * g.ldq - n0) * 2);
+#pragma unroll
+        for (int i = 0; i < B_LOADS; ++i) {
+          const int q = wave * B_LOADS + i;
+          const int byte = q * 1024 + 16 * ln;
+          const int n = byte / (TN * 2), slot = (byte % (TN * 2)) / 16;
+          const int vo = (k0 + n < g.C) ? (n * (int)g.ldq + 8 * (slot ^ nn_swz(n))) * 2 : (int)0x7FFFFFF0;
+          llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sb + q * 1024), 16, vo, 0, 0, 0);
+        }
       }
     }
   };
