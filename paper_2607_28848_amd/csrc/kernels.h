@@ -62,7 +62,12 @@ struct SkinnyArgs {
   uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train (nullptr: none)
   int64_t ld2;
   const int32_t* row_train;
+  float* part;           // fp32 chunk sums when the contraction is split
 };
+
+// Contraction chunks the rank-r contractions use for contraction length C:
+// the launch needs part = chunks * n_items * rows * 64 floats when it is > 1.
+int skinny_chunks(int32_t C, int32_t r_max);
 
 // Per-chunk fp32 partial sums over training tokens:
 //   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Q[t][j]

@@ -561,6 +561,27 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs g) {
 // ---------------------------------------------------------------------------
 constexpr int SW = 8;  // waves per rank-contraction workgroup
 
+// Final value of one entry (item row `row`, rank column j) from its fp32 sum.
+template <int MODE>
+__device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int begin, int row, int j, float sum) {
+  const int pr = g.rows ? g.rows[begin + row] : begin + row;
+  if (MODE == 0) {
+    const uint16_t hb = f2bf(sum);
+    if (g.out1) g.out1[(int64_t)pr * g.ld1 + j] = hb;
+    if (g.out2) {
+      const int tr = g.row_train[pr];
+      if (tr >= 0) g.out2[(int64_t)tr * g.ld2 + j] = hb;
+    }
+  } else {
+    const float s = g.scales ? g.scales[a] : 1.f;
+    g.out1[(int64_t)pr * g.ld1 + j] = f2bf(s * sum);
+  }
+}
+
+// blockIdx.y = chunk of the contraction (gridDim.y chunks of whole 64-wide
+// slices).  One chunk: the item's values are finished here.  Several: each
+// chunk's fp32 sums go to g.part, and skinny_reduce_kernel adds the chunks in
+// order and finishes them.
 template <int MODE, int NJ, int ROWS>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
 __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
   constexpr int U = NJ <= 2 ? 4 : 2;
@@ -588,14 +609,16 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
   // a wave takes 64-wide slices (two 32-wide MFMA steps), so each row is read
   // in whole 128-byte lines
   const int nslices = (g.C + 63) / 64;
-  for (int s0 = wave; s0 < nslices; s0 += SW * U) {
+  const int s_lo = (int)((int64_t)blockIdx.y * nslices / gridDim.y);
+  const int s_hi = (int)((int64_t)(blockIdx.y + 1) * nslices / gridDim.y);
+  for (int s0 = s_lo + wave; s0 < s_hi; s0 += SW * U) {
     u32x4 av[U][2][RT], bv[U][2][NJ];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int k = (s0 + SW * u) * 64 + 32 * h + 8 * (lane >> 4);
-        const bool kin = k < g.C;
+        const bool kin = s0 + SW * u < s_hi && k < g.C;
 #pragma unroll
         for (int t = 0; t < RT; ++t) av[u][h][t] = (prow[t] >= 0 && kin) ? ld16(pp[t] + k) : zero4();
 #pragma unroll
@@ -621,7 +644,6 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) red[wave][16 * t + 4 * (lane >> 4) + v][16 * jt + (lane & 15)] = acc[t][jt][v];
   __syncthreads();
-  const float s = g.scales ? g.scales[a] : 1.f;
 #pragma unroll
   for (int q = 0; q < (ROWS * 64 + 64 * SW - 1) / (64 * SW); ++q) {
     const int idx = tid + 64 * SW * q;
@@ -630,18 +652,26 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
       float sum = 0.f;
 #pragma unroll
       for (int w = 0; w < SW; ++w) sum += red[w][row][j];
-      const int pr = g.rows ? g.rows[begin + row] : begin + row;
-      if (MODE == 0) {
-        const uint16_t hb = f2bf(sum);
-        if (g.out1) g.out1[(int64_t)pr * g.ld1 + j] = hb;
-        if (g.out2) {
-          const int tr = g.row_train[pr];
-          if (tr >= 0) g.out2[(int64_t)tr * g.ld2 + j] = hb;
-        }
-      } else {
-        g.out1[(int64_t)pr * g.ld1 + j] = f2bf(s * sum);
-      }
+      if (gridDim.y == 1)
+        skinny_store<MODE>(g, a, begin, row, j, sum);
+      else
+        g.part[(((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * ROWS + row) * 64 + j] = sum;
     }
+  }
+}
+
+// Chunk sums of a split contraction, added in chunk order, then finished.
+template <int MODE, int ROWS>
+__global__ __launch_bounds__(256) void skinny_reduce_kernel(SkinnyArgs g, int32_t chunks) {
+  const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
+  const int a = it[0], begin = it[1], cnt = it[2];
+  const int r = g.ranks[a];
+  for (int idx = threadIdx.x; idx < ROWS * 64; idx += 256) {
+    const int row = idx >> 6, j = idx & 63;
+    if (row >= cnt || j >= r) continue;
+    float sum = 0.f;
+    for (int c = 0; c < chunks; ++c) sum += g.part[(((int64_t)c * gridDim.x + blockIdx.x) * ROWS + row) * 64 + j];
+    skinny_store<MODE>(g, a, begin, row, j, sum);
   }
 }
 
@@ -871,15 +901,29 @@ namespace {
 template <int MODE, int ROWS>
 hipError_t launch_skinny(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
+  const int chunks = skinny_chunks(a.C, r_max);
+  if (chunks > 1 && !a.part) return hipErrorInvalidValue;
+  const dim3 grid(n_items, chunks);
   if (r_max <= 16)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS>), grid, dim3(64 * SW), 0, s, a);
   else if (r_max <= 32)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS>), grid, dim3(64 * SW), 0, s, a);
   else
-    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS>), grid, dim3(64 * SW), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || chunks == 1) return e;
+  hipLaunchKernelGGL((skinny_reduce_kernel<MODE, ROWS>), dim3(n_items), dim3(256), 0, s, a, chunks);
   return hipGetLastError();
 }
 }  // namespace
+
+int skinny_chunks(int32_t C, int32_t r_max) {
+  // about one pass of the workgroup's waves over its slices per chunk, 1 to 4
+  // chunks: enough workgroups to cover the CUs without short chunks
+  const int per_pass = SW * (r_max <= 32 ? 4 : 2);
+  const int nsl = (C + 63) / 64;
+  return nsl / per_pass < 1 ? 1 : (nsl / per_pass > 4 ? 4 : nsl / per_pass);
+}
 
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   return launch_skinny<0, kRankItemRows>(a, n_items, r_max, s);

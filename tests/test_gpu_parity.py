@@ -110,13 +110,14 @@ def test_split_tiles_ragged():
                dx_rows=dx_rows.astype(np.int32))
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_residual_only_retention_recomputes_h_bit_exact(dtype):
+@pytest.mark.parametrize("dtype,K,N", [("bf16", 520, 776), ("f32", 520, 776), ("bf16", 4096, 4096)])
+def test_residual_only_retention_recomputes_h_bit_exact(dtype, K, N):
     """A forward that keeps no H_save (the caller keeps X) and a backward that
     recomputes h from X and A give bit-identical Y, dA, dB and dX to keeping H_save
-    (the recompute is the forward's own shrink over the training rows)."""
+    (the recompute is the forward's own shrink over the training rows; at K = 4096 both
+    split the contraction into chunks)."""
     import torch
-    w = wl.custom(MIXED, MIXED_RANKS, K=520, N=776, dtype=dtype, r_max=64, name="recompute")
+    w = wl.custom(MIXED, MIXED_RANKS, K=K, N=N, dtype=dtype, r_max=64, name="recompute")
     run = Run(w)
     Y1, H = run.fwd()
     dA1, dB1, dX1 = run.bwd(H)
@@ -127,6 +128,22 @@ def test_residual_only_retention_recomputes_h_bit_exact(dtype):
     bits = lambda t: t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)  # noqa: E731
     for a, b in ((Y1, Y2), (dA1, dA2), (dB1, dB2), (dX1, dX2)):
         assert torch.equal(bits(a), bits(b))
+
+
+def test_split_contraction_rank_kernels():
+    """K = N = 4096 with r_max 16: the shrink (over K) and g (over N) split their
+    contraction into chunks summed by a second kernel; Y and dX on sampled rows,
+    H_save, dA and dB in full."""
+    ranks = [16, 8, 16, 12, 5]
+    w = wl.custom(MIXED, ranks, K=4096, N=4096, r_max=16, name="split_rank")
+    run = Run(w, pad=np.nan)
+    Y, H = run.fwd()
+    dA, dB, dX = run.bwd(H)
+    import torch
+    torch.cuda.synchronize()
+    rows = np.unique(np.concatenate([np.arange(0, w.n_tokens, 9), [99, 100, 101, 102, 401, 402, 704]]))
+    dx_rows = np.unique(np.concatenate([np.arange(0, run.plan.train_tokens, 7), [299, 300, 428]]))
+    _check_all(w, run, Y, H, dA, dB, dX, TOL_BF16, rows=rows.astype(np.int32), dx_rows=dx_rows.astype(np.int32))
 
 
 def test_mixed_f32_ragged():
