@@ -87,10 +87,10 @@ GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C) {
 }
 
 struct FwdWs {
-  size_t h_all, delta, rpart, sk_part, total;
+  size_t h_all, delta, sk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, hrec, part_b, part_a, rpart, sk_part, total;
+  size_t bt, g, hrec, part_b, part_a, sk_part, total;
 };
 
 // Split-tile scratch of a GEMM plan: one fp32 partial tile per piece.
@@ -108,8 +108,6 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N, const GemmPlan& gp) {
     off = align256(off + (size_t)p.T * ld_rank(p.r_max) * 2);
     w.delta = off;
     off = align256(off + (size_t)p.n_gather * N * 4);
-    w.rpart = off;  // chunk sums of the shrink when its contraction is split
-    off = align256(off + (size_t)4 * p.n_shrink * kRankItemRows * 64 * 4);
     off = carve_sk(gp, off, &w.sk_part);
   } else {
     w.h_all = off;
@@ -134,8 +132,6 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     off = align256(off + (size_t)p.n_chunks * N * p.r_max * 4);
     w.part_a = off;
     off = align256(off + (size_t)p.n_chunks * K * p.r_max * 4);
-    w.rpart = off;  // chunk sums of g / the recomputed h when their contraction is split
-    off = align256(off + (size_t)4 * p.n_titems * kItemRows * 64 * 4);
     off = carve_sk(gp, off, &w.sk_part);
   } else {
     w.g = off;
@@ -382,7 +378,6 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   sk.out2 = p->T_t > 0 ? static_cast<uint16_t*>(H_save) : nullptr;
   sk.ld2 = p->r_max;
   sk.row_train = p->dptr(L.row_train);
-  sk.part = at<float>(workspace, ws.rpart);
   if ((e = launch_shrink(sk, p->n_shrink, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2. gathered rows: fp32 low-rank term, each touched adapter read once.
@@ -508,7 +503,6 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   sk.out1 = gm;
   sk.ld1 = ldh;
   sk.out2 = nullptr;
-  sk.part = at<float>(workspace, ws.rpart);
   if ((e = launch_gmat(sk, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2b. H_save not kept (residual-only retention): recompute h of the training
@@ -533,7 +527,6 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     sh.out2 = hrec;
     sh.ld2 = ldh;
     sh.row_train = p->dptr(L.row_train);
-    sh.part = at<float>(workspace, ws.rpart);
     if ((e = launch_shrink_train(sh, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
     hs = hrec;
     ldhs = ldh;
@@ -551,7 +544,6 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   tb.C = N;
   tb.r_max = p->r_max;
   tb.part = part_b;
-  if ((e = launch_token_reduce(tb, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
   TokenReduceArgs ta = tb;
   ta.P = static_cast<const uint16_t*>(X);
   ta.ldp = K;
@@ -560,16 +552,15 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   ta.ldq = ldh;
   ta.C = K;
   ta.part = part_a;
-  if ((e = launch_token_reduce(ta, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  if ((e = launch_token_reduce(tb, ta, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 4. fixed-order sums into dB (scaled by s_a) and dA.
   const int32_t* tad_ptr = p->dptr(L.tad_chunk_ptr);
   const int32_t* tad_chunks = p->dptr(L.tad_chunks);
-  if ((e = launch_reduce_out(part_b, N, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks,
-                             scales, false, accumulate, dB, s)) != hipSuccess)
-    return DSV_ERR_DEVICE;
-  if ((e = launch_reduce_out(part_a, K, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks,
-                             nullptr, true, accumulate, dA, s)) != hipSuccess)
+  const ReduceOutArgs ob{part_b, N, scales, 0, dB};
+  const ReduceOutArgs oa{part_a, K, nullptr, 1, dA};
+  if ((e = launch_reduce_out(ob, oa, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks, accumulate, s)) !=
+      hipSuccess)
     return DSV_ERR_DEVICE;
 
   // 5. dx = dy W + g A_a on the matrix cores (W read with a transposing load).

@@ -62,12 +62,7 @@ struct SkinnyArgs {
   uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train (nullptr: none)
   int64_t ld2;
   const int32_t* row_train;
-  float* part;           // fp32 chunk sums when the contraction is split
 };
-
-// Contraction chunks the rank-r contractions use for contraction length C:
-// the launch needs part = chunks * n_items * rows * 64 floats when it is > 1.
-int skinny_chunks(int32_t C, int32_t r_max);
 
 // Per-chunk fp32 partial sums over training tokens:
 //   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Q[t][j]
@@ -97,11 +92,21 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
                                 int32_t r_max, const int32_t* items, int32_t n_items,
                                 const int32_t* gather_rows, const int32_t* ranks,
                                 const float* scales, float* delta, hipStream_t s);
-hipError_t launch_token_reduce(const TokenReduceArgs& a, int32_t n_chunks, hipStream_t s);
-hipError_t launch_reduce_out(const float* part, int32_t C, int32_t r_max, const int32_t* train_ads,
-                             int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
-                             const int32_t* ranks, const float* scales, bool a_layout,
-                             int32_t accumulate, float* out, hipStream_t s);
+// Both token reductions of a backward (dB partials, dA partials) in one launch.
+hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
+                               hipStream_t s);
+// Fixed-order sum of one reduction's chunk partials into its output.
+struct ReduceOutArgs {
+  const float* part;
+  int32_t C;
+  const float* scales;  // nullptr: scale 1
+  int32_t a_layout;     // 1: out[a][j][c] (dA), 0: out[a][c][j] (dB)
+  float* out;
+};
+// Both final sums of a backward in one launch.
+hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
+                             const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
+                             const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s);
 hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
                               int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
 

@@ -555,9 +555,9 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs g) {
 // ---------------------------------------------------------------------------
 // Skinny rank-r contraction: one workgroup per item of <= 32 rows of one
 // adapter (two 16-row tiles sharing each fragment of the adapter operand);
-// the SW waves take interleaved 32-wide slices of the contraction with
-// v_mfma_f32_16x16x32_bf16 (NJ = ceil(r/16) output tiles), U slices in flight
-// per wave, and combine their sums in LDS in a fixed order.
+// the SW waves take contiguous ranges of the contraction in 64-wide slices
+// with v_mfma_f32_16x16x32_bf16 (NJ = ceil(r/16) output tiles), U slices in
+// flight per wave, and combine their sums in LDS in a fixed order.
 // ---------------------------------------------------------------------------
 constexpr int SW = 8;  // waves per rank-contraction workgroup
 
@@ -578,10 +578,6 @@ __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int beg
   }
 }
 
-// blockIdx.y = chunk of the contraction (gridDim.y chunks of whole 64-wide
-// slices).  One chunk: the item's values are finished here.  Several: each
-// chunk's fp32 sums go to g.part, and skinny_reduce_kernel adds the chunks in
-// order and finishes them.
 template <int MODE, int NJ, int ROWS>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
 __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
   constexpr int U = NJ <= 2 ? 4 : 2;
@@ -606,19 +602,20 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
   for (int t = 0; t < RT; ++t)
 #pragma unroll
     for (int jt = 0; jt < NJ; ++jt) acc[t][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // a wave takes 64-wide slices (two 32-wide MFMA steps), so each row is read
-  // in whole 128-byte lines
+  // each wave takes a contiguous range of 64-wide slices (two 32-wide MFMA
+  // steps each), U consecutive slices per pass, so every row is read in runs
+  // of U * 128 bytes
   const int nslices = (g.C + 63) / 64;
-  const int s_lo = (int)((int64_t)blockIdx.y * nslices / gridDim.y);
-  const int s_hi = (int)((int64_t)(blockIdx.y + 1) * nslices / gridDim.y);
-  for (int s0 = s_lo + wave; s0 < s_hi; s0 += SW * U) {
+  const int per_wave = (nslices + SW - 1) / SW;
+  const int s_lo = wave * per_wave, s_hi = min(nslices, s_lo + per_wave);
+  for (int s0 = s_lo; s0 < s_hi; s0 += U) {
     u32x4 av[U][2][RT], bv[U][2][NJ];
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const int k = (s0 + SW * u) * 64 + 32 * h + 8 * (lane >> 4);
-        const bool kin = s0 + SW * u < s_hi && k < g.C;
+        const int k = (s0 + u) * 64 + 32 * h + 8 * (lane >> 4);
+        const bool kin = s0 + u < s_hi && k < g.C;
 #pragma unroll
         for (int t = 0; t < RT; ++t) av[u][h][t] = (prow[t] >= 0 && kin) ? ld16(pp[t] + k) : zero4();
 #pragma unroll
@@ -652,26 +649,8 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
       float sum = 0.f;
 #pragma unroll
       for (int w = 0; w < SW; ++w) sum += red[w][row][j];
-      if (gridDim.y == 1)
-        skinny_store<MODE>(g, a, begin, row, j, sum);
-      else
-        g.part[(((int64_t)blockIdx.y * gridDim.x + blockIdx.x) * ROWS + row) * 64 + j] = sum;
+      skinny_store<MODE>(g, a, begin, row, j, sum);
     }
-  }
-}
-
-// Chunk sums of a split contraction, added in chunk order, then finished.
-template <int MODE, int ROWS>
-__global__ __launch_bounds__(256) void skinny_reduce_kernel(SkinnyArgs g, int32_t chunks) {
-  const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
-  const int a = it[0], begin = it[1], cnt = it[2];
-  const int r = g.ranks[a];
-  for (int idx = threadIdx.x; idx < ROWS * 64; idx += 256) {
-    const int row = idx >> 6, j = idx & 63;
-    if (row >= cnt || j >= r) continue;
-    float sum = 0.f;
-    for (int c = 0; c < chunks; ++c) sum += g.part[(((int64_t)c * gridDim.x + blockIdx.x) * ROWS + row) * 64 + j];
-    skinny_store<MODE>(g, a, begin, row, j, sum);
   }
 }
 
@@ -732,16 +711,21 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
 // c = base + 8 rho + m); the rank side Q[t][j] (h or g, row layout) is read
 // with 8 strided loads per fragment.
 // ---------------------------------------------------------------------------
+// Both reductions of a backward in one launch: blockIdx.y < y0 runs g0's
+// column blocks, the rest g1's.
 template <int NJ>
-__global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g) {
+__global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g0, TokenReduceArgs g1, int32_t y0) {
   constexpr int TQ = kChunkRows / 4;  // tokens per wave
   __shared__ f32x4 red[3][8 * NJ][64];
+  const bool second = (int)blockIdx.y >= y0;
+  const TokenReduceArgs& g = second ? g1 : g0;
+  const int by = second ? (int)blockIdx.y - y0 : (int)blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
   const int a = ck[0], begin = ck[1], cnt = ck[2];
   const int r = g.ranks[a];
   const int q = lane >> 4, rho = lane & 15;
-  const int cbase = blockIdx.y * 128;
+  const int cbase = by * 128;
   const int c0 = cbase + 8 * rho;
   const bool cin = c0 < g.C;
   f32x4 acc[8][NJ];
@@ -814,16 +798,22 @@ __global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g) {
 }
 
 // Fixed-order sum of one training adapter's chunk partials.
-__global__ __launch_bounds__(256) void reduce_out_kernel(
-    const float* __restrict__ part, int32_t C, int32_t r_max, const int32_t* __restrict__ train_ads,
-    const int32_t* __restrict__ tad_ptr, const int32_t* __restrict__ tad_chunks,
-    const int32_t* __restrict__ ranks, const float* __restrict__ scales, int a_layout,
-    int32_t accumulate, float* __restrict__ out) {
-  const int ta = blockIdx.y;
+// Both final sums of a backward in one launch: blockIdx.y = which * n_tads +
+// training adapter; which 0 is o0 (dB, scaled, [c][j]), 1 is o1 (dA, [j][c]).
+__global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutArgs o0, ReduceOutArgs o1, int32_t r_max,
+                                                         const int32_t* __restrict__ train_ads, int32_t n_tads,
+                                                         const int32_t* __restrict__ tad_ptr,
+                                                         const int32_t* __restrict__ tad_chunks,
+                                                         const int32_t* __restrict__ ranks, int32_t accumulate) {
+  const bool second = (int)blockIdx.y >= n_tads;
+  const ReduceOutArgs& g = second ? o1 : o0;
+  const int ta = second ? (int)blockIdx.y - n_tads : (int)blockIdx.y;
+  const int C = g.C;
   const int a = train_ads[ta], r = ranks[a];
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= (int64_t)C * r_max) return;
   int c, j;
-  if (a_layout) {  // out[a][j][c], c fastest
+  if (g.a_layout) {  // out[a][j][c], c fastest
     j = (int)(idx / C);
     c = (int)(idx % C);
   } else {  // out[a][c][j], j fastest
@@ -833,9 +823,9 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(
   if (c >= C || j >= r) return;
   float sum = 0.f;
   for (int p = tad_ptr[ta]; p < tad_ptr[ta + 1]; ++p)
-    sum += part[((int64_t)tad_chunks[p] * C + c) * r_max + j];
-  if (scales) sum *= scales[a];
-  float* o = a_layout ? out + ((int64_t)a * r_max + j) * C + c : out + ((int64_t)a * C + c) * r_max + j;
+    sum += g.part[((int64_t)tad_chunks[p] * C + c) * r_max + j];
+  if (g.scales) sum *= g.scales[a];
+  float* o = g.a_layout ? g.out + ((int64_t)a * r_max + j) * C + c : g.out + ((int64_t)a * C + c) * r_max + j;
   *o = accumulate ? *o + sum : sum;
 }
 
@@ -901,29 +891,15 @@ namespace {
 template <int MODE, int ROWS>
 hipError_t launch_skinny(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  const int chunks = skinny_chunks(a.C, r_max);
-  if (chunks > 1 && !a.part) return hipErrorInvalidValue;
-  const dim3 grid(n_items, chunks);
   if (r_max <= 16)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS>), grid, dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
   else if (r_max <= 32)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS>), grid, dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
   else
-    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS>), grid, dim3(64 * SW), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || chunks == 1) return e;
-  hipLaunchKernelGGL((skinny_reduce_kernel<MODE, ROWS>), dim3(n_items), dim3(256), 0, s, a, chunks);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
   return hipGetLastError();
 }
 }  // namespace
-
-int skinny_chunks(int32_t C, int32_t r_max) {
-  // about one pass of the workgroup's waves over its slices per chunk, 1 to 4
-  // chunks: enough workgroups to cover the CUs without short chunks
-  const int per_pass = SW * (r_max <= 32 ? 4 : 2);
-  const int nsl = (C + 63) / 64;
-  return nsl / per_pass < 1 ? 1 : (nsl / per_pass > 4 ? 4 : nsl / per_pass);
-}
 
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   return launch_skinny<0, kRankItemRows>(a, n_items, r_max, s);
@@ -947,27 +923,28 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
   return hipGetLastError();
 }
 
-hipError_t launch_token_reduce(const TokenReduceArgs& a, int32_t n_chunks, hipStream_t s) {
+hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
+                               hipStream_t s) {
   if (n_chunks <= 0) return hipSuccess;
-  const dim3 grid(n_chunks, (a.C + 127) / 128);
-  if (a.r_max <= 16)
-    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(256), 0, s, a);
-  else if (a.r_max <= 32)
-    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(256), 0, s, a);
+  if (a0.r_max != a1.r_max) return hipErrorInvalidValue;
+  const int y0 = (a0.C + 127) / 128;
+  const dim3 grid(n_chunks, y0 + (a1.C + 127) / 128);
+  if (a0.r_max <= 16)
+    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(256), 0, s, a0, a1, y0);
+  else if (a0.r_max <= 32)
+    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(256), 0, s, a0, a1, y0);
   else
-    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(256), 0, s, a0, a1, y0);
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_out(const float* part, int32_t C, int32_t r_max, const int32_t* train_ads,
-                             int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
-                             const int32_t* ranks, const float* scales, bool a_layout,
-                             int32_t accumulate, float* out, hipStream_t s) {
+hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
+                             const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
+                             const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s) {
   if (n_tads <= 0) return hipSuccess;
-  const int64_t total = (int64_t)C * r_max;
-  hipLaunchKernelGGL(reduce_out_kernel, dim3((unsigned)((total + 255) / 256), n_tads), dim3(256), 0, s,
-                     part, C, r_max, train_ads, tad_ptr, tad_chunks, ranks, scales, a_layout ? 1 : 0,
-                     accumulate, out);
+  const int64_t total = (int64_t)(o0.C > o1.C ? o0.C : o1.C) * r_max;
+  hipLaunchKernelGGL(reduce_out_kernel, dim3((unsigned)((total + 255) / 256), 2 * n_tads), dim3(256), 0, s, o0, o1,
+                     r_max, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate);
   return hipGetLastError();
 }
 
