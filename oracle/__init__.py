@@ -51,10 +51,10 @@ def _load():
         lib.dsvo_rows.argtypes = [ci, ci, i32p, ci, i32p, i32p]
         lib.dsvo_rows.restype = ci
         lib.dsvo_forward.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, f64p, ci,
-                                     f64p, f64p, f64p, f64p, ci, i32p, f64p, f64p]
+                                     f64p, f64p, f64p, f64p, f64p, ci, i32p, f64p, f64p]
         lib.dsvo_forward.restype = ci
         lib.dsvo_backward.argtypes = [ci, ci, ci, ci, i32p, ci, i32p, f64p, ci,
-                                      f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p,
+                                      f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p,
                                       ci, i32p, f64p]
         lib.dsvo_backward.restype = ci
         _lib = lib
@@ -87,10 +87,18 @@ def rows(segments, n_tokens: int, n_adapters: int):
     return ra[:n_tokens].copy(), tr[:tt].copy()
 
 
-def forward(segments, ranks, scales, r_max, X, W, A, B, rows_sel=None):
+def _drop_ptr(drop):
+    if drop is None:
+        return None, ctypes.POINTER(ctypes.c_double)()
+    return _f64(drop)
+
+
+def forward(segments, ranks, scales, r_max, X, W, A, B, rows_sel=None, drop=None):
     """fp64 forward.  Returns (Y[rows][N], H[rows][r_max]); rows default to all.
 
-    H entries at j >= r_a are NaN (never written by the definition)."""
+    H entries at j >= r_a are NaN (never written by the definition).  drop: the
+    LoRA-dropout multipliers of the training rows, [T_t][K] (dropout_multipliers),
+    or None."""
     X, Xp = _f64(X)
     W, Wp = _f64(W)
     A, Ap = _f64(A)
@@ -105,10 +113,11 @@ def forward(segments, ranks, scales, r_max, X, W, A, B, rows_sel=None):
     if rows_sel is None:
         rows_sel = np.arange(T, dtype=np.int32)
     rs, rsp = _i32(rows_sel)
+    dr_, drp_ = _drop_ptr(drop)
     Y = np.empty((rs.shape[0], N), np.float64)
     H = np.full((rs.shape[0], r_max), np.nan, np.float64)
     rc = _load().dsvo_forward(T, K, N, seg.shape[0], segp, n_ad, rkp, scp, r_max,
-                              Xp, Wp, Ap, Bp, rs.shape[0], rsp,
+                              Xp, Wp, Ap, Bp, drp_, rs.shape[0], rsp,
                               Y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
                               H.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
     if rc != 0:
@@ -116,8 +125,9 @@ def forward(segments, ranks, scales, r_max, X, W, A, B, rows_sel=None):
     return Y, H
 
 
-def backward(segments, ranks, scales, r_max, X, W, A, B, dY, dA=None, dB=None, dx_rows=None):
-    """fp64 backward.  Returns (G, dA, dB, dX).
+def backward(segments, ranks, scales, r_max, X, W, A, B, dY, dA=None, dB=None, dx_rows=None,
+             drop=None):
+    """fp64 backward.  Returns (G, dA, dB, dX).  drop as in forward.
 
     dA/dB are copies of the given arrays (NaN-filled when None) with the slices
     of adapters that own training rows overwritten.  dX covers the compact
@@ -140,10 +150,11 @@ def backward(segments, ranks, scales, r_max, X, W, A, B, dY, dA=None, dB=None, d
     if dx_rows is None:
         dx_rows = np.arange(tt, dtype=np.int32)
     dr, drp = _i32(dx_rows)
+    dq_, dqp_ = _drop_ptr(drop)
     dX = np.empty((dr.shape[0], K), np.float64)
     f64p = ctypes.POINTER(ctypes.c_double)
     rc = _load().dsvo_backward(T, K, N, seg.shape[0], segp, n_ad, rkp, scp, r_max,
-                               Xp, Wp, Ap, Bp, dYp, G.ctypes.data_as(f64p),
+                               Xp, Wp, Ap, Bp, dqp_, dYp, G.ctypes.data_as(f64p),
                                dA.ctypes.data_as(f64p), dB.ctypes.data_as(f64p),
                                dr.shape[0], drp, dX.ctypes.data_as(f64p))
     if rc != 0:
@@ -181,3 +192,48 @@ def adamw(p, g, m, v, step, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_de
     v_hat = v_t / (1.0 - beta2 ** step)
     p_t = p - lr * (m_hat / (np.sqrt(v_hat) + eps) + weight_decay * p)
     return p_t, m_t, v_t
+
+
+# ---------------------------------------------------------------------------
+# LoRA dropout (Sec. 4.1: dropout 0.05 on the adapter input of the training
+# rows) with a counter-based generator: Philox4x32-10 (Salmon, Moraes, Dror and
+# Shaw, "Parallel random numbers: as easy as 1, 2, 3", SC 2011), written from
+# its published definition.
+# ---------------------------------------------------------------------------
+_PHILOX_M = (0xD2511F53, 0xCD9E8D57)   # round multipliers
+_PHILOX_W = (0x9E3779B9, 0xBB67AE85)   # key increments (Weyl sequence)
+
+
+def philox4x32_10(c0, c1, c2, c3, k0, k1):
+    """Philox4x32 with 10 rounds, elementwise over equally shaped uint32 arrays
+    (counter words c0..c3, key words k0, k1).  Returns the four output words."""
+    c = [np.asarray(x, np.uint64) & 0xFFFFFFFF for x in (c0, c1, c2, c3)]
+    k = [np.asarray(x, np.uint64) & 0xFFFFFFFF for x in (k0, k1)]
+    for rnd in range(10):
+        if rnd:
+            k = [(k[0] + _PHILOX_W[0]) & 0xFFFFFFFF, (k[1] + _PHILOX_W[1]) & 0xFFFFFFFF]
+        p0 = c[0] * np.uint64(_PHILOX_M[0])     # 32 x 32 -> 64 bit products
+        p1 = c[2] * np.uint64(_PHILOX_M[1])
+        c = [((p1 >> 32) ^ c[1] ^ k[0]) & 0xFFFFFFFF, p1 & 0xFFFFFFFF,
+             ((p0 >> 32) ^ c[3] ^ k[1]) & 0xFFFFFFFF, p0 & 0xFFFFFFFF]
+    return [x.astype(np.uint32) for x in c]
+
+
+def dropout_keep(n_rows: int, K: int, p: float, seed: int, offset: int = 0):
+    """Kept-element mask [n_rows][K] of the training rows (compact order i):
+    element (i, k) takes word k % 4 of Philox4x32-10 at counter
+    (k // 4, i, offset low, offset high) and key (seed low, seed high), and is
+    dropped when that word is below floor(p * 2^32)."""
+    thr = min(int(p * 4294967296.0), 0xFFFFFFFF)
+    q = np.arange((K + 3) // 4, dtype=np.uint64)
+    i = np.arange(n_rows, dtype=np.uint64)
+    Q, I = np.meshgrid(q, i)
+    words = philox4x32_10(Q, I, np.full_like(Q, offset & 0xFFFFFFFF), np.full_like(Q, offset >> 32),
+                          np.full_like(Q, seed & 0xFFFFFFFF), np.full_like(Q, seed >> 32))
+    u = np.stack(words, axis=-1).reshape(n_rows, -1)[:, :K]
+    return u >= thr
+
+
+def dropout_multipliers(n_rows: int, K: int, p: float, seed: int, offset: int = 0):
+    """[n_rows][K] fp64: kept mask / (1 - p) (inverted dropout), for forward / backward."""
+    return dropout_keep(n_rows, K, p, seed, offset).astype(np.float64) / (1.0 - p)

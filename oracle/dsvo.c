@@ -54,10 +54,16 @@ static void shrink_row(int K, int r, int r_max, const double* x, const double* A
   (void)r_max;
 }
 
+/* The input of the low-rank path of token row t: x itself, or for a training
+ * row under dropout x[k] * drop[i][k] (i = compact index of t). */
+static void lora_input(int K, const double* x, const double* drop_row, double* out) {
+  for (int k = 0; k < K; ++k) out[k] = drop_row ? x[k] * drop_row[k] : x[k];
+}
+
 int dsvo_forward(int T, int K, int N, int n_seg, const int32_t* seg,
                  int n_ad, const int32_t* rank, const double* scale, int r_max,
                  const double* X, const double* W, const double* A, const double* B,
-                 int n_rows, const int32_t* rows, double* Y, double* H) {
+                 const double* drop, int n_rows, const int32_t* rows, double* Y, double* H) {
   if (K <= 0 || N <= 0 || r_max <= 0) return -1;
   int32_t* row_adapter = (int32_t*)malloc(sizeof(int32_t) * ((size_t)T + 1));
   int32_t* train_rows = (int32_t*)malloc(sizeof(int32_t) * ((size_t)T + 1));
@@ -68,7 +74,14 @@ int dsvo_forward(int T, int K, int N, int n_seg, const int32_t* seg,
     if (rows[i] < 0 || rows[i] >= T) bad = 1;
   for (int a = 0; a < n_ad && !bad; ++a)
     if (rank[a] < 1 || rank[a] > r_max) bad = 1;
+  int32_t* compact = NULL;  /* token row -> compact training index, or -1 */
   if (!bad) {
+    compact = (int32_t*)malloc(sizeof(int32_t) * ((size_t)T + 1));
+    if (!compact) bad = 1;
+  }
+  if (!bad) {
+    for (int t = 0; t < T; ++t) compact[t] = -1;
+    for (int i = 0; i < tt; ++i) compact[train_rows[i]] = i;
 #pragma omp parallel for schedule(dynamic, 4)
     for (int i = 0; i < n_rows; ++i) {
       const int t = rows[i];
@@ -79,7 +92,10 @@ int dsvo_forward(int T, int K, int N, int n_seg, const int32_t* seg,
       const double* Aa = A + (size_t)a * r_max * K;
       const double* Ba = B + (size_t)a * N * r_max;
       double* h = H + (size_t)i * r_max;
-      shrink_row(K, r, r_max, x, Aa, h);
+      double* xl = (double*)malloc(sizeof(double) * (size_t)K);
+      lora_input(K, x, (drop && compact[t] >= 0) ? drop + (size_t)compact[t] * K : NULL, xl);
+      shrink_row(K, r, r_max, xl, Aa, h);
+      free(xl);
       for (int n = 0; n < N; ++n) {
         /* base term: the frozen weight, shared by every row (Sec. 2.2) */
         double base = 0.0;
@@ -93,6 +109,7 @@ int dsvo_forward(int T, int K, int N, int n_seg, const int32_t* seg,
       }
     }
   }
+  free(compact);
   free(row_adapter);
   free(train_rows);
   return bad ? -1 : 0;
@@ -101,7 +118,7 @@ int dsvo_forward(int T, int K, int N, int n_seg, const int32_t* seg,
 int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
                   int n_ad, const int32_t* rank, const double* scale, int r_max,
                   const double* X, const double* W, const double* A, const double* B,
-                  const double* dY, double* G, double* dA, double* dB,
+                  const double* drop, const double* dY, double* G, double* dA, double* dB,
                   int n_dx, const int32_t* dx_rows, double* dX) {
   if (K <= 0 || N <= 0 || r_max <= 0) return -1;
   int32_t* row_adapter = (int32_t*)malloc(sizeof(int32_t) * ((size_t)T + 1));
@@ -114,20 +131,23 @@ int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
   for (int m = 0; m < n_dx && !bad; ++m)
     if (dx_rows[m] < 0 || dx_rows[m] >= tt) bad = 1;
   double* Hs = NULL;
+  double* XL = NULL;  /* low-rank-path input of every training row */
   char* owns = NULL;
   if (!bad) {
     Hs = (double*)malloc(sizeof(double) * ((size_t)tt * r_max + 1));
+    XL = (double*)malloc(sizeof(double) * ((size_t)tt * K + 1));
     owns = (char*)calloc((size_t)n_ad, 1);
-    if (!Hs || !owns) bad = 1;
+    if (!Hs || !XL || !owns) bad = 1;
   }
   if (!bad) {
     for (int i = 0; i < tt; ++i) owns[row_adapter[train_rows[i]]] = 1;
 
-    /* H of every training row, recomputed exactly from X and A. */
+    /* H of every training row, recomputed exactly from its low-rank input. */
 #pragma omp parallel for schedule(static)
     for (int i = 0; i < tt; ++i) {
       const int t = train_rows[i], a = row_adapter[t];
-      shrink_row(K, rank[a], r_max, X + (size_t)t * K, A + (size_t)a * r_max * K,
+      lora_input(K, X + (size_t)t * K, drop ? drop + (size_t)i * K : NULL, XL + (size_t)i * K);
+      shrink_row(K, rank[a], r_max, XL + (size_t)i * K, A + (size_t)a * r_max * K,
                  Hs + (size_t)i * r_max);
     }
 
@@ -160,7 +180,8 @@ int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
       }
     }
 
-    /* dA[a][j][k] = sum_{i of a} G[i][j] X[t_i][k]; columns k in parallel. */
+    /* dA[a][j][k] = sum_{i of a} G[i][j] XL[i][k] (XL: the low-rank input of
+     * training row i); columns k in parallel. */
 #pragma omp parallel for schedule(static)
     for (int k = 0; k < K; ++k) {
       for (int a = 0; a < n_ad; ++a) {
@@ -171,7 +192,7 @@ int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
           for (int i = 0; i < tt; ++i) {
             const int t = train_rows[i];
             if (row_adapter[t] != a) continue;
-            acc += G[(size_t)i * r_max + j] * X[(size_t)t * K + k];
+            acc += G[(size_t)i * r_max + j] * XL[(size_t)i * K + k];
           }
           dA[((size_t)a * r_max + j) * K + k] = acc;
         }
@@ -189,11 +210,13 @@ int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
         for (int n = 0; n < N; ++n) base += dY[(size_t)i * N + n] * W[(size_t)n * K + k];
         double low = 0.0;
         for (int j = 0; j < r; ++j) low += G[(size_t)i * r_max + j] * Aa[(size_t)j * K + k];
+        if (drop) low *= drop[(size_t)i * K + k];  /* through the fixed mask */
         dX[(size_t)m * K + k] = base + low;
       }
     }
   }
   free(Hs);
+  free(XL);
   free(owns);
   free(row_adapter);
   free(train_rows);

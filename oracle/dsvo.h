@@ -52,24 +52,31 @@ int dsvo_rows(int T, int n_seg, const int32_t* seg, int n_ad,
  *   H[i][j] = sum_k X[t][k] A[a][j][k]                       (j < r_a)
  *   Y[i][n] = sum_k X[t][k] W[n][k] + s_a sum_j H[i][j] B[a][n][j]
  * with t = rows[i], a = adapter of row t.  Y is [n_rows][N], H [n_rows][r_max].
- * Returns 0, or -1 on an invalid table / row. */
+ * LoRA dropout (Sec. 4.1 trains with dropout 0.05 on the adapter input): when
+ * drop is not NULL it holds [T_t][K] multipliers (the kept-element mask times
+ * 1 / (1 - p), compact training order) and a training row's low-rank path
+ * reads x[k] * drop[i][k] instead of x[k]; the base path and inference rows
+ * are unchanged.  Returns 0, or -1 on an invalid table / row. */
 int dsvo_forward(int T, int K, int N, int n_seg, const int32_t* seg,
                  int n_ad, const int32_t* rank, const double* scale, int r_max,
                  const double* X, const double* W, const double* A, const double* B,
-                 int n_rows, const int32_t* rows, double* Y, double* H);
+                 const double* drop, int n_rows, const int32_t* rows, double* Y, double* H);
 
 /* Backward for the training rows (compact index i, token row t = train_rows[i]):
  *   G[i][j]    = s_a sum_n dY[i][n] B[a][n][j]
  *   dB[a][n][j] = s_a sum_{i of a} H[i][j] dY[i][n]      (H recomputed exactly)
  *   dA[a][j][k] = sum_{i of a} G[i][j] X[t][k]
  *   dX[m][k]   = sum_n dY[i][n] W[n][k] + sum_j G[i][j] A[a][j][k],  i = dx_rows[m]
+ * With drop (see dsvo_forward) X[t][k] in H and dA reads X[t][k] drop[i][k],
+ * and the low-rank term of dX[m][k] is multiplied by drop[i][k] (the chain
+ * rule through the fixed mask).
  * These are the exact gradients of L = sum_i <dY[i], Y[t]>.  dA and dB slices
  * of adapters that own training rows are overwritten; other slices are left
  * untouched.  G is [T_t][r_max], dX [n_dx][K].  Returns 0 or -1. */
 int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
                   int n_ad, const int32_t* rank, const double* scale, int r_max,
                   const double* X, const double* W, const double* A, const double* B,
-                  const double* dY, double* G, double* dA, double* dB,
+                  const double* drop, const double* dY, double* G, double* dA, double* dB,
                   int n_dx, const int32_t* dx_rows, double* dX);
 
 #ifdef __cplusplus

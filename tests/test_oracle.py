@@ -333,3 +333,100 @@ def test_adamw_matches_torch_optimizer_fp64():
         opt.step()
         p, m, v = oracle.adamw(p, g, m, v, k, **HP)
     np.testing.assert_allclose(p, t.detach().numpy(), rtol=1e-13, atol=1e-16)
+
+
+# ---------------------------------------------------------------------------
+# LoRA dropout on the training rows (Sec. 4.1: dropout 0.05)
+# ---------------------------------------------------------------------------
+def test_philox4x32_10_known_answers():
+    """Known-answer vectors of Philox4x32 with 10 rounds, as distributed with the
+    Random123 library of Salmon et al. (SC 2011): counter, key -> output."""
+    cases = [((0, 0, 0, 0), (0, 0), (0x6627e8d5, 0xe169c58d, 0xbc57ac4c, 0x9b00dbd8)),
+             ((0xffffffff,) * 4, (0xffffffff,) * 2, (0x408f276d, 0x41c83b0e, 0xa20bc7c6, 0x6d5451fd)),
+             ((0x243f6a88, 0x85a308d3, 0x13198a2e, 0x03707344), (0xa4093822, 0x299f31d0),
+              (0xd16cfe09, 0x94fdcceb, 0x5001e420, 0x24126ea1))]
+    for ctr, key, out in cases:
+        got = oracle.philox4x32_10(*[np.uint32(c) for c in ctr], *[np.uint32(k) for k in key])
+        assert tuple(int(x) for x in got) == out
+
+
+def test_dropout_mask_rate_and_streams():
+    """The drop rate is p within 5 binomial standard deviations; another seed or
+    offset gives another mask; p = 0 keeps everything."""
+    n, K, p = 256, 4096, 0.05
+    keep = oracle.dropout_keep(n, K, p, seed=1234, offset=7)
+    rate = 1.0 - keep.mean()
+    assert abs(rate - p) < 5 * np.sqrt(p * (1 - p) / keep.size)
+    # rows and column groups are not copies of each other
+    assert (keep[0] != keep[1]).any() and (keep[:, :4] != keep[:, 4:8]).any()
+    assert (oracle.dropout_keep(n, K, p, seed=1235, offset=7) != keep).mean() > 0.05
+    assert (oracle.dropout_keep(n, K, p, seed=1234, offset=8) != keep).mean() > 0.05
+    assert oracle.dropout_keep(8, 64, 0.0, seed=9).all()
+
+
+def test_dropout_forward_closed_form():
+    """With dropout the low-rank path of a training row reads x * m / (1 - p); the base
+    path and inference rows are unchanged: per-row numpy matmuls of that definition."""
+    w, t = _small(SEGS, RANKS, pad=0.0)
+    _, tr = oracle.rows(w.segments, w.n_tokens, 3)
+    D = oracle.dropout_multipliers(len(tr), 40, 0.3, seed=5)
+    Y, H = oracle.forward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B, drop=D)
+    ra, _ = oracle.rows(w.segments, w.n_tokens, 3)
+    compact = {int(row): i for i, row in enumerate(tr)}
+    for row in range(w.n_tokens):
+        a, r, s = int(ra[row]), int(w.ranks[ra[row]]), float(w.scales[ra[row]])
+        x = t.X[row]
+        xl = x * D[compact[row]] if row in compact else x
+        h = t.A[a, :r] @ xl
+        np.testing.assert_allclose(H[row, :r], h, rtol=1e-13, atol=1e-14)
+        np.testing.assert_allclose(Y[row], t.W @ x + s * t.B[a, :, :r] @ h, rtol=1e-12, atol=1e-13)
+
+
+def test_dropout_finite_differences():
+    """With the mask fixed, L is still linear in each of X, A and B: central differences
+    pin dA, dB and dX of the dropout backward (the mask enters h, dA and dX)."""
+    w, t = _small(SEGS, RANKS, pad=0.0)
+    _, tr = oracle.rows(w.segments, w.n_tokens, 3)
+    D = oracle.dropout_multipliers(len(tr), 40, 0.3, seed=6, offset=2)
+    assert (D == 0).any()
+    G, dA, dB, dX = _bwd(w, t, drop=D)
+
+    def loss(X, A, B):
+        Y, _ = oracle.forward(w.segments, w.ranks, w.scales, w.r_max, X, t.W, A, B, tr, drop=D)
+        return float(np.sum(t.dY * Y))
+    rng = np.random.default_rng(8)
+    h = 0.5
+    for a in (0, 1):
+        r = int(w.ranks[a])
+        for _ in range(6):
+            j, k = int(rng.integers(r)), int(rng.integers(40))
+            Ap, Am = t.A.copy(), t.A.copy()
+            Ap[a, j, k] += h
+            Am[a, j, k] -= h
+            fd = (loss(t.X, Ap, t.B) - loss(t.X, Am, t.B)) / (2 * h)
+            assert abs(fd - dA[a, j, k]) <= 1e-9 * max(1.0, abs(fd))
+            n = int(rng.integers(24))
+            Bp, Bm = t.B.copy(), t.B.copy()
+            Bp[a, n, j] += h
+            Bm[a, n, j] -= h
+            fd = (loss(t.X, t.A, Bp) - loss(t.X, t.A, Bm)) / (2 * h)
+            assert abs(fd - dB[a, n, j]) <= 1e-9 * max(1.0, abs(fd))
+    for i, row in enumerate(tr):
+        for k in (int(rng.integers(40)), int(np.argmin(D[i]))):   # include a dropped column
+            Xp, Xm = t.X.copy(), t.X.copy()
+            Xp[row, k] += h
+            Xm[row, k] -= h
+            fd = (loss(Xp, t.A, t.B) - loss(Xm, t.A, t.B)) / (2 * h)
+            assert abs(fd - dX[i, k]) <= 1e-9 * max(1.0, abs(fd))
+
+
+def test_dropout_p0_is_no_dropout():
+    w, t = _small(SEGS, RANKS, pad=0.0)
+    _, tr = oracle.rows(w.segments, w.n_tokens, 3)
+    D = oracle.dropout_multipliers(len(tr), 40, 0.0, seed=1)
+    Y0, H0 = _fwd(w, t)
+    Y1, H1 = oracle.forward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B, drop=D)
+    assert np.array_equal(Y0, Y1) and np.array_equal(np.nan_to_num(H0), np.nan_to_num(H1))
+    b0, b1 = _bwd(w, t), _bwd(w, t, drop=D)
+    for x, y in zip(b0, b1):
+        assert np.array_equal(np.nan_to_num(x), np.nan_to_num(y))
