@@ -192,6 +192,63 @@ int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
                  void* hip_stream);
 
 /*
+ * LoRA dropout of the training rows (Sec. 4.1 fine-tunes the adapter with
+ * dropout 0.05).  The low-rank branch of a training row reads its input
+ * through a mask: x~[i][k] = x[i][k] keep(i, k) / (1 - p); the base product
+ * X W^T and the inference rows are unchanged.  keep(i, k) for compact training
+ * row i (ascending token order) and column k is decided by Philox4x32-10
+ * (Salmon et al., SC 2011): output word k mod 4 of the generator at counter
+ * (k / 4, i, offset mod 2^32, offset / 2^32) and key (seed mod 2^32,
+ * seed / 2^32) is compared with floor(p 2^32); words below it drop the
+ * element.  The mask is a pure function of (seed, offset, i, k): the backward
+ * regenerates the forward's mask from the same three values, and a caller
+ * draws a fresh mask per step by advancing offset.  0 <= p < 1; p = 0 gives
+ * the plain entry points' results bit for bit.
+ */
+typedef struct {
+  double p;
+  uint64_t seed;
+  uint64_t offset;
+} dsv_dropout;
+
+/*
+ * dsv_cobatch_fwd_dropout -- dsv_cobatch_fwd with LoRA dropout on the
+ * training rows:  y = x W^T + s_a (x~ A_a^T) B_a^T,  H_save = x~ A_a^T.
+ * Same arguments, layouts and workspace size (dsv_cobatch_fwd_workspace) as
+ * dsv_cobatch_fwd.  Returns DSV_ERR_ARG for a NULL dropout, DSV_ERR_RANGE for
+ * p outside [0, 1), else as dsv_cobatch_fwd.
+ */
+int dsv_cobatch_fwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                            const void* X, const void* W, const void* A, const void* B,
+                            void* Y, void* H_save, const dsv_dropout* dropout, void* workspace,
+                            size_t workspace_bytes, void* hip_stream);
+
+/*
+ * dsv_lora_bwd_dropout_workspace -- bytes of device workspace
+ * dsv_lora_bwd_dropout needs (dsv_lora_bwd's, plus the regenerated mask and,
+ * for bf16, an fp32 [T_t][K] buffer for the masked low-rank term of dX).
+ */
+int dsv_lora_bwd_dropout_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                                   size_t* bytes);
+
+/*
+ * dsv_lora_bwd_dropout -- backward of dsv_cobatch_fwd_dropout with the same
+ * dropout values: with g = s_a dY B_a and x~ the forward's masked, scaled
+ * adapter input,
+ *     dB_a  (+)=  s_a dY^T H_save      dA_a  (+)=  g^T X~_train
+ *     dX     =   dY W + (g A_a) masked and scaled like the input
+ * H_save is the forward's (already masked); H_save == NULL recomputes it from
+ * X through the regenerated mask.  Arguments as dsv_lora_bwd, workspace of at
+ * least dsv_lora_bwd_dropout_workspace bytes.  Returns DSV_ERR_ARG for a NULL
+ * dropout, DSV_ERR_RANGE for p outside [0, 1), else as dsv_lora_bwd.
+ */
+int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                         const void* X, const void* W, const void* A, const void* B,
+                         const void* H_save, const void* dY, float* dA, float* dB, void* dX,
+                         int32_t accumulate, const dsv_dropout* dropout, void* workspace,
+                         size_t workspace_bytes, void* hip_stream);
+
+/*
  * Kernel timing for benchmarks.  While enabled (on = 1), every
  * dsv_cobatch_fwd / dsv_lora_bwd call records a HIP event pair on its own
  * stream immediately around its matrix-core GEMM launch (forward: the base

@@ -87,11 +87,14 @@ GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C) {
 }
 
 struct FwdWs {
-  size_t h_all, delta, sk_part, total;
+  size_t h_all, delta, keep, sk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, hrec, part_b, part_a, sk_part, total;
+  size_t bt, g, hrec, part_b, part_a, keep, ddx, sk_part, total;
 };
+
+// Dropout bitmask of the training rows: ceil(K / 32) words per row.
+size_t keep_bytes(const dsv_plan& p, int32_t K) { return (size_t)p.T_t * ((K + 31) / 32) * 4; }
 
 // Split-tile scratch of a GEMM plan: one fp32 partial tile per piece.
 size_t carve_sk(const GemmPlan& gp, size_t off, size_t* part) {
@@ -100,7 +103,7 @@ size_t carve_sk(const GemmPlan& gp, size_t off, size_t* part) {
   return align256(off + (size_t)gp.sk_tiles * gp.sk_split * gp.tm * gp.tn * 4);
 }
 
-FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N, const GemmPlan& gp) {
+FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPlan& gp) {
   FwdWs w{};
   size_t off = 0;
   if (dt == DSV_BF16) {
@@ -114,11 +117,13 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t N, const GemmPlan& gp) {
     off = align256(off + (size_t)p.T * p.r_max * 4);
     w.delta = off;
   }
+  w.keep = off;  // dropout mask of the training rows
+  off = align256(off + keep_bytes(p, K));
   w.total = off;
   return w;
 }
 
-BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPlan& gp) {
+BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPlan& gp, bool dropout) {
   BwdWs w{};
   size_t off = 0;
   if (dt == DSV_BF16) {
@@ -139,6 +144,10 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     w.hrec = off;
     off = align256(off + (size_t)p.T_t * p.r_max * 4);
   }
+  w.keep = off;  // dropout mask of the training rows
+  off = align256(off + keep_bytes(p, K));
+  w.ddx = off;   // dropout: masked fp32 low-rank term of dX (bf16 path)
+  if (dropout && dt == DSV_BF16) off = align256(off + (size_t)p.T_t * K * 4);
   w.total = off;
   return w;
 }
@@ -300,7 +309,7 @@ extern "C" int dsv_cobatch_fwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   if (!bytes) return DSV_ERR_ARG;
-  *bytes = fwd_ws(*p, dt, N, fwd_gemm_plan(*p, dt, K, N)).total;
+  *bytes = fwd_ws(*p, dt, K, N, fwd_gemm_plan(*p, dt, K, N)).total;
   return DSV_OK;
 }
 
@@ -309,21 +318,46 @@ extern "C" int dsv_lora_bwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   if (!bytes) return DSV_ERR_ARG;
-  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N)).total;
+  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N), false).total;
   return DSV_OK;
 }
 
-extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
-                               const void* W, const void* A, const void* B, void* Y, void* H_save,
-                               void* workspace, size_t workspace_bytes, void* hip_stream) {
+extern "C" int dsv_lora_bwd_dropout_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N,
+                                              size_t* bytes) {
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
+  if (!bytes) return DSV_ERR_ARG;
+  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N), true).total;
+  return DSV_OK;
+}
+
+namespace {
+
+// Dropout parameters -> mask spec; false when they are out of range.
+bool dropout_spec(const dsv_dropout* d, DropoutSpec* out) {
+  if (!d || !std::isfinite(d->p) || d->p < 0.0 || d->p >= 1.0) return false;
+  const double t = std::floor(d->p * 4294967296.0);
+  out->thr = t >= 4294967295.0 ? 0xFFFFFFFFu : (uint32_t)t;
+  out->scale = (float)(1.0 / (1.0 - d->p));
+  out->seed = d->seed;
+  out->offset = d->offset;
+  return true;
+}
+
+int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
+             const void* B, void* Y, void* H_save, const dsv_dropout* drop, void* workspace,
+             size_t workspace_bytes, void* hip_stream) {
+  int rc = check_common(p, dt, K, N);
+  if (rc != DSV_OK) return rc;
+  DropoutSpec ds{};
+  if (drop && !dropout_spec(drop, &ds)) return DSV_ERR_RANGE;
+  const bool dropping = drop && drop->p > 0.0 && p->T_t > 0;
   if (!p->d_meta) return DSV_ERR_ARG;
   if (p->T == 0) return DSV_OK;  // empty batch: nothing to read or write
   if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(Y)) return DSV_ERR_ARG;
   if (H_save && !aligned16(H_save)) return DSV_ERR_ARG;
   const GemmPlan gp = fwd_gemm_plan(*p, dt, K, N);
-  const FwdWs ws = fwd_ws(*p, dt, N, gp);
+  const FwdWs ws = fwd_ws(*p, dt, K, N, gp);
   if (ws.total > 0) {
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
     if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
@@ -334,6 +368,12 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   hipError_t e = hipSuccess;
 
+  // 0. dropout mask of the training rows' adapter input.
+  const uint32_t* keep = dropping ? at<uint32_t>(workspace, ws.keep) : nullptr;
+  const int32_t keep_words = (K + 31) / 32;
+  if (dropping && (e = launch_dropout_mask(at<uint32_t>(workspace, ws.keep), p->T_t, K, ds, s)) != hipSuccess)
+    return DSV_ERR_DEVICE;
+
   if (dt == DSV_F32) {
     F32Args a{};
     a.T = p->T;
@@ -341,6 +381,9 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
     a.K = K;
     a.N = N;
     a.r_max = p->r_max;
+    a.keep = keep;
+    a.keep_words = keep_words;
+    a.drop_scale = ds.scale;
     a.row_adapter = p->dptr(L.row_adapter);
     a.row_train = p->dptr(L.row_train);
     a.ranks = ranks;
@@ -378,6 +421,9 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   sk.out2 = p->T_t > 0 ? static_cast<uint16_t*>(H_save) : nullptr;
   sk.ld2 = p->r_max;
   sk.row_train = p->dptr(L.row_train);
+  sk.keep = keep;
+  sk.keep_words = keep_words;
+  sk.drop_scale = ds.scale;
   if ((e = launch_shrink(sk, p->n_shrink, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2. gathered rows: fp32 low-rank term, each touched adapter read once.
@@ -418,12 +464,15 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
   return DSV_OK;
 }
 
-extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
-                            const void* W, const void* A, const void* B, const void* H_save,
-                            const void* dY, float* dA, float* dB, void* dX, int32_t accumulate,
-                            void* workspace, size_t workspace_bytes, void* hip_stream) {
+int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
+             const void* B, const void* H_save, const void* dY, float* dA, float* dB, void* dX,
+             int32_t accumulate, const dsv_dropout* drop, void* workspace, size_t workspace_bytes,
+             void* hip_stream) {
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
+  DropoutSpec ds{};
+  if (drop && !dropout_spec(drop, &ds)) return DSV_ERR_RANGE;
+  const bool dropping = drop && drop->p > 0.0;
   if (accumulate != 0 && accumulate != 1) return DSV_ERR_RANGE;
   if (!p->d_meta) return DSV_ERR_ARG;
   if (p->T_t == 0) return DSV_OK;  // no training rows: nothing to read or write
@@ -432,7 +481,7 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   if (dX && !aligned16(dX)) return DSV_ERR_ARG;
   if (!ptr_ok(dY) || (H_save && !aligned16(H_save))) return DSV_ERR_ARG;
   const GemmPlan gp = bwd_gemm_plan(*p, dt, K, N);
-  const BwdWs ws = bwd_ws(*p, dt, K, N, gp);
+  const BwdWs ws = bwd_ws(*p, dt, K, N, gp, drop != nullptr);
   if (ws.total > 0) {
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
     if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
@@ -443,6 +492,11 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   hipError_t e = hipSuccess;
 
+  // 0. the forward's dropout mask, regenerated from the same seed and offset.
+  uint32_t* keep = dropping ? at<uint32_t>(workspace, ws.keep) : nullptr;
+  const int32_t keep_words = (K + 31) / 32;
+  if (dropping && (e = launch_dropout_mask(keep, p->T_t, K, ds, s)) != hipSuccess) return DSV_ERR_DEVICE;
+
   if (dt == DSV_F32) {
     F32Args a{};
     a.T = p->T;
@@ -450,6 +504,9 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     a.K = K;
     a.N = N;
     a.r_max = p->r_max;
+    a.keep = keep;
+    a.keep_words = keep_words;
+    a.drop_scale = ds.scale;
     a.train_rows = p->dptr(L.train_rows);
     a.train_adapter = p->dptr(L.train_adapter);
     a.train_ads = p->dptr(L.train_ads);
@@ -527,6 +584,9 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     sh.out2 = hrec;
     sh.ld2 = ldh;
     sh.row_train = p->dptr(L.row_train);
+    sh.keep = keep;
+    sh.keep_words = keep_words;
+    sh.drop_scale = ds.scale;
     if ((e = launch_shrink_train(sh, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
     hs = hrec;
     ldhs = ldh;
@@ -552,18 +612,40 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
   ta.ldq = ldh;
   ta.C = K;
   ta.part = part_a;
+  ta.keep = keep;  // dA contracts the masked input
+  ta.keep_words = keep_words;
   if ((e = launch_token_reduce(tb, ta, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 4. fixed-order sums into dB (scaled by s_a) and dA.
   const int32_t* tad_ptr = p->dptr(L.tad_chunk_ptr);
   const int32_t* tad_chunks = p->dptr(L.tad_chunks);
-  const ReduceOutArgs ob{part_b, N, scales, 0, dB};
-  const ReduceOutArgs oa{part_a, K, nullptr, 1, dA};
+  const ReduceOutArgs ob{part_b, N, scales, 0, dB, 1.f};
+  const ReduceOutArgs oa{part_a, K, nullptr, 1, dA, dropping ? ds.scale : 1.f};
   if ((e = launch_reduce_out(ob, oa, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks, accumulate, s)) !=
       hipSuccess)
     return DSV_ERR_DEVICE;
 
   // 5. dx = dy W + g A_a on the matrix cores (W read with a transposing load).
+  //    Under dropout the low-rank term passes through the mask first, so it is
+  //    formed apart (fp32, masked and scaled) and added in the epilogue.
+  float* ddx = nullptr;
+  if (dX && dropping) {
+    ddx = at<float>(workspace, ws.ddx);
+    DropoutDxArgs dd{};
+    dd.Tt = p->T_t;
+    dd.K = K;
+    dd.r_max = p->r_max;
+    dd.G = gm;
+    dd.ldg = ldh;
+    dd.A = static_cast<const uint16_t*>(A);
+    dd.train_adapter = p->dptr(L.train_adapter);
+    dd.ranks = ranks;
+    dd.keep = keep;
+    dd.keep_words = keep_words;
+    dd.scale = ds.scale;
+    dd.delta = ddx;
+    if ((e = launch_dropout_dx_low(dd, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  }
   if (dX) {
     GemmArgs g{};
     g.P = static_cast<const uint16_t*>(dY);
@@ -585,12 +667,48 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
     g.lq_col = 1;
     g.ranks = ranks;
     g.scales = nullptr;
-    g.delta = nullptr;
+    g.delta = ddx;
     g.gslot = nullptr;
+    g.no_prologue = ddx != nullptr;
+    g.delta_rows = ddx != nullptr;
     const int tk = timing_begin(1, s);
     e = launch_gemm_nn(g, gp.tm, gp.tn, s);
     timing_end(tk, s);
     if (e != hipSuccess) return DSV_ERR_DEVICE;
   }
   return DSV_OK;
+}
+
+}  // namespace
+
+extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                               const void* W, const void* A, const void* B, void* Y, void* H_save,
+                               void* workspace, size_t workspace_bytes, void* hip_stream) {
+  return fwd_impl(p, dt, K, N, X, W, A, B, Y, H_save, nullptr, workspace, workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_cobatch_fwd_dropout(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                                       const void* W, const void* A, const void* B, void* Y, void* H_save,
+                                       const dsv_dropout* dropout, void* workspace, size_t workspace_bytes,
+                                       void* hip_stream) {
+  if (!dropout) return DSV_ERR_ARG;
+  return fwd_impl(p, dt, K, N, X, W, A, B, Y, H_save, dropout, workspace, workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                            const void* W, const void* A, const void* B, const void* H_save,
+                            const void* dY, float* dA, float* dB, void* dX, int32_t accumulate,
+                            void* workspace, size_t workspace_bytes, void* hip_stream) {
+  return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, nullptr, workspace,
+                  workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_lora_bwd_dropout(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                                    const void* W, const void* A, const void* B, const void* H_save,
+                                    const void* dY, float* dA, float* dB, void* dX, int32_t accumulate,
+                                    const dsv_dropout* dropout, void* workspace, size_t workspace_bytes,
+                                    void* hip_stream) {
+  if (!dropout) return DSV_ERR_ARG;
+  return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, dropout, workspace,
+                  workspace_bytes, hip_stream);
 }

@@ -41,6 +41,10 @@ struct GemmArgs {
   // slot per piece); a second kernel sums them and writes those tiles.
   int32_t dp_tiles, sk_tiles, sk_split;
   float* sk_part;
+  // no_prologue: the low-rank term is not added in the prologue;
+  // delta_rows: every row r adds delta[r][n] (its own fp32 term) instead of
+  // only the gathered rows through gslot
+  int32_t no_prologue, delta_rows;
 };
 
 // Rank-r contraction of a few rows of one adapter (shrink h = x A^T, and
@@ -62,6 +66,11 @@ struct SkinnyArgs {
   uint16_t* out2;        // shrink: H_save [T_t][ld2] via row_train (nullptr: none)
   int64_t ld2;
   const int32_t* row_train;
+  // dropout of the training rows (shrink only; keep == nullptr: none):
+  // masked input elements, sum scaled by drop_scale
+  const uint32_t* keep;
+  int32_t keep_words;
+  float drop_scale;
 };
 
 // Per-chunk fp32 partial sums over training tokens:
@@ -76,6 +85,8 @@ struct TokenReduceArgs {
   const int32_t* ranks;
   int32_t C, r_max;
   float* part;
+  const uint32_t* keep;  // dropout mask of P's elements (compact rows), nullptr: none
+  int32_t keep_words;
 };
 
 // Launchers (bf16).  Each returns hipSuccess or the launch error.
@@ -102,6 +113,7 @@ struct ReduceOutArgs {
   const float* scales;  // nullptr: scale 1
   int32_t a_layout;     // 1: out[a][j][c] (dA), 0: out[a][c][j] (dB)
   float* out;
+  float post;           // extra factor (dropout scale of dA), 1 otherwise
 };
 // Both final sums of a backward in one launch.
 hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
@@ -128,6 +140,29 @@ struct AdamWArgs {
 };
 hipError_t launch_adamw(const AdamWArgs& a, int32_t n_tads, hipStream_t s);
 
+// LoRA dropout of the training rows: mask parameters (thr = floor(p 2^32),
+// scale = 1 / (1 - p)), the bitmask kernel, and the masked low-rank dX term.
+struct DropoutSpec {
+  uint32_t thr;
+  float scale;
+  uint64_t seed, offset;
+};
+// bits: [Tt][ceil(K / 32)] words, bit b of word w keeps column 32 w + b.
+hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const DropoutSpec& d, hipStream_t s);
+struct DropoutDxArgs {
+  int32_t Tt, K, r_max;
+  const uint16_t* G;            // g of the training rows [Tt][ldg] bf16
+  int64_t ldg;
+  const uint16_t* A;            // adapter stacks [n_ad][r_max][K] bf16
+  const int32_t* train_adapter; // compact row -> adapter
+  const int32_t* ranks;
+  const uint32_t* keep;         // bitmask
+  int32_t keep_words;
+  float scale;
+  float* delta;                 // [Tt][K] fp32 out
+};
+hipError_t launch_dropout_dx_low(const DropoutDxArgs& a, hipStream_t s);
+
 // Launchers (fp32 mode: plain FMA kernels, same semantics).
 struct F32Args {
   int32_t T, Tt, K, N, r_max;
@@ -145,6 +180,9 @@ struct F32Args {
   const float *X, *W, *A, *B, *Hs, *dY;
   float *Y, *Hsave, *Hall, *G, *dA, *dB, *dX;
   float* Hrec;   // backward with Hs == nullptr: h of the training rows recomputed here
+  const uint32_t* keep;  // dropout mask of the training rows (nullptr: none)
+  int32_t keep_words;
+  float drop_scale;
   int32_t accumulate;
 };
 hipError_t launch_f32_fwd(const F32Args& a, hipStream_t s);

@@ -49,6 +49,20 @@ __device__ __forceinline__ uint16_t f2bf(float f) {
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
+// Eight bf16 values with element e zeroed unless bit e of b is set (dropout).
+__device__ __forceinline__ u32x4 keep8(u32x4 v, uint32_t b) {
+  u32x4 o;
+#pragma unroll
+  for (int d = 0; d < 4; ++d)
+    o[d] = v[d] & (((b >> (2 * d)) & 1u ? 0x0000ffffu : 0u) | ((b >> (2 * d + 1)) & 1u ? 0xffff0000u : 0u));
+  return o;
+}
+
+// Byte of the dropout bitmask that covers columns c .. c+7 (c a multiple of 8).
+__device__ __forceinline__ uint32_t keep_byte(const uint32_t* keep, int keep_words, int row, int c) {
+  return (keep[(int64_t)row * keep_words + (c >> 5)] >> (c & 31)) & 0xffu;
+}
+
 // Eight bf16 values read with a per-element predicate, from p[e * stride].
 __device__ __forceinline__ u32x4 ld8_masked(const uint16_t* p, int64_t stride, int n_valid) {
   uint32_t w[4] = {0u, 0u, 0u, 0u};
@@ -303,7 +317,7 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // and split into bf16 hi + lo (|lo| <= 2^-9 |hi|), so the product carries
   // the scale to about 2^-16 relative with no VALU work on the accumulators;
   // with scale 1 (or a power of two) lo is exactly zero and is skipped.
-  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
+  for (int gi = 0; kb == 0 && !g.no_prologue && gi < ngroups; ++gi) {
     const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
     if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
     const int r = g.ranks[a];
@@ -466,14 +480,19 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // ---- epilogue: one rounding, staged through LDS for 16-byte stores ----
   __syncthreads();
   uint16_t* st = reinterpret_cast<uint16_t*>(smem);
-  const bool gather_tile = has_gather && g.delta != nullptr;
+  // fp32 low-rank terms added before the rounding: 0 none, 1 the gathered
+  // rows' (through gslot), 2 every row's own (delta_rows)
+  const int dsel = g.delta == nullptr ? 0 : g.delta_rows ? 2 : has_gather ? 1 : 0;
+  // opaque copy of the tile's first row: keeps the compiler from hoisting the
+  // per-row delta addresses above the main loop, where they would spill
+  int m0e = m0;
+  asm volatile("" : "+s"(m0e));
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-      // rows of the gathered path add their fp32 low-rank term before the rounding
-      const int gs = (gather_tile && row < nrows) ? g.gslot[m0 + row] : -1;
+      const int gs = (dsel == 0 || row >= nrows) ? -1 : dsel == 2 ? m0e + row : g.gslot[m0 + row];
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = wn * WN + 32 * j + (lane & 31);
@@ -542,9 +561,9 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs g) {
   const f32x4* src = reinterpret_cast<const f32x4*>(g.sk_part + (int64_t)t_sk * g.sk_split * (TM * TN)) + idx;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < g.sk_split; ++p) acc += src[(int64_t)p * (TM * TN / 4)];
-  if (has_gather && g.delta != nullptr) {
+  if ((has_gather || g.delta_rows) && g.delta != nullptr) {
     // rows of the gathered path add their fp32 low-rank term before the rounding
-    const int gs = g.gslot[m0 + row];
+    const int gs = g.delta_rows ? m0 + row : g.gslot[m0 + row];
     if (gs >= 0) acc += *reinterpret_cast<const f32x4*>(g.delta + (int64_t)gs * g.Nout + col);
   }
   const uint32_t lo = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
@@ -566,6 +585,7 @@ template <int MODE>
 __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int begin, int row, int j, float sum) {
   const int pr = g.rows ? g.rows[begin + row] : begin + row;
   if (MODE == 0) {
+    if (g.keep && g.row_train[pr] >= 0) sum *= g.drop_scale;  // dropout of a training row
     const uint16_t hb = f2bf(sum);
     if (g.out1) g.out1[(int64_t)pr * g.ld1 + j] = hb;
     if (g.out2) {
@@ -597,6 +617,10 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
     prow[t] = (i < cnt) ? (g.rows ? g.rows[begin + i] : begin + i) : -1;
     pp[t] = g.P + (int64_t)max(prow[t], 0) * g.ldp;
   }
+  // dropout: compact index of a lane's training row (-1: no mask)
+  int trl[RT];
+#pragma unroll
+  for (int t = 0; t < RT; ++t) trl[t] = (MODE == 0 && g.keep && prow[t] >= 0) ? g.row_train[prow[t]] : -1;
   f32x4 acc[RT][NJ];
 #pragma unroll
   for (int t = 0; t < RT; ++t)
@@ -617,7 +641,10 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
         const int k = (s0 + u) * 64 + 32 * h + 8 * (lane >> 4);
         const bool kin = s0 + u < s_hi && k < g.C;
 #pragma unroll
-        for (int t = 0; t < RT; ++t) av[u][h][t] = (prow[t] >= 0 && kin) ? ld16(pp[t] + k) : zero4();
+        for (int t = 0; t < RT; ++t) {
+          av[u][h][t] = (prow[t] >= 0 && kin) ? ld16(pp[t] + k) : zero4();
+          if (trl[t] >= 0 && kin) av[u][h][t] = keep8(av[u][h][t], keep_byte(g.keep, g.keep_words, trl[t], k));
+        }
 #pragma unroll
         for (int jt = 0; jt < NJ; ++jt) {
           const int j = 16 * jt + (lane & 15);
@@ -747,6 +774,7 @@ __global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g0, T
         if (t < thi && cin) {
           const int pr = g.prow ? g.prow[begin + t] : begin + t;
           v[u][e] = ld16(g.P + (int64_t)pr * g.ldp + c0);
+          if (g.keep) v[u][e] = keep8(v[u][e], keep_byte(g.keep, g.keep_words, begin + t, c0));
         }
       }
       const int nt = min(8, thi - tb);
@@ -825,6 +853,7 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutArgs o0, Reduc
   for (int p = tad_ptr[ta]; p < tad_ptr[ta + 1]; ++p)
     sum += g.part[((int64_t)tad_chunks[p] * C + c) * r_max + j];
   if (g.scales) sum *= g.scales[a];
+  sum *= g.post;
   float* o = g.a_layout ? g.out + ((int64_t)a * r_max + j) * C + c : g.out + ((int64_t)a * C + c) * r_max + j;
   *o = accumulate ? *o + sum : sum;
 }

@@ -10,6 +10,11 @@
 namespace dsv {
 namespace {
 
+// Dropout: is element k of compact training row i kept?
+__device__ __forceinline__ bool kept(const F32Args& g, int i, int k) {
+  return (g.keep[(int64_t)i * g.keep_words + (k >> 5)] >> (k & 31)) & 1u;
+}
+
 // h = x A_a^T for every row (j < r_a); training rows also into H_save.
 __global__ void f32_shrink(F32Args g) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -19,10 +24,12 @@ __global__ void f32_shrink(F32Args g) {
   if (j >= g.ranks[a]) return;
   const float* x = g.X + (int64_t)t * g.K;
   const float* Aj = g.A + ((int64_t)a * g.r_max + j) * g.K;
-  float acc = 0.f;
-  for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], Aj[k], acc);
-  g.Hall[(int64_t)t * g.r_max + j] = acc;
   const int tr = g.row_train[t];
+  const bool drop = g.keep && tr >= 0;  // dropout on a training row's low-rank input
+  float acc = 0.f;
+  for (int k = 0; k < g.K; ++k) acc = fmaf((drop && !kept(g, tr, k)) ? 0.f : x[k], Aj[k], acc);
+  if (drop) acc *= g.drop_scale;
+  g.Hall[(int64_t)t * g.r_max + j] = acc;
   if (tr >= 0 && g.Hsave) g.Hsave[(int64_t)tr * g.r_max + j] = acc;
 }
 
@@ -36,8 +43,10 @@ __global__ void f32_hrec(F32Args g) {
   if (j >= g.ranks[a]) return;
   const float* x = g.X + (int64_t)g.train_rows[i] * g.K;
   const float* Aj = g.A + ((int64_t)a * g.r_max + j) * g.K;
+  const bool drop = g.keep != nullptr;
   float acc = 0.f;
-  for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], Aj[k], acc);
+  for (int k = 0; k < g.K; ++k) acc = fmaf((drop && !kept(g, i, k)) ? 0.f : x[k], Aj[k], acc);
+  if (drop) acc *= g.drop_scale;
   g.Hrec[(int64_t)i * g.r_max + j] = acc;
 }
 
@@ -103,9 +112,12 @@ __global__ void f32_da(F32Args g) {
   float acc = 0.f;
   for (int p = g.tad_ptr[slot]; p < g.tad_ptr[slot + 1]; ++p) {
     const int32_t* ck = g.chunks + (int64_t)g.tad_chunks[p] * kItemWords;
-    for (int i = ck[1]; i < ck[1] + ck[2]; ++i)
-      acc = fmaf(g.G[(int64_t)i * g.r_max + j], g.X[(int64_t)g.train_rows[i] * g.K + k], acc);
+    for (int i = ck[1]; i < ck[1] + ck[2]; ++i) {
+      const float x = g.X[(int64_t)g.train_rows[i] * g.K + k];
+      acc = fmaf(g.G[(int64_t)i * g.r_max + j], (g.keep && !kept(g, i, k)) ? 0.f : x, acc);
+    }
   }
+  if (g.keep) acc *= g.drop_scale;
   float* o = g.dA + ((int64_t)a * g.r_max + j) * g.K + k;
   *o = g.accumulate ? *o + acc : acc;
 }
@@ -120,6 +132,7 @@ __global__ void f32_dx(F32Args g) {
   const float* gi = g.G + (int64_t)i * g.r_max;
   const float* Aa = g.A + (int64_t)a * g.r_max * g.K + k;
   for (int j = 0; j < r; ++j) acc = fmaf(gi[j], Aa[(int64_t)j * g.K], acc);
+  if (g.keep) acc = kept(g, i, k) ? acc * g.drop_scale : 0.f;  // through the dropout mask
   const float* dy = g.dY + (int64_t)i * g.N;
   for (int n = 0; n < g.N; ++n) acc = fmaf(dy[n], g.W[(int64_t)n * g.K + k], acc);
   g.dX[(int64_t)i * g.K + k] = acc;

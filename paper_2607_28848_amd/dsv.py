@@ -66,6 +66,18 @@ _lib.dsv_lora_bwd_workspace.restype = ctypes.c_int
 _lib.dsv_lora_bwd.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                               _vp, _vp, _i32, _vp, _sz, _vp]
 _lib.dsv_lora_bwd.restype = ctypes.c_int
+class Dropout(ctypes.Structure):
+    _fields_ = [("p", ctypes.c_double), ("seed", ctypes.c_uint64), ("offset", ctypes.c_uint64)]
+
+
+_lib.dsv_cobatch_fwd_dropout.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
+                                         ctypes.POINTER(Dropout), _vp, _sz, _vp]
+_lib.dsv_cobatch_fwd_dropout.restype = ctypes.c_int
+_lib.dsv_lora_bwd_dropout_workspace.argtypes = [_vp, ctypes.c_int, _i32, _i32, ctypes.POINTER(_sz)]
+_lib.dsv_lora_bwd_dropout_workspace.restype = ctypes.c_int
+_lib.dsv_lora_bwd_dropout.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
+                                      _vp, _vp, _i32, ctypes.POINTER(Dropout), _vp, _sz, _vp]
+_lib.dsv_lora_bwd_dropout.restype = ctypes.c_int
 _lib.dsv_timing_enable.argtypes = [_i32]
 _lib.dsv_timing_enable.restype = ctypes.c_int
 _lib.dsv_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), _i32p,
@@ -202,11 +214,23 @@ def fwd_workspace_bytes(plan: Plan, dtype_code: int, K: int, N: int) -> int:
     return int(n.value)
 
 
-def bwd_workspace_bytes(plan: Plan, dtype_code: int, K: int, N: int) -> int:
+def bwd_workspace_bytes(plan: Plan, dtype_code: int, K: int, N: int, dropout: bool = False) -> int:
     n = _sz(0)
-    _check(_lib.dsv_lora_bwd_workspace(plan.handle, dtype_code, K, N, ctypes.byref(n)),
-           "dsv_lora_bwd_workspace")
+    if dropout:
+        _check(_lib.dsv_lora_bwd_dropout_workspace(plan.handle, dtype_code, K, N, ctypes.byref(n)),
+               "dsv_lora_bwd_dropout_workspace")
+    else:
+        _check(_lib.dsv_lora_bwd_workspace(plan.handle, dtype_code, K, N, ctypes.byref(n)),
+               "dsv_lora_bwd_workspace")
     return int(n.value)
+
+
+def _dropout(dropout):
+    """(p, seed, offset) -> the C struct (None stays None)."""
+    if dropout is None:
+        return None
+    p, seed, offset = dropout
+    return Dropout(float(p), int(seed), int(offset))
 
 
 def _workspace(nbytes, device, given):
@@ -217,9 +241,11 @@ def _workspace(nbytes, device, given):
 
 
 def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, stream=None,
-                keep_h: bool = True):
+                keep_h: bool = True, dropout=None):
     """Y = X W^T + s_a (X A_a^T) B_a^T per row; H_save = X A_a^T of the training rows
-    (keep_h=False keeps none: lora_bwd with H_save=None recomputes it from X)."""
+    (keep_h=False keeps none: lora_bwd with H_save=None recomputes it from X).
+    dropout=(p, seed, offset): LoRA dropout on the training rows' adapter input
+    (dsv_cobatch_fwd_dropout)."""
     import torch
     dt = _dtype_code(X)
     T, K = X.shape
@@ -229,15 +255,23 @@ def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, str
     if H_save is None and plan.train_tokens > 0 and keep_h:
         H_save = torch.empty((plan.train_tokens, plan.r_max), dtype=X.dtype, device=X.device)
     ws = _workspace(fwd_workspace_bytes(plan, dt, K, N), X.device, workspace)
-    _check(_lib.dsv_cobatch_fwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y),
-                                _ptr(H_save), _ptr(ws), ws.numel() * ws.element_size(),
-                                _stream_handle(stream)), "dsv_cobatch_fwd")
+    d = _dropout(dropout)
+    if d is None:
+        _check(_lib.dsv_cobatch_fwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y),
+                                    _ptr(H_save), _ptr(ws), ws.numel() * ws.element_size(),
+                                    _stream_handle(stream)), "dsv_cobatch_fwd")
+    else:
+        _check(_lib.dsv_cobatch_fwd_dropout(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B),
+                                            _ptr(Y), _ptr(H_save), ctypes.byref(d), _ptr(ws),
+                                            ws.numel() * ws.element_size(), _stream_handle(stream)),
+               "dsv_cobatch_fwd_dropout")
     return Y, H_save
 
 
 def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want_dx=True,
-             accumulate: bool = False, workspace=None, stream=None):
-    """LoRA gradients of the training rows: dA, dB (fp32) and dX."""
+             accumulate: bool = False, workspace=None, stream=None, dropout=None):
+    """LoRA gradients of the training rows: dA, dB (fp32) and dX.  dropout=(p, seed,
+    offset) must repeat the forward's (dsv_lora_bwd_dropout)."""
     import torch
     dt = _dtype_code(X)
     T, K = X.shape
@@ -249,11 +283,19 @@ def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want
         dB = torch.zeros((n_ad, N, plan.r_max), dtype=torch.float32, device=X.device)
     if dX is None and want_dx and plan.train_tokens > 0:
         dX = torch.empty((plan.train_tokens, K), dtype=X.dtype, device=X.device)
-    ws = _workspace(bwd_workspace_bytes(plan, dt, K, N), X.device, workspace)
-    _check(_lib.dsv_lora_bwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H_save),
-                             _ptr(dY), _ptr(dA), _ptr(dB), _ptr(dX if want_dx else None),
-                             1 if accumulate else 0, _ptr(ws), ws.numel() * ws.element_size(),
-                             _stream_handle(stream)), "dsv_lora_bwd")
+    d = _dropout(dropout)
+    ws = _workspace(bwd_workspace_bytes(plan, dt, K, N, d is not None), X.device, workspace)
+    if d is None:
+        _check(_lib.dsv_lora_bwd(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H_save),
+                                 _ptr(dY), _ptr(dA), _ptr(dB), _ptr(dX if want_dx else None),
+                                 1 if accumulate else 0, _ptr(ws), ws.numel() * ws.element_size(),
+                                 _stream_handle(stream)), "dsv_lora_bwd")
+    else:
+        _check(_lib.dsv_lora_bwd_dropout(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B),
+                                         _ptr(H_save), _ptr(dY), _ptr(dA), _ptr(dB),
+                                         _ptr(dX if want_dx else None), 1 if accumulate else 0,
+                                         ctypes.byref(d), _ptr(ws), ws.numel() * ws.element_size(),
+                                         _stream_handle(stream)), "dsv_lora_bwd_dropout")
     return dA, dB, dX
 
 

@@ -53,13 +53,13 @@ class Run:
                                  dA=dA, dB=dB, want_dx=want_dx, accumulate=accumulate)
 
 
-def oracle_fwd(w, t, rows=None):
-    return oracle.forward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B, rows)
+def oracle_fwd(w, t, rows=None, drop=None):
+    return oracle.forward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B, rows, drop=drop)
 
 
-def oracle_bwd(w, t, dx_rows=None, dA=None, dB=None):
+def oracle_bwd(w, t, dx_rows=None, dA=None, dB=None, drop=None):
     return oracle.backward(w.segments, w.ranks, w.scales, w.r_max, t.X, t.W, t.A, t.B, t.dY,
-                           dA=dA, dB=dB, dx_rows=dx_rows)
+                           dA=dA, dB=dB, dx_rows=dx_rows, drop=drop)
 
 
 def train_mask_slices(w):

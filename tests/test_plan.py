@@ -296,3 +296,35 @@ def test_library_exports_every_declared_symbol():
     lib = dsv.lib_handle()
     for n in names:
         assert getattr(lib, n) is not None
+
+
+def test_dropout_argument_checks_on_host():
+    """dsv_cobatch_fwd_dropout / dsv_lora_bwd_dropout reject a missing dropout
+    (ERR_ARG) and p outside [0, 1) (ERR_RANGE) before looking at the plan's device
+    state; the dropout workspace of the backward is at least the plain one."""
+    import ctypes
+    dsv = _dsv()
+    lib = dsv.lib_handle()
+    plan = dsv.segments_build([(0, 16, 0, 1)], 16, [4], [2.0], 4)
+    fake = ctypes.c_void_p(4096)
+    args = [fake] * 4
+    for p in (-0.1, 1.0, 1.5, float("nan"), float("inf")):
+        d = dsv.Dropout(p, 1, 0)
+        assert lib.dsv_cobatch_fwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, ctypes.byref(d),
+                                           fake, 1 << 20, None) == dsv.ERR_RANGE
+        assert lib.dsv_lora_bwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, fake, fake, fake, 0,
+                                        ctypes.byref(d), fake, 1 << 20, None) == dsv.ERR_RANGE
+    assert lib.dsv_cobatch_fwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, None, fake, 1 << 20,
+                                       None) == dsv.ERR_ARG
+    assert lib.dsv_lora_bwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, fake, fake, fake, 0, None,
+                                    fake, 1 << 20, None) == dsv.ERR_ARG
+    d = dsv.Dropout(0.05, 1, 0)  # valid: the host-only plan is what is rejected
+    assert lib.dsv_cobatch_fwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, ctypes.byref(d), fake,
+                                       1 << 20, None) == dsv.ERR_ARG
+    for dt in (dsv.BF16, dsv.F32):
+        plain = dsv.bwd_workspace_bytes(plan, dt, 520, 64)
+        drop = dsv.bwd_workspace_bytes(plan, dt, 520, 64, dropout=True)
+        assert drop >= plain
+    # bf16 also holds the fp32 masked low-rank term of dX: T_t x K
+    assert (dsv.bwd_workspace_bytes(plan, dsv.BF16, 520, 64, dropout=True)
+            - dsv.bwd_workspace_bytes(plan, dsv.BF16, 520, 64)) >= 16 * 520 * 4
