@@ -149,6 +149,8 @@ def main():
     ap.add_argument("--cpu-dx-rows", type=int, default=24)
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timing of the steps that follow the layer (the AdamW update)")
+    ap.add_argument("--dropout", type=float, default=0.0, metavar="P",
+                    help="LoRA dropout P on the training rows in the timed step (fresh mask per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 3 plain device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -204,7 +206,8 @@ def main():
         d["dA"] = torch.zeros((w.n_adapters, w.r_max, K), dtype=torch.float32, device=dev)
         d["dB"] = torch.zeros((w.n_adapters, N, w.r_max), dtype=torch.float32, device=dev)
         d["wsf"] = torch.empty(max(dsv.fwd_workspace_bytes(probe, code, K, N), 256), dtype=torch.uint8, device=dev)
-        d["wsb"] = torch.empty(max(dsv.bwd_workspace_bytes(probe, code, K, N), 256), dtype=torch.uint8, device=dev)
+        d["wsb"] = torch.empty(max(dsv.bwd_workspace_bytes(probe, code, K, N, dropout=args.dropout > 0), 256),
+                               dtype=torch.uint8, device=dev)
         P.append(d)
     torch.cuda.synchronize()
     log("inputs resident on %s" % torch.cuda.get_device_name(dev))
@@ -235,13 +238,25 @@ def main():
         for p, proj in enumerate(w.projections):
             d = P[p]
             K, N = proj.K, proj.N
-            rc = lib.dsv_cobatch_fwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
-                                     ptr(d["Y"]), ptr(d["H"]), ptr(d["wsf"]), d["wsf"].numel(), sh)
+            if args.dropout > 0:
+                # one mask stream per projection and step: offset = step * projections + p
+                dr = ctypes.byref(dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p))
+                rc = lib.dsv_cobatch_fwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]),
+                                                 ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]), dr, ptr(d["wsf"]),
+                                                 d["wsf"].numel(), sh)
+            else:
+                rc = lib.dsv_cobatch_fwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                         ptr(d["Y"]), ptr(d["H"]), ptr(d["wsf"]), d["wsf"].numel(), sh)
             if rc != 0:
                 raise RuntimeError("dsv_cobatch_fwd failed: %d" % rc)
-            rc = lib.dsv_lora_bwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
-                                  ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
-                                  0, ptr(d["wsb"]), d["wsb"].numel(), sh)
+            if args.dropout > 0:
+                rc = lib.dsv_lora_bwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                              ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
+                                              0, dr, ptr(d["wsb"]), d["wsb"].numel(), sh)
+            else:
+                rc = lib.dsv_lora_bwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                      ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
+                                      0, ptr(d["wsb"]), d["wsb"].numel(), sh)
             if rc != 0:
                 raise RuntimeError("dsv_lora_bwd failed: %d" % rc)
         lib.dsv_plan_free(h)  # the blob's copy was issued; the device metadata stays valid
@@ -345,6 +360,35 @@ def main():
                                                                       for _ in w.projections))}
         log("backward with kept h %.1f us, with recomputed h %.1f us per step" % (bt[True], bt[False]))
 
+        # LoRA dropout 0.05 on the training rows (the fine-tuning setting of Sec. 4.1):
+        # the whole step (forward + backward of every projection) with and without it.
+        wsd = [torch.empty(max(dsv.bwd_workspace_bytes(probe, code, proj.K, proj.N, dropout=True), 256),
+                           dtype=torch.uint8, device=dev) for proj in w.projections]
+
+        def step_all(drop):
+            for p, proj in enumerate(w.projections):
+                d = P[p]
+                dsv.cobatch_fwd(probe_dev, d["X"], d["W"], d["A"], d["B"], Y=d["Y"], H_save=d["H"],
+                                workspace=d["wsf"], stream=stream, dropout=drop)
+                dsv.lora_bwd(probe_dev, d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], dA=d["dA"],
+                             dB=d["dB"], dX=d["dX"], workspace=wsd[p], stream=stream, dropout=drop)
+        dt_ = {}
+        for key in ("off", "p0.05", "off", "p0.05"):
+            drop = None if key == "off" else (0.05, 1234, 0)
+            step_all(drop)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(10):
+                step_all(drop)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            dt_[key] = e0.elapsed_time(e1) * 1e3 / 10
+        extras["dropout"] = {"p": 0.05, "step_us_without": round(dt_["off"], 2),
+                             "step_us_with": round(dt_["p0.05"], 2),
+                             "overhead_frac": round(dt_["p0.05"] / dt_["off"] - 1.0, 4)}
+        log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
+        del wsd
+
     def cfg_str(c):
         if not c["tile_m"]:
             return None
@@ -390,6 +434,7 @@ def main():
             "ranks": sorted(set(int(r) for r in w.ranks)),
             "algorithmic_gflop_per_step": round(step_flops / 1e9, 2),
             "plan_build_ms": round(float(np.median(plan_ms)), 4) if plan_ms else None,
+            "lora_dropout": args.dropout,
         },
         "roofline": {
             "kernel": "gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the "

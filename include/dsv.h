@@ -225,8 +225,8 @@ int dsv_cobatch_fwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, in
 
 /*
  * dsv_lora_bwd_dropout_workspace -- bytes of device workspace
- * dsv_lora_bwd_dropout needs (dsv_lora_bwd's, plus the regenerated mask and,
- * for bf16, an fp32 [T_t][K] buffer for the masked low-rank term of dX).
+ * dsv_lora_bwd_dropout needs (the regenerated mask, T_t ceil(K / 32) words,
+ * lives in it; at present the same size as dsv_lora_bwd_workspace).
  */
 int dsv_lora_bwd_dropout_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
                                    size_t* bytes);

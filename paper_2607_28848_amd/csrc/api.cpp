@@ -90,7 +90,7 @@ struct FwdWs {
   size_t h_all, delta, keep, sk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, hrec, part_b, part_a, keep, ddx, sk_part, total;
+  size_t bt, g, hrec, part_b, part_a, keep, sk_part, total;
 };
 
 // Dropout bitmask of the training rows: ceil(K / 32) words per row.
@@ -123,7 +123,7 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
   return w;
 }
 
-BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPlan& gp, bool dropout) {
+BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPlan& gp) {
   BwdWs w{};
   size_t off = 0;
   if (dt == DSV_BF16) {
@@ -146,8 +146,6 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
   }
   w.keep = off;  // dropout mask of the training rows
   off = align256(off + keep_bytes(p, K));
-  w.ddx = off;   // dropout: masked fp32 low-rank term of dX (bf16 path)
-  if (dropout && dt == DSV_BF16) off = align256(off + (size_t)p.T_t * K * 4);
   w.total = off;
   return w;
 }
@@ -318,7 +316,7 @@ extern "C" int dsv_lora_bwd_workspace(const dsv_plan* p, dsv_dtype dt, int32_t K
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   if (!bytes) return DSV_ERR_ARG;
-  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N), false).total;
+  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N)).total;
   return DSV_OK;
 }
 
@@ -327,7 +325,7 @@ extern "C" int dsv_lora_bwd_dropout_workspace(const dsv_plan* p, dsv_dtype dt, i
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   if (!bytes) return DSV_ERR_ARG;
-  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N), true).total;
+  *bytes = bwd_ws(*p, dt, K, N, bwd_gemm_plan(*p, dt, K, N)).total;
   return DSV_OK;
 }
 
@@ -481,7 +479,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   if (dX && !aligned16(dX)) return DSV_ERR_ARG;
   if (!ptr_ok(dY) || (H_save && !aligned16(H_save))) return DSV_ERR_ARG;
   const GemmPlan gp = bwd_gemm_plan(*p, dt, K, N);
-  const BwdWs ws = bwd_ws(*p, dt, K, N, gp, drop != nullptr);
+  const BwdWs ws = bwd_ws(*p, dt, K, N, gp);
   if (ws.total > 0) {
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
     if (workspace_bytes < ws.total) return DSV_ERR_SIZE;
@@ -626,26 +624,8 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     return DSV_ERR_DEVICE;
 
   // 5. dx = dy W + g A_a on the matrix cores (W read with a transposing load).
-  //    Under dropout the low-rank term passes through the mask first, so it is
-  //    formed apart (fp32, masked and scaled) and added in the epilogue.
-  float* ddx = nullptr;
-  if (dX && dropping) {
-    ddx = at<float>(workspace, ws.ddx);
-    DropoutDxArgs dd{};
-    dd.Tt = p->T_t;
-    dd.K = K;
-    dd.r_max = p->r_max;
-    dd.G = gm;
-    dd.ldg = ldh;
-    dd.A = static_cast<const uint16_t*>(A);
-    dd.train_adapter = p->dptr(L.train_adapter);
-    dd.ranks = ranks;
-    dd.keep = keep;
-    dd.keep_words = keep_words;
-    dd.scale = ds.scale;
-    dd.delta = ddx;
-    if ((e = launch_dropout_dx_low(dd, s)) != hipSuccess) return DSV_ERR_DEVICE;
-  }
+  //    Under dropout g A_a passes through the input's mask (in the accumulators,
+  //    between the low-rank prologue and the main loop).
   if (dX) {
     GemmArgs g{};
     g.P = static_cast<const uint16_t*>(dY);
@@ -667,10 +647,11 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     g.lq_col = 1;
     g.ranks = ranks;
     g.scales = nullptr;
-    g.delta = ddx;
+    g.delta = nullptr;
     g.gslot = nullptr;
-    g.no_prologue = ddx != nullptr;
-    g.delta_rows = ddx != nullptr;
+    g.keep = keep;
+    g.keep_words = keep_words;
+    g.keep_scale = ds.scale;
     const int tk = timing_begin(1, s);
     e = launch_gemm_nn(g, gp.tm, gp.tn, s);
     timing_end(tk, s);

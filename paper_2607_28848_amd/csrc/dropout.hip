@@ -26,8 +26,9 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
       k0 += W0;
       k1 += W1;
     }
-    const uint32_t hi0 = __umulhi(M0, c[0]), lo0 = M0 * c[0];
-    const uint32_t hi1 = __umulhi(M1, c[2]), lo1 = M1 * c[2];
+    const uint64_t p0 = (uint64_t)M0 * c[0], p1 = (uint64_t)M1 * c[2];
+    const uint32_t hi0 = (uint32_t)(p0 >> 32), lo0 = (uint32_t)p0;
+    const uint32_t hi1 = (uint32_t)(p1 >> 32), lo1 = (uint32_t)p1;
     const uint32_t n0 = hi1 ^ c[1] ^ k0, n2 = hi0 ^ c[3] ^ k1;
     c[0] = n0;
     c[1] = lo1;
@@ -55,43 +56,6 @@ __global__ __launch_bounds__(256) void dropout_mask_kernel(uint32_t* __restrict_
   bits[idx] = m;
 }
 
-// Low-rank term of dX under dropout (bf16 path): for compact training row i,
-// delta[i][k] = scale * keep(i, k) * sum_j g[i][j] A_a[j][k], fp32, added to
-// dy W in the dX GEMM's epilogue.  8 columns per thread.
-__global__ __launch_bounds__(256) void dropout_dx_low_kernel(DropoutDxArgs a) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int kb = a.K / 8;
-  if (idx >= (int64_t)a.Tt * kb) return;
-  const int i = (int)(idx / kb), k0 = 8 * (int)(idx % kb);
-  const int ad = a.train_adapter[i], r = a.ranks[ad];
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  const uint16_t* gi = a.G + (int64_t)i * a.ldg;
-  const uint16_t* Aa = a.A + (int64_t)ad * a.r_max * a.K + k0;
-  for (int j = 0; j < r; ++j) {
-    const float gj = __uint_as_float((uint32_t)gi[j] << 16);
-    const uint4 v = *reinterpret_cast<const uint4*>(Aa + (int64_t)j * a.K);
-    const uint32_t w[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      acc[2 * e] = fmaf(gj, __uint_as_float(w[e] << 16), acc[2 * e]);
-      acc[2 * e + 1] = fmaf(gj, __uint_as_float(w[e] & 0xffff0000u), acc[2 * e + 1]);
-    }
-  }
-  const uint32_t m = (a.keep[(int64_t)i * a.keep_words + (k0 >> 5)] >> (k0 & 31)) & 0xffu;
-  float* out = a.delta + (int64_t)i * a.K + k0;
-  float4 lo, hi;
-  lo.x = (m & 1u) ? a.scale * acc[0] : 0.f;
-  lo.y = (m & 2u) ? a.scale * acc[1] : 0.f;
-  lo.z = (m & 4u) ? a.scale * acc[2] : 0.f;
-  lo.w = (m & 8u) ? a.scale * acc[3] : 0.f;
-  hi.x = (m & 16u) ? a.scale * acc[4] : 0.f;
-  hi.y = (m & 32u) ? a.scale * acc[5] : 0.f;
-  hi.z = (m & 64u) ? a.scale * acc[6] : 0.f;
-  hi.w = (m & 128u) ? a.scale * acc[7] : 0.f;
-  *reinterpret_cast<float4*>(out) = lo;
-  *reinterpret_cast<float4*>(out + 4) = hi;
-}
-
 }  // namespace
 
 hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const DropoutSpec& d, hipStream_t s) {
@@ -101,13 +65,6 @@ hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const Drop
   hipLaunchKernelGGL(dropout_mask_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, bits, Tt, words,
                      d.thr, (uint32_t)d.seed, (uint32_t)(d.seed >> 32), (uint32_t)d.offset,
                      (uint32_t)(d.offset >> 32));
-  return hipGetLastError();
-}
-
-hipError_t launch_dropout_dx_low(const DropoutDxArgs& a, hipStream_t s) {
-  if (a.Tt <= 0) return hipSuccess;
-  const int64_t n = (int64_t)a.Tt * (a.K / 8);
-  hipLaunchKernelGGL(dropout_dx_low_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -41,10 +41,12 @@ struct GemmArgs {
   // slot per piece); a second kernel sums them and writes those tiles.
   int32_t dp_tiles, sk_tiles, sk_split;
   float* sk_part;
-  // no_prologue: the low-rank term is not added in the prologue;
-  // delta_rows: every row r adds delta[r][n] (its own fp32 term) instead of
-  // only the gathered rows through gslot
-  int32_t no_prologue, delta_rows;
+  // dX under LoRA dropout: the prologue's low-rank term of row r, column c is
+  // kept (times keep_scale) when bit c % 32 of keep[r][c / 32] is set, else
+  // zeroed, before the main loop adds the base product (keep == nullptr: none)
+  const uint32_t* keep;
+  int32_t keep_words;
+  float keep_scale;
 };
 
 // Rank-r contraction of a few rows of one adapter (shrink h = x A^T, and
@@ -141,7 +143,7 @@ struct AdamWArgs {
 hipError_t launch_adamw(const AdamWArgs& a, int32_t n_tads, hipStream_t s);
 
 // LoRA dropout of the training rows: mask parameters (thr = floor(p 2^32),
-// scale = 1 / (1 - p)), the bitmask kernel, and the masked low-rank dX term.
+// scale = 1 / (1 - p)) and the bitmask kernel.
 struct DropoutSpec {
   uint32_t thr;
   float scale;
@@ -149,19 +151,7 @@ struct DropoutSpec {
 };
 // bits: [Tt][ceil(K / 32)] words, bit b of word w keeps column 32 w + b.
 hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const DropoutSpec& d, hipStream_t s);
-struct DropoutDxArgs {
-  int32_t Tt, K, r_max;
-  const uint16_t* G;            // g of the training rows [Tt][ldg] bf16
-  int64_t ldg;
-  const uint16_t* A;            // adapter stacks [n_ad][r_max][K] bf16
-  const int32_t* train_adapter; // compact row -> adapter
-  const int32_t* ranks;
-  const uint32_t* keep;         // bitmask
-  int32_t keep_words;
-  float scale;
-  float* delta;                 // [Tt][K] fp32 out
-};
-hipError_t launch_dropout_dx_low(const DropoutDxArgs& a, hipStream_t s);
+
 
 // Launchers (fp32 mode: plain FMA kernels, same semantics).
 struct F32Args {

@@ -317,7 +317,7 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // and split into bf16 hi + lo (|lo| <= 2^-9 |hi|), so the product carries
   // the scale to about 2^-16 relative with no VALU work on the accumulators;
   // with scale 1 (or a power of two) lo is exactly zero and is skipped.
-  for (int gi = 0; kb == 0 && !g.no_prologue && gi < ngroups; ++gi) {
+  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
     const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
     if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
     const int r = g.ranks[a];
@@ -370,6 +370,31 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
           for (int j = 0; j < FN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af_lo[i], bq[j], acc[i][j], 0, 0, 0);
       }
+    }
+  }
+
+  // ---- dropout of the low-rank term (dX under LoRA dropout) --------------
+  // The prologue left g A_a in the accumulators; it passes through the input's
+  // mask before dy W is added: kept elements scaled by 1 / (1 - p), dropped
+  // ones zeroed.  Lane columns are fixed per j, so a row needs FN mask words.
+  if (NN && kb == 0 && g.keep != nullptr) {  // the dX GEMM only
+    const int wcol = (n0 + wn * WN) >> 5;  // first mask word of the wave's columns
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      uint32_t mw[16][FN];
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          mw[v][j] = (row < nrows && wcol + j < g.keep_words)
+                         ? g.keep[(int64_t)(m0 + row) * g.keep_words + wcol + j] : 0u;
+      }
+#pragma unroll
+      for (int v = 0; v < 16; ++v)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j][v] = ((mw[v][j] >> (lane & 31)) & 1u) ? acc[i][j][v] * g.keep_scale : 0.f;
     }
   }
 
@@ -480,19 +505,14 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // ---- epilogue: one rounding, staged through LDS for 16-byte stores ----
   __syncthreads();
   uint16_t* st = reinterpret_cast<uint16_t*>(smem);
-  // fp32 low-rank terms added before the rounding: 0 none, 1 the gathered
-  // rows' (through gslot), 2 every row's own (delta_rows)
-  const int dsel = g.delta == nullptr ? 0 : g.delta_rows ? 2 : has_gather ? 1 : 0;
-  // opaque copy of the tile's first row: keeps the compiler from hoisting the
-  // per-row delta addresses above the main loop, where they would spill
-  int m0e = m0;
-  asm volatile("" : "+s"(m0e));
+  const bool gather_tile = has_gather && g.delta != nullptr;
 #pragma unroll
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int v = 0; v < 16; ++v) {
       const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-      const int gs = (dsel == 0 || row >= nrows) ? -1 : dsel == 2 ? m0e + row : g.gslot[m0 + row];
+      // rows of the gathered path add their fp32 low-rank term before the rounding
+      const int gs = (gather_tile && row < nrows) ? g.gslot[m0 + row] : -1;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = wn * WN + 32 * j + (lane & 31);
@@ -561,9 +581,9 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs g) {
   const f32x4* src = reinterpret_cast<const f32x4*>(g.sk_part + (int64_t)t_sk * g.sk_split * (TM * TN)) + idx;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int p = 0; p < g.sk_split; ++p) acc += src[(int64_t)p * (TM * TN / 4)];
-  if ((has_gather || g.delta_rows) && g.delta != nullptr) {
+  if (has_gather && g.delta != nullptr) {
     // rows of the gathered path add their fp32 low-rank term before the rounding
-    const int gs = g.delta_rows ? m0 + row : g.gslot[m0 + row];
+    const int gs = g.gslot[m0 + row];
     if (gs >= 0) acc += *reinterpret_cast<const f32x4*>(g.delta + (int64_t)gs * g.Nout + col);
   }
   const uint32_t lo = (uint32_t)f2bf(acc[0]) | ((uint32_t)f2bf(acc[1]) << 16);
