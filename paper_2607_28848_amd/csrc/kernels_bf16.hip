@@ -618,10 +618,14 @@ __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int beg
   }
 }
 
-template <int MODE, int NJ, int ROWS>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
+// DROP (shrink only): the training rows' input passes through the dropout mask.
+template <int MODE, int NJ, int ROWS, bool DROP>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
 __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
-  constexpr int U = NJ <= 2 ? 4 : 2;
   constexpr int RT = ROWS / 16;  // 16-row tiles per item
+  // U slices per batch; two batches in registers (the next one loads while
+  // the current one feeds the matrix cores)
+  constexpr int U0 = RT + NJ <= 3 ? 4 : RT + NJ <= 4 ? 2 : 1;
+  constexpr int U = DROP && U0 > 2 ? 2 : U0;  // room for the mask bytes
   __shared__ float red[SW][ROWS][DSV_MAX_RANK + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
@@ -640,46 +644,67 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
   // dropout: compact index of a lane's training row (-1: no mask)
   int trl[RT];
 #pragma unroll
-  for (int t = 0; t < RT; ++t) trl[t] = (MODE == 0 && g.keep && prow[t] >= 0) ? g.row_train[prow[t]] : -1;
+  for (int t = 0; t < RT; ++t) trl[t] = (DROP && prow[t] >= 0) ? g.row_train[prow[t]] : -1;
   f32x4 acc[RT][NJ];
 #pragma unroll
   for (int t = 0; t < RT; ++t)
 #pragma unroll
     for (int jt = 0; jt < NJ; ++jt) acc[t][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
   // each wave takes a contiguous range of 64-wide slices (two 32-wide MFMA
-  // steps each), U consecutive slices per pass, so every row is read in runs
-  // of U * 128 bytes
+  // steps each), U consecutive slices per batch, so every row is read in
+  // runs of U * 128 bytes
   const int nslices = (g.C + 63) / 64;
   const int per_wave = (nslices + SW - 1) / SW;
   const int s_lo = wave * per_wave, s_hi = min(nslices, s_lo + per_wave);
-  for (int s0 = s_lo; s0 < s_hi; s0 += U) {
-    u32x4 av[U][2][RT], bv[U][2][NJ];
+  // Every lane issues every load (out-of-range lanes read a valid address and
+  // drop the value), so the loads are straight-line code and the wait before
+  // a batch's MFMAs counts only that batch's loads.
+  // Under dropout the mask bytes travel with the batch and are applied where
+  // the batch is consumed, so the loads of the next batch are not held up.
+  auto load = [&](int s0, u32x4 (&av)[U][2][RT], u32x4 (&bv)[U][2][NJ], uint32_t (&mb)[U][2][RT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const int k = (s0 + u) * 64 + 32 * h + 8 * (lane >> 4);
         const bool kin = s0 + u < s_hi && k < g.C;
+        const int kc = kin ? k : 0;
 #pragma unroll
         for (int t = 0; t < RT; ++t) {
-          av[u][h][t] = (prow[t] >= 0 && kin) ? ld16(pp[t] + k) : zero4();
-          if (trl[t] >= 0 && kin) av[u][h][t] = keep8(av[u][h][t], keep_byte(g.keep, g.keep_words, trl[t], k));
+          const u32x4 v = ld16(pp[t] + kc);
+          av[u][h][t] = (prow[t] >= 0 && kin) ? v : zero4();
+          if constexpr (DROP) mb[u][h][t] = keep_byte(g.keep, g.keep_words, max(trl[t], 0), kc);
         }
 #pragma unroll
         for (int jt = 0; jt < NJ; ++jt) {
           const int j = 16 * jt + (lane & 15);
-          bv[u][h][jt] = (j < r && kin) ? ld16(Qa + (int64_t)j * g.ldq + k) : zero4();
+          const u32x4 w = ld16(Qa + (int64_t)min(j, r - 1) * g.ldq + kc);
+          bv[u][h][jt] = (j < r && kin) ? w : zero4();
         }
       }
+  };
+  auto mma = [&](const u32x4 (&av)[U][2][RT], const u32x4 (&bv)[U][2][NJ], const uint32_t (&mb)[U][2][RT]) {
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int t = 0; t < RT; ++t)
+        for (int t = 0; t < RT; ++t) {
+          const u32x4 x = (DROP && trl[t] >= 0) ? keep8(av[u][h][t], mb[u][h][t]) : av[u][h][t];
 #pragma unroll
           for (int jt = 0; jt < NJ; ++jt)
-            acc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av[u][h][t]), as_bf(bv[u][h][jt]), acc[t][jt], 0, 0, 0);
+            acc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(x), as_bf(bv[u][h][jt]), acc[t][jt], 0, 0, 0);
+        }
+  };
+  u32x4 av0[U][2][RT], bv0[U][2][NJ], av1[U][2][RT], bv1[U][2][NJ];
+  uint32_t mb0[U][2][RT], mb1[U][2][RT];
+  if (s_lo < s_hi) load(s_lo, av0, bv0, mb0);
+  for (int s0 = s_lo; s0 < s_hi; s0 += 2 * U) {
+    if (s0 + U < s_hi) load(s0 + U, av1, bv1, mb1);
+    mma(av0, bv0, mb0);
+    if (s0 + U >= s_hi) break;
+    if (s0 + 2 * U < s_hi) load(s0 + 2 * U, av0, bv0, mb0);
+    mma(av1, bv1, mb1);
   }
 #pragma unroll
   for (int t = 0; t < RT; ++t)
@@ -937,15 +962,25 @@ hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
 }
 
 namespace {
+template <int MODE, int ROWS, bool DROP>
+void launch_skinny_nj(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
+  if (r_max <= 16)
+    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS, DROP>), dim3(n_items), dim3(64 * SW), 0, s, a);
+  else if (r_max <= 32)
+    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS, DROP>), dim3(n_items), dim3(64 * SW), 0, s, a);
+  else
+    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS, DROP>), dim3(n_items), dim3(64 * SW), 0, s, a);
+}
+
 template <int MODE, int ROWS>
 hipError_t launch_skinny(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   if (n_items <= 0) return hipSuccess;
-  if (r_max <= 16)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
-  else if (r_max <= 32)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
-  else
-    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS>), dim3(n_items), dim3(64 * SW), 0, s, a);
+  if constexpr (MODE == 0) {
+    if (a.keep != nullptr) launch_skinny_nj<MODE, ROWS, true>(a, n_items, r_max, s);
+    else launch_skinny_nj<MODE, ROWS, false>(a, n_items, r_max, s);
+  } else {
+    launch_skinny_nj<MODE, ROWS, false>(a, n_items, r_max, s);
+  }
   return hipGetLastError();
 }
 }  // namespace
