@@ -149,6 +149,8 @@ def main():
     ap.add_argument("--cpu-dx-rows", type=int, default=24)
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timing of the steps that follow the layer (the AdamW update)")
+    ap.add_argument("--grouped", action="store_true",
+                    help="run the layer set through the grouped entry points (one launch per step kind)")
     ap.add_argument("--dropout", type=float, default=0.0, metavar="P",
                     help="LoRA dropout P on the training rows in the timed step (fresh mask per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -224,6 +226,21 @@ def main():
     sh = ctypes.c_void_p(int(stream.cuda_stream))
     ptr = lambda t: ctypes.c_void_p(int(t.data_ptr()))  # noqa: E731
     plan_ms = []
+    if args.grouped:
+        if args.dropout > 0:
+            raise SystemExit("--grouped has no dropout form")
+        shapes = [(proj.K, proj.N) for proj in w.projections]
+        fproj = (dsv.FwdProj * len(P))()
+        bproj = (dsv.BwdProj * len(P))()
+        for p, (K, N) in enumerate(shapes):
+            d = P[p]
+            fproj[p] = dsv.FwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]))
+            bproj[p] = dsv.BwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["H"]), ptr(d["dY"]),
+                                   ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]))
+        gws_f = torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes), 256), dtype=torch.uint8,
+                            device=dev)
+        gws_b = torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes), 256), dtype=torch.uint8,
+                            device=dev)
 
     def step(i):
         h = ctypes.c_void_p()
@@ -235,6 +252,15 @@ def main():
         plan_ms.append((time.perf_counter() - tp) * 1e3)
         if rc != 0:
             raise RuntimeError("dsv_segments_build failed: %d" % rc)
+        if args.grouped:
+            rc = lib.dsv_cobatch_fwd_grouped(h, code, len(w.projections), fproj, ptr(gws_f), gws_f.numel(), sh)
+            if rc != 0:
+                raise RuntimeError("dsv_cobatch_fwd_grouped failed: %d" % rc)
+            rc = lib.dsv_lora_bwd_grouped(h, code, len(w.projections), bproj, 0, ptr(gws_b), gws_b.numel(), sh)
+            if rc != 0:
+                raise RuntimeError("dsv_lora_bwd_grouped failed: %d" % rc)
+            lib.dsv_plan_free(h)
+            return
         for p, proj in enumerate(w.projections):
             d = P[p]
             K, N = proj.K, proj.N
@@ -289,8 +315,9 @@ def main():
     fwd_gemm_flops = sum(gemm_fwd_flops(w, proj, gathered) for proj in w.projections)
     bwd_gemm_flops = sum(gemm_bwd_flops(w, proj) for proj in w.projections)
     fwd_avg_ms = fwd_ms / max(fwd_n, 1)
-    achieved = fwd_gemm_flops * (fwd_n / len(w.projections)) / (fwd_ms / 1e3) / 1e12 if fwd_ms > 0 else None
-    bwd_achieved = bwd_gemm_flops * (bwd_n / len(w.projections)) / (bwd_ms / 1e3) / 1e12 if bwd_ms > 0 else None
+    per_step = 1 if args.grouped else len(w.projections)  # timed GEMM launches per step
+    achieved = fwd_gemm_flops * (fwd_n / per_step) / (fwd_ms / 1e3) / 1e12 if fwd_ms > 0 else None
+    bwd_achieved = bwd_gemm_flops * (bwd_n / per_step) / (bwd_ms / 1e3) / 1e12 if bwd_ms > 0 else None
     log("timed %d steps: %.3f ms/step, %.1f TFLOP/s; fwd GEMM %.1f TFLOP/s avg %.1f us; dX GEMM %s TFLOP/s"
         % (args.steps, ms_per_step, value, achieved or 0, fwd_avg_ms * 1e3,
            "%.1f" % bwd_achieved if bwd_achieved else "n/a"))
@@ -435,6 +462,7 @@ def main():
             "algorithmic_gflop_per_step": round(step_flops / 1e9, 2),
             "plan_build_ms": round(float(np.median(plan_ms)), 4) if plan_ms else None,
             "lora_dropout": args.dropout,
+            "launch": "grouped" if args.grouped else "per projection",
         },
         "roofline": {
             "kernel": "gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the "

@@ -249,6 +249,62 @@ int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32
                          size_t workspace_bytes, void* hip_stream);
 
 /*
+ * Grouped launches over several projections of one batch (the paper's layer
+ * set: q/k/v/o and gate/up/down all see the same segment table, Sec. 4.1).
+ * dsv_cobatch_fwd_grouped and dsv_lora_bwd_grouped compute, for every entry of
+ * projs[0 .. n_proj), exactly what dsv_cobatch_fwd / dsv_lora_bwd compute for
+ * it, with one launch per step for all projections instead of one per
+ * projection: the rank-r kernels, token reductions and final sums run the
+ * projections side by side, and the base GEMMs of all projections form one
+ * launch of whole 256 x 256 tiles ordered by contraction length (longest
+ * first), so one projection's last partial wave is filled by the next one's
+ * tiles.  Operands may alias across entries (q/k/v read one X); outputs must
+ * not.  1 <= n_proj <= DSV_MAX_GROUP; n_proj = 1 is the single-projection
+ * call.  Each entry follows the single call's shape, layout and alignment
+ * rules; any entry that fails them fails the whole call before any launch.
+ * The bf16 results may differ from the single calls in the last bit where
+ * those split a tile along the contraction (another summation order);
+ * repeated grouped calls are bit-identical.  The workspace holds the
+ * single-call regions of every projection, 256-byte aligned, of at least the
+ * *_grouped_workspace size.  Dropout is not offered in grouped form.
+ */
+#define DSV_MAX_GROUP 8
+
+typedef struct {
+  int32_t K, N;           /* in / out features of this projection */
+  const void* X;          /* [T][K] */
+  const void* W;          /* [N][K] */
+  const void* A;          /* [n_ad][r_max][K] */
+  const void* B;          /* [n_ad][N][r_max] */
+  void* Y;                /* [T][N] out */
+  void* H_save;           /* [T_t][r_max] out, or NULL (residual-only retention) */
+} dsv_fwd_proj;
+
+typedef struct {
+  int32_t K, N;
+  const void* X;          /* [T][K] */
+  const void* W;          /* [N][K] */
+  const void* A;          /* [n_ad][r_max][K] */
+  const void* B;          /* [n_ad][N][r_max] */
+  const void* H_save;     /* [T_t][r_max], or NULL: recomputed from X */
+  const void* dY;         /* [T_t][N] */
+  float* dA;              /* [n_ad][r_max][K] fp32 */
+  float* dB;              /* [n_ad][N][r_max] fp32 */
+  void* dX;               /* [T_t][K], or NULL: not computed */
+} dsv_bwd_proj;
+
+int dsv_cobatch_fwd_grouped_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                                      const dsv_fwd_proj* projs, size_t* bytes);
+int dsv_cobatch_fwd_grouped(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                            const dsv_fwd_proj* projs, void* workspace, size_t workspace_bytes,
+                            void* hip_stream);
+int dsv_lora_bwd_grouped_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                                   const dsv_bwd_proj* projs, size_t* bytes);
+int dsv_lora_bwd_grouped(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                         const dsv_bwd_proj* projs, int32_t accumulate, void* workspace,
+                         size_t workspace_bytes, void* hip_stream);
+
+/*
  * Kernel timing for benchmarks.  While enabled (on = 1), every
  * dsv_cobatch_fwd / dsv_lora_bwd call records a HIP event pair on its own
  * stream immediately around its matrix-core GEMM launch (forward: the base

@@ -693,3 +693,396 @@ extern "C" int dsv_lora_bwd_dropout(const dsv_plan* p, dsv_dtype dt, int32_t K, 
   return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, dropout, workspace,
                   workspace_bytes, hip_stream);
 }
+
+// ---------------------------------------------------------------------------
+// Grouped launches: several projections of one batch (one plan) with one
+// launch per step kind.  GEMMs take whole 256x256 tiles of every projection in
+// one launch, longest contraction first, so the tail of one projection is
+// filled by the tiles of the next instead of being split.
+// ---------------------------------------------------------------------------
+namespace {
+
+static_assert(kMaxGroup == DSV_MAX_GROUP, "group size of the kernels and the interface");
+
+GemmPlan whole256(int32_t m256, int32_t n_out) {
+  GemmPlan g;
+  g.tm = g.tn = 256;
+  g.n_mtiles = m256;
+  g.n_ntiles = (n_out + 255) / 256;
+  g.dp_tiles = g.n_mtiles * g.n_ntiles;
+  return g;
+}
+
+int check_group(const dsv_plan* p, dsv_dtype dt, int32_t n, const void* projs) {
+  if (!p || !projs) return DSV_ERR_ARG;
+  if (n < 1 || n > DSV_MAX_GROUP) return DSV_ERR_RANGE;
+  if (dt != DSV_BF16 && dt != DSV_F32) return DSV_ERR_RANGE;
+  return DSV_OK;
+}
+
+// Workspace of a grouped call: each projection's single-call regions (without
+// split-tile partials for bf16), one after the other.
+size_t fwd_group_ws(const dsv_plan& p, dsv_dtype dt, int32_t n, const dsv_fwd_proj* pr, size_t* base,
+                    FwdWs* w) {
+  size_t off = 0;
+  for (int i = 0; i < n; ++i) {
+    const GemmPlan gp = dt == DSV_BF16 ? whole256(p.n_ftiles, pr[i].N) : GemmPlan{};
+    w[i] = fwd_ws(p, dt, pr[i].K, pr[i].N, gp);
+    base[i] = off;
+    off = align256(off + w[i].total);
+  }
+  return off;
+}
+
+size_t bwd_group_ws(const dsv_plan& p, dsv_dtype dt, int32_t n, const dsv_bwd_proj* pr, size_t* base,
+                    BwdWs* w) {
+  size_t off = 0;
+  for (int i = 0; i < n; ++i) {
+    const GemmPlan gp = dt == DSV_BF16 ? whole256(p.n_btiles, pr[i].K) : GemmPlan{};
+    w[i] = bwd_ws(p, dt, pr[i].K, pr[i].N, gp);
+    base[i] = off;
+    off = align256(off + w[i].total);
+  }
+  return off;
+}
+
+// projections in launch order: longest contraction first (stable)
+void by_contraction(int32_t n, const int32_t* C, int32_t* order) {
+  for (int i = 0; i < n; ++i) order[i] = i;
+  std::stable_sort(order, order + n, [&](int32_t a, int32_t b) { return C[a] > C[b]; });
+}
+
+}  // namespace
+
+extern "C" int dsv_cobatch_fwd_grouped_workspace(const dsv_plan* p, dsv_dtype dt, int32_t n_proj,
+                                                 const dsv_fwd_proj* projs, size_t* bytes) {
+  int rc = check_group(p, dt, n_proj, projs);
+  if (rc != DSV_OK) return rc;
+  if (!bytes) return DSV_ERR_ARG;
+  if (n_proj == 1) return dsv_cobatch_fwd_workspace(p, dt, projs[0].K, projs[0].N, bytes);
+  for (int i = 0; i < n_proj; ++i)
+    if ((rc = check_common(p, dt, projs[i].K, projs[i].N)) != DSV_OK) return rc;
+  size_t base[DSV_MAX_GROUP];
+  FwdWs w[DSV_MAX_GROUP];
+  *bytes = fwd_group_ws(*p, dt, n_proj, projs, base, w);
+  return DSV_OK;
+}
+
+extern "C" int dsv_lora_bwd_grouped_workspace(const dsv_plan* p, dsv_dtype dt, int32_t n_proj,
+                                              const dsv_bwd_proj* projs, size_t* bytes) {
+  int rc = check_group(p, dt, n_proj, projs);
+  if (rc != DSV_OK) return rc;
+  if (!bytes) return DSV_ERR_ARG;
+  if (n_proj == 1) return dsv_lora_bwd_workspace(p, dt, projs[0].K, projs[0].N, bytes);
+  for (int i = 0; i < n_proj; ++i)
+    if ((rc = check_common(p, dt, projs[i].K, projs[i].N)) != DSV_OK) return rc;
+  size_t base[DSV_MAX_GROUP];
+  BwdWs w[DSV_MAX_GROUP];
+  *bytes = bwd_group_ws(*p, dt, n_proj, projs, base, w);
+  return DSV_OK;
+}
+
+extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_fwd_proj* projs,
+                                       void* workspace, size_t workspace_bytes, void* hip_stream) {
+  int rc = check_group(p, dt, n_proj, projs);
+  if (rc != DSV_OK) return rc;
+  if (n_proj == 1) {
+    const dsv_fwd_proj& q = projs[0];
+    return dsv_cobatch_fwd(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, workspace, workspace_bytes,
+                           hip_stream);
+  }
+  // every check before any launch
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_fwd_proj& q = projs[i];
+    if ((rc = check_common(p, dt, q.K, q.N)) != DSV_OK) return rc;
+  }
+  if (!p->d_meta) return DSV_ERR_ARG;
+  if (p->T == 0) return DSV_OK;
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_fwd_proj& q = projs[i];
+    if (!ptr_ok(q.X) || !ptr_ok(q.W) || !ptr_ok(q.A) || !ptr_ok(q.B) || !ptr_ok(q.Y)) return DSV_ERR_ARG;
+    if (q.H_save && !aligned16(q.H_save)) return DSV_ERR_ARG;
+  }
+  size_t base[DSV_MAX_GROUP];
+  FwdWs w[DSV_MAX_GROUP];
+  const size_t total = fwd_group_ws(*p, dt, n_proj, projs, base, w);
+  if (total > 0) {
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
+    if (workspace_bytes < total) return DSV_ERR_SIZE;
+  }
+  char* wsb = static_cast<char*>(workspace);
+  if (dt == DSV_F32) {  // the fp32 check path: the single-projection kernels, one projection at a time
+    for (int i = 0; i < n_proj; ++i) {
+      const dsv_fwd_proj& q = projs[i];
+      rc = fwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, nullptr, wsb + base[i], w[i].total,
+                    hip_stream);
+      if (rc != DSV_OK) return rc;
+    }
+    return DSV_OK;
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const MetaLayout& L = p->lay;
+  const int32_t* ranks = p->dptr(L.ranks);
+  const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
+  const int64_t ldh = ld_rank(p->r_max);
+
+  // 1. shrink of every projection in one launch
+  SkinnyGroup sg{};
+  sg.n = n_proj;
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_fwd_proj& q = projs[i];
+    SkinnyArgs& sk = sg.a[i];
+    sk.P = static_cast<const uint16_t*>(q.X);
+    sk.ldp = q.K;
+    sk.rows = p->dptr(L.shrink_rows);
+    sk.items = p->dptr(L.shrink_items);
+    sk.Q = static_cast<const uint16_t*>(q.A);
+    sk.q_ad = (int64_t)p->r_max * q.K;
+    sk.ldq = q.K;
+    sk.ranks = ranks;
+    sk.C = q.K;
+    sk.out1 = at<uint16_t>(wsb + base[i], w[i].h_all);
+    sk.ld1 = ldh;
+    sk.out2 = p->T_t > 0 ? static_cast<uint16_t*>(q.H_save) : nullptr;
+    sk.ld2 = p->r_max;
+    sk.row_train = p->dptr(L.row_train);
+  }
+  if (launch_shrink_group(sg, p->n_shrink, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 2. gathered rows of every projection in one launch
+  if (p->n_gather > 0) {
+    GatherGroup gg{};
+    gg.n = n_proj;
+    for (int i = 0; i < n_proj; ++i) {
+      gg.a[i] = GatherArgs{sg.a[i].out1, static_cast<const uint16_t*>(projs[i].B), projs[i].N,
+                           at<float>(wsb + base[i], w[i].delta)};
+      gg.yoff[i + 1] = gg.yoff[i] + (projs[i].N + 255) / 256;
+    }
+    if (launch_gather_group(gg, ldh, p->r_max, p->dptr(L.gather_items), p->n_gitems, p->dptr(L.gather_rows),
+                            ranks, scales, s) != hipSuccess)
+      return DSV_ERR_DEVICE;
+  }
+
+  // 3. every base GEMM in one launch, longest contraction first
+  int32_t Cs[DSV_MAX_GROUP], order[DSV_MAX_GROUP];
+  for (int i = 0; i < n_proj; ++i) Cs[i] = projs[i].K;
+  by_contraction(n_proj, Cs, order);
+  GemmGroup G{};
+  G.n = n_proj;
+  for (int k = 0; k < n_proj; ++k) {
+    const int i = order[k];
+    const dsv_fwd_proj& q = projs[i];
+    GemmArgs& g = G.a[k];
+    g.P = static_cast<const uint16_t*>(q.X);
+    g.ldp = q.K;
+    g.Q = static_cast<const uint16_t*>(q.W);
+    g.ldq = q.K;
+    g.out = static_cast<uint16_t*>(q.Y);
+    g.ldo = q.N;
+    g.M = p->T;
+    g.Nout = q.N;
+    g.C = q.K;
+    g.tiles = p->dptr(L.fwd_tiles);
+    set_split(g, whole256(p->n_ftiles, q.N), nullptr, 0);
+    g.Lp = sg.a[i].out1;
+    g.ldl = ldh;
+    g.Lq = static_cast<const uint16_t*>(q.B);
+    g.lq_ad = (int64_t)q.N * p->r_max;
+    g.lq_j = 1;
+    g.lq_col = p->r_max;
+    g.ranks = ranks;
+    g.scales = scales;
+    g.delta = p->n_gather > 0 ? at<float>(wsb + base[i], w[i].delta) : nullptr;
+    g.gslot = p->dptr(L.gslot);
+    G.off[k + 1] = G.off[k] + g.n_mtiles * g.n_ntiles;
+  }
+  const int tk = timing_begin(0, s);
+  const hipError_t e = launch_gemm_group_nt(G, s);
+  timing_end(tk, s);
+  return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
+}
+
+extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_bwd_proj* projs,
+                                    int32_t accumulate, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  int rc = check_group(p, dt, n_proj, projs);
+  if (rc != DSV_OK) return rc;
+  if (n_proj == 1) {
+    const dsv_bwd_proj& q = projs[0];
+    return dsv_lora_bwd(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate,
+                        workspace, workspace_bytes, hip_stream);
+  }
+  for (int i = 0; i < n_proj; ++i)
+    if ((rc = check_common(p, dt, projs[i].K, projs[i].N)) != DSV_OK) return rc;
+  if (accumulate != 0 && accumulate != 1) return DSV_ERR_RANGE;
+  if (!p->d_meta) return DSV_ERR_ARG;
+  if (p->T_t == 0) return DSV_OK;
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_bwd_proj& q = projs[i];
+    if (!ptr_ok(q.X) || !ptr_ok(q.W) || !ptr_ok(q.A) || !ptr_ok(q.B) || !ptr_ok(q.dA) || !ptr_ok(q.dB) ||
+        !ptr_ok(q.dY))
+      return DSV_ERR_ARG;
+    if ((q.dX && !aligned16(q.dX)) || (q.H_save && !aligned16(q.H_save))) return DSV_ERR_ARG;
+  }
+  size_t base[DSV_MAX_GROUP];
+  BwdWs w[DSV_MAX_GROUP];
+  const size_t total = bwd_group_ws(*p, dt, n_proj, projs, base, w);
+  if (total > 0) {
+    if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
+    if (workspace_bytes < total) return DSV_ERR_SIZE;
+  }
+  char* wsb = static_cast<char*>(workspace);
+  if (dt == DSV_F32) {
+    for (int i = 0; i < n_proj; ++i) {
+      const dsv_bwd_proj& q = projs[i];
+      rc = bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate, nullptr,
+                    wsb + base[i], w[i].total, hip_stream);
+      if (rc != DSV_OK) return rc;
+    }
+    return DSV_OK;
+  }
+  hipStream_t s = static_cast<hipStream_t>(hip_stream);
+  const MetaLayout& L = p->lay;
+  const int32_t* ranks = p->dptr(L.ranks);
+  const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
+  const int64_t ldh = ld_rank(p->r_max);
+  const int32_t* train_ads = p->dptr(L.train_ads);
+  uint16_t* bt[DSV_MAX_GROUP];
+  uint16_t* gm[DSV_MAX_GROUP];
+  for (int i = 0; i < n_proj; ++i) {
+    bt[i] = at<uint16_t>(wsb + base[i], w[i].bt);
+    gm[i] = at<uint16_t>(wsb + base[i], w[i].g);
+  }
+
+  // 1. transposed B of the training adapters, every projection
+  TransposeGroup tg{};
+  tg.n = n_proj;
+  for (int i = 0; i < n_proj; ++i) tg.a[i] = TransposeArgs{static_cast<const uint16_t*>(projs[i].B), projs[i].N, bt[i]};
+  if (launch_transpose_group(tg, p->r_max, train_ads, p->n_tads, ranks, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 2. g = s_a dy B_a, every projection
+  SkinnyGroup gg{};
+  gg.n = n_proj;
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_bwd_proj& q = projs[i];
+    SkinnyArgs& sk = gg.a[i];
+    sk.P = static_cast<const uint16_t*>(q.dY);
+    sk.ldp = q.N;
+    sk.items = p->dptr(L.train_items);
+    sk.Q = bt[i];
+    sk.q_ad = (int64_t)p->r_max * q.N;
+    sk.ldq = q.N;
+    sk.qsel = p->dptr(L.ad_slot);
+    sk.ranks = ranks;
+    sk.scales = scales;
+    sk.C = q.N;
+    sk.out1 = gm[i];
+    sk.ld1 = ldh;
+  }
+  if (launch_gmat_group(gg, p->n_titems, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 2b. h of the training rows for projections whose forward kept no H_save
+  const uint16_t* hs[DSV_MAX_GROUP];
+  int64_t ldhs[DSV_MAX_GROUP];
+  SkinnyGroup rg{};
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_bwd_proj& q = projs[i];
+    hs[i] = static_cast<const uint16_t*>(q.H_save);
+    ldhs[i] = p->r_max;
+    if (hs[i]) continue;
+    uint16_t* hrec = at<uint16_t>(wsb + base[i], w[i].hrec);
+    SkinnyArgs& sh = rg.a[rg.n++];
+    sh.P = static_cast<const uint16_t*>(q.X);
+    sh.ldp = q.K;
+    sh.rows = p->dptr(L.train_rows);
+    sh.items = p->dptr(L.train_items);
+    sh.Q = static_cast<const uint16_t*>(q.A);
+    sh.q_ad = (int64_t)p->r_max * q.K;
+    sh.ldq = q.K;
+    sh.ranks = ranks;
+    sh.C = q.K;
+    sh.out2 = hrec;
+    sh.ld2 = ldh;
+    sh.row_train = p->dptr(L.row_train);
+    hs[i] = hrec;
+    ldhs[i] = ldh;
+  }
+  if (rg.n > 0 && launch_shrink_train_group(rg, p->n_titems, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 3. chunk partials of dy^T h (dB) and x^T g (dA), every projection
+  TokenReduceGroup trg{};
+  trg.n = 2 * n_proj;
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_bwd_proj& q = projs[i];
+    TokenReduceArgs& tb = trg.a[2 * i];
+    tb.P = static_cast<const uint16_t*>(q.dY);
+    tb.ldp = q.N;
+    tb.Q = hs[i];
+    tb.ldq = ldhs[i];
+    tb.chunks = p->dptr(L.chunks);
+    tb.ranks = ranks;
+    tb.C = q.N;
+    tb.r_max = p->r_max;
+    tb.part = at<float>(wsb + base[i], w[i].part_b);
+    TokenReduceArgs& ta = trg.a[2 * i + 1];
+    ta = tb;
+    ta.P = static_cast<const uint16_t*>(q.X);
+    ta.ldp = q.K;
+    ta.prow = p->dptr(L.train_rows);
+    ta.Q = gm[i];
+    ta.ldq = ldh;
+    ta.C = q.K;
+    ta.part = at<float>(wsb + base[i], w[i].part_a);
+  }
+  for (int k = 0; k < trg.n; ++k) trg.yoff[k + 1] = trg.yoff[k] + (trg.a[k].C + 127) / 128;
+  if (launch_token_reduce_group(trg, p->n_chunks, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 4. fixed-order sums into dB (scaled by s_a) and dA, every projection
+  ReduceOutGroup og{};
+  og.n = 2 * n_proj;
+  for (int i = 0; i < n_proj; ++i) {
+    og.a[2 * i] = ReduceOutArgs{trg.a[2 * i].part, projs[i].N, scales, 0, projs[i].dB, 1.f};
+    og.a[2 * i + 1] = ReduceOutArgs{trg.a[2 * i + 1].part, projs[i].K, nullptr, 1, projs[i].dA, 1.f};
+  }
+  if (launch_reduce_out_group(og, p->r_max, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr), p->dptr(L.tad_chunks),
+                              ranks, accumulate, s) != hipSuccess)
+    return DSV_ERR_DEVICE;
+
+  // 5. every dX GEMM in one launch, longest contraction first
+  int32_t Cs[DSV_MAX_GROUP], order[DSV_MAX_GROUP];
+  for (int i = 0; i < n_proj; ++i) Cs[i] = projs[i].N;
+  by_contraction(n_proj, Cs, order);
+  GemmGroup G{};
+  for (int k = 0; k < n_proj; ++k) {
+    const int i = order[k];
+    const dsv_bwd_proj& q = projs[i];
+    if (!q.dX) continue;
+    GemmArgs& g = G.a[G.n];
+    g.P = static_cast<const uint16_t*>(q.dY);
+    g.ldp = q.N;
+    g.Q = static_cast<const uint16_t*>(q.W);
+    g.ldq = q.K;
+    g.out = static_cast<uint16_t*>(q.dX);
+    g.ldo = q.K;
+    g.M = p->T_t;
+    g.Nout = q.K;
+    g.C = q.N;
+    g.tiles = p->dptr(L.bwd_tiles);
+    set_split(g, whole256(p->n_btiles, q.K), nullptr, 0);
+    g.Lp = gm[i];
+    g.ldl = ldh;
+    g.Lq = static_cast<const uint16_t*>(q.A);
+    g.lq_ad = (int64_t)p->r_max * q.K;
+    g.lq_j = q.K;
+    g.lq_col = 1;
+    g.ranks = ranks;
+    G.off[G.n + 1] = G.off[G.n] + g.n_mtiles * g.n_ntiles;
+    ++G.n;
+  }
+  if (G.n > 0) {
+    const int tk = timing_begin(1, s);
+    const hipError_t e = launch_gemm_group_nn(G, s);
+    timing_end(tk, s);
+    if (e != hipSuccess) return DSV_ERR_DEVICE;
+  }
+  return DSV_OK;
+}

@@ -91,6 +91,48 @@ struct TokenReduceArgs {
   int32_t keep_words;
 };
 
+// Grouped launches: one kernel runs the same step of up to kMaxGroup
+// projections (same plan, per-projection operands), the projection picked
+// from the workgroup id.  The single-projection launchers below are groups
+// of one.
+constexpr int kMaxGroup = 8;
+struct SkinnyGroup {
+  SkinnyArgs a[kMaxGroup];
+  int32_t n;
+};
+struct GatherArgs {           // gathered low-rank term of one projection
+  const uint16_t* H;          // h of every row [T][ldh]
+  const uint16_t* B;          // adapter stacks [n_ad][N][r_max]
+  int32_t N;
+  float* delta;               // [n_gather][N] fp32 out
+};
+struct GatherGroup {
+  GatherArgs a[kMaxGroup];
+  int32_t yoff[kMaxGroup + 1];  // prefix of the 256-column blocks
+  int32_t n;
+};
+struct TokenReduceGroup {
+  TokenReduceArgs a[2 * kMaxGroup];
+  int32_t yoff[2 * kMaxGroup + 1];  // prefix of the 128-column blocks
+  int32_t n;
+};
+struct TransposeArgs {
+  const uint16_t* B;  // [n_ad][N][r_max]
+  int32_t N;
+  uint16_t* Bt;       // [n_tads][r_max][N]
+};
+struct TransposeGroup {
+  TransposeArgs a[kMaxGroup];
+  int32_t n;
+};
+// GEMM group: whole 256x256 tiles, workgroups [off[p], off[p+1]) take the
+// tiles of projection a[p] (XCD-major within the projection).
+struct GemmGroup {
+  GemmArgs a[kMaxGroup];
+  int32_t off[kMaxGroup + 1];
+  int32_t n;
+};
+
 // Launchers (bf16).  Each returns hipSuccess or the launch error.
 // Tile shapes (tm x tn): 256x256, 256x128 or 128x128; `tiles` must be the
 // plan's row-tile list of height tm.  Split tiles (sk_tiles > 0) are
@@ -117,12 +159,33 @@ struct ReduceOutArgs {
   float* out;
   float post;           // extra factor (dropout scale of dA), 1 otherwise
 };
+struct ReduceOutGroup {
+  ReduceOutArgs a[2 * kMaxGroup];
+  int32_t n;
+};
 // Both final sums of a backward in one launch.
 hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
                              const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
                              const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s);
 hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
                               int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
+
+// Grouped forms (n >= 1 entries filled).
+hipError_t launch_shrink_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s);
+hipError_t launch_gmat_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s);
+hipError_t launch_shrink_train_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s);
+hipError_t launch_gather_group(const GatherGroup& g, int64_t ldh, int32_t r_max, const int32_t* items,
+                               int32_t n_items, const int32_t* gather_rows, const int32_t* ranks,
+                               const float* scales, hipStream_t s);
+// entries 2p and 2p+1: the dB and dA reductions of projection p (all with one r_max)
+hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s);
+hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, const int32_t* train_ads,
+                                   int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
+                                   const int32_t* ranks, int32_t accumulate, hipStream_t s);
+hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const int32_t* train_ads,
+                                  int32_t n_tads, const int32_t* ranks, hipStream_t s);
+hipError_t launch_gemm_group_nt(const GemmGroup& g, hipStream_t s);
+hipError_t launch_gemm_group_nn(const GemmGroup& g, hipStream_t s);
 
 // Fused AdamW step of the training adapters' A and B slices (fp32 master
 // weights and moments in the A / B layouts; the parameter copy A / B is bf16

@@ -560,6 +560,23 @@ __global__ __launch_bounds__(64 * WGM * WGN) void gemm_lora_kernel(GemmArgs g) {
   gemm_piece<NN, TM, TN, WGM, WGN, TK, NS, SK>(g, smem, tid0, lin, t_sk, piece, kb, ke, nk);
 }
 
+// Several projections' GEMMs in one launch: whole 256x256 tiles, workgroups
+// [off[p], off[p+1]) take projection p's tiles (XCD-major within it).  The
+// host orders the projections by contraction length, longest first, so the
+// long tiles start first and the short ones fill the last wave.
+template <bool NN>
+__global__ __launch_bounds__(512) void gemm_group_kernel(GemmGroup G) {
+  using S = GemmShape<256, 256, 2, 4, 64, 2>;
+  __shared__ __attribute__((aligned(1024))) char smem[S::LDS];
+  int pj = 0;
+  while (pj + 1 < G.n && (int)blockIdx.x >= G.off[pj + 1]) ++pj;
+  const GemmArgs& g = G.a[pj];
+  const int local = (int)blockIdx.x - G.off[pj];
+  const int lin = xcd_major(local, G.off[pj + 1] - G.off[pj]);
+  const int nk = (g.C + 63) / 64;
+  gemm_piece<NN, 256, 256, 2, 4, 64, 2, false>(g, smem, threadIdx.x, lin, -1, 0, 0, nk, nk);
+}
+
 // ---------------------------------------------------------------------------
 // Split tiles: sum the fp32 partials of a tile's pieces in K order, add the
 // gathered rows' term, round once to bf16 and store -- the GEMM epilogue for
@@ -620,7 +637,8 @@ __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int beg
 
 // DROP (shrink only): the training rows' input passes through the dropout mask.
 template <int MODE, int NJ, int ROWS, bool DROP>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
-__global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
+__global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
+  const SkinnyArgs& g = G.a[blockIdx.y];  // the projection
   constexpr int RT = ROWS / 16;  // 16-row tiles per item
   // U slices per batch; two batches in registers (the next one loads while
   // the current one feeds the matrix cores)
@@ -731,9 +749,15 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyArgs g) {
 // workgroup per (item, 256-column block); fp32 result, already scaled.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void gather_expand_kernel(
-    const uint16_t* __restrict__ H, int64_t ldh, const uint16_t* __restrict__ B, int32_t N,
-    int32_t r_max, const int32_t* __restrict__ items, const int32_t* __restrict__ gather_rows,
-    const int32_t* __restrict__ ranks, const float* __restrict__ scales, float* __restrict__ delta) {
+    GatherGroup G, int64_t ldh, int32_t r_max, const int32_t* __restrict__ items,
+    const int32_t* __restrict__ gather_rows, const int32_t* __restrict__ ranks, const float* __restrict__ scales) {
+  int pj = 0;  // the projection: blockIdx.y runs over every projection's column blocks
+  while (pj + 1 < G.n && (int)blockIdx.y >= G.yoff[pj + 1]) ++pj;
+  const uint16_t* __restrict__ H = G.a[pj].H;
+  const uint16_t* __restrict__ B = G.a[pj].B;
+  const int32_t N = G.a[pj].N;
+  float* __restrict__ delta = G.a[pj].delta;
+  const int by = (int)blockIdx.y - G.yoff[pj];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* it = items + (int64_t)blockIdx.x * kItemWords;
   const int a = it[0], sbeg = it[1], cnt = it[2];
@@ -741,7 +765,7 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
   const int i = lane & 15;
   const int row = (i < cnt) ? gather_rows[sbeg + i] : -1;
   const uint16_t* Ba = B + (int64_t)a * N * r_max;
-  const int nb = blockIdx.y * 256 + wave * 64;
+  const int nb = by * 256 + wave * 64;
   f32x4 acc[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -786,12 +810,13 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
 // Both reductions of a backward in one launch: blockIdx.y < y0 runs g0's
 // column blocks, the rest g1's.
 template <int NJ>
-__global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g0, TokenReduceArgs g1, int32_t y0) {
+__global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceGroup G) {
   constexpr int TQ = kChunkRows / 4;  // tokens per wave
   __shared__ f32x4 red[3][8 * NJ][64];
-  const bool second = (int)blockIdx.y >= y0;
-  const TokenReduceArgs& g = second ? g1 : g0;
-  const int by = second ? (int)blockIdx.y - y0 : (int)blockIdx.y;
+  int k = 0;  // the reduction: blockIdx.y runs over every reduction's column blocks
+  while (k + 1 < G.n && (int)blockIdx.y >= G.yoff[k + 1]) ++k;
+  const TokenReduceArgs& g = G.a[k];
+  const int by = (int)blockIdx.y - G.yoff[k];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
   const int a = ck[0], begin = ck[1], cnt = ck[2];
@@ -871,16 +896,17 @@ __global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceArgs g0, T
 }
 
 // Fixed-order sum of one training adapter's chunk partials.
-// Both final sums of a backward in one launch: blockIdx.y = which * n_tads +
-// training adapter; which 0 is o0 (dB, scaled, [c][j]), 1 is o1 (dA, [j][c]).
-__global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutArgs o0, ReduceOutArgs o1, int32_t r_max,
+// Every final sum of a (grouped) backward in one launch: blockIdx.y = which *
+// n_tads + training adapter (which: dB, dA of the first projection, then the
+// next projection's).
+__global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32_t r_max,
                                                          const int32_t* __restrict__ train_ads, int32_t n_tads,
                                                          const int32_t* __restrict__ tad_ptr,
                                                          const int32_t* __restrict__ tad_chunks,
                                                          const int32_t* __restrict__ ranks, int32_t accumulate) {
-  const bool second = (int)blockIdx.y >= n_tads;
-  const ReduceOutArgs& g = second ? o1 : o0;
-  const int ta = second ? (int)blockIdx.y - n_tads : (int)blockIdx.y;
+  const int which = (int)blockIdx.y / n_tads;
+  const ReduceOutArgs& g = G.a[which];
+  const int ta = (int)blockIdx.y - which * n_tads;
   const int C = g.C;
   const int a = train_ads[ta], r = ranks[a];
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
@@ -904,11 +930,13 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutArgs o0, Reduc
 }
 
 // Bt[slot][j][n] = B[a][n][j]  (j < r_a; other rows zero).
-__global__ __launch_bounds__(256) void transpose_b_kernel(const uint16_t* __restrict__ B, int32_t N,
-                                                          int32_t r_max, const int32_t* __restrict__ train_ads,
-                                                          const int32_t* __restrict__ ranks,
-                                                          uint16_t* __restrict__ Bt) {
-  const int slot = blockIdx.z, j = blockIdx.y;
+__global__ __launch_bounds__(256) void transpose_b_kernel(TransposeGroup G, int32_t r_max,
+                                                          const int32_t* __restrict__ train_ads, int32_t n_tads,
+                                                          const int32_t* __restrict__ ranks) {
+  const int pj = (int)blockIdx.z / n_tads, slot = (int)blockIdx.z - pj * n_tads, j = blockIdx.y;
+  const uint16_t* __restrict__ B = G.a[pj].B;
+  uint16_t* __restrict__ Bt = G.a[pj].Bt;
+  const int32_t N = G.a[pj].N;
   const int n = blockIdx.x * 256 + threadIdx.x;
   if (n >= N) return;
   const int a = train_ads[slot];
@@ -963,81 +991,169 @@ hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
 
 namespace {
 template <int MODE, int ROWS, bool DROP>
-void launch_skinny_nj(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
+void launch_skinny_nj(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
+  const dim3 grid(n_items, g.n);
   if (r_max <= 16)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS, DROP>), dim3(n_items), dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS, DROP>), grid, dim3(64 * SW), 0, s, g);
   else if (r_max <= 32)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS, DROP>), dim3(n_items), dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS, DROP>), grid, dim3(64 * SW), 0, s, g);
   else
-    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS, DROP>), dim3(n_items), dim3(64 * SW), 0, s, a);
+    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS, DROP>), grid, dim3(64 * SW), 0, s, g);
 }
 
+// Every projection of a group takes the dropout path or none does.
 template <int MODE, int ROWS>
-hipError_t launch_skinny(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
+hipError_t launch_skinny(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
+  if (n_items <= 0 || g.n <= 0) return hipSuccess;
+  if (g.n > kMaxGroup) return hipErrorInvalidValue;
+  for (int p = 1; p < g.n; ++p)
+    if ((g.a[p].keep != nullptr) != (g.a[0].keep != nullptr)) return hipErrorInvalidValue;
   if constexpr (MODE == 0) {
-    if (a.keep != nullptr) launch_skinny_nj<MODE, ROWS, true>(a, n_items, r_max, s);
-    else launch_skinny_nj<MODE, ROWS, false>(a, n_items, r_max, s);
+    if (g.a[0].keep != nullptr) launch_skinny_nj<MODE, ROWS, true>(g, n_items, r_max, s);
+    else launch_skinny_nj<MODE, ROWS, false>(g, n_items, r_max, s);
   } else {
-    launch_skinny_nj<MODE, ROWS, false>(a, n_items, r_max, s);
+    launch_skinny_nj<MODE, ROWS, false>(g, n_items, r_max, s);
   }
+  return hipGetLastError();
+}
+
+SkinnyGroup one(const SkinnyArgs& a) {
+  SkinnyGroup g{};
+  g.a[0] = a;
+  g.n = 1;
+  return g;
+}
+
+template <bool NN>
+hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
+  if (g.n <= 0 || g.n > kMaxGroup || g.off[0] != 0) return hipErrorInvalidValue;
+  for (int p = 0; p < g.n; ++p) {
+    const GemmArgs& a = g.a[p];
+    if (g.off[p + 1] - g.off[p] != a.n_mtiles * a.n_ntiles || a.sk_tiles != 0) return hipErrorInvalidValue;
+  }
+  if (g.off[g.n] <= 0) return hipSuccess;
+  hipLaunchKernelGGL((gemm_group_kernel<NN>), dim3((unsigned)g.off[g.n]), dim3(512), 0, s, g);
   return hipGetLastError();
 }
 }  // namespace
 
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
-  return launch_skinny<0, kRankItemRows>(a, n_items, r_max, s);
+  return launch_skinny<0, kRankItemRows>(one(a), n_items, r_max, s);
 }
 
 hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
-  return launch_skinny<1, kItemRows>(a, n_items, r_max, s);
+  return launch_skinny<1, kItemRows>(one(a), n_items, r_max, s);
 }
 
 hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
-  return launch_skinny<0, kItemRows>(a, n_items, r_max, s);
+  return launch_skinny<0, kItemRows>(one(a), n_items, r_max, s);
+}
+
+hipError_t launch_shrink_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
+  return launch_skinny<0, kRankItemRows>(g, n_items, r_max, s);
+}
+
+hipError_t launch_gmat_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
+  return launch_skinny<1, kItemRows>(g, n_items, r_max, s);
+}
+
+hipError_t launch_shrink_train_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
+  return launch_skinny<0, kItemRows>(g, n_items, r_max, s);
+}
+
+hipError_t launch_gather_group(const GatherGroup& g, int64_t ldh, int32_t r_max, const int32_t* items,
+                               int32_t n_items, const int32_t* gather_rows, const int32_t* ranks,
+                               const float* scales, hipStream_t s) {
+  if (n_items <= 0 || g.n <= 0) return hipSuccess;
+  if (g.n > kMaxGroup || g.yoff[0] != 0) return hipErrorInvalidValue;
+  for (int p = 0; p < g.n; ++p)
+    if (g.yoff[p + 1] - g.yoff[p] != (g.a[p].N + 255) / 256) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(gather_expand_kernel, dim3(n_items, g.yoff[g.n]), dim3(256), 0, s, g, ldh, r_max, items,
+                     gather_rows, ranks, scales);
+  return hipGetLastError();
 }
 
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
                                 int32_t r_max, const int32_t* items, int32_t n_items,
                                 const int32_t* gather_rows, const int32_t* ranks,
                                 const float* scales, float* delta, hipStream_t s) {
-  if (n_items <= 0) return hipSuccess;
-  hipLaunchKernelGGL(gather_expand_kernel, dim3(n_items, (N + 255) / 256), dim3(256), 0, s, H, ldh,
-                     B, N, r_max, items, gather_rows, ranks, scales, delta);
+  GatherGroup g{};
+  g.a[0] = GatherArgs{H, B, N, delta};
+  g.yoff[1] = (N + 255) / 256;
+  g.n = 1;
+  return launch_gather_group(g, ldh, r_max, items, n_items, gather_rows, ranks, scales, s);
+}
+
+hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s) {
+  if (n_chunks <= 0 || g.n <= 0) return hipSuccess;
+  if (g.n > 2 * kMaxGroup || g.yoff[0] != 0) return hipErrorInvalidValue;
+  for (int k = 0; k < g.n; ++k)
+    if (g.a[k].r_max != g.a[0].r_max || g.yoff[k + 1] - g.yoff[k] != (g.a[k].C + 127) / 128)
+      return hipErrorInvalidValue;
+  const dim3 grid(n_chunks, g.yoff[g.n]);
+  if (g.a[0].r_max <= 16)
+    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(256), 0, s, g);
+  else if (g.a[0].r_max <= 32)
+    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(256), 0, s, g);
+  else
+    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
 hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
                                hipStream_t s) {
-  if (n_chunks <= 0) return hipSuccess;
-  if (a0.r_max != a1.r_max) return hipErrorInvalidValue;
-  const int y0 = (a0.C + 127) / 128;
-  const dim3 grid(n_chunks, y0 + (a1.C + 127) / 128);
-  if (a0.r_max <= 16)
-    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(256), 0, s, a0, a1, y0);
-  else if (a0.r_max <= 32)
-    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(256), 0, s, a0, a1, y0);
-  else
-    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(256), 0, s, a0, a1, y0);
+  TokenReduceGroup g{};
+  g.a[0] = a0;
+  g.a[1] = a1;
+  g.yoff[1] = (a0.C + 127) / 128;
+  g.yoff[2] = g.yoff[1] + (a1.C + 127) / 128;
+  g.n = 2;
+  return launch_token_reduce_group(g, n_chunks, s);
+}
+
+hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, const int32_t* train_ads,
+                                   int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
+                                   const int32_t* ranks, int32_t accumulate, hipStream_t s) {
+  if (n_tads <= 0 || g.n <= 0) return hipSuccess;
+  if (g.n > 2 * kMaxGroup) return hipErrorInvalidValue;
+  int64_t cmax = 0;
+  for (int k = 0; k < g.n; ++k) cmax = g.a[k].C > cmax ? g.a[k].C : cmax;
+  const int64_t total = cmax * r_max;
+  hipLaunchKernelGGL(reduce_out_kernel, dim3((unsigned)((total + 255) / 256), g.n * n_tads), dim3(256), 0, s, g,
+                     r_max, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate);
   return hipGetLastError();
 }
 
 hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
                              const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
                              const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s) {
-  if (n_tads <= 0) return hipSuccess;
-  const int64_t total = (int64_t)(o0.C > o1.C ? o0.C : o1.C) * r_max;
-  hipLaunchKernelGGL(reduce_out_kernel, dim3((unsigned)((total + 255) / 256), 2 * n_tads), dim3(256), 0, s, o0, o1,
-                     r_max, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate);
+  ReduceOutGroup g{};
+  g.a[0] = o0;
+  g.a[1] = o1;
+  g.n = 2;
+  return launch_reduce_out_group(g, r_max, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate, s);
+}
+
+hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const int32_t* train_ads,
+                                  int32_t n_tads, const int32_t* ranks, hipStream_t s) {
+  if (n_tads <= 0 || g.n <= 0) return hipSuccess;
+  if (g.n > kMaxGroup) return hipErrorInvalidValue;
+  int32_t nmax = 0;
+  for (int p = 0; p < g.n; ++p) nmax = g.a[p].N > nmax ? g.a[p].N : nmax;
+  hipLaunchKernelGGL(transpose_b_kernel, dim3((nmax + 255) / 256, r_max, n_tads * g.n), dim3(256), 0, s, g, r_max,
+                     train_ads, n_tads, ranks);
   return hipGetLastError();
 }
 
 hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
                               int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s) {
-  if (n_tads <= 0) return hipSuccess;
-  hipLaunchKernelGGL(transpose_b_kernel, dim3((N + 255) / 256, r_max, n_tads), dim3(256), 0, s, B, N,
-                     r_max, train_ads, ranks, Bt);
-  return hipGetLastError();
+  TransposeGroup g{};
+  g.a[0] = TransposeArgs{B, N, Bt};
+  g.n = 1;
+  return launch_transpose_group(g, r_max, train_ads, n_tads, ranks, s);
 }
+
+hipError_t launch_gemm_group_nt(const GemmGroup& g, hipStream_t s) { return launch_gemm_group<false>(g, s); }
+hipError_t launch_gemm_group_nn(const GemmGroup& g, hipStream_t s) { return launch_gemm_group<true>(g, s); }
 
 }  // namespace dsv

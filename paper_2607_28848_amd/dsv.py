@@ -78,6 +78,27 @@ _lib.dsv_lora_bwd_dropout_workspace.restype = ctypes.c_int
 _lib.dsv_lora_bwd_dropout.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
                                       _vp, _vp, _i32, ctypes.POINTER(Dropout), _vp, _sz, _vp]
 _lib.dsv_lora_bwd_dropout.restype = ctypes.c_int
+class FwdProj(ctypes.Structure):
+    _fields_ = [("K", _i32), ("N", _i32), ("X", _vp), ("W", _vp), ("A", _vp), ("B", _vp), ("Y", _vp),
+                ("H_save", _vp)]
+
+
+class BwdProj(ctypes.Structure):
+    _fields_ = [("K", _i32), ("N", _i32), ("X", _vp), ("W", _vp), ("A", _vp), ("B", _vp), ("H_save", _vp),
+                ("dY", _vp), ("dA", _vp), ("dB", _vp), ("dX", _vp)]
+
+
+MAX_GROUP = 8
+_lib.dsv_cobatch_fwd_grouped_workspace.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(FwdProj),
+                                                   ctypes.POINTER(_sz)]
+_lib.dsv_cobatch_fwd_grouped_workspace.restype = ctypes.c_int
+_lib.dsv_cobatch_fwd_grouped.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(FwdProj), _vp, _sz, _vp]
+_lib.dsv_cobatch_fwd_grouped.restype = ctypes.c_int
+_lib.dsv_lora_bwd_grouped_workspace.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(BwdProj),
+                                                ctypes.POINTER(_sz)]
+_lib.dsv_lora_bwd_grouped_workspace.restype = ctypes.c_int
+_lib.dsv_lora_bwd_grouped.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(BwdProj), _i32, _vp, _sz, _vp]
+_lib.dsv_lora_bwd_grouped.restype = ctypes.c_int
 _lib.dsv_timing_enable.argtypes = [_i32]
 _lib.dsv_timing_enable.restype = ctypes.c_int
 _lib.dsv_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), _i32p,
@@ -297,6 +318,85 @@ def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want
                                          ctypes.byref(d), _ptr(ws), ws.numel() * ws.element_size(),
                                          _stream_handle(stream)), "dsv_lora_bwd_dropout")
     return dA, dB, dX
+
+
+def _fwd_projs(items):
+    arr = (FwdProj * len(items))()
+    for i, (X, W, A, B, Y, H) in enumerate(items):
+        arr[i] = FwdProj(X.shape[1], W.shape[0], _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y), _ptr(H))
+    return arr
+
+
+def fwd_grouped_workspace_bytes(plan: Plan, dtype_code: int, shapes) -> int:
+    """shapes: [(K, N)] of the projections."""
+    arr = (FwdProj * len(shapes))()
+    for i, (K, N) in enumerate(shapes):
+        arr[i].K, arr[i].N = K, N
+    n = _sz(0)
+    _check(_lib.dsv_cobatch_fwd_grouped_workspace(plan.handle, dtype_code, len(shapes), arr, ctypes.byref(n)),
+           "dsv_cobatch_fwd_grouped_workspace")
+    return int(n.value)
+
+
+def bwd_grouped_workspace_bytes(plan: Plan, dtype_code: int, shapes) -> int:
+    arr = (BwdProj * len(shapes))()
+    for i, (K, N) in enumerate(shapes):
+        arr[i].K, arr[i].N = K, N
+    n = _sz(0)
+    _check(_lib.dsv_lora_bwd_grouped_workspace(plan.handle, dtype_code, len(shapes), arr, ctypes.byref(n)),
+           "dsv_lora_bwd_grouped_workspace")
+    return int(n.value)
+
+
+def cobatch_fwd_grouped(plan: Plan, projs, workspace=None, stream=None, keep_h: bool = True):
+    """dsv_cobatch_fwd_grouped.  projs: [(X, W, A, B)] or [(X, W, A, B, Y, H_save)];
+    returns [(Y, H_save)] in the same order."""
+    import torch
+    items = []
+    for pr in projs:
+        X, W, A, B = pr[:4]
+        Y = pr[4] if len(pr) > 4 and pr[4] is not None else torch.empty((X.shape[0], W.shape[0]), dtype=X.dtype,
+                                                                          device=X.device)
+        H = pr[5] if len(pr) > 5 else None
+        if H is None and keep_h and plan.train_tokens > 0:
+            H = torch.empty((plan.train_tokens, plan.r_max), dtype=X.dtype, device=X.device)
+        items.append((X, W, A, B, Y, H))
+    dt = _dtype_code(items[0][0])
+    ws = _workspace(fwd_grouped_workspace_bytes(plan, dt, [(it[0].shape[1], it[1].shape[0]) for it in items]),
+                    items[0][0].device, workspace)
+    arr = _fwd_projs(items)
+    _check(_lib.dsv_cobatch_fwd_grouped(plan.handle, dt, len(items), arr, _ptr(ws), ws.numel() * ws.element_size(),
+                                        _stream_handle(stream)), "dsv_cobatch_fwd_grouped")
+    return [(it[4], it[5]) for it in items]
+
+
+def lora_bwd_grouped(plan: Plan, projs, accumulate: bool = False, want_dx: bool = True, workspace=None,
+                     stream=None):
+    """dsv_lora_bwd_grouped.  projs: [(X, W, A, B, H_save, dY)] or with (dA, dB, dX) appended;
+    returns [(dA, dB, dX)]."""
+    import torch
+    items = []
+    for pr in projs:
+        X, W, A, B, H, dY = pr[:6]
+        K, N, n_ad = X.shape[1], W.shape[0], A.shape[0]
+        dA = pr[6] if len(pr) > 6 and pr[6] is not None else torch.zeros((n_ad, plan.r_max, K), dtype=torch.float32,
+                                                                          device=X.device)
+        dB = pr[7] if len(pr) > 7 and pr[7] is not None else torch.zeros((n_ad, N, plan.r_max), dtype=torch.float32,
+                                                                          device=X.device)
+        dX = pr[8] if len(pr) > 8 else None
+        if dX is None and want_dx and plan.train_tokens > 0:
+            dX = torch.empty((plan.train_tokens, K), dtype=X.dtype, device=X.device)
+        items.append((X, W, A, B, H, dY, dA, dB, dX if want_dx else None))
+    dt = _dtype_code(items[0][0])
+    ws = _workspace(bwd_grouped_workspace_bytes(plan, dt, [(it[0].shape[1], it[1].shape[0]) for it in items]),
+                    items[0][0].device, workspace)
+    arr = (BwdProj * len(items))()
+    for i, (X, W, A, B, H, dY, dA, dB, dX) in enumerate(items):
+        arr[i] = BwdProj(X.shape[1], W.shape[0], _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H), _ptr(dY), _ptr(dA),
+                         _ptr(dB), _ptr(dX))
+    _check(_lib.dsv_lora_bwd_grouped(plan.handle, dt, len(items), arr, 1 if accumulate else 0, _ptr(ws),
+                                     ws.numel() * ws.element_size(), _stream_handle(stream)), "dsv_lora_bwd_grouped")
+    return [(it[6], it[7], it[8]) for it in items]
 
 
 def adamw_step(plan: Plan, step: int, dA, dB, A_master, B_master, A_m, A_v, B_m, B_v, A=None, B=None,

@@ -1,0 +1,170 @@
+"""GPU parity of the grouped launches (dsv_cobatch_fwd_grouped /
+dsv_lora_bwd_grouped): several projections of one batch, one launch per step.
+
+Bar: every output of every projection within 2e-2 (bf16) or 1e-5 (fp32) of the
+fp64 reference; bit-identical to the single-projection calls wherever those do
+not split a GEMM tile along the contraction (same summation order); a repeat
+is bit-identical.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2607_28848_amd import workloads as wl
+from gpu_util import TOL_BF16, TOL_F32, oracle_bwd, oracle_fwd, to_dev, to_host, train_mask_slices
+
+pytestmark = pytest.mark.gpu
+
+MIXED = [(0, 100, 3, 0), (100, 1, 1, 0), (101, 1, 2, 0), (102, 300, 0, 1), (402, 1, 3, 0),
+         (403, 57, 2, 0), (460, 2, 1, 0), (462, 129, 1, 1), (591, 3, 0, 0), (594, 111, 4, 0)]
+MIXED_RANKS = [16, 8, 64, 32, 5]
+
+
+def _say(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+def _bits(t):
+    import torch
+    return t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)
+
+
+def _layer(dtype, shapes, segments=MIXED, ranks=MIXED_RANKS, r_max=64, name="grouped"):
+    """Workload whose projections have the given (K, N) shapes, inputs on the device."""
+    w = wl.custom(segments, ranks, K=shapes[0][0], N=shapes[0][1], dtype=dtype, r_max=r_max, name=name)
+    w.projections = [wl.Projection("p%d" % i, K, N) for i, (K, N) in enumerate(shapes)]
+    ts = [w.tensors(i) for i in range(len(shapes))]
+    dev = [{k: to_dev(t.store[k], dtype) for k in ("X", "W", "A", "B", "dY")} for t in ts]
+    return w, ts, dev
+
+
+def _check_proj(w, t, tr, Y, H, dA, dB, dX, tol, rows=None, dx_rows=None):
+    Yr, _ = oracle_fwd(w, t, rows)
+    Yg = to_host(Y) if rows is None else to_host(Y)[rows]
+    errs = {"Y": oracle.rel_err(Yg, Yr)}
+    if H is not None:
+        errs["H_save"] = oracle.rel_err(to_host(H), oracle_fwd(w, t, tr)[1])
+    _, dAr, dBr, dXr = oracle_bwd(w, t, dx_rows=dx_rows)
+    dAg, dBg = to_host(dA), to_host(dB)
+    for a, r in train_mask_slices(w):
+        errs["dA%d" % a] = oracle.rel_err(dAg[a, :r], dAr[a, :r])
+        errs["dB%d" % a] = oracle.rel_err(dBg[a, :, :r], dBr[a, :, :r])
+    if dX is not None:
+        dXg = to_host(dX) if dx_rows is None else to_host(dX)[dx_rows]
+        errs["dX"] = oracle.rel_err(dXg, dXr)
+    _say("  rel errors: " + ", ".join("%s=%.2e" % kv for kv in errs.items()))
+    for k, v in errs.items():
+        assert v <= tol, (k, v)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_grouped_mixed_shapes_against_reference(dtype):
+    """Four projections with different K and N (ragged against 64 and 256), one of
+    them keeping no H_save (h recomputed in the backward) and one without dX;
+    every output of every projection against the reference."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(520, 776), (136, 1040), (1040, 264), (520, 136)]
+    _say("case grouped %s %s" % (dtype, shapes))
+    w, ts, dev = _layer(dtype, shapes)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    fw = []
+    for i, d in enumerate(dev):
+        H = None if i == 1 else torch.zeros((plan.train_tokens, w.r_max), dtype=d["X"].dtype, device="cuda")
+        fw.append((d["X"], d["W"], d["A"], d["B"], None, H))
+    out = dsv.cobatch_fwd_grouped(plan, fw, keep_h=False)
+    bw = [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"], None, None,
+           None if i == 3 else torch.empty((plan.train_tokens, shapes[i][0]), dtype=d["X"].dtype, device="cuda"))
+          for i, d in enumerate(dev)]
+    grads = dsv.lora_bwd_grouped(plan, bw, want_dx=True)
+    torch.cuda.synchronize()
+    tr = plan.train_rows()
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    for i in range(len(shapes)):
+        w.projections = [wl.Projection("p", *shapes[i])]
+        _say(" projection %d K=%d N=%d" % ((i,) + shapes[i]))
+        dX = grads[i][2] if i != 3 else None
+        _check_proj(w, ts[i], tr, out[i][0], out[i][1], grads[i][0], grads[i][1], dX, tol)
+
+
+def test_grouped_matches_single_calls_and_repeats():
+    """bf16: the grouped results equal the single calls bit for bit on every
+    projection whose single call splits no tile (and within the bar on the others);
+    a second grouped call is bit-identical to the first."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(4096, 1024), (1024, 4096), (4096, 2048), (2048, 776)]
+    _say("case grouped vs single %s" % shapes)
+    w, ts, dev = _layer("bf16", shapes)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    Tt = plan.train_tokens
+
+    def hbuf():
+        return torch.zeros((Tt, w.r_max), dtype=torch.bfloat16, device="cuda")
+
+    runs = []
+    for rep in range(2):
+        out = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], None, hbuf()) for d in dev])
+        grads = dsv.lora_bwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"])
+                                            for i, d in enumerate(dev)])
+        runs.append((out, grads))
+    singles = []
+    for i, d in enumerate(dev):
+        Y, H = dsv.cobatch_fwd(plan, d["X"], d["W"], d["A"], d["B"], H_save=hbuf())
+        g = dsv.lora_bwd(plan, d["X"], d["W"], d["A"], d["B"], H, d["dY"])
+        singles.append(((Y, H), g))
+    torch.cuda.synchronize()
+    (o1, g1), (o2, g2) = runs
+    for i, (K, N) in enumerate(shapes):
+        for a, b in list(zip(o1[i], o2[i])) + list(zip(g1[i], g2[i])):
+            assert torch.equal(_bits(a), _bits(b))
+        fsplit = dsv.gemm_config(plan, dsv.BF16, K, N, 0)["split_tiles"]
+        bsplit = dsv.gemm_config(plan, dsv.BF16, K, N, 1)["split_tiles"]
+        (Ys, Hs), (dAs, dBs, dXs) = singles[i]
+        _say("  projection %d K=%d N=%d: single-call splits fwd %d dX %d" % (i, K, N, fsplit, bsplit))
+        assert torch.equal(_bits(o1[i][1]), _bits(Hs))
+        assert torch.equal(_bits(g1[i][0]), _bits(dAs)) and torch.equal(_bits(g1[i][1]), _bits(dBs))
+        if fsplit == 0:
+            assert torch.equal(_bits(o1[i][0]), _bits(Ys))
+        else:
+            assert oracle.rel_err(to_host(o1[i][0]), to_host(Ys)) <= 1e-2
+        if bsplit == 0:
+            assert torch.equal(_bits(g1[i][2]), _bits(dXs))
+        else:
+            assert oracle.rel_err(to_host(g1[i][2]), to_host(dXs)) <= 1e-2
+
+
+@pytest.mark.timeout(900)
+def test_grouped_llama8b_layer_set_full_size():
+    """The whole Llama-3-8B layer set (q, k, v, o, gate, up, down) of the mixed
+    4096-token batch in one grouped forward and one grouped backward: Y and dX of
+    every projection on sampled rows, H_save, dA, dB in full."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    w = wl.llama8b_mixed()
+    _say("case grouped %s" % w.name)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    ts, dev = [], []
+    for i in range(len(w.projections)):
+        t = w.tensors(i)
+        ts.append(t)
+        dev.append({k: to_dev(t.store[k], "bf16") for k in ("X", "W", "A", "B", "dY")})
+    out = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"]) for d in dev])
+    grads = dsv.lora_bwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"])
+                                        for i, d in enumerate(dev)])
+    torch.cuda.synchronize()
+    tr = plan.train_rows()
+    rng = np.random.default_rng(11)
+    Tt = w.train_tokens
+    projs = list(w.projections)
+    for i, proj in enumerate(projs):
+        _say(" projection %s K=%d N=%d" % (proj.name, proj.K, proj.N))
+        rows = np.unique(np.concatenate([rng.choice(w.n_tokens, 12, replace=False), tr[:1], tr[-1:]]))
+        dx_rows = np.unique(np.concatenate([rng.choice(Tt, 12, replace=False), [0, Tt - 1]]))
+        w.projections = [proj]
+        _check_proj(w, ts[i], tr, out[i][0], out[i][1], grads[i][0], grads[i][1], grads[i][2], TOL_BF16,
+                    rows=rows.astype(np.int32), dx_rows=dx_rows.astype(np.int32))
+    w.projections = projs

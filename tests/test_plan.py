@@ -325,3 +325,39 @@ def test_dropout_argument_checks_on_host():
         plain = dsv.bwd_workspace_bytes(plan, dt, 520, 64)
         drop = dsv.bwd_workspace_bytes(plan, dt, 520, 64, dropout=True)
         assert drop >= plain
+
+
+def test_grouped_argument_checks_on_host():
+    """The grouped entry points reject a bad group size (ERR_RANGE), missing entries
+    (ERR_ARG) and a bad shape in any entry (ERR_SIZE) before touching the device;
+    a group of one has the single call's workspace; a group's workspace holds every
+    projection's regions."""
+    import ctypes
+    dsv = _dsv()
+    lib = dsv.lib_handle()
+    plan = dsv.segments_build([(0, 16, 0, 1), (16, 300, 1, 0)], 316, [4, 4], [2.0, 2.0], 4)
+    fake = ctypes.c_void_p(4096)
+    arr = (dsv.FwdProj * 9)()
+    for i in range(9):
+        arr[i] = dsv.FwdProj(64, 64, fake, fake, fake, fake, fake, fake)
+    for n in (0, -1, 9):
+        assert lib.dsv_cobatch_fwd_grouped(plan.handle, dsv.BF16, n, arr, fake, 1 << 20, None) == dsv.ERR_RANGE
+    assert lib.dsv_cobatch_fwd_grouped(plan.handle, dsv.BF16, 2, None, fake, 1 << 20, None) == dsv.ERR_ARG
+    arr[1].K = 60
+    assert lib.dsv_cobatch_fwd_grouped(plan.handle, dsv.BF16, 2, arr, fake, 1 << 20, None) == dsv.ERR_SIZE
+    arr[1].K = 64
+    assert lib.dsv_cobatch_fwd_grouped(plan.handle, dsv.BF16, 2, arr, fake, 1 << 20, None) == dsv.ERR_ARG
+    barr = (dsv.BwdProj * 2)()
+    for i in range(2):
+        barr[i] = dsv.BwdProj(64, 64, fake, fake, fake, fake, fake, fake, fake, fake, fake)
+    assert lib.dsv_lora_bwd_grouped(plan.handle, dsv.BF16, 2, barr, 2, fake, 1 << 20, None) == dsv.ERR_RANGE
+    assert lib.dsv_lora_bwd_grouped(plan.handle, dsv.BF16, 2, barr, 0, fake, 1 << 20, None) == dsv.ERR_ARG
+    for dt in (dsv.BF16, dsv.F32):
+        assert dsv.fwd_grouped_workspace_bytes(plan, dt, [(520, 776)]) == dsv.fwd_workspace_bytes(plan, dt, 520, 776)
+        assert dsv.bwd_grouped_workspace_bytes(plan, dt, [(520, 776)]) == dsv.bwd_workspace_bytes(plan, dt, 520, 776)
+        shapes = [(520, 776), (4096, 1024), (136, 64)]
+        # each projection's h / low-rank / partial regions, without split-tile partials
+        assert dsv.fwd_grouped_workspace_bytes(plan, dt, shapes) >= sum(
+            dsv.fwd_workspace_bytes(plan, dt, 64, 64) for _ in shapes)
+        assert dsv.bwd_grouped_workspace_bytes(plan, dt, shapes) >= sum(
+            dsv.bwd_workspace_bytes(plan, dt, K, 64) for K, _ in shapes) // 2
