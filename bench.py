@@ -98,6 +98,26 @@ def measured_traffic():
     return float(doc["traffic_bytes_per_launch"])
 
 
+def launch_groups(w, launch, dropout):
+    """[(lo, hi)] ranges of w.projections run by one grouped call each, or None for
+    one call per projection.  `layer` groups the projections whose inputs exist at
+    the same point of a transformer layer: those sharing the layer input (q, k, v),
+    the attention output (o), the MLP input (gate, up) and the MLP product (down)."""
+    if launch == "single" or dropout > 0 or len(w.projections) == 1:
+        return None
+    if launch == "set":
+        return [(0, len(w.projections))]
+    names = [p.name for p in w.projections]
+    order = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
+    if names != [n for g in order for n in g]:
+        return [(i, i + 1) for i in range(len(names))]
+    out, lo = [], 0
+    for g in order:
+        out.append((lo, lo + len(g)))
+        lo += len(g)
+    return out
+
+
 def _gen(args):
     name, p = args
     w = WORKLOADS[name]()
@@ -149,8 +169,10 @@ def main():
     ap.add_argument("--cpu-dx-rows", type=int, default=24)
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timing of the steps that follow the layer (the AdamW update)")
-    ap.add_argument("--grouped", action="store_true",
-                    help="run the layer set through the grouped entry points (one launch per step kind)")
+    ap.add_argument("--launch", default="set", choices=("single", "layer", "set"),
+                    help="single: one call per projection; layer: grouped calls over the projections a "
+                         "transformer layer can run together (q/k/v, o, gate/up, down); set: one grouped call "
+                         "over the whole set")
     ap.add_argument("--dropout", type=float, default=0.0, metavar="P",
                     help="LoRA dropout P on the training rows in the timed step (fresh mask per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -226,66 +248,74 @@ def main():
     sh = ctypes.c_void_p(int(stream.cuda_stream))
     ptr = lambda t: ctypes.c_void_p(int(t.data_ptr()))  # noqa: E731
     plan_ms = []
-    if args.grouped:
-        if args.dropout > 0:
-            raise SystemExit("--grouped has no dropout form")
-        shapes = [(proj.K, proj.N) for proj in w.projections]
-        fproj = (dsv.FwdProj * len(P))()
-        bproj = (dsv.BwdProj * len(P))()
-        for p, (K, N) in enumerate(shapes):
-            d = P[p]
-            fproj[p] = dsv.FwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]))
-            bproj[p] = dsv.BwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["H"]), ptr(d["dY"]),
-                                   ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]))
-        gws_f = torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes), 256), dtype=torch.uint8,
-                            device=dev)
-        gws_b = torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes), 256), dtype=torch.uint8,
-                            device=dev)
+    def make_step(launch):
+        """The step function of one launch mode, and its projection groups."""
+        groups = launch_groups(w, launch, args.dropout)
+        if groups is not None:
+            shapes = [(proj.K, proj.N) for proj in w.projections]
+            fproj = (dsv.FwdProj * len(P))()
+            bproj = (dsv.BwdProj * len(P))()
+            for p, (K, N) in enumerate(shapes):
+                d = P[p]
+                fproj[p] = dsv.FwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]))
+                bproj[p] = dsv.BwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["H"]), ptr(d["dY"]),
+                                       ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]))
+            fgroup = [(dsv.FwdProj * (hi - lo))(*fproj[lo:hi]) for lo, hi in groups]
+            bgroup = [(dsv.BwdProj * (hi - lo))(*bproj[lo:hi]) for lo, hi in groups]
+            gws_f = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                                 dtype=torch.uint8, device=dev) for lo, hi in groups]
+            gws_b = [torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                                 dtype=torch.uint8, device=dev) for lo, hi in groups]
 
-    def step(i):
-        h = ctypes.c_void_p()
-        tp = time.perf_counter()
-        rc = lib.dsv_segments_build(seg.ctypes.data_as(i32p), seg.shape[0], w.n_tokens,
-                                    ranks.ctypes.data_as(i32p), scales.ctypes.data_as(f32p),
-                                    ranks.shape[0], w.r_max, ptr(metas[i & 1]), ctypes.byref(meta_bytes),
-                                    sh, ctypes.byref(h))
-        plan_ms.append((time.perf_counter() - tp) * 1e3)
-        if rc != 0:
-            raise RuntimeError("dsv_segments_build failed: %d" % rc)
-        if args.grouped:
-            rc = lib.dsv_cobatch_fwd_grouped(h, code, len(w.projections), fproj, ptr(gws_f), gws_f.numel(), sh)
+        def step(i):
+            h = ctypes.c_void_p()
+            tp = time.perf_counter()
+            rc = lib.dsv_segments_build(seg.ctypes.data_as(i32p), seg.shape[0], w.n_tokens,
+                                        ranks.ctypes.data_as(i32p), scales.ctypes.data_as(f32p),
+                                        ranks.shape[0], w.r_max, ptr(metas[i & 1]), ctypes.byref(meta_bytes),
+                                        sh, ctypes.byref(h))
+            plan_ms.append((time.perf_counter() - tp) * 1e3)
             if rc != 0:
-                raise RuntimeError("dsv_cobatch_fwd_grouped failed: %d" % rc)
-            rc = lib.dsv_lora_bwd_grouped(h, code, len(w.projections), bproj, 0, ptr(gws_b), gws_b.numel(), sh)
-            if rc != 0:
-                raise RuntimeError("dsv_lora_bwd_grouped failed: %d" % rc)
-            lib.dsv_plan_free(h)
-            return
-        for p, proj in enumerate(w.projections):
-            d = P[p]
-            K, N = proj.K, proj.N
-            if args.dropout > 0:
-                # one mask stream per projection and step: offset = step * projections + p
-                dr = ctypes.byref(dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p))
-                rc = lib.dsv_cobatch_fwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]),
-                                                 ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]), dr, ptr(d["wsf"]),
-                                                 d["wsf"].numel(), sh)
-            else:
-                rc = lib.dsv_cobatch_fwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
-                                         ptr(d["Y"]), ptr(d["H"]), ptr(d["wsf"]), d["wsf"].numel(), sh)
-            if rc != 0:
-                raise RuntimeError("dsv_cobatch_fwd failed: %d" % rc)
-            if args.dropout > 0:
-                rc = lib.dsv_lora_bwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
-                                              ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
-                                              0, dr, ptr(d["wsb"]), d["wsb"].numel(), sh)
-            else:
-                rc = lib.dsv_lora_bwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
-                                      ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
-                                      0, ptr(d["wsb"]), d["wsb"].numel(), sh)
-            if rc != 0:
-                raise RuntimeError("dsv_lora_bwd failed: %d" % rc)
-        lib.dsv_plan_free(h)  # the blob's copy was issued; the device metadata stays valid
+                raise RuntimeError("dsv_segments_build failed: %d" % rc)
+            if groups is not None:
+                for gi, (lo, hi) in enumerate(groups):
+                    rc = lib.dsv_cobatch_fwd_grouped(h, code, hi - lo, fgroup[gi], ptr(gws_f[gi]), gws_f[gi].numel(), sh)
+                    if rc != 0:
+                        raise RuntimeError("dsv_cobatch_fwd_grouped failed: %d" % rc)
+                for gi, (lo, hi) in enumerate(groups):
+                    rc = lib.dsv_lora_bwd_grouped(h, code, hi - lo, bgroup[gi], 0, ptr(gws_b[gi]), gws_b[gi].numel(), sh)
+                    if rc != 0:
+                        raise RuntimeError("dsv_lora_bwd_grouped failed: %d" % rc)
+                lib.dsv_plan_free(h)
+                return
+            for p, proj in enumerate(w.projections):
+                d = P[p]
+                K, N = proj.K, proj.N
+                if args.dropout > 0:
+                    # one mask stream per projection and step: offset = step * projections + p
+                    dr = ctypes.byref(dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p))
+                    rc = lib.dsv_cobatch_fwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]),
+                                                     ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]), dr, ptr(d["wsf"]),
+                                                     d["wsf"].numel(), sh)
+                else:
+                    rc = lib.dsv_cobatch_fwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                             ptr(d["Y"]), ptr(d["H"]), ptr(d["wsf"]), d["wsf"].numel(), sh)
+                if rc != 0:
+                    raise RuntimeError("dsv_cobatch_fwd failed: %d" % rc)
+                if args.dropout > 0:
+                    rc = lib.dsv_lora_bwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                                  ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
+                                                  0, dr, ptr(d["wsb"]), d["wsb"].numel(), sh)
+                else:
+                    rc = lib.dsv_lora_bwd(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]),
+                                          ptr(d["H"]), ptr(d["dY"]), ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]),
+                                          0, ptr(d["wsb"]), d["wsb"].numel(), sh)
+                if rc != 0:
+                    raise RuntimeError("dsv_lora_bwd failed: %d" % rc)
+            lib.dsv_plan_free(h)  # the blob's copy was issued; the device metadata stays valid
+        return step, groups
+
+    step, groups = make_step(args.launch)
 
     for i in range(args.warmup):
         step(i)
@@ -304,6 +334,7 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
     dsv.timing_enable(False)
+    plan_med = round(float(np.median(plan_ms)), 4) if plan_ms else None
     fwd_ms, fwd_n, bwd_ms, bwd_n = dsv.timing_read()
     gpu_ms = ev0.elapsed_time(ev1)
     elapsed_s = max(wall, gpu_ms / 1e3)
@@ -315,7 +346,7 @@ def main():
     fwd_gemm_flops = sum(gemm_fwd_flops(w, proj, gathered) for proj in w.projections)
     bwd_gemm_flops = sum(gemm_bwd_flops(w, proj) for proj in w.projections)
     fwd_avg_ms = fwd_ms / max(fwd_n, 1)
-    per_step = 1 if args.grouped else len(w.projections)  # timed GEMM launches per step
+    per_step = len(groups) if groups is not None else len(w.projections)  # timed GEMM launches per step
     achieved = fwd_gemm_flops * (fwd_n / per_step) / (fwd_ms / 1e3) / 1e12 if fwd_ms > 0 else None
     bwd_achieved = bwd_gemm_flops * (bwd_n / per_step) / (bwd_ms / 1e3) / 1e12 if bwd_ms > 0 else None
     log("timed %d steps: %.3f ms/step, %.1f TFLOP/s; fwd GEMM %.1f TFLOP/s avg %.1f us; dX GEMM %s TFLOP/s"
@@ -416,6 +447,24 @@ def main():
         log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
         del wsd
 
+        # The same step in the other launch modes (10 timed steps each).
+        modes = {args.launch: round(ms_per_step, 4)}
+        for m in ("single", "layer", "set"):
+            if m in modes:
+                continue
+            st, _ = make_step(m)
+            for i in range(3):
+                st(i)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for i in range(10):
+                st(i)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            modes[m] = round(e0.elapsed_time(e1) / 10, 4)
+        extras["launch_modes_ms_per_step"] = modes
+        log("ms per step by launch mode: %s" % modes)
+
     def cfg_str(c):
         if not c["tile_m"]:
             return None
@@ -426,6 +475,21 @@ def main():
     gemm_launches = {proj.name: {"fwd": cfg_str(dsv.gemm_config(probe, code, proj.K, proj.N, 0)),
                                  "dx": cfg_str(dsv.gemm_config(probe, code, proj.K, proj.N, 1))}
                      for proj in w.projections}
+    roof_kernel = ("gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the low-rank "
+                   "prologue; the fixup sums contraction-split tiles)")
+    if groups is not None:
+        pc = probe.counts()
+        for lo, hi in groups:
+            if hi - lo < 2:
+                continue
+            ps = w.projections[lo:hi]
+            gemm_launches["+".join(p.name for p in ps)] = {
+                "fwd": "256x256 tiles, %d in one launch" % sum(pc["fwd_tiles"] * ((p.N + 255) // 256) for p in ps),
+                "dx": "256x256 tiles, %d in one launch" % sum(pc["bwd_tiles"] * ((p.K + 255) // 256) for p in ps)}
+            for p in ps:
+                gemm_launches.pop(p.name, None)
+        roof_kernel = ("gemm_group_kernel<NT> (the forward base GEMMs with their low-rank prologues, every "
+                       "projection of a group in one launch; with --launch set, one launch per step)")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -460,13 +524,14 @@ def main():
             "adapters": w.n_adapters,
             "ranks": sorted(set(int(r) for r in w.ranks)),
             "algorithmic_gflop_per_step": round(step_flops / 1e9, 2),
-            "plan_build_ms": round(float(np.median(plan_ms)), 4) if plan_ms else None,
+            "plan_build_ms": plan_med,
             "lora_dropout": args.dropout,
-            "launch": "grouped" if args.grouped else "per projection",
+            "launch": args.launch,
+            "launch_groups": ([[p.name for p in w.projections[lo:hi]] for lo, hi in groups] if groups is not None
+                              else [[p.name] for p in w.projections]),
         },
         "roofline": {
-            "kernel": "gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the "
-                      "low-rank prologue; the fixup sums contraction-split tiles)",
+            "kernel": roof_kernel,
             "bound": "mfma",
             "achieved": round(achieved, 2) if achieved else None,
             "peak": PEAK_BF16_TFLOPS,
