@@ -103,7 +103,7 @@ def launch_groups(w, launch, dropout):
     one call per projection.  `layer` groups the projections whose inputs exist at
     the same point of a transformer layer: those sharing the layer input (q, k, v),
     the attention output (o), the MLP input (gate, up) and the MLP product (down)."""
-    if launch == "single" or dropout > 0 or len(w.projections) == 1:
+    if launch == "single" or len(w.projections) == 1:
         return None
     if launch == "set":
         return [(0, len(w.projections))]
@@ -278,12 +278,26 @@ def main():
             if rc != 0:
                 raise RuntimeError("dsv_segments_build failed: %d" % rc)
             if groups is not None:
+                drs = None
+                if args.dropout > 0:  # one mask stream per projection and step
+                    drs = [(dsv.Dropout * (hi - lo))(*[dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p)
+                                                        for p in range(lo, hi)]) for lo, hi in groups]
                 for gi, (lo, hi) in enumerate(groups):
-                    rc = lib.dsv_cobatch_fwd_grouped(h, code, hi - lo, fgroup[gi], ptr(gws_f[gi]), gws_f[gi].numel(), sh)
+                    if drs is None:
+                        rc = lib.dsv_cobatch_fwd_grouped(h, code, hi - lo, fgroup[gi], ptr(gws_f[gi]),
+                                                         gws_f[gi].numel(), sh)
+                    else:
+                        rc = lib.dsv_cobatch_fwd_grouped_dropout(h, code, hi - lo, fgroup[gi], drs[gi],
+                                                                 ptr(gws_f[gi]), gws_f[gi].numel(), sh)
                     if rc != 0:
                         raise RuntimeError("dsv_cobatch_fwd_grouped failed: %d" % rc)
                 for gi, (lo, hi) in enumerate(groups):
-                    rc = lib.dsv_lora_bwd_grouped(h, code, hi - lo, bgroup[gi], 0, ptr(gws_b[gi]), gws_b[gi].numel(), sh)
+                    if drs is None:
+                        rc = lib.dsv_lora_bwd_grouped(h, code, hi - lo, bgroup[gi], 0, ptr(gws_b[gi]),
+                                                      gws_b[gi].numel(), sh)
+                    else:
+                        rc = lib.dsv_lora_bwd_grouped_dropout(h, code, hi - lo, bgroup[gi], 0, drs[gi],
+                                                              ptr(gws_b[gi]), gws_b[gi].numel(), sh)
                     if rc != 0:
                         raise RuntimeError("dsv_lora_bwd_grouped failed: %d" % rc)
                 lib.dsv_plan_free(h)
@@ -419,20 +433,30 @@ def main():
         log("backward with kept h %.1f us, with recomputed h %.1f us per step" % (bt[True], bt[False]))
 
         # LoRA dropout 0.05 on the training rows (the fine-tuning setting of Sec. 4.1):
-        # the whole step (forward + backward of every projection) with and without it.
-        wsd = [torch.empty(max(dsv.bwd_workspace_bytes(probe, code, proj.K, proj.N, dropout=True), 256),
-                           dtype=torch.uint8, device=dev) for proj in w.projections]
+        # the whole step (forward + backward of every projection, in the bench's launch
+        # mode) with and without it.
+        gl = groups if groups is not None else [(p, p + 1) for p in range(len(w.projections))]
+        shapes = [(proj.K, proj.N) for proj in w.projections]
+        wsf_d = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                             dtype=torch.uint8, device=dev) for lo, hi in gl]
+        wsb_d = [torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                             dtype=torch.uint8, device=dev) for lo, hi in gl]
 
         def step_all(drop):
-            for p, proj in enumerate(w.projections):
-                d = P[p]
-                dsv.cobatch_fwd(probe_dev, d["X"], d["W"], d["A"], d["B"], Y=d["Y"], H_save=d["H"],
-                                workspace=d["wsf"], stream=stream, dropout=drop)
-                dsv.lora_bwd(probe_dev, d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], dA=d["dA"],
-                             dB=d["dB"], dX=d["dX"], workspace=wsd[p], stream=stream, dropout=drop)
+            for gi, (lo, hi) in enumerate(gl):
+                ds = [P[p] for p in range(lo, hi)]
+                drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
+                dsv.cobatch_fwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["Y"], d["H"]) for d in ds],
+                                        workspace=wsf_d[gi], stream=stream, dropouts=drops)
+            for gi, (lo, hi) in enumerate(gl):
+                ds = [P[p] for p in range(lo, hi)]
+                drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
+                dsv.lora_bwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], d["dA"], d["dB"],
+                                                  d["dX"]) for d in ds],
+                                     workspace=wsb_d[gi], stream=stream, dropouts=drops)
         dt_ = {}
         for key in ("off", "p0.05", "off", "p0.05"):
-            drop = None if key == "off" else (0.05, 1234, 0)
+            drop = None if key == "off" else 0.05
             step_all(drop)
             torch.cuda.synchronize()
             e0.record(stream)
@@ -445,7 +469,7 @@ def main():
                              "step_us_with": round(dt_["p0.05"], 2),
                              "overhead_frac": round(dt_["p0.05"] / dt_["off"] - 1.0, 4)}
         log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
-        del wsd
+        del wsf_d, wsb_d
 
         # The same step in the other launch modes (10 timed steps each).
         modes = {args.launch: round(ms_per_step, 4)}

@@ -266,7 +266,11 @@ int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32
  * those split a tile along the contraction (another summation order);
  * repeated grouped calls are bit-identical.  The workspace holds the
  * single-call regions of every projection, 256-byte aligned, of at least the
- * *_grouped_workspace size.  Dropout is not offered in grouped form.
+ * *_grouped_workspace size.  The _dropout forms take dropouts[n_proj], one
+ * dsv_dropout per projection (a caller gives each projection its own seed or
+ * offset), and compute what dsv_cobatch_fwd_dropout / dsv_lora_bwd_dropout
+ * compute for each entry; they return DSV_ERR_ARG for a NULL dropouts and
+ * DSV_ERR_RANGE for any p outside [0, 1), and use the same workspace sizes.
  */
 #define DSV_MAX_GROUP 8
 
@@ -303,6 +307,13 @@ int dsv_lora_bwd_grouped_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_
 int dsv_lora_bwd_grouped(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
                          const dsv_bwd_proj* projs, int32_t accumulate, void* workspace,
                          size_t workspace_bytes, void* hip_stream);
+int dsv_cobatch_fwd_grouped_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                                    const dsv_fwd_proj* projs, const dsv_dropout* dropouts,
+                                    void* workspace, size_t workspace_bytes, void* hip_stream);
+int dsv_lora_bwd_grouped_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                                 const dsv_bwd_proj* projs, int32_t accumulate,
+                                 const dsv_dropout* dropouts, void* workspace,
+                                 size_t workspace_bytes, void* hip_stream);
 
 /*
  * Kernel timing for benchmarks.  While enabled (on = 1), every

@@ -782,20 +782,39 @@ extern "C" int dsv_lora_bwd_grouped_workspace(const dsv_plan* p, dsv_dtype dt, i
   return DSV_OK;
 }
 
-extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_fwd_proj* projs,
-                                       void* workspace, size_t workspace_bytes, void* hip_stream) {
+namespace {
+
+// Dropout of a grouped call: every projection's mask spec (projections with
+// p = 0 get an all-keeping mask of scale 1 when another one drops, which
+// leaves their results bit for bit as without dropout).
+int group_dropout(const dsv_dropout* drops, int32_t n, int32_t T_t, DropoutSpec* ds, bool* any) {
+  *any = false;
+  for (int i = 0; i < n; ++i) ds[i] = DropoutSpec{0u, 1.f, 0, 0};
+  if (!drops) return DSV_OK;
+  for (int i = 0; i < n; ++i) {
+    if (!dropout_spec(&drops[i], &ds[i])) return DSV_ERR_RANGE;
+    if (drops[i].p > 0.0 && T_t > 0) *any = true;
+  }
+  return DSV_OK;
+}
+
+int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_fwd_proj* projs,
+                     const dsv_dropout* drops, void* workspace, size_t workspace_bytes, void* hip_stream) {
   int rc = check_group(p, dt, n_proj, projs);
   if (rc != DSV_OK) return rc;
   if (n_proj == 1) {
     const dsv_fwd_proj& q = projs[0];
-    return dsv_cobatch_fwd(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, workspace, workspace_bytes,
-                           hip_stream);
+    return fwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, drops, workspace, workspace_bytes,
+                    hip_stream);
   }
   // every check before any launch
   for (int i = 0; i < n_proj; ++i) {
     const dsv_fwd_proj& q = projs[i];
     if ((rc = check_common(p, dt, q.K, q.N)) != DSV_OK) return rc;
   }
+  DropoutSpec ds[DSV_MAX_GROUP];
+  bool dropping = false;
+  if ((rc = group_dropout(drops, n_proj, p->T_t, ds, &dropping)) != DSV_OK) return rc;
   if (!p->d_meta) return DSV_ERR_ARG;
   if (p->T == 0) return DSV_OK;
   for (int i = 0; i < n_proj; ++i) {
@@ -814,8 +833,8 @@ extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t 
   if (dt == DSV_F32) {  // the fp32 check path: the single-projection kernels, one projection at a time
     for (int i = 0; i < n_proj; ++i) {
       const dsv_fwd_proj& q = projs[i];
-      rc = fwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, nullptr, wsb + base[i], w[i].total,
-                    hip_stream);
+      rc = fwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, drops ? &drops[i] : nullptr, wsb + base[i],
+                    w[i].total, hip_stream);
       if (rc != DSV_OK) return rc;
     }
     return DSV_OK;
@@ -825,6 +844,12 @@ extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t 
   const int32_t* ranks = p->dptr(L.ranks);
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   const int64_t ldh = ld_rank(p->r_max);
+
+  // 0. dropout masks of the training rows' adapter input
+  if (dropping)
+    for (int i = 0; i < n_proj; ++i)
+      if (launch_dropout_mask(at<uint32_t>(wsb + base[i], w[i].keep), p->T_t, projs[i].K, ds[i], s) != hipSuccess)
+        return DSV_ERR_DEVICE;
 
   // 1. shrink of every projection in one launch
   SkinnyGroup sg{};
@@ -846,6 +871,11 @@ extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t 
     sk.out2 = p->T_t > 0 ? static_cast<uint16_t*>(q.H_save) : nullptr;
     sk.ld2 = p->r_max;
     sk.row_train = p->dptr(L.row_train);
+    if (dropping) {
+      sk.keep = at<uint32_t>(wsb + base[i], w[i].keep);
+      sk.keep_words = (q.K + 31) / 32;
+      sk.drop_scale = ds[i].scale;
+    }
   }
   if (launch_shrink_group(sg, p->n_shrink, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
 
@@ -902,17 +932,20 @@ extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t 
   return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
 }
 
-extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_bwd_proj* projs,
-                                    int32_t accumulate, void* workspace, size_t workspace_bytes, void* hip_stream) {
+int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_bwd_proj* projs, int32_t accumulate,
+                     const dsv_dropout* drops, void* workspace, size_t workspace_bytes, void* hip_stream) {
   int rc = check_group(p, dt, n_proj, projs);
   if (rc != DSV_OK) return rc;
   if (n_proj == 1) {
     const dsv_bwd_proj& q = projs[0];
-    return dsv_lora_bwd(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate,
-                        workspace, workspace_bytes, hip_stream);
+    return bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate, drops,
+                    workspace, workspace_bytes, hip_stream);
   }
   for (int i = 0; i < n_proj; ++i)
     if ((rc = check_common(p, dt, projs[i].K, projs[i].N)) != DSV_OK) return rc;
+  DropoutSpec ds[DSV_MAX_GROUP];
+  bool dropping = false;
+  if ((rc = group_dropout(drops, n_proj, p->T_t, ds, &dropping)) != DSV_OK) return rc;
   if (accumulate != 0 && accumulate != 1) return DSV_ERR_RANGE;
   if (!p->d_meta) return DSV_ERR_ARG;
   if (p->T_t == 0) return DSV_OK;
@@ -934,8 +967,8 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
   if (dt == DSV_F32) {
     for (int i = 0; i < n_proj; ++i) {
       const dsv_bwd_proj& q = projs[i];
-      rc = bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate, nullptr,
-                    wsb + base[i], w[i].total, hip_stream);
+      rc = bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate,
+                    drops ? &drops[i] : nullptr, wsb + base[i], w[i].total, hip_stream);
       if (rc != DSV_OK) return rc;
     }
     return DSV_OK;
@@ -948,10 +981,17 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
   const int32_t* train_ads = p->dptr(L.train_ads);
   uint16_t* bt[DSV_MAX_GROUP];
   uint16_t* gm[DSV_MAX_GROUP];
+  uint32_t* keep[DSV_MAX_GROUP];
   for (int i = 0; i < n_proj; ++i) {
     bt[i] = at<uint16_t>(wsb + base[i], w[i].bt);
     gm[i] = at<uint16_t>(wsb + base[i], w[i].g);
+    keep[i] = dropping ? at<uint32_t>(wsb + base[i], w[i].keep) : nullptr;
   }
+
+  // 0. the forward's dropout masks, regenerated from the same seeds and offsets
+  if (dropping)
+    for (int i = 0; i < n_proj; ++i)
+      if (launch_dropout_mask(keep[i], p->T_t, projs[i].K, ds[i], s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 1. transposed B of the training adapters, every projection
   TransposeGroup tg{};
@@ -1003,6 +1043,9 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
     sh.out2 = hrec;
     sh.ld2 = ldh;
     sh.row_train = p->dptr(L.row_train);
+    sh.keep = keep[i];
+    sh.keep_words = (q.K + 31) / 32;
+    sh.drop_scale = ds[i].scale;
     hs[i] = hrec;
     ldhs[i] = ldh;
   }
@@ -1032,6 +1075,8 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
     ta.ldq = ldh;
     ta.C = q.K;
     ta.part = at<float>(wsb + base[i], w[i].part_a);
+    ta.keep = keep[i];  // dA contracts the masked input
+    ta.keep_words = (q.K + 31) / 32;
   }
   for (int k = 0; k < trg.n; ++k) trg.yoff[k + 1] = trg.yoff[k] + (trg.a[k].C + 127) / 128;
   if (launch_token_reduce_group(trg, p->n_chunks, s) != hipSuccess) return DSV_ERR_DEVICE;
@@ -1041,7 +1086,8 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
   og.n = 2 * n_proj;
   for (int i = 0; i < n_proj; ++i) {
     og.a[2 * i] = ReduceOutArgs{trg.a[2 * i].part, projs[i].N, scales, 0, projs[i].dB, 1.f};
-    og.a[2 * i + 1] = ReduceOutArgs{trg.a[2 * i + 1].part, projs[i].K, nullptr, 1, projs[i].dA, 1.f};
+    og.a[2 * i + 1] = ReduceOutArgs{trg.a[2 * i + 1].part, projs[i].K, nullptr, 1, projs[i].dA,
+                                    dropping ? ds[i].scale : 1.f};
   }
   if (launch_reduce_out_group(og, p->r_max, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr), p->dptr(L.tad_chunks),
                               ranks, accumulate, s) != hipSuccess)
@@ -1075,6 +1121,9 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
     g.lq_j = q.K;
     g.lq_col = 1;
     g.ranks = ranks;
+    g.keep = keep[i];  // dropout: g A_a through the input's mask
+    g.keep_words = (q.K + 31) / 32;
+    g.keep_scale = ds[i].scale;
     G.off[G.n + 1] = G.off[G.n] + g.n_mtiles * g.n_ntiles;
     ++G.n;
   }
@@ -1085,4 +1134,31 @@ extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_p
     if (e != hipSuccess) return DSV_ERR_DEVICE;
   }
   return DSV_OK;
+}
+
+}  // namespace
+
+extern "C" int dsv_cobatch_fwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_fwd_proj* projs,
+                                       void* workspace, size_t workspace_bytes, void* hip_stream) {
+  return fwd_grouped_impl(p, dt, n_proj, projs, nullptr, workspace, workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_cobatch_fwd_grouped_dropout(const dsv_plan* p, dsv_dtype dt, int32_t n_proj,
+                                               const dsv_fwd_proj* projs, const dsv_dropout* dropouts,
+                                               void* workspace, size_t workspace_bytes, void* hip_stream) {
+  if (!dropouts) return DSV_ERR_ARG;
+  return fwd_grouped_impl(p, dt, n_proj, projs, dropouts, workspace, workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_lora_bwd_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_bwd_proj* projs,
+                                    int32_t accumulate, void* workspace, size_t workspace_bytes, void* hip_stream) {
+  return bwd_grouped_impl(p, dt, n_proj, projs, accumulate, nullptr, workspace, workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_lora_bwd_grouped_dropout(const dsv_plan* p, dsv_dtype dt, int32_t n_proj,
+                                            const dsv_bwd_proj* projs, int32_t accumulate,
+                                            const dsv_dropout* dropouts, void* workspace, size_t workspace_bytes,
+                                            void* hip_stream) {
+  if (!dropouts) return DSV_ERR_ARG;
+  return bwd_grouped_impl(p, dt, n_proj, projs, accumulate, dropouts, workspace, workspace_bytes, hip_stream);
 }

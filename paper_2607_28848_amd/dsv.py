@@ -99,6 +99,12 @@ _lib.dsv_lora_bwd_grouped_workspace.argtypes = [_vp, ctypes.c_int, _i32, ctypes.
 _lib.dsv_lora_bwd_grouped_workspace.restype = ctypes.c_int
 _lib.dsv_lora_bwd_grouped.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(BwdProj), _i32, _vp, _sz, _vp]
 _lib.dsv_lora_bwd_grouped.restype = ctypes.c_int
+_lib.dsv_cobatch_fwd_grouped_dropout.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(FwdProj),
+                                                 ctypes.POINTER(Dropout), _vp, _sz, _vp]
+_lib.dsv_cobatch_fwd_grouped_dropout.restype = ctypes.c_int
+_lib.dsv_lora_bwd_grouped_dropout.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(BwdProj), _i32,
+                                              ctypes.POINTER(Dropout), _vp, _sz, _vp]
+_lib.dsv_lora_bwd_grouped_dropout.restype = ctypes.c_int
 _lib.dsv_timing_enable.argtypes = [_i32]
 _lib.dsv_timing_enable.restype = ctypes.c_int
 _lib.dsv_timing_read.argtypes = [ctypes.POINTER(ctypes.c_double), _i32p,
@@ -348,9 +354,22 @@ def bwd_grouped_workspace_bytes(plan: Plan, dtype_code: int, shapes) -> int:
     return int(n.value)
 
 
-def cobatch_fwd_grouped(plan: Plan, projs, workspace=None, stream=None, keep_h: bool = True):
+def _dropouts(dropouts, n):
+    """[(p, seed, offset)] * n -> C array (None stays None)."""
+    if dropouts is None:
+        return None
+    if len(dropouts) != n:
+        raise ValueError("one dropout per projection")
+    arr = (Dropout * n)()
+    for i, d in enumerate(dropouts):
+        arr[i] = _dropout(d)
+    return arr
+
+
+def cobatch_fwd_grouped(plan: Plan, projs, workspace=None, stream=None, keep_h: bool = True, dropouts=None):
     """dsv_cobatch_fwd_grouped.  projs: [(X, W, A, B)] or [(X, W, A, B, Y, H_save)];
-    returns [(Y, H_save)] in the same order."""
+    returns [(Y, H_save)] in the same order.  dropouts: one (p, seed, offset) per
+    projection (dsv_cobatch_fwd_grouped_dropout)."""
     import torch
     items = []
     for pr in projs:
@@ -365,13 +384,20 @@ def cobatch_fwd_grouped(plan: Plan, projs, workspace=None, stream=None, keep_h: 
     ws = _workspace(fwd_grouped_workspace_bytes(plan, dt, [(it[0].shape[1], it[1].shape[0]) for it in items]),
                     items[0][0].device, workspace)
     arr = _fwd_projs(items)
-    _check(_lib.dsv_cobatch_fwd_grouped(plan.handle, dt, len(items), arr, _ptr(ws), ws.numel() * ws.element_size(),
-                                        _stream_handle(stream)), "dsv_cobatch_fwd_grouped")
+    dr = _dropouts(dropouts, len(items))
+    if dr is None:
+        _check(_lib.dsv_cobatch_fwd_grouped(plan.handle, dt, len(items), arr, _ptr(ws),
+                                            ws.numel() * ws.element_size(), _stream_handle(stream)),
+               "dsv_cobatch_fwd_grouped")
+    else:
+        _check(_lib.dsv_cobatch_fwd_grouped_dropout(plan.handle, dt, len(items), arr, dr, _ptr(ws),
+                                                    ws.numel() * ws.element_size(), _stream_handle(stream)),
+               "dsv_cobatch_fwd_grouped_dropout")
     return [(it[4], it[5]) for it in items]
 
 
 def lora_bwd_grouped(plan: Plan, projs, accumulate: bool = False, want_dx: bool = True, workspace=None,
-                     stream=None):
+                     stream=None, dropouts=None):
     """dsv_lora_bwd_grouped.  projs: [(X, W, A, B, H_save, dY)] or with (dA, dB, dX) appended;
     returns [(dA, dB, dX)]."""
     import torch
@@ -394,8 +420,15 @@ def lora_bwd_grouped(plan: Plan, projs, accumulate: bool = False, want_dx: bool 
     for i, (X, W, A, B, H, dY, dA, dB, dX) in enumerate(items):
         arr[i] = BwdProj(X.shape[1], W.shape[0], _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H), _ptr(dY), _ptr(dA),
                          _ptr(dB), _ptr(dX))
-    _check(_lib.dsv_lora_bwd_grouped(plan.handle, dt, len(items), arr, 1 if accumulate else 0, _ptr(ws),
-                                     ws.numel() * ws.element_size(), _stream_handle(stream)), "dsv_lora_bwd_grouped")
+    dr = _dropouts(dropouts, len(items))
+    if dr is None:
+        _check(_lib.dsv_lora_bwd_grouped(plan.handle, dt, len(items), arr, 1 if accumulate else 0, _ptr(ws),
+                                         ws.numel() * ws.element_size(), _stream_handle(stream)),
+               "dsv_lora_bwd_grouped")
+    else:
+        _check(_lib.dsv_lora_bwd_grouped_dropout(plan.handle, dt, len(items), arr, 1 if accumulate else 0, dr,
+                                                 _ptr(ws), ws.numel() * ws.element_size(), _stream_handle(stream)),
+               "dsv_lora_bwd_grouped_dropout")
     return [(it[6], it[7], it[8]) for it in items]
 
 

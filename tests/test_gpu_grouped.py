@@ -168,3 +168,57 @@ def test_grouped_llama8b_layer_set_full_size():
         _check_proj(w, ts[i], tr, out[i][0], out[i][1], grads[i][0], grads[i][1], grads[i][2], TOL_BF16,
                     rows=rows.astype(np.int32), dx_rows=dx_rows.astype(np.int32))
     w.projections = projs
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_grouped_dropout_against_reference(dtype):
+    """Grouped calls with one dropout per projection (two seeds, an offset, one
+    projection at p = 0 and one keeping no H_save): every output of every
+    projection against the reference fed each projection's own mask; the p = 0
+    projection matches the plain single call."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(520, 776), (136, 1040), (1040, 264)]
+    drops = [(0.3, 0x0123456789ABCDEF, 5), (0.0, 7, 0), (0.05, 0xFEDCBA9876543210, (3 << 32) | 1)]
+    _say("case grouped dropout %s %s" % (dtype, shapes))
+    w, ts, dev = _layer(dtype, shapes)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    Tt = plan.train_tokens
+    fw = []
+    for i, d in enumerate(dev):
+        H = None if i == 2 else torch.zeros((Tt, w.r_max), dtype=d["X"].dtype, device="cuda")
+        fw.append((d["X"], d["W"], d["A"], d["B"], None, H))
+    out = dsv.cobatch_fwd_grouped(plan, fw, keep_h=False, dropouts=drops)
+    grads = dsv.lora_bwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"])
+                                        for i, d in enumerate(dev)], dropouts=drops)
+    Hp = torch.zeros((Tt, w.r_max), dtype=dev[1]["X"].dtype, device="cuda")
+    Y1, H1 = dsv.cobatch_fwd(plan, dev[1]["X"], dev[1]["W"], dev[1]["A"], dev[1]["B"], H_save=Hp)
+    g1 = dsv.lora_bwd(plan, dev[1]["X"], dev[1]["W"], dev[1]["A"], dev[1]["B"], H1, dev[1]["dY"])
+    torch.cuda.synchronize()
+    tr = plan.train_rows()
+    tol = TOL_BF16 if dtype == "bf16" else TOL_F32
+    for i, (K, N) in enumerate(shapes):
+        _say(" projection %d K=%d N=%d p=%.2f" % (i, K, N, drops[i][0]))
+        drop = oracle.dropout_multipliers(Tt, K, *drops[i])
+        Yr, _ = oracle_fwd(w, ts[i], drop=drop)
+        errs = {"Y": oracle.rel_err(to_host(out[i][0]), Yr)}
+        if out[i][1] is not None:
+            errs["H_save"] = oracle.rel_err(to_host(out[i][1]), oracle_fwd(w, ts[i], tr, drop=drop)[1])
+        _, dAr, dBr, dXr = oracle_bwd(w, ts[i], drop=drop)
+        dAg, dBg = to_host(grads[i][0]), to_host(grads[i][1])
+        for a, r in train_mask_slices(w):
+            errs["dA%d" % a] = oracle.rel_err(dAg[a, :r], dAr[a, :r])
+            errs["dB%d" % a] = oracle.rel_err(dBg[a, :, :r], dBr[a, :, :r])
+        errs["dX"] = oracle.rel_err(to_host(grads[i][2]), dXr)
+        _say("  rel errors: " + ", ".join("%s=%.2e" % kv for kv in errs.items()))
+        for k, v in errs.items():
+            assert v <= tol, (k, v)
+    K, N = shapes[1]
+    same_fwd = dsv.gemm_config(plan, dsv.BF16, K, N, 0)["split_tiles"] == 0 or dtype == "f32"
+    same_bwd = dsv.gemm_config(plan, dsv.BF16, K, N, 1)["split_tiles"] == 0 or dtype == "f32"
+    assert torch.equal(_bits(out[1][1]), _bits(H1))
+    assert torch.equal(_bits(grads[1][0]), _bits(g1[0])) and torch.equal(_bits(grads[1][1]), _bits(g1[1]))
+    if same_fwd:
+        assert torch.equal(_bits(out[1][0]), _bits(Y1))
+    if same_bwd:
+        assert torch.equal(_bits(grads[1][2]), _bits(g1[2]))
