@@ -173,6 +173,9 @@ def main():
                     help="single: one call per projection; layer: grouped calls over the projections a "
                          "transformer layer can run together (q/k/v, o, gate/up, down); set: one grouped call "
                          "over the whole set")
+    ap.add_argument("--no-wt", action="store_true",
+                    help="grouped backward without the transposed copy of the frozen weights (the dX GEMM "
+                         "then transposes W in the kernel)")
     ap.add_argument("--dropout", type=float, default=0.0, metavar="P",
                     help="LoRA dropout P on the training rows in the timed step (fresh mask per step)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -229,6 +232,8 @@ def main():
         d["dX"] = torch.empty((max(Tt, 1), K), dtype=tdt, device=dev)
         d["dA"] = torch.zeros((w.n_adapters, w.r_max, K), dtype=torch.float32, device=dev)
         d["dB"] = torch.zeros((w.n_adapters, N, w.r_max), dtype=torch.float32, device=dev)
+        # the frozen weight kept a second time, transposed, for the dX GEMM (set up once, like W)
+        d["Wt"] = d["W"].t().contiguous()
         d["wsf"] = torch.empty(max(dsv.fwd_workspace_bytes(probe, code, K, N), 256), dtype=torch.uint8, device=dev)
         d["wsb"] = torch.empty(max(dsv.bwd_workspace_bytes(probe, code, K, N, dropout=args.dropout > 0), 256),
                                dtype=torch.uint8, device=dev)
@@ -248,7 +253,7 @@ def main():
     sh = ctypes.c_void_p(int(stream.cuda_stream))
     ptr = lambda t: ctypes.c_void_p(int(t.data_ptr()))  # noqa: E731
     plan_ms = []
-    def make_step(launch):
+    def make_step(launch, use_wt=not args.no_wt):
         """The step function of one launch mode, and its projection groups."""
         groups = launch_groups(w, launch, args.dropout)
         if groups is not None:
@@ -259,7 +264,7 @@ def main():
                 d = P[p]
                 fproj[p] = dsv.FwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]))
                 bproj[p] = dsv.BwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["H"]), ptr(d["dY"]),
-                                       ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]))
+                                       ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]), ptr(d["Wt"]) if use_wt else None)
             fgroup = [(dsv.FwdProj * (hi - lo))(*fproj[lo:hi]) for lo, hi in groups]
             bgroup = [(dsv.BwdProj * (hi - lo))(*bproj[lo:hi]) for lo, hi in groups]
             gws_f = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
@@ -453,7 +458,8 @@ def main():
                 drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
                 dsv.lora_bwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], d["dA"], d["dB"],
                                                   d["dX"]) for d in ds],
-                                     workspace=wsb_d[gi], stream=stream, dropouts=drops)
+                                     workspace=wsb_d[gi], stream=stream, dropouts=drops,
+                                     wts=None if args.no_wt else [d["Wt"] for d in ds])
         dt_ = {}
         for key in ("off", "p0.05", "off", "p0.05"):
             drop = None if key == "off" else 0.05
@@ -471,12 +477,13 @@ def main():
         log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
         del wsf_d, wsb_d
 
-        # The same step in the other launch modes (10 timed steps each).
-        modes = {args.launch: round(ms_per_step, 4)}
-        for m in ("single", "layer", "set"):
-            if m in modes:
+        # The same step in the other launch modes (10 timed steps each); "<mode>_no_wt":
+        # the grouped backward without the transposed weights.
+        modes = {args.launch + ("_no_wt" if args.no_wt else ""): round(ms_per_step, 4)}
+        for m in ("single", "layer", "set", "layer_no_wt", "set_no_wt"):
+            if m in modes or (m == args.launch and not args.no_wt):
                 continue
-            st, _ = make_step(m)
+            st, _ = make_step(m.replace("_no_wt", ""), use_wt=not m.endswith("_no_wt"))
             for i in range(3):
                 st(i)
             torch.cuda.synchronize()
@@ -551,6 +558,7 @@ def main():
             "plan_build_ms": plan_med,
             "lora_dropout": args.dropout,
             "launch": args.launch,
+            "dx_weight": "W transposed (kept once, like W)" if groups is not None and not args.no_wt else "W",
             "launch_groups": ([[p.name for p in w.projections[lo:hi]] for lo, hi in groups] if groups is not None
                               else [[p.name] for p in w.projections]),
         },

@@ -462,10 +462,12 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   return DSV_OK;
 }
 
+// Wt (optional, bf16): the frozen weight transposed, [K][N]; the dX GEMM then
+// reads it K-contiguous like the forward's W instead of transposing W on the fly.
 int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
              const void* B, const void* H_save, const void* dY, float* dA, float* dB, void* dX,
-             int32_t accumulate, const dsv_dropout* drop, void* workspace, size_t workspace_bytes,
-             void* hip_stream) {
+             int32_t accumulate, const dsv_dropout* drop, const void* Wt, void* workspace,
+             size_t workspace_bytes, void* hip_stream) {
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   DropoutSpec ds{};
@@ -477,7 +479,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(dA) || !ptr_ok(dB))
     return DSV_ERR_ARG;
   if (dX && !aligned16(dX)) return DSV_ERR_ARG;
-  if (!ptr_ok(dY) || (H_save && !aligned16(H_save))) return DSV_ERR_ARG;
+  if (!ptr_ok(dY) || (H_save && !aligned16(H_save)) || (Wt && !aligned16(Wt))) return DSV_ERR_ARG;
   const GemmPlan gp = bwd_gemm_plan(*p, dt, K, N);
   const BwdWs ws = bwd_ws(*p, dt, K, N, gp);
   if (ws.total > 0) {
@@ -630,8 +632,8 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     GemmArgs g{};
     g.P = static_cast<const uint16_t*>(dY);
     g.ldp = N;
-    g.Q = static_cast<const uint16_t*>(W);
-    g.ldq = K;
+    g.Q = static_cast<const uint16_t*>(Wt ? Wt : W);
+    g.ldq = Wt ? N : K;
     g.out = static_cast<uint16_t*>(dX);
     g.ldo = K;
     g.M = p->T_t;
@@ -653,7 +655,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     g.keep_words = keep_words;
     g.keep_scale = ds.scale;
     const int tk = timing_begin(1, s);
-    e = launch_gemm_nn(g, gp.tm, gp.tn, s);
+    e = Wt ? launch_gemm_nt(g, gp.tm, gp.tn, s) : launch_gemm_nn(g, gp.tm, gp.tn, s);
     timing_end(tk, s);
     if (e != hipSuccess) return DSV_ERR_DEVICE;
   }
@@ -680,7 +682,7 @@ extern "C" int dsv_lora_bwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t 
                             const void* W, const void* A, const void* B, const void* H_save,
                             const void* dY, float* dA, float* dB, void* dX, int32_t accumulate,
                             void* workspace, size_t workspace_bytes, void* hip_stream) {
-  return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, nullptr, workspace,
+  return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, nullptr, nullptr, workspace,
                   workspace_bytes, hip_stream);
 }
 
@@ -690,7 +692,7 @@ extern "C" int dsv_lora_bwd_dropout(const dsv_plan* p, dsv_dtype dt, int32_t K, 
                                     const dsv_dropout* dropout, void* workspace, size_t workspace_bytes,
                                     void* hip_stream) {
   if (!dropout) return DSV_ERR_ARG;
-  return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, dropout, workspace,
+  return bwd_impl(p, dt, K, N, X, W, A, B, H_save, dY, dA, dB, dX, accumulate, dropout, nullptr, workspace,
                   workspace_bytes, hip_stream);
 }
 
@@ -938,7 +940,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   if (rc != DSV_OK) return rc;
   if (n_proj == 1) {
     const dsv_bwd_proj& q = projs[0];
-    return bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate, drops,
+    return bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate, drops, q.Wt,
                     workspace, workspace_bytes, hip_stream);
   }
   for (int i = 0; i < n_proj; ++i)
@@ -954,7 +956,8 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     if (!ptr_ok(q.X) || !ptr_ok(q.W) || !ptr_ok(q.A) || !ptr_ok(q.B) || !ptr_ok(q.dA) || !ptr_ok(q.dB) ||
         !ptr_ok(q.dY))
       return DSV_ERR_ARG;
-    if ((q.dX && !aligned16(q.dX)) || (q.H_save && !aligned16(q.H_save))) return DSV_ERR_ARG;
+    if ((q.dX && !aligned16(q.dX)) || (q.H_save && !aligned16(q.H_save)) || (q.Wt && !aligned16(q.Wt)))
+      return DSV_ERR_ARG;
   }
   size_t base[DSV_MAX_GROUP];
   BwdWs w[DSV_MAX_GROUP];
@@ -968,7 +971,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     for (int i = 0; i < n_proj; ++i) {
       const dsv_bwd_proj& q = projs[i];
       rc = bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate,
-                    drops ? &drops[i] : nullptr, wsb + base[i], w[i].total, hip_stream);
+                    drops ? &drops[i] : nullptr, q.Wt, wsb + base[i], w[i].total, hip_stream);
       if (rc != DSV_OK) return rc;
     }
     return DSV_OK;
@@ -1093,45 +1096,48 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
                               ranks, accumulate, s) != hipSuccess)
     return DSV_ERR_DEVICE;
 
-  // 5. every dX GEMM in one launch, longest contraction first
+  // 5. every dX GEMM in one launch, longest contraction first (projections with a
+  //    transposed weight in one NT launch, the others in one NN launch)
   int32_t Cs[DSV_MAX_GROUP], order[DSV_MAX_GROUP];
   for (int i = 0; i < n_proj; ++i) Cs[i] = projs[i].N;
   by_contraction(n_proj, Cs, order);
-  GemmGroup G{};
-  for (int k = 0; k < n_proj; ++k) {
-    const int i = order[k];
-    const dsv_bwd_proj& q = projs[i];
-    if (!q.dX) continue;
-    GemmArgs& g = G.a[G.n];
-    g.P = static_cast<const uint16_t*>(q.dY);
-    g.ldp = q.N;
-    g.Q = static_cast<const uint16_t*>(q.W);
-    g.ldq = q.K;
-    g.out = static_cast<uint16_t*>(q.dX);
-    g.ldo = q.K;
-    g.M = p->T_t;
-    g.Nout = q.K;
-    g.C = q.N;
-    g.tiles = p->dptr(L.bwd_tiles);
-    set_split(g, whole256(p->n_btiles, q.K), nullptr, 0);
-    g.Lp = gm[i];
-    g.ldl = ldh;
-    g.Lq = static_cast<const uint16_t*>(q.A);
-    g.lq_ad = (int64_t)p->r_max * q.K;
-    g.lq_j = q.K;
-    g.lq_col = 1;
-    g.ranks = ranks;
-    g.keep = keep[i];  // dropout: g A_a through the input's mask
-    g.keep_words = (q.K + 31) / 32;
-    g.keep_scale = ds[i].scale;
-    G.off[G.n + 1] = G.off[G.n] + g.n_mtiles * g.n_ntiles;
-    ++G.n;
-  }
-  if (G.n > 0) {
-    const int tk = timing_begin(1, s);
-    const hipError_t e = launch_gemm_group_nn(G, s);
-    timing_end(tk, s);
-    if (e != hipSuccess) return DSV_ERR_DEVICE;
+  for (int nt = 1; nt >= 0; --nt) {
+    GemmGroup G{};
+    for (int k = 0; k < n_proj; ++k) {
+      const int i = order[k];
+      const dsv_bwd_proj& q = projs[i];
+      if (!q.dX || (q.Wt != nullptr) != (nt == 1)) continue;
+      GemmArgs& g = G.a[G.n];
+      g.P = static_cast<const uint16_t*>(q.dY);
+      g.ldp = q.N;
+      g.Q = static_cast<const uint16_t*>(nt ? q.Wt : q.W);
+      g.ldq = nt ? q.N : q.K;
+      g.out = static_cast<uint16_t*>(q.dX);
+      g.ldo = q.K;
+      g.M = p->T_t;
+      g.Nout = q.K;
+      g.C = q.N;
+      g.tiles = p->dptr(L.bwd_tiles);
+      set_split(g, whole256(p->n_btiles, q.K), nullptr, 0);
+      g.Lp = gm[i];
+      g.ldl = ldh;
+      g.Lq = static_cast<const uint16_t*>(q.A);
+      g.lq_ad = (int64_t)p->r_max * q.K;
+      g.lq_j = q.K;
+      g.lq_col = 1;
+      g.ranks = ranks;
+      g.keep = keep[i];  // dropout: g A_a through the input's mask
+      g.keep_words = (q.K + 31) / 32;
+      g.keep_scale = ds[i].scale;
+      G.off[G.n + 1] = G.off[G.n] + g.n_mtiles * g.n_ntiles;
+      ++G.n;
+    }
+    if (G.n > 0) {
+      const int tk = timing_begin(1, s);
+      const hipError_t e = nt ? launch_gemm_group_nt(G, s) : launch_gemm_group_nn(G, s);
+      timing_end(tk, s);
+      if (e != hipSuccess) return DSV_ERR_DEVICE;
+    }
   }
   return DSV_OK;
 }

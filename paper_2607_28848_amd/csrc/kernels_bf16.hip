@@ -378,7 +378,7 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // The prologue left g A_a in the accumulators; it passes through the input's
   // mask before dy W is added: kept elements scaled by 1 / (1 - p), dropped
   // ones zeroed.  Lane columns are fixed per j, so a row needs FN mask words.
-  if (NN && kb == 0 && g.keep != nullptr) {  // the dX GEMM only
+  if (kb == 0 && g.keep != nullptr) {  // dX GEMMs only (the forward passes no mask)
     const int wcol = (n0 + wn * WN) >> 5;  // first mask word of the wave's columns
 #pragma unroll
     for (int i = 0; i < FM; ++i) {

@@ -85,7 +85,7 @@ class FwdProj(ctypes.Structure):
 
 class BwdProj(ctypes.Structure):
     _fields_ = [("K", _i32), ("N", _i32), ("X", _vp), ("W", _vp), ("A", _vp), ("B", _vp), ("H_save", _vp),
-                ("dY", _vp), ("dA", _vp), ("dB", _vp), ("dX", _vp)]
+                ("dY", _vp), ("dA", _vp), ("dB", _vp), ("dX", _vp), ("Wt", _vp)]
 
 
 MAX_GROUP = 8
@@ -397,9 +397,10 @@ def cobatch_fwd_grouped(plan: Plan, projs, workspace=None, stream=None, keep_h: 
 
 
 def lora_bwd_grouped(plan: Plan, projs, accumulate: bool = False, want_dx: bool = True, workspace=None,
-                     stream=None, dropouts=None):
+                     stream=None, dropouts=None, wts=None):
     """dsv_lora_bwd_grouped.  projs: [(X, W, A, B, H_save, dY)] or with (dA, dB, dX) appended;
-    returns [(dA, dB, dX)]."""
+    returns [(dA, dB, dX)].  wts: optional transposed weights [K][N] per projection (or None
+    entries)."""
     import torch
     items = []
     for pr in projs:
@@ -418,8 +419,9 @@ def lora_bwd_grouped(plan: Plan, projs, accumulate: bool = False, want_dx: bool 
                     items[0][0].device, workspace)
     arr = (BwdProj * len(items))()
     for i, (X, W, A, B, H, dY, dA, dB, dX) in enumerate(items):
+        Wt = wts[i] if wts is not None else None
         arr[i] = BwdProj(X.shape[1], W.shape[0], _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H), _ptr(dY), _ptr(dA),
-                         _ptr(dB), _ptr(dX))
+                         _ptr(dB), _ptr(dX), _ptr(Wt))
     dr = _dropouts(dropouts, len(items))
     if dr is None:
         _check(_lib.dsv_lora_bwd_grouped(plan.handle, dt, len(items), arr, 1 if accumulate else 0, _ptr(ws),

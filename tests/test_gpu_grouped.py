@@ -222,3 +222,35 @@ def test_grouped_dropout_against_reference(dtype):
         assert torch.equal(_bits(out[1][0]), _bits(Y1))
     if same_bwd:
         assert torch.equal(_bits(grads[1][2]), _bits(g1[2]))
+
+
+@pytest.mark.parametrize("n_proj", [1, 3])
+def test_grouped_transposed_weight_bit_identical(n_proj):
+    """bf16 backward with the frozen weight also given transposed (dsv_bwd_proj.Wt):
+    the dX GEMM reads it contraction-contiguous (NT) instead of transposing W in the
+    kernel; dA, dB and dX are bit-identical to the plain call, with and without
+    dropout (the dropout mask of g A_a sits in the NT GEMM's prologue then), and
+    within the bar of the reference."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(520, 776), (136, 1040), (4096, 2048)][:n_proj]
+    _say("case transposed weight %s" % shapes)
+    w, ts, dev = _layer("bf16", shapes)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    out = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"]) for d in dev])
+    bw = [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"]) for i, d in enumerate(dev)]
+    wts = [d["W"].t().contiguous() for d in dev]
+    drops = [(0.1, 99, i) for i in range(n_proj)]
+    plain = dsv.lora_bwd_grouped(plan, bw)
+    viat = dsv.lora_bwd_grouped(plan, bw, wts=wts)
+    plain_d = dsv.lora_bwd_grouped(plan, bw, dropouts=drops)
+    viat_d = dsv.lora_bwd_grouped(plan, bw, dropouts=drops, wts=wts)
+    torch.cuda.synchronize()
+    for i in range(n_proj):
+        for a, b in list(zip(plain[i], viat[i])) + list(zip(plain_d[i], viat_d[i])):
+            assert torch.equal(_bits(a), _bits(b))
+        w.projections = [wl.Projection("p", *shapes[i])]
+        _, _, _, dXr = oracle_bwd(w, ts[i])
+        err = oracle.rel_err(to_host(viat[i][2]), dXr)
+        _say("  projection %d dX rel err %.2e" % (i, err))
+        assert err <= TOL_BF16
