@@ -571,7 +571,7 @@ __global__ __launch_bounds__(512) void gemm_group_kernel(GemmGroup G) {
   __shared__ __attribute__((aligned(1024))) char smem[S::LDS];
   int pj = 0;
   while (pj + 1 < G.n && (int)blockIdx.x >= G.off[pj + 1]) ++pj;
-  const GemmArgs& g = G.a[pj];
+  const GemmArgs g = G.a[pj];  // a copy: uniform fields held in scalar registers
   const int local = (int)blockIdx.x - G.off[pj];
   const int lin = xcd_major(local, G.off[pj + 1] - G.off[pj]);
   const int nk = (g.C + 63) / 64;
