@@ -639,7 +639,7 @@ __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int beg
 // DROP (shrink only): the training rows' input passes through the dropout mask.
 template <int MODE, int NJ, int ROWS, bool DROP>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
 __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
-  const SkinnyArgs& g = G.a[blockIdx.y];  // the projection
+  const SkinnyArgs g = G.a[blockIdx.y];  // the projection's arguments (a copy: scalar registers)
   constexpr int RT = ROWS / 16;  // 16-row tiles per item
   // U slices per batch; two batches in registers (the next one loads while
   // the current one feeds the matrix cores)
@@ -816,7 +816,7 @@ __global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceGroup G) {
   __shared__ f32x4 red[3][8 * NJ][64];
   int k = 0;  // the reduction: blockIdx.y runs over every reduction's column blocks
   while (k + 1 < G.n && (int)blockIdx.y >= G.yoff[k + 1]) ++k;
-  const TokenReduceArgs& g = G.a[k];
+  const TokenReduceArgs g = G.a[k];
   const int by = (int)blockIdx.y - G.yoff[k];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
@@ -906,7 +906,7 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32
                                                          const int32_t* __restrict__ tad_chunks,
                                                          const int32_t* __restrict__ ranks, int32_t accumulate) {
   const int which = (int)blockIdx.y / n_tads;
-  const ReduceOutArgs& g = G.a[which];
+  const ReduceOutArgs g = G.a[which];
   const int ta = (int)blockIdx.y - which * n_tads;
   const int C = g.C;
   const int a = train_ads[ta], r = ranks[a];
