@@ -254,3 +254,46 @@ def test_grouped_transposed_weight_bit_identical(n_proj):
         err = oracle.rel_err(to_host(viat[i][2]), dXr)
         _say("  projection %d dX rel err %.2e" % (i, err))
         assert err <= TOL_BF16
+
+
+def test_grouped_inference_only_training_only_and_empty():
+    """Degenerate batches through the grouped calls: no training rows (the backward is
+    a no-op, dA/dB untouched), training rows only, and an empty batch (nothing
+    written)."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(264, 136), (136, 264)]
+    for segs, name in (([(0, 40, 0, 0), (40, 3, 1, 0), (43, 20, 2, 0)], "inference only"),
+                       ([(0, 40, 0, 1), (40, 30, 2, 1)], "training only")):
+        _say("case grouped %s" % name)
+        w, ts, dev = _layer("bf16", shapes, segments=segs, ranks=[8, 4, 16], r_max=16)
+        plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+        out = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"]) for d in dev])
+        sent = [(torch.full_like(torch.zeros(3, w.r_max, shapes[i][0]), 7.0).cuda(),
+                 torch.full_like(torch.zeros(3, shapes[i][1], w.r_max), 7.0).cuda()) for i in range(2)]
+        Tt = plan.train_tokens
+        dY = [d["dY"] if Tt else None for d in dev]
+        grads = dsv.lora_bwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], out[i][1], dY[i] if Tt else d["X"],
+                                             sent[i][0], sent[i][1]) for i, d in enumerate(dev)])
+        torch.cuda.synchronize()
+        for i in range(2):
+            w.projections = [wl.Projection("p", *shapes[i])]
+            Yr, _ = oracle_fwd(w, ts[i])
+            assert oracle.rel_err(to_host(out[i][0]), Yr) <= TOL_BF16
+            if not Tt:
+                assert (sent[i][0] == 7.0).all() and (sent[i][1] == 7.0).all()
+            else:
+                _, dAr, dBr, dXr = oracle_bwd(w, ts[i])
+                for a, r in train_mask_slices(w):
+                    assert oracle.rel_err(to_host(grads[i][0])[a, :r], dAr[a, :r]) <= TOL_BF16
+                    assert oracle.rel_err(to_host(grads[i][1])[a, :, :r], dBr[a, :, :r]) <= TOL_BF16
+                assert oracle.rel_err(to_host(grads[i][2]), dXr) <= TOL_BF16
+    # empty batch: nothing is launched or written
+    plan = dsv.segments_build([], 0, [4], [1.0], 4, device="cuda")
+    X = torch.zeros((0, 64), dtype=torch.bfloat16, device="cuda")
+    W = torch.zeros((64, 64), dtype=torch.bfloat16, device="cuda")
+    A = torch.zeros((1, 4, 64), dtype=torch.bfloat16, device="cuda")
+    B = torch.zeros((1, 64, 4), dtype=torch.bfloat16, device="cuda")
+    out = dsv.cobatch_fwd_grouped(plan, [(X, W, A, B), (X, W, A, B)])
+    torch.cuda.synchronize()
+    assert out[0][0].shape == (0, 64)
