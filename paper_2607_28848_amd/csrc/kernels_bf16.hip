@@ -63,6 +63,19 @@ __device__ __forceinline__ uint32_t keep_byte(const uint32_t* keep, int keep_wor
   return (keep[(int64_t)row * keep_words + (c >> 5)] >> (c & 31)) & 0xffu;
 }
 
+// Eight bf16 values p[e * stride], e < n_valid (1 <= n_valid), the rest zero.
+// Every lane loads all eight (the index is clamped to n_valid - 1, so every
+// address is one the caller vouches for): straight-line code, no branches.
+__device__ __forceinline__ u32x4 ld8_sel(const uint16_t* p, int64_t stride, int n_valid) {
+  uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const uint32_t x = (uint32_t)p[(int64_t)min(e, n_valid - 1) * stride];
+    w[e >> 1] |= (e < n_valid ? x : 0u) << (16 * (e & 1));
+  }
+  return u32x4{w[0], w[1], w[2], w[3]};
+}
+
 // Eight bf16 values read with a per-element predicate, from p[e * stride].
 __device__ __forceinline__ u32x4 ld8_masked(const uint16_t* p, int64_t stride, int n_valid) {
   uint32_t w[4] = {0u, 0u, 0u, 0u};
@@ -324,19 +337,26 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
     const int r = g.ranks[a];
     const float sc = g.scales ? g.scales[a] : 1.f;
     const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
+    // Loads are straight-line: lanes outside the group's rows, past the rank or
+    // past the columns read a valid element (row lo, rank 0, the last column)
+    // and drop it.  With r a multiple of 16 every lane's 8 ranks are valid, and
+    // the h rows (and, for contiguous ranks with an 8-aligned stride, the B
+    // rows) are read 16 bytes at a time.
+    const bool full16 = (r & 15) == 0;
+    const bool lq_vec = full16 && g.lq_j == 1 && (g.lq_col & 7) == 0;
     for (int j0 = 0; j0 < r; j0 += 16) {
       const int jb = j0 + 8 * (lane >> 5);
       const int nv = min(8, r - jb);
+      const int jbc = nv > 0 ? jb : 0, nvc = max(nv, 1);
       bf16x8 af_hi[FM], af_lo[FM], bq[FN];
       bool any_lo = false;
 #pragma unroll
       for (int i = 0; i < FM; ++i) {
         const int row = wm * WM + 32 * i + (lane & 31);
-        u32x4 v = zero4();
-        if (row >= lo && row < hi && nv > 0) {
-          const uint16_t* p = g.Lp + (int64_t)(m0 + row) * g.ldl + jb;
-          v = (nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
-        }
+        const bool rin = row >= lo && row < hi && nv > 0;
+        const uint16_t* p = g.Lp + (int64_t)(m0 + (rin ? row : lo)) * g.ldl + jbc;
+        u32x4 v = full16 ? ld16(p) : ld8_sel(p, 1, nvc);
+        v = rin ? v : zero4();
         uint32_t wh[4], wl[4];
 #pragma unroll
         for (int d = 0; d < 4; ++d) {
@@ -354,10 +374,10 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = n0 + wn * WN + 32 * j + (lane & 31);
-        u32x4 v = zero4();
-        if (col < g.Nout && nv > 0)
-          v = ld8_masked(lq + (int64_t)jb * g.lq_j + (int64_t)col * g.lq_col, g.lq_j, nv);
-        bq[j] = as_bf(v);
+        const bool cin = col < g.Nout && nv > 0;
+        const uint16_t* p = lq + (int64_t)jbc * g.lq_j + (int64_t)min(col, g.Nout - 1) * g.lq_col;
+        u32x4 v = lq_vec ? ld16(p) : ld8_sel(p, g.lq_j, nvc);
+        bq[j] = as_bf(cin ? v : zero4());
       }
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -387,9 +407,12 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
       for (int v = 0; v < 16; ++v) {
         const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-          mw[v][j] = (row < nrows && wcol + j < g.keep_words)
-                         ? g.keep[(int64_t)(m0 + row) * g.keep_words + wcol + j] : 0u;
+        for (int j = 0; j < FN; ++j) {
+          const uint32_t x = g.keep[(int64_t)(m0 + min(row, nrows - 1)) * g.keep_words + min(wcol + j, g.keep_words - 1)];
+          // arithmetic masking keeps the load unconditional (a select would let the
+          // compiler move it under a branch with a wait of its own)
+          mw[v][j] = x & (0u - (uint32_t)(row < nrows && wcol + j < g.keep_words));
+        }
       }
 #pragma unroll
       for (int v = 0; v < 16; ++v)
@@ -506,22 +529,33 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // ---- epilogue: one rounding, staged through LDS for 16-byte stores ----
   __syncthreads();
   uint16_t* st = reinterpret_cast<uint16_t*>(smem);
-  const bool gather_tile = has_gather && g.delta != nullptr;
+  if (has_gather && g.delta != nullptr) {
+    // a tile holding rows of the gathered path: their fp32 low-rank term joins
+    // before the rounding
 #pragma unroll
-  for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i)
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-      // rows of the gathered path add their fp32 low-rank term before the rounding
-      const int gs = (gather_tile && row < nrows) ? g.gslot[m0 + row] : -1;
+      for (int v = 0; v < 16; ++v) {
+        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        const int gs = row < nrows ? g.gslot[m0 + row] : -1;
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = wn * WN + 32 * j + (lane & 31);
-        float x = acc[i][j][v];
-        if (gs >= 0 && n0 + col < g.Nout) x += g.delta[(int64_t)gs * g.Nout + n0 + col];
-        st[row * S::STG_LD + col] = f2bf(x);
+        for (int j = 0; j < FN; ++j) {
+          const int col = wn * WN + 32 * j + (lane & 31);
+          float x = acc[i][j][v];
+          if (gs >= 0 && n0 + col < g.Nout) x += g.delta[(int64_t)gs * g.Nout + n0 + col];
+          st[row * S::STG_LD + col] = f2bf(x);
+        }
       }
-    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) st[row * S::STG_LD + wn * WN + 32 * j + (lane & 31)] = f2bf(acc[i][j][v]);
+      }
+  }
   __syncthreads();
   constexpr int CH = TN / 8;  // 16-byte chunks per staged row
 #pragma unroll 4
