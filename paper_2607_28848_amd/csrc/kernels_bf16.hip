@@ -37,15 +37,15 @@ __device__ __forceinline__ u32x4 ld16(const uint16_t* p) {
 
 __device__ __forceinline__ u32x4 zero4() { return u32x4{0u, 0u, 0u, 0u}; }
 
-// fp32 -> bf16, round to nearest even (NaN kept quiet).  Written as a select,
-// not a branch: a branch per element makes the compiler spill accumulators
-// around every conversion of an epilogue.
-__device__ __forceinline__ uint16_t f2bf(float f) {
-  const uint32_t u = __float_as_uint(f);
-  const uint32_t rounded = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-  const uint32_t quiet = (u >> 16) | 0x40u;
-  return (uint16_t)(((u & 0x7fffffffu) > 0x7f800000u) ? quiet : rounded);
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+// fp32 -> bf16, round to nearest even (NaN stays NaN): gfx950's conversion
+// instruction, two values per instruction.
+__device__ __forceinline__ uint32_t f2bf2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
 }
+__device__ __forceinline__ uint16_t f2bf(float f) { return __builtin_bit_cast(uint16_t, (__bf16)f); }
 
 __device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float((uint32_t)h << 16); }
 
@@ -547,13 +547,19 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
         }
       }
   } else {
+    // rows v and v+1 of a lane are converted together
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
+      for (int v = 0; v < 16; v += 2) {
         const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) st[row * S::STG_LD + wn * WN + 32 * j + (lane & 31)] = f2bf(acc[i][j][v]);
+        for (int j = 0; j < FN; ++j) {
+          const uint32_t w = f2bf2(acc[i][j][v], acc[i][j][v + 1]);
+          uint16_t* p = st + row * S::STG_LD + wn * WN + 32 * j + (lane & 31);
+          p[0] = (uint16_t)w;
+          p[S::STG_LD] = (uint16_t)(w >> 16);
+        }
       }
   }
   __syncthreads();
