@@ -18,6 +18,8 @@
 //   gemm (NN)        dx = dy W + g A_a (prologue adds g A_a).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "kernels.h"
 #include "plan.h"
 
@@ -650,13 +652,23 @@ __global__ __launch_bounds__(256) void split_fixup_kernel(GemmArgs g) {
 }
 
 // ---------------------------------------------------------------------------
-// Skinny rank-r contraction: one workgroup per item of <= 32 rows of one
-// adapter (two 16-row tiles sharing each fragment of the adapter operand);
-// the SW waves take contiguous ranges of the contraction in 64-wide slices
-// with v_mfma_f32_16x16x32_bf16 (NJ = ceil(r/16) output tiles), U slices in
-// flight per wave, and combine their sums in LDS in a fixed order.
+// Skinny rank-r contraction out[row][j] = sum_k P[row][k] Q_a[j][k]: one
+// workgroup per item of <= ROWS rows of one adapter, 8 waves.  The
+// contraction runs in chunks of 256 columns; a chunk's ROWS input rows and
+// 16*NJ adapter rows go from global memory straight into LDS, 512 contiguous
+// bytes per row (two rows per wave instruction), double-buffered, so the input
+// streams in long runs.  Wave w multiplies columns [32w, 32w+32) of every chunk
+// with v_mfma_f32_16x16x32_bf16; the 8 partial sums of a row are combined in
+// LDS in a fixed order, so a row's result does not depend on the item it sits
+// in.  The LDS image of a row is swizzled (16-byte chunk c in slot c ^ (row & 7))
+// so the fragment reads are free of bank conflicts.
 // ---------------------------------------------------------------------------
-constexpr int SW = 8;  // waves per rank-contraction workgroup
+constexpr int SW = 8;       // waves per rank-contraction workgroup
+constexpr int SK_CK = 256;  // contraction columns per chunk
+
+typedef __attribute__((address_space(1))) const void global_cv;
+extern "C" __device__ void llvm_amdgcn_global_load_lds(global_cv* src, lds_u32* lds, int size, int offset,
+                                                       int aux) __asm("llvm.amdgcn.global.load.lds");
 
 // Final value of one entry (item row `row`, rank column j) from its fp32 sum.
 template <int MODE>
@@ -676,101 +688,129 @@ __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int beg
   }
 }
 
-// DROP (shrink only): the training rows' input passes through the dropout mask.
+// DROP (shrink only): the training rows' input passes through the dropout mask
+// (a mask byte per 8 columns, applied to the fragment as it is read).
 template <int MODE, int NJ, int ROWS, bool DROP>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
 __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
   const SkinnyArgs g = G.a[blockIdx.y];  // the projection's arguments (a copy: scalar registers)
-  constexpr int RT = ROWS / 16;  // 16-row tiles per item
-  // U slices per batch; two batches in registers (the next one loads while
-  // the current one feeds the matrix cores)
-  constexpr int U0 = RT + NJ <= 3 ? 4 : RT + NJ <= 4 ? 2 : 1;
-  constexpr int U = DROP && U0 > 2 ? 2 : U0;  // room for the mask bytes
-  __shared__ float red[SW][ROWS][DSV_MAX_RANK + 1];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  constexpr int RT = ROWS / 16;           // 16-row tiles per item
+  constexpr int SR = ROWS + 16 * NJ;      // LDS rows of a chunk: input rows, then adapter rows
+  constexpr int RB = SK_CK * 2;           // bytes per LDS row
+  constexpr int L = SR / 2 / SW;          // 1 KiB load instructions per wave per chunk
+  constexpr int STAGE = SR * RB;
+  static_assert(L * 2 * SW == SR, "loads per wave");
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
   const int a = it[0], begin = it[1], cnt = it[2];
   const int r = g.ranks[a];
-  const int slot = g.qsel ? g.qsel[a] : a;
-  const uint16_t* Qa = g.Q + (int64_t)slot * g.q_ad;
-  int prow[RT];
-  const uint16_t* pp[RT];
+  const int qslot = g.qsel ? g.qsel[a] : a;
+  const uint16_t* Qa = g.Q + (int64_t)qslot * g.q_ad;
+  // Wave instruction q loads LDS rows 2q and 2q+1; lane = 32 * (row - 2q) +
+  // slot.  Rows past the item repeat its last row (their sums are not stored),
+  // adapter rows past the rank load nothing and are written with zeros, as are
+  // the columns past the contraction.
+  const int sub = lane >> 5, sl = lane & 31;
+  const uint16_t* src[L];
+  int kcap[L];  // columns the lane's row provides
 #pragma unroll
-  for (int t = 0; t < RT; ++t) {
-    const int i = 16 * t + (lane & 15);
-    prow[t] = (i < cnt) ? (g.rows ? g.rows[begin + i] : begin + i) : -1;
-    pp[t] = g.P + (int64_t)max(prow[t], 0) * g.ldp;
+  for (int i = 0; i < L; ++i) {
+    const int q = wave * L + i;
+    const int sr = 2 * q + sub;
+    if (2 * q < ROWS) {
+      const int e = max(min(sr, cnt - 1), 0);
+      const int pr = g.rows ? g.rows[begin + e] : begin + e;
+      src[i] = g.P + (int64_t)pr * g.ldp + 8 * (sl ^ (sr & 7));
+      kcap[i] = g.C;
+    } else {
+      const int j = sr - ROWS;
+      src[i] = Qa + (int64_t)min(j, r - 1) * g.ldq + 8 * (sl ^ (sr & 7));
+      kcap[i] = j < r ? g.C : 0;
+    }
   }
-  // dropout: compact index of a lane's training row (-1: no mask)
+  auto issue = [&](int c, int st) {
+    char* base = smem + st * STAGE;
+#pragma unroll
+    for (int i = 0; i < L; ++i) {
+      const int q = wave * L + i;
+      const int k = c * SK_CK + 8 * (sl ^ ((2 * q + sub) & 7));
+      if (k < kcap[i])
+        llvm_amdgcn_global_load_lds((global_cv*)(src[i] + c * SK_CK), (lds_u32*)(base + q * 1024), 16, 0, 0);
+      else
+        *reinterpret_cast<u32x4*>(base + q * 1024 + 16 * lane) = zero4();
+    }
+  };
+  // dropout: compact training index of each fragment row of the lane (-1: none)
   int trl[RT];
 #pragma unroll
-  for (int t = 0; t < RT; ++t) trl[t] = (DROP && prow[t] >= 0) ? g.row_train[prow[t]] : -1;
+  for (int t = 0; t < RT; ++t) {
+    trl[t] = -1;
+    if constexpr (DROP) {
+      const int i = 16 * t + (lane & 15);
+      const int pr = g.rows ? g.rows[begin + min(i, cnt - 1)] : begin + min(i, cnt - 1);
+      trl[t] = i < cnt ? g.row_train[pr] : -1;
+    }
+  }
+  const int lc = 4 * wave + (lane >> 4);  // logical 16-byte chunk of the lane's fragments
+  const int nch = (g.C + SK_CK - 1) / SK_CK;
   f32x4 acc[RT][NJ];
 #pragma unroll
   for (int t = 0; t < RT; ++t)
 #pragma unroll
     for (int jt = 0; jt < NJ; ++jt) acc[t][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  // each wave takes a contiguous range of 64-wide slices (two 32-wide MFMA
-  // steps each), U consecutive slices per batch, so every row is read in
-  // runs of U * 128 bytes
-  const int nslices = (g.C + 63) / 64;
-  const int per_wave = (nslices + SW - 1) / SW;
-  const int s_lo = wave * per_wave, s_hi = min(nslices, s_lo + per_wave);
-  // Every lane issues every load (out-of-range lanes read a valid address and
-  // drop the value), so the loads are straight-line code and the wait before
-  // a batch's MFMAs counts only that batch's loads.
-  // Under dropout the mask bytes travel with the batch and are applied where
-  // the batch is consumed, so the loads of the next batch are not held up.
-  auto load = [&](int s0, u32x4 (&av)[U][2][RT], u32x4 (&bv)[U][2][NJ], uint32_t (&mb)[U][2][RT]) {
+  // Mask bytes of chunk c + 1 are loaded during chunk c, into the other of two
+  // register sets (the loop is unrolled by two), so the wait at the top of a
+  // chunk covers them and nothing waits on a load issued after them.
+  auto load_mask = [&](int c, uint32_t (&m)[RT]) {
+    const int col = min(c * SK_CK + 8 * lc, 32 * g.keep_words - 8);
 #pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int k = (s0 + u) * 64 + 32 * h + 8 * (lane >> 4);
-        const bool kin = s0 + u < s_hi && k < g.C;
-        const int kc = kin ? k : 0;
-#pragma unroll
-        for (int t = 0; t < RT; ++t) {
-          const u32x4 v = ld16(pp[t] + kc);
-          av[u][h][t] = (prow[t] >= 0 && kin) ? v : zero4();
-          if constexpr (DROP) mb[u][h][t] = keep_byte(g.keep, g.keep_words, max(trl[t], 0), kc);
-        }
-#pragma unroll
-        for (int jt = 0; jt < NJ; ++jt) {
-          const int j = 16 * jt + (lane & 15);
-          const u32x4 w = ld16(Qa + (int64_t)min(j, r - 1) * g.ldq + kc);
-          bv[u][h][jt] = (j < r && kin) ? w : zero4();
-        }
-      }
+    for (int t = 0; t < RT; ++t) m[t] = keep_byte(g.keep, g.keep_words, max(trl[t], 0), col);
   };
-  auto mma = [&](const u32x4 (&av)[U][2][RT], const u32x4 (&bv)[U][2][NJ], const uint32_t (&mb)[U][2][RT]) {
+  auto chunk = [&](int c, const uint32_t (&mu)[RT], uint32_t (&ml)[RT]) {
+    vmem_wait_all();
+    __syncthreads();  // chunk c is in; every wave is done with chunk c - 1's buffer
+    if (c + 1 < nch) issue(c + 1, (c + 1) & 1);
+    if constexpr (DROP) load_mask(min(c + 1, nch - 1), ml);  // unconditional: no merge to wait on
+    const char* sb = smem + (c & 1) * STAGE;
+    bf16x8 xf[RT], qf[NJ];
 #pragma unroll
-    for (int u = 0; u < U; ++u)
+    for (int t = 0; t < RT; ++t) {
+      const int row = 16 * t + (lane & 15);
+      u32x4 x = *reinterpret_cast<const u32x4*>(sb + row * RB + 16 * (lc ^ (row & 7)));
+      if constexpr (DROP) x = trl[t] >= 0 ? keep8(x, mu[t]) : x;
+      xf[t] = as_bf(x);
+    }
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+    for (int jt = 0; jt < NJ; ++jt) {
+      const int row = ROWS + 16 * jt + (lane & 15);
+      qf[jt] = as_bf(*reinterpret_cast<const u32x4*>(sb + row * RB + 16 * (lc ^ (row & 7))));
+    }
 #pragma unroll
-        for (int t = 0; t < RT; ++t) {
-          const u32x4 x = (DROP && trl[t] >= 0) ? keep8(av[u][h][t], mb[u][h][t]) : av[u][h][t];
+    for (int t = 0; t < RT; ++t)
 #pragma unroll
-          for (int jt = 0; jt < NJ; ++jt)
-            acc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(x), as_bf(bv[u][h][jt]), acc[t][jt], 0, 0, 0);
-        }
+      for (int jt = 0; jt < NJ; ++jt)
+        acc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[t], qf[jt], acc[t][jt], 0, 0, 0);
   };
-  u32x4 av0[U][2][RT], bv0[U][2][NJ], av1[U][2][RT], bv1[U][2][NJ];
-  uint32_t mb0[U][2][RT], mb1[U][2][RT];
-  if (s_lo < s_hi) load(s_lo, av0, bv0, mb0);
-  for (int s0 = s_lo; s0 < s_hi; s0 += 2 * U) {
-    if (s0 + U < s_hi) load(s0 + U, av1, bv1, mb1);
-    mma(av0, bv0, mb0);
-    if (s0 + U >= s_hi) break;
-    if (s0 + 2 * U < s_hi) load(s0 + 2 * U, av0, bv0, mb0);
-    mma(av1, bv1, mb1);
+  uint32_t m0[RT] = {}, m1[RT] = {};
+  if (nch > 0) {
+    issue(0, 0);
+    if constexpr (DROP) load_mask(0, m0);
   }
+  for (int c = 0; c < nch; c += 2) {
+    chunk(c, m0, m1);
+    if (c + 1 < nch) chunk(c + 1, m1, m0);
+  }
+  __syncthreads();  // the stage buffers become the reduction buffer
+  constexpr int RW = 16 * NJ + 1;
+  static_assert(SW * ROWS * RW * 4 <= 2 * STAGE, "reduction buffer");
+  float* red = reinterpret_cast<float*>(smem);  // [SW][ROWS][RW]
 #pragma unroll
   for (int t = 0; t < RT; ++t)
 #pragma unroll
     for (int jt = 0; jt < NJ; ++jt)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) red[wave][16 * t + 4 * (lane >> 4) + v][16 * jt + (lane & 15)] = acc[t][jt][v];
+      for (int v = 0; v < 4; ++v)
+        red[(wave * ROWS + 16 * t + 4 * (lane >> 4) + v) * RW + 16 * jt + (lane & 15)] = acc[t][jt][v];
   __syncthreads();
 #pragma unroll
   for (int q = 0; q < (ROWS * 64 + 64 * SW - 1) / (64 * SW); ++q) {
@@ -779,7 +819,7 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
     if (row < ROWS && row < cnt && j < r) {
       float sum = 0.f;
 #pragma unroll
-      for (int w = 0; w < SW; ++w) sum += red[w][row][j];
+      for (int w = 0; w < SW; ++w) sum += red[(w * ROWS + row) * RW + j];
       skinny_store<MODE>(g, a, begin, row, j, sum);
     }
   }
@@ -1031,24 +1071,30 @@ hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
 }
 
 namespace {
-template <int MODE, int ROWS, bool DROP>
-void launch_skinny_nj(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
-  const dim3 grid(n_items, g.n);
-  if (r_max <= 16)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 1, ROWS, DROP>), grid, dim3(64 * SW), 0, s, g);
-  else if (r_max <= 32)
-    hipLaunchKernelGGL((skinny_kernel<MODE, 2, ROWS, DROP>), grid, dim3(64 * SW), 0, s, g);
-  else
-    hipLaunchKernelGGL((skinny_kernel<MODE, 4, ROWS, DROP>), grid, dim3(64 * SW), 0, s, g);
+template <int MODE, int NJ, int ROWS, bool DROP>
+void launch_skinny_kernel(const SkinnyGroup& g, int32_t n_items, hipStream_t s) {
+  hipLaunchKernelGGL((skinny_kernel<MODE, NJ, ROWS, DROP>), dim3(n_items, g.n), dim3(64 * SW), 0, s, g);
 }
 
-// Every projection of a group takes the dropout path or none does.
+template <int MODE, int ROWS, bool DROP>
+void launch_skinny_nj(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
+  if (r_max <= 16) launch_skinny_kernel<MODE, 1, ROWS, DROP>(g, n_items, s);
+  else if (r_max <= 32) launch_skinny_kernel<MODE, 2, ROWS, DROP>(g, n_items, s);
+  else launch_skinny_kernel<MODE, 4, ROWS, DROP>(g, n_items, s);
+}
+
+// Every projection of a group takes the dropout path or none does.  The
+// projections are launched longest contraction first (workgroups are
+// dispatched projection by projection), so the long items start first and the
+// short ones fill in behind them.
 template <int MODE, int ROWS>
-hipError_t launch_skinny(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
-  if (n_items <= 0 || g.n <= 0) return hipSuccess;
-  if (g.n > kMaxGroup) return hipErrorInvalidValue;
-  for (int p = 1; p < g.n; ++p)
-    if ((g.a[p].keep != nullptr) != (g.a[0].keep != nullptr)) return hipErrorInvalidValue;
+hipError_t launch_skinny(const SkinnyGroup& g0, int32_t n_items, int32_t r_max, hipStream_t s) {
+  if (n_items <= 0 || g0.n <= 0) return hipSuccess;
+  if (g0.n > kMaxGroup) return hipErrorInvalidValue;
+  for (int p = 1; p < g0.n; ++p)
+    if ((g0.a[p].keep != nullptr) != (g0.a[0].keep != nullptr)) return hipErrorInvalidValue;
+  SkinnyGroup g = g0;
+  std::stable_sort(g.a, g.a + g.n, [](const SkinnyArgs& x, const SkinnyArgs& y) { return x.C > y.C; });
   if constexpr (MODE == 0) {
     if (g.a[0].keep != nullptr) launch_skinny_nj<MODE, ROWS, true>(g, n_items, r_max, s);
     else launch_skinny_nj<MODE, ROWS, false>(g, n_items, r_max, s);
