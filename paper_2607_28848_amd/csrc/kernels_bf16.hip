@@ -161,8 +161,7 @@ struct GemmShape {
   static constexpr int WM = TM / WGM, WN = TN / WGN, FM = WM / 32, FN = WN / 32;
   static constexpr int A_BYTES = TM * TK * 2, B_BYTES = TN * TK * 2;
   static constexpr int STAGE = A_BYTES + B_BYTES;
-  static constexpr int STG_LD = TN + 8;  // epilogue staging row stride (elements)
-  static constexpr int LDS = (NS * STAGE > TM * STG_LD * 2) ? NS * STAGE : TM * STG_LD * 2;
+  static constexpr int LDS = NS * STAGE;
 };
 
 // s_waitcnt immediate (gfx9 encoding): wait until at most n vector-memory
@@ -385,13 +384,13 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af_hi[i], bq[j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bq[j], af_hi[i], acc[i][j], 0, 0, 0);
       if (__builtin_amdgcn_ballot_w64(any_lo) != 0) {
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af_lo[i], bq[j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bq[j], af_lo[i], acc[i][j], 0, 0, 0);
       }
     }
   }
@@ -399,28 +398,28 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   // ---- dropout of the low-rank term (dX under LoRA dropout) --------------
   // The prologue left g A_a in the accumulators; it passes through the input's
   // mask before dy W is added: kept elements scaled by 1 / (1 - p), dropped
-  // ones zeroed.  Lane columns are fixed per j, so a row needs FN mask words.
+  // ones zeroed.  A lane holds one row and 16 columns of each 32 x 32 block,
+  // all inside one 32-column mask word: one word per block.
   if (kb == 0 && g.keep != nullptr) {  // dX GEMMs only (the forward passes no mask)
     const int wcol = (n0 + wn * WN) >> 5;  // first mask word of the wave's columns
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
-      uint32_t mw[16][FN];
+      const int row = wm * WM + 32 * i + (lane & 31);
+      uint32_t mw[FN];
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const uint32_t x = g.keep[(int64_t)(m0 + min(row, nrows - 1)) * g.keep_words + min(wcol + j, g.keep_words - 1)];
-          // arithmetic masking keeps the load unconditional (a select would let the
-          // compiler move it under a branch with a wait of its own)
-          mw[v][j] = x & (0u - (uint32_t)(row < nrows && wcol + j < g.keep_words));
-        }
+      for (int j = 0; j < FN; ++j) {
+        const uint32_t x = g.keep[(int64_t)(m0 + min(row, nrows - 1)) * g.keep_words + min(wcol + j, g.keep_words - 1)];
+        // arithmetic masking keeps the load unconditional (a select would let the
+        // compiler move it under a branch with a wait of its own)
+        mw[j] = x & (0u - (uint32_t)(row < nrows && wcol + j < g.keep_words));
       }
 #pragma unroll
-      for (int v = 0; v < 16; ++v)
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j][v] = ((mw[v][j] >> (lane & 31)) & 1u) ? acc[i][j][v] * g.keep_scale : 0.f;
+        for (int v = 0; v < 16; ++v) {
+          const int bit = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          acc[i][j][v] = ((mw[j] >> bit) & 1u) ? acc[i][j][v] * g.keep_scale : 0.f;
+        }
     }
   }
 
@@ -484,7 +483,7 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[s & 1][i], bq[s & 1][j], acc[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bq[s & 1][j], af[s & 1][i], acc[i][j], 0, 0, 0);
     }
 #pragma unroll
     for (int s = 0; s < kSteps - 1; ++s) {
@@ -509,71 +508,79 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[L][i], bq[L][j], acc[i][j], 0, 0, 0);
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bq[L][j], af[L][i], acc[i][j], 0, 0, 0);
     stage = next;
   }
+
+  // Accumulator layout (the MFMAs take the weight fragment as their first
+  // operand): acc[i][j][v] is output row wm*WM + 32i + lane%32, column
+  // wn*WN + 32j + 8(v/4) + 4(lane/32) + v%4 -- four consecutive columns of one
+  // row per group of four v.
 
   // ---- a piece of a split tile: its fp32 partial goes to its slot (row-major
   // tm x tn); a follow-up kernel sums the pieces and writes the tile ----
   if (SK && !(kb == 0 && ke == nk)) {
     float* part = g.sk_part + (int64_t)(t_sk * g.sk_split + piece) * (TM * TN);
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 32 * i + (lane & 31);
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) part[row * TN + wn * WN + 32 * j + (lane & 31)] = acc[i][j][v];
-      }
+        for (int q = 0; q < 4; ++q) {
+          const int col = wn * WN + 32 * j + 8 * q + 4 * (lane >> 5);
+          *reinterpret_cast<f32x4*>(part + row * TN + col) =
+              f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        }
+    }
     return;
   }
 
   // ---- epilogue: one rounding, staged through LDS for 16-byte stores ----
-  __syncthreads();
-  uint16_t* st = reinterpret_cast<uint16_t*>(smem);
-  if (has_gather && g.delta != nullptr) {
-    // a tile holding rows of the gathered path: their fp32 low-rank term joins
-    // before the rounding
+  // Each wave stages its own rows, 32 at a time, in a private slice of the
+  // pipeline buffer that the last K-step did not use (no wave reads it again),
+  // so no workgroup barrier is needed: a lane writes 4 columns (8 bytes) of its
+  // row, then the wave reads the slice back as 16-byte row chunks and stores
+  // whole 128-byte row segments.  The slice row stride (WN + 4 elements, 2
+  // dwords past a multiple of 32 banks) keeps the 8-byte writes of 16
+  // consecutive rows on distinct banks.
+  constexpr int SRS = WN * 2 + 8;  // slice row stride in bytes
+  static_assert(NS == 2 && NW * 32 * SRS <= S::STAGE, "epilogue slices fit the idle pipeline buffer");
+  char* slice = smem + ((ke - kb) & 1) * S::STAGE + wave * 32 * SRS;
+  const bool gathered = has_gather && g.delta != nullptr;
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+  for (int i = 0; i < FM; ++i) {
+    const int row = wm * WM + 32 * i + (lane & 31);
+    const int gs = (gathered && row < nrows) ? g.gslot[m0 + row] : -1;
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-        const int gs = row < nrows ? g.gslot[m0 + row] : -1;
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int col = wn * WN + 32 * j + (lane & 31);
-          float x = acc[i][j][v];
-          if (gs >= 0 && n0 + col < g.Nout) x += g.delta[(int64_t)gs * g.Nout + n0 + col];
-          st[row * S::STG_LD + col] = f2bf(x);
+      for (int q = 0; q < 4; ++q) {
+        const int col = wn * WN + 32 * j + 8 * q + 4 * (lane >> 5);
+        f32x4 x = f32x4{acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2], acc[i][j][4 * q + 3]};
+        // rows of the gathered path add their fp32 low-rank term before the
+        // rounding (a straight-line load from a clamped address, then a select)
+        if (gathered) {
+          const f32x4 d = *reinterpret_cast<const f32x4*>(g.delta + (int64_t)max(gs, 0) * g.Nout +
+                                                          min(n0 + col, g.Nout - 4));
+          x += (gs >= 0 && n0 + col < g.Nout) ? d : f32x4{0.f, 0.f, 0.f, 0.f};
         }
+        const uint32_t w0 = f2bf2(x[0], x[1]), w1 = f2bf2(x[2], x[3]);
+        *reinterpret_cast<uint2*>(slice + (lane & 31) * SRS + 2 * (col - wn * WN)) = make_uint2(w0, w1);
       }
-  } else {
-    // rows v and v+1 of a lane are converted together
+    asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: the slice is complete
+    constexpr int CPR = WN / 8;  // 16-byte chunks per slice row
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int v = 0; v < 16; v += 2) {
-        const int row = wm * WM + 32 * i + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const uint32_t w = f2bf2(acc[i][j][v], acc[i][j][v + 1]);
-          uint16_t* p = st + row * S::STG_LD + wn * WN + 32 * j + (lane & 31);
-          p[0] = (uint16_t)w;
-          p[S::STG_LD] = (uint16_t)(w >> 16);
-        }
-      }
-  }
-  __syncthreads();
-  constexpr int CH = TN / 8;  // 16-byte chunks per staged row
-#pragma unroll 4
-  for (int q = 0; q < (TM * CH) / S::THREADS; ++q) {
-    const int idx = tid + S::THREADS * q;
-    const int row = idx / CH, ch = idx % CH;
-    const int col = n0 + ch * 8;
-    if (row < nrows && col < g.Nout)
-      *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + row) * g.ldo + col) =
-          *reinterpret_cast<const u32x4*>(st + row * S::STG_LD + ch * 8);
+    for (int q = 0; q < 32 * CPR / 64; ++q) {
+      const int id = 64 * q + lane;
+      const int rr = id / CPR, ch = id % CPR;
+      const uint2 lo = *reinterpret_cast<const uint2*>(slice + rr * SRS + 16 * ch);
+      const uint2 hi = *reinterpret_cast<const uint2*>(slice + rr * SRS + 16 * ch + 8);
+      const int orow = wm * WM + 32 * i + rr, ocol = n0 + wn * WN + 8 * ch;
+      if (orow < nrows && ocol < g.Nout)
+        *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + orow) * g.ldo + ocol) = u32x4{lo.x, lo.y, hi.x, hi.y};
+    }
+    asm volatile("" ::: "memory");  // the slice is read before the next rows overwrite it
   }
 }
 
