@@ -424,15 +424,16 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
   }
 
   // ---- main loop ----------------------------------------------------------
+  // Fragment reads in the order the MFMAs consume them (weight column block
+  // j outer, row block i inner): bq[0], af[0..FM), then bq[1..FN), so the first
+  // MFMA of a 16-wide step waits for two reads, not for all of them.
   auto load_frags = [&](const char* sa, const char* sb, int s, bf16x8* af, bf16x8* bq) {
     const int ch = 2 * s + (lane >> 5);
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
+    auto read_a = [&](int i) {
       const int row = wm * WM + 32 * i + (lane & 31);
       af[i] = as_bf(*reinterpret_cast<const u32x4*>(sa + row * ROWB + 16 * (ch ^ swz<TK>(row))));
-    }
-#pragma unroll
-    for (int j = 0; j < FN; ++j) {
+    };
+    auto read_b = [&](int j) {
       if constexpr (!NN) {
         const int col = wn * WN + 32 * j + (lane & 31);
         bq[j] = as_bf(*reinterpret_cast<const u32x4*>(sb + col * ROWB + 16 * (ch ^ swz<TK>(col))));
@@ -453,7 +454,12 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
         v[3] = (uint32_t)(uint16_t)h[1][2] | ((uint32_t)(uint16_t)h[1][3] << 16);
         bq[j] = as_bf(v);
       }
-    }
+    };
+    read_b(0);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) read_a(i);
+#pragma unroll
+    for (int j = 1; j < FN; ++j) read_b(j);
   };
 
   // Pipeline: NS K-steps in flight.  In iteration kt the barrier that
@@ -480,9 +486,9 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
     for (int s = 0; s < kSteps - 1; ++s) {
       load_frags(sa, sb, s + 1, af[(s + 1) & 1], bq[(s + 1) & 1]);
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int j = 0; j < FN; ++j)
+        for (int i = 0; i < FM; ++i)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bq[s & 1][j], af[s & 1][i], acc[i][j], 0, 0, 0);
     }
 #pragma unroll
@@ -505,9 +511,9 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
       load_frags(na, na + S::A_BYTES, 0, af[L ^ 1], bq[L ^ 1]);
     }
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+    for (int j = 0; j < FN; ++j)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int i = 0; i < FM; ++i)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(bq[L][j], af[L][i], acc[i][j], 0, 0, 0);
     stage = next;
   }
