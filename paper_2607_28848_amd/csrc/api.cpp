@@ -1081,7 +1081,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     ta.keep = keep[i];  // dA contracts the masked input
     ta.keep_words = (q.K + 31) / 32;
   }
-  for (int k = 0; k < trg.n; ++k) trg.yoff[k + 1] = trg.yoff[k] + (trg.a[k].C + 127) / 128;
+  for (int k = 0; k < trg.n; ++k) trg.yoff[k + 1] = trg.yoff[k] + token_col_blocks(trg.a[k].C);
   if (launch_token_reduce_group(trg, p->n_chunks, s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 4. fixed-order sums into dB (scaled by s_a) and dA, every projection

@@ -96,6 +96,9 @@ struct TokenReduceArgs {
 // from the workgroup id.  The single-projection launchers below are groups
 // of one.
 constexpr int kMaxGroup = 8;
+// Columns per workgroup of the token reductions.
+constexpr int kTokenCols = 256;
+inline int32_t token_col_blocks(int32_t C) { return (C + kTokenCols - 1) / kTokenCols; }
 struct SkinnyGroup {
   SkinnyArgs a[kMaxGroup];
   int32_t n;
@@ -113,7 +116,7 @@ struct GatherGroup {
 };
 struct TokenReduceGroup {
   TokenReduceArgs a[2 * kMaxGroup];
-  int32_t yoff[2 * kMaxGroup + 1];  // prefix of the 128-column blocks
+  int32_t yoff[2 * kMaxGroup + 1];  // prefix of the kTokenCols-column blocks
   int32_t n;
 };
 struct TransposeArgs {

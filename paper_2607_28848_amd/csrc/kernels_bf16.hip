@@ -893,99 +893,161 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
 // ---------------------------------------------------------------------------
 // Reduction over training tokens, per single-adapter chunk:
 //   part[chunk][c][j] = sum_t P[prow(t)][c] Q[t][j]
-// One workgroup per (chunk, 128 columns); its 4 waves take consecutive
-// quarters of the chunk's tokens and their sums are added in LDS in wave
-// order.  A lane loads an 8 (tokens) x 8 (columns) block, transposes it in
-// registers and feeds the 8 columns as A-operands of 8
-// v_mfma_f32_16x16x32_bf16 tiles (tile m, row rho <-> column
-// c = base + 8 rho + m); the rank side Q[t][j] (h or g, row layout) is read
-// with 8 strided loads per fragment.
+// One workgroup per (chunk, kTokenCols = 256 columns), 8 waves; wave w owns
+// columns [32w, 32w+32).  Tokens go in steps of 32: the step's 32 P rows (512
+// contiguous bytes each, two rows per wave instruction) go from global memory
+// straight into LDS, double-buffered, and come out transposed
+// (ds_read_b64_tr_b16), so a lane holds one column c and 8 consecutive tokens:
+// the A operand of v_mfma_f32_16x16x32_bf16 with the columns as rows and the
+// tokens as the contraction.  The B operand (rank j, 8 tokens of Q, the small
+// rank-wide matrix) is read from global memory a step ahead.  A row of the
+// LDS image keeps its 16-byte slot s at s ^ 2(t % 4), so the 4 rows x 32
+// bytes of one transposed read hit distinct banks.  Tokens past the chunk and
+// columns past C are written as zeros instead of loaded.  Each column's sum
+// runs over the tokens in order, so it does not depend on the column blocking.
 // ---------------------------------------------------------------------------
-// Both reductions of a backward in one launch: blockIdx.y < y0 runs g0's
-// column blocks, the rest g1's.
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
 template <int NJ>
-__global__ __launch_bounds__(256) void token_reduce_kernel(TokenReduceGroup G) {
-  constexpr int TQ = kChunkRows / 4;  // tokens per wave
-  __shared__ f32x4 red[3][8 * NJ][64];
+__global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
+  constexpr int TS = 32;                     // tokens per step
+  constexpr int STAGE = TS * kTokenCols * 2;  // P bytes per stage
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
   int k = 0;  // the reduction: blockIdx.y runs over every reduction's column blocks
   while (k + 1 < G.n && (int)blockIdx.y >= G.yoff[k + 1]) ++k;
   const TokenReduceArgs g = G.a[k];
-  const int by = (int)blockIdx.y - G.yoff[k];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int cbase = ((int)blockIdx.y - G.yoff[k]) * kTokenCols;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
   const int a = ck[0], begin = ck[1], cnt = ck[2];
   const int r = g.ranks[a];
-  const int q = lane >> 4, rho = lane & 15;
-  const int cbase = by * 128;
-  const int c0 = cbase + 8 * rho;
-  const bool cin = c0 < g.C;
-  f32x4 acc[8][NJ];
+  const int nsteps = (cnt + TS - 1) / TS;
+  const int sub = lane >> 5, sl = lane & 31;  // staging: row within the instruction, slot
+  const int gq = lane >> 4, lam = lane & 15;  // fragments: token octet, column / rank
+  // P rows 2q + sub of the step, q = 2 wave + i; slot sl holds the row's
+  // 16-byte chunk sl ^ 2(row % 4).  The P row numbers of a step are looked up
+  // a step before its loads are issued.
+  auto rows_of = [&](int step, int (&pr)[2]) {
 #pragma unroll
-  for (int m = 0; m < 8; ++m)
-#pragma unroll
-    for (int jt = 0; jt < NJ; ++jt) acc[m][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int tlo = wave * TQ, thi = min(cnt, tlo + TQ);
-  constexpr int U = 2;
-  for (int t0 = tlo; t0 < thi; t0 += 32 * U) {
-    u32x4 v[U][8], bv[U][NJ];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int tb = t0 + 32 * u + 8 * q;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const int t = tb + e;
-        v[u][e] = zero4();
-        if (t < thi && cin) {
-          const int pr = g.prow ? g.prow[begin + t] : begin + t;
-          v[u][e] = ld16(g.P + (int64_t)pr * g.ldp + c0);
-          if (g.keep) v[u][e] = keep8(v[u][e], keep_byte(g.keep, g.keep_words, begin + t, c0));
-        }
-      }
-      const int nt = min(8, thi - tb);
-#pragma unroll
-      for (int jt = 0; jt < NJ; ++jt) {
-        const int j = 16 * jt + rho;
-        bv[u][jt] = (j < r && nt > 0) ? ld8_masked(g.Q + (int64_t)(begin + tb) * g.ldq + j, g.ldq, nt)
-                                      : zero4();
-      }
+    for (int i = 0; i < 2; ++i) {
+      const int t = min(step * TS + 2 * (2 * wave + i) + sub, cnt - 1);
+      pr[i] = g.prow ? g.prow[begin + t] : begin + t;
     }
+  };
+  auto issue = [&](int step, int st, const int (&pr)[2]) {
+    char* base = smem + st * STAGE;
+    const int t0 = step * TS;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      u32x4 V[8];
-      transpose8x8(v[u], V);
+    for (int i = 0; i < 2; ++i) {
+      const int q = 2 * wave + i;
+      const int row = 2 * q + sub;
+      const int c = cbase + 8 * (sl ^ (2 * (row & 3)));
+      char* dst = base + q * 1024;
+      if (t0 + row < cnt && c < g.C)
+        llvm_amdgcn_global_load_lds((global_cv*)(g.P + (int64_t)pr[i] * g.ldp + c), (lds_u32*)dst, 16, 0, 0);
+      else
+        *reinterpret_cast<u32x4*>(dst + 16 * lane) = zero4();
+    }
+  };
+  // B fragments of a step: Q[begin + 8 gq + e][16 jt + lam], zero past the rank
+  // and past the chunk (straight-line loads from clamped addresses)
+  auto load_q = [&](int step, u32x4 (&bq)[NJ]) {
+    const int t = step * TS + 8 * gq;
+    const int nt = max(1, min(8, cnt - t));
+    const uint16_t* row = g.Q + (int64_t)(begin + min(t, cnt - 1)) * g.ldq;
+#pragma unroll
+    for (int jt = 0; jt < NJ; ++jt) {
+      const int j = 16 * jt + lam;
+      const u32x4 v = ld8_sel(row + min(j, r - 1), g.ldq, nt);
+      bq[jt] = (j < r && t < cnt) ? v : zero4();
+    }
+  };
+  // dropout: each token's mask word for the wave's 32 columns, a step ahead
+  const bool masked = g.keep != nullptr;
+  const int kw = masked ? min((cbase + 32 * wave) >> 5, g.keep_words - 1) : 0;
+  auto load_mask = [&](int step, uint32_t (&m)[8]) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const int t = min(step * TS + 8 * gq + e, cnt - 1);
+      m[e] = g.keep[(int64_t)(begin + t) * g.keep_words + kw];
+    }
+  };
+  auto tr_read = [&](const char* p) -> u32x2 {
+    const s16x4 h = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+    return u32x2{(uint32_t)(uint16_t)h[0] | ((uint32_t)(uint16_t)h[1] << 16),
+                 (uint32_t)(uint16_t)h[2] | ((uint32_t)(uint16_t)h[3] << 16)};
+  };
+  f32x4 acc[2][NJ];
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+    for (int jt = 0; jt < NJ; ++jt) acc[ct][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // One step; the B fragments and mask words of the next step load into the
+  // other register set (the loop is unrolled by two), so the wait at the top
+  // of a step covers them and nothing waits on a load issued after them.
+  auto step_fn = [&](int step, const u32x4 (&qu)[NJ], u32x4 (&ql)[NJ], const uint32_t (&mu)[8],
+                     uint32_t (&ml)[8], const int (&pu)[2], int (&pl)[2]) {
+    vmem_wait_all();
+    __syncthreads();  // the step is in; every wave is done with the previous step's buffer
+    // the step's fragments are read before the next step's loads into LDS are
+    // issued, so no read has to wait for those loads
+    const char* sb = smem + (step & 1) * STAGE;
+    u32x4 x[2];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+      u32x2 h[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int t = 8 * gq + 4 * hh + (lam >> 2);
+        const int col = 32 * wave + 16 * ct + 4 * (lam & 3);  // within the block
+        h[hh] = tr_read(sb + t * (kTokenCols * 2) + 16 * ((col >> 3) ^ (2 * (t & 3))) + 2 * (col & 7));
+      }
+      x[ct] = u32x4{h[0][0], h[0][1], h[1][0], h[1][1]};
+    }
+    if (step + 1 < nsteps) issue(step + 1, (step + 1) & 1, pu);
+    rows_of(min(step + 2, nsteps - 1), pl);
+    load_q(min(step + 1, nsteps - 1), ql);
+    if (masked) load_mask(min(step + 1, nsteps - 1), ml);
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+      if (masked) {
+        // element e is token 8 gq + e of column 32 wave + 16 ct + lam
+        const int bit = 16 * ct + lam;
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+          x[ct][d] &= (((mu[2 * d] >> bit) & 1u) ? 0x0000ffffu : 0u) | (((mu[2 * d + 1] >> bit) & 1u) ? 0xffff0000u : 0u);
+      }
 #pragma unroll
       for (int jt = 0; jt < NJ; ++jt)
-#pragma unroll
-        for (int m = 0; m < 8; ++m)
-          acc[m][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(V[m]), as_bf(bv[u][jt]), acc[m][jt], 0, 0, 0);
+        acc[ct][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(x[ct]), as_bf(qu[jt]), acc[ct][jt], 0, 0, 0);
     }
+  };
+  u32x4 q0[NJ], q1[NJ];
+  uint32_t m0[8] = {}, m1[8] = {};
+  int p0[2], p1[2];
+  if (nsteps > 0) {
+    rows_of(0, p0);
+    issue(0, 0, p0);
+    rows_of(min(1, nsteps - 1), p0);
+    load_q(0, q0);
+    if (masked) load_mask(0, m0);
   }
-  // waves 1..3 hand their sums to wave 0, which adds them in wave order
-  if (wave > 0) {
-#pragma unroll
-    for (int m = 0; m < 8; ++m)
-#pragma unroll
-      for (int jt = 0; jt < NJ; ++jt) red[wave - 1][m * NJ + jt][lane] = acc[m][jt];
+  // p0 holds the rows of the next step to issue, p1 receives the one after
+  for (int step = 0; step < nsteps; step += 2) {
+    step_fn(step, q0, q1, m0, m1, p0, p1);
+    if (step + 1 < nsteps) step_fn(step + 1, q1, q0, m1, m0, p1, p0);
   }
-  __syncthreads();
-  if (wave != 0) return;
-#pragma unroll
-  for (int w = 0; w < 3; ++w)
-#pragma unroll
-    for (int m = 0; m < 8; ++m)
-#pragma unroll
-      for (int jt = 0; jt < NJ; ++jt) acc[m][jt] += red[w][m * NJ + jt][lane];
+  // acc[ct][jt][v]: column 32 wave + 16 ct + 4 gq + v of the block, rank 16 jt + lam
   float* out = g.part + (int64_t)blockIdx.x * g.C * g.r_max;
 #pragma unroll
-  for (int m = 0; m < 8; ++m)
+  for (int ct = 0; ct < 2; ++ct)
 #pragma unroll
     for (int jt = 0; jt < NJ; ++jt)
 #pragma unroll
-      for (int vv = 0; vv < 4; ++vv) {
-        const int rr = 4 * q + vv;
-        const int c = cbase + 8 * rr + m;
-        const int j = 16 * jt + rho;
-        if (j < r && c < g.C) out[(int64_t)c * g.r_max + j] = acc[m][jt][vv];
+      for (int v = 0; v < 4; ++v) {
+        const int c = cbase + 32 * wave + 16 * ct + 4 * gq + v;
+        const int j = 16 * jt + lam;
+        if (j < r && c < g.C) out[(int64_t)c * g.r_max + j] = acc[ct][jt][v];
       }
 }
 
@@ -1188,15 +1250,15 @@ hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks
   if (n_chunks <= 0 || g.n <= 0) return hipSuccess;
   if (g.n > 2 * kMaxGroup || g.yoff[0] != 0) return hipErrorInvalidValue;
   for (int k = 0; k < g.n; ++k)
-    if (g.a[k].r_max != g.a[0].r_max || g.yoff[k + 1] - g.yoff[k] != (g.a[k].C + 127) / 128)
+    if (g.a[k].r_max != g.a[0].r_max || g.yoff[k + 1] - g.yoff[k] != token_col_blocks(g.a[k].C))
       return hipErrorInvalidValue;
   const dim3 grid(n_chunks, g.yoff[g.n]);
   if (g.a[0].r_max <= 16)
-    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(256), 0, s, g);
+    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(512), 0, s, g);
   else if (g.a[0].r_max <= 32)
-    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(256), 0, s, g);
+    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(512), 0, s, g);
   else
-    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(256), 0, s, g);
+    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(512), 0, s, g);
   return hipGetLastError();
 }
 
@@ -1205,8 +1267,8 @@ hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs&
   TokenReduceGroup g{};
   g.a[0] = a0;
   g.a[1] = a1;
-  g.yoff[1] = (a0.C + 127) / 128;
-  g.yoff[2] = g.yoff[1] + (a1.C + 127) / 128;
+  g.yoff[1] = token_col_blocks(a0.C);
+  g.yoff[2] = g.yoff[1] + token_col_blocks(a1.C);
   g.n = 2;
   return launch_token_reduce_group(g, n_chunks, s);
 }
