@@ -908,7 +908,7 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
 // ---------------------------------------------------------------------------
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-template <int NJ>
+template <int NJ, bool DROP>
 __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
   constexpr int TS = 32;                     // tokens per step
   constexpr int STAGE = TS * kTokenCols * 2;  // P bytes per stage
@@ -963,7 +963,7 @@ __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
     }
   };
   // dropout: each token's mask word for the wave's 32 columns, a step ahead
-  const bool masked = g.keep != nullptr;
+  const bool masked = DROP && g.keep != nullptr;  // DROP: the launch has masked reductions
   const int kw = masked ? min((cbase + 32 * wave) >> 5, g.keep_words - 1) : 0;
   auto load_mask = [&](int step, uint32_t (&m)[8]) {
 #pragma unroll
@@ -1246,19 +1246,30 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
   return launch_gather_group(g, ldh, r_max, items, n_items, gather_rows, ranks, scales, s);
 }
 
+template <bool DROP>
+void launch_token_reduce_nj(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s) {
+  const dim3 grid(n_chunks, g.yoff[g.n]);
+  if (g.a[0].r_max <= 16)
+    hipLaunchKernelGGL((token_reduce_kernel<1, DROP>), grid, dim3(512), 0, s, g);
+  else if (g.a[0].r_max <= 32)
+    hipLaunchKernelGGL((token_reduce_kernel<2, DROP>), grid, dim3(512), 0, s, g);
+  else
+    hipLaunchKernelGGL((token_reduce_kernel<4, DROP>), grid, dim3(512), 0, s, g);
+}
+
+// A launch whose reductions include a masked one runs the kernel with the
+// masking code; it masks the reductions that carry a mask.
 hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s) {
   if (n_chunks <= 0 || g.n <= 0) return hipSuccess;
   if (g.n > 2 * kMaxGroup || g.yoff[0] != 0) return hipErrorInvalidValue;
-  for (int k = 0; k < g.n; ++k)
+  bool any_keep = false;
+  for (int k = 0; k < g.n; ++k) {
     if (g.a[k].r_max != g.a[0].r_max || g.yoff[k + 1] - g.yoff[k] != token_col_blocks(g.a[k].C))
       return hipErrorInvalidValue;
-  const dim3 grid(n_chunks, g.yoff[g.n]);
-  if (g.a[0].r_max <= 16)
-    hipLaunchKernelGGL((token_reduce_kernel<1>), grid, dim3(512), 0, s, g);
-  else if (g.a[0].r_max <= 32)
-    hipLaunchKernelGGL((token_reduce_kernel<2>), grid, dim3(512), 0, s, g);
-  else
-    hipLaunchKernelGGL((token_reduce_kernel<4>), grid, dim3(512), 0, s, g);
+    any_keep |= g.a[k].keep != nullptr;
+  }
+  if (any_keep) launch_token_reduce_nj<true>(g, n_chunks, s);
+  else launch_token_reduce_nj<false>(g, n_chunks, s);
   return hipGetLastError();
 }
 
