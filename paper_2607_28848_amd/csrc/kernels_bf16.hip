@@ -1067,14 +1067,9 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32
   const int a = train_ads[ta], r = ranks[a];
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (idx >= (int64_t)C * r_max) return;
-  int c, j;
-  if (g.a_layout) {  // out[a][j][c], c fastest
-    j = (int)(idx / C);
-    c = (int)(idx % C);
-  } else {  // out[a][c][j], j fastest
-    c = (int)(idx / r_max);
-    j = (int)(idx % r_max);
-  }
+  // j fastest, the partials' layout: the reads are coalesced in both output
+  // layouts (the partials outweigh the output by the number of chunks)
+  const int c = (int)(idx / r_max), j = (int)(idx % r_max);
   if (c >= C || j >= r) return;
   float sum = 0.f;
   for (int p = tad_ptr[ta]; p < tad_ptr[ta + 1]; ++p)
