@@ -168,7 +168,10 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=48, help="forward rows per projection in the CPU sample")
     ap.add_argument("--cpu-dx-rows", type=int, default=24)
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the timing of the steps that follow the layer (the AdamW update)")
+                    help="skip the timings after the main loop (AdamW, recomputed h, dropout, co-batching "
+                         "overhead, launch modes)")
+    ap.add_argument("--extras", default="all", choices=("all", "overhead"),
+                    help="overhead: of the timings after the main loop, only the co-batching overhead")
     ap.add_argument("--launch", default="set", choices=("single", "layer", "set"),
                     help="single: one call per projection; layer: grouped calls over the projections a "
                          "transformer layer can run together (q/k/v, o, gate/up, down); set: one grouped call "
@@ -377,124 +380,159 @@ def main():
     # master, m and v read (16), master, m and v written (12), bf16 copy written (2).
     extras = None
     if not args.no_extras and bf:
-        hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
-        opt = []
-        for p, proj in enumerate(w.projections):
-            d = P[p]
-            st = [d["A"].float(), d["B"].float()]
-            opt.append(st + [torch.zeros_like(st[0]), torch.zeros_like(st[0]),
-                             torch.zeros_like(st[1]), torch.zeros_like(st[1])])
-        torch.cuda.synchronize()
-
-        def opt_step(t):
-            for p, proj in enumerate(w.projections):
-                d, o = P[p], opt[p]
-                dsv.adamw_step(probe_dev, t, d["dA"], d["dB"], o[0], o[1], o[2], o[3], o[4], o[5],
-                               A=d["A"], B=d["B"], stream=stream, **hp)
-        probe_dev = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device=dev)
-        for t in range(1, 6):
-            opt_step(t)
-        torch.cuda.synchronize()
-        n_opt = 50
+        extras = {}
+        full = args.extras == "all"
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for t in range(6, 6 + n_opt):
-            opt_step(t)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        us = e0.elapsed_time(e1) * 1e3 / n_opt
-        tr = [a for a in range(w.n_adapters) if any(s[2] == a and s[3] and s[1] for s in w.segments)]
-        elems = sum(int(w.ranks[a]) * (proj.K + proj.N) for a in tr for proj in w.projections)
-        nbytes = 30 * elems
-        extras = {"adamw": {"kernel": "adamw_kernel (fused AdamW of the training adapters' A and B)",
-                            "launches_per_step": len(w.projections), "us_per_step": round(us, 2),
-                            "bytes_per_step": nbytes, "achieved_GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
-                            "peak_GBps": 8000.0, "frac": round(nbytes / (us * 1e-6) / 8e12, 4),
-                            "bound": "hbm (at these sizes: launch latency)"}}
-        log("adamw: %.2f us per step (%d launches), %.1f GB/s" % (us, len(w.projections),
-                                                                  nbytes / (us * 1e-6) / 1e9))
-
-        # Residual-only retention: the backward of every projection with h recomputed
-        # from X (H_save not kept) against the backward that reads the kept H_save.
-        def bwd_all(keep):
-            for p, proj in enumerate(w.projections):
-                d = P[p]
-                dsv.lora_bwd(probe_dev, d["X"], d["W"], d["A"], d["B"], d["H"] if keep else None, d["dY"],
-                             dA=d["dA"], dB=d["dB"], dX=d["dX"], workspace=d["wsb"], stream=stream)
-        bt = {}
-        for keep in (True, False, True, False):
-            bwd_all(keep)
-            torch.cuda.synchronize()
-            e0.record(stream)
-            for _ in range(10):
-                bwd_all(keep)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            bt[keep] = e0.elapsed_time(e1) * 1e3 / 10
-        extras["recompute_h"] = {"bwd_us_per_step_kept_h": round(bt[True], 2),
-                                 "bwd_us_per_step_recomputed_h": round(bt[False], 2),
-                                 "h_bytes_not_kept_per_step": int(sum(w.train_tokens * w.r_max * 2
-                                                                      for _ in w.projections))}
-        log("backward with kept h %.1f us, with recomputed h %.1f us per step" % (bt[True], bt[False]))
-
-        # LoRA dropout 0.05 on the training rows (the fine-tuning setting of Sec. 4.1):
-        # the whole step (forward + backward of every projection, in the bench's launch
-        # mode) with and without it.
+        probe_dev = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device=dev)
         gl = groups if groups is not None else [(p, p + 1) for p in range(len(w.projections))]
         shapes = [(proj.K, proj.N) for proj in w.projections]
-        wsf_d = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
-                             dtype=torch.uint8, device=dev) for lo, hi in gl]
-        wsb_d = [torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
-                             dtype=torch.uint8, device=dev) for lo, hi in gl]
-
-        def step_all(drop):
-            for gi, (lo, hi) in enumerate(gl):
-                ds = [P[p] for p in range(lo, hi)]
-                drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
-                dsv.cobatch_fwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["Y"], d["H"]) for d in ds],
-                                        workspace=wsf_d[gi], stream=stream, dropouts=drops)
-            for gi, (lo, hi) in enumerate(gl):
-                ds = [P[p] for p in range(lo, hi)]
-                drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
-                dsv.lora_bwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], d["dA"], d["dB"],
-                                                  d["dX"]) for d in ds],
-                                     workspace=wsb_d[gi], stream=stream, dropouts=drops,
-                                     wts=None if args.no_wt else [d["Wt"] for d in ds])
-        dt_ = {}
-        for key in ("off", "p0.05", "off", "p0.05"):
-            drop = None if key == "off" else 0.05
-            step_all(drop)
+        if full:
+            hp = dict(lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, weight_decay=0.01)
+            opt = []
+            for p, proj in enumerate(w.projections):
+                d = P[p]
+                st = [d["A"].float(), d["B"].float()]
+                opt.append(st + [torch.zeros_like(st[0]), torch.zeros_like(st[0]),
+                                 torch.zeros_like(st[1]), torch.zeros_like(st[1])])
             torch.cuda.synchronize()
+
+            def opt_step(t):
+                for p, proj in enumerate(w.projections):
+                    d, o = P[p], opt[p]
+                    dsv.adamw_step(probe_dev, t, d["dA"], d["dB"], o[0], o[1], o[2], o[3], o[4], o[5],
+                                   A=d["A"], B=d["B"], stream=stream, **hp)
+            for t in range(1, 6):
+                opt_step(t)
+            torch.cuda.synchronize()
+            n_opt = 50
             e0.record(stream)
-            for _ in range(10):
+            for t in range(6, 6 + n_opt):
+                opt_step(t)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / n_opt
+            tr = [a for a in range(w.n_adapters) if any(s[2] == a and s[3] and s[1] for s in w.segments)]
+            elems = sum(int(w.ranks[a]) * (proj.K + proj.N) for a in tr for proj in w.projections)
+            nbytes = 30 * elems
+            extras["adamw"] = {"kernel": "adamw_kernel (fused AdamW of the training adapters' A and B)",
+                               "launches_per_step": len(w.projections), "us_per_step": round(us, 2),
+                               "bytes_per_step": nbytes, "achieved_GBps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                               "peak_GBps": 8000.0, "frac": round(nbytes / (us * 1e-6) / 8e12, 4),
+                               "bound": "hbm (at these sizes: launch latency)"}
+            log("adamw: %.2f us per step (%d launches), %.1f GB/s" % (us, len(w.projections),
+                                                                      nbytes / (us * 1e-6) / 1e9))
+
+            # Residual-only retention: the backward of every projection with h recomputed
+            # from X (H_save not kept) against the backward that reads the kept H_save.
+            def bwd_all(keep):
+                for p, proj in enumerate(w.projections):
+                    d = P[p]
+                    dsv.lora_bwd(probe_dev, d["X"], d["W"], d["A"], d["B"], d["H"] if keep else None, d["dY"],
+                                 dA=d["dA"], dB=d["dB"], dX=d["dX"], workspace=d["wsb"], stream=stream)
+            bt = {}
+            for keep in (True, False, True, False):
+                bwd_all(keep)
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for _ in range(10):
+                    bwd_all(keep)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                bt[keep] = e0.elapsed_time(e1) * 1e3 / 10
+            extras["recompute_h"] = {"bwd_us_per_step_kept_h": round(bt[True], 2),
+                                     "bwd_us_per_step_recomputed_h": round(bt[False], 2),
+                                     "h_bytes_not_kept_per_step": int(sum(w.train_tokens * w.r_max * 2
+                                                                          for _ in w.projections))}
+            log("backward with kept h %.1f us, with recomputed h %.1f us per step" % (bt[True], bt[False]))
+
+            # LoRA dropout 0.05 on the training rows (the fine-tuning setting of Sec. 4.1):
+            # the whole step (forward + backward of every projection, in the bench's launch
+            # mode) with and without it.
+            wsf_d = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                                 dtype=torch.uint8, device=dev) for lo, hi in gl]
+            wsb_d = [torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                                 dtype=torch.uint8, device=dev) for lo, hi in gl]
+
+            def step_all(drop):
+                for gi, (lo, hi) in enumerate(gl):
+                    ds = [P[p] for p in range(lo, hi)]
+                    drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
+                    dsv.cobatch_fwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["Y"], d["H"]) for d in ds],
+                                            workspace=wsf_d[gi], stream=stream, dropouts=drops)
+                for gi, (lo, hi) in enumerate(gl):
+                    ds = [P[p] for p in range(lo, hi)]
+                    drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
+                    dsv.lora_bwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], d["dA"], d["dB"],
+                                                      d["dX"]) for d in ds],
+                                         workspace=wsb_d[gi], stream=stream, dropouts=drops,
+                                         wts=None if args.no_wt else [d["Wt"] for d in ds])
+            dt_ = {}
+            for key in ("off", "p0.05", "off", "p0.05"):
+                drop = None if key == "off" else 0.05
                 step_all(drop)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            dt_[key] = e0.elapsed_time(e1) * 1e3 / 10
-        extras["dropout"] = {"p": 0.05, "step_us_without": round(dt_["off"], 2),
-                             "step_us_with": round(dt_["p0.05"], 2),
-                             "overhead_frac": round(dt_["p0.05"] / dt_["off"] - 1.0, 4)}
-        log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
-        del wsf_d, wsb_d
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for _ in range(10):
+                    step_all(drop)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                dt_[key] = e0.elapsed_time(e1) * 1e3 / 10
+            extras["dropout"] = {"p": 0.05, "step_us_without": round(dt_["off"], 2),
+                                 "step_us_with": round(dt_["p0.05"], 2),
+                                 "overhead_frac": round(dt_["p0.05"] / dt_["off"] - 1.0, 4)}
+            log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
+            del wsf_d, wsb_d
 
-        # The same step in the other launch modes (10 timed steps each); "<mode>_no_wt":
-        # the grouped backward without the transposed weights.
-        modes = {args.launch + ("_no_wt" if args.no_wt else ""): round(ms_per_step, 4)}
-        for m in ("single", "layer", "set", "layer_no_wt", "set_no_wt"):
-            if m in modes or (m == args.launch and not args.no_wt):
-                continue
-            st, _ = make_step(m.replace("_no_wt", ""), use_wt=not m.endswith("_no_wt"))
-            for i in range(3):
-                st(i)
-            torch.cuda.synchronize()
-            e0.record(stream)
-            for i in range(10):
-                st(i)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            modes[m] = round(e0.elapsed_time(e1) / 10, 4)
-        extras["launch_modes_ms_per_step"] = modes
-        log("ms per step by launch mode: %s" % modes)
+        # Co-batching overhead: the forward of the batch as it is against the forward of
+        # the same segment table with every is_train flag cleared (no H_save rows, no
+        # training-row bookkeeping), both in the bench's launch mode.
+        if w.train_tokens > 0:
+            inf_segs = [(s, l, a, 0) for (s, l, a, _) in w.segments]
+            plan_inf = dsv.segments_build(inf_segs, w.n_tokens, w.ranks, w.scales, w.r_max, device=dev)
+            wsf_o = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
+                                 dtype=torch.uint8, device=dev) for lo, hi in gl]
+
+            def fwd_all(plan_, keep):
+                for gi, (lo, hi) in enumerate(gl):
+                    ds = [P[p] for p in range(lo, hi)]
+                    dsv.cobatch_fwd_grouped(plan_, [(d["X"], d["W"], d["A"], d["B"], d["Y"], d["H"] if keep else None)
+                                                    for d in ds], workspace=wsf_o[gi], stream=stream, keep_h=keep)
+            ft = {}
+            for key in ("mixed", "inference", "mixed", "inference"):
+                pl, keep = (probe_dev, True) if key == "mixed" else (plan_inf, False)
+                fwd_all(pl, keep)
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for _ in range(20):
+                    fwd_all(pl, keep)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                ft[key] = e0.elapsed_time(e1) * 1e3 / 20
+            extras["cobatch_overhead"] = {
+                "fwd_us_mixed": round(ft["mixed"], 2), "fwd_us_is_train_cleared": round(ft["inference"], 2),
+                "overhead_frac": round(ft["mixed"] / ft["inference"] - 1.0, 4)}
+            log("forward: mixed batch %.1f us, is_train cleared %.1f us" % (ft["mixed"], ft["inference"]))
+            del wsf_o, plan_inf
+
+        if full:
+            # The same step in the other launch modes (10 timed steps each); "<mode>_no_wt":
+            # the grouped backward without the transposed weights.
+            modes = {args.launch + ("_no_wt" if args.no_wt else ""): round(ms_per_step, 4)}
+            for m in ("single", "layer", "set", "layer_no_wt", "set_no_wt"):
+                if m in modes or (m == args.launch and not args.no_wt):
+                    continue
+                st, _ = make_step(m.replace("_no_wt", ""), use_wt=not m.endswith("_no_wt"))
+                for i in range(3):
+                    st(i)
+                torch.cuda.synchronize()
+                e0.record(stream)
+                for i in range(10):
+                    st(i)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                modes[m] = round(e0.elapsed_time(e1) / 10, 4)
+            extras["launch_modes_ms_per_step"] = modes
+            log("ms per step by launch mode: %s" % modes)
 
     def cfg_str(c):
         if not c["tile_m"]:
