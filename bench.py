@@ -18,6 +18,7 @@ Prints one JSON line on stdout; progress goes to stderr.
 from __future__ import annotations
 
 import argparse
+import gc
 import json
 import os
 import sys
@@ -102,10 +103,12 @@ def launch_groups(w, launch, dropout):
     """[(lo, hi)] ranges of w.projections run by one grouped call each, or None for
     one call per projection.  `layer` groups the projections whose inputs exist at
     the same point of a transformer layer: those sharing the layer input (q, k, v),
-    the attention output (o), the MLP input (gate, up) and the MLP product (down)."""
-    if launch == "single" or len(w.projections) == 1:
+    the attention output (o), the MLP input (gate, up) and the MLP product (down).
+    A workload of one projection is a group of one outside `single` mode, so its dX
+    GEMM reads the transposed weight as in the grouped modes."""
+    if launch == "single":
         return None
-    if launch == "set":
+    if launch == "set" or len(w.projections) == 1:
         return [(0, len(w.projections))]
     names = [p.name for p in w.projections]
     order = [["q", "k", "v"], ["o"], ["gate", "up"], ["down"]]
@@ -339,6 +342,10 @@ def main():
 
     step, groups = make_step(args.launch)
 
+    # No garbage-collector pass inside the timed loops: a full pass over the heap
+    # (tens of ms) stalls the host, which stays only one step ahead of the GPU.
+    gc.collect()
+    gc.disable()
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
@@ -546,7 +553,7 @@ def main():
                      for proj in w.projections}
     roof_kernel = ("gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the low-rank "
                    "prologue; the fixup sums contraction-split tiles)")
-    if groups is not None:
+    if groups is not None and any(hi - lo > 1 for lo, hi in groups):
         pc = probe.counts()
         for lo, hi in groups:
             if hi - lo < 2:

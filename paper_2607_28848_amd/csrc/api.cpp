@@ -87,10 +87,10 @@ GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C) {
 }
 
 struct FwdWs {
-  size_t h_all, delta, keep, sk_part, total;
+  size_t h_all, delta, keep, sk_part, rk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, hrec, part_b, part_a, keep, sk_part, total;
+  size_t bt, g, hrec, part_b, part_a, keep, sk_part, g_part, h_part, total;
 };
 
 // Dropout bitmask of the training rows: ceil(K / 32) words per row.
@@ -112,6 +112,8 @@ FwdWs fwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     w.delta = off;
     off = align256(off + (size_t)p.n_gather * N * 4);
     off = carve_sk(gp, off, &w.sk_part);
+    w.rk_part = off;  // pieces of a split shrink
+    off = align256(off + skinny_part_bytes(K, p.n_shrink, p.T, p.r_max));
   } else {
     w.h_all = off;
     off = align256(off + (size_t)p.T * p.r_max * 4);
@@ -138,6 +140,10 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     w.part_a = off;
     off = align256(off + (size_t)p.n_chunks * K * p.r_max * 4);
     off = carve_sk(gp, off, &w.sk_part);
+    w.g_part = off;  // pieces of a split g contraction
+    off = align256(off + skinny_part_bytes(N, p.n_titems, p.T_t, p.r_max));
+    w.h_part = off;  // pieces of a split recomputed h
+    off = align256(off + skinny_part_bytes(K, p.n_shrink, p.T_t, p.r_max));
   } else {
     w.g = off;
     off = align256(off + (size_t)p.T_t * p.r_max * 4);
@@ -422,7 +428,11 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   sk.keep = keep;
   sk.keep_words = keep_words;
   sk.drop_scale = ds.scale;
-  if ((e = launch_shrink(sk, p->n_shrink, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  sk.part = at<float>(workspace, ws.rk_part);
+  sk.part_n = p->T;
+  sk.r_max = p->r_max;
+  sk.split_items = p->n_shrink;
+  if ((e = launch_shrink(sk, p->n_shrink, p->r_used, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2. gathered rows: fp32 low-rank term, each touched adapter read once.
   if (p->n_gather > 0) {
@@ -560,7 +570,11 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   sk.out1 = gm;
   sk.ld1 = ldh;
   sk.out2 = nullptr;
-  if ((e = launch_gmat(sk, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  sk.part = at<float>(workspace, ws.g_part);
+  sk.part_n = p->T_t;
+  sk.r_max = p->r_max;
+  sk.split_items = p->n_titems;
+  if ((e = launch_gmat(sk, p->n_titems, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2b. H_save not kept (residual-only retention): recompute h of the training
   //     rows from X with the forward's shrink (same values, bit for bit).
@@ -587,7 +601,11 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     sh.keep = keep;
     sh.keep_words = keep_words;
     sh.drop_scale = ds.scale;
-    if ((e = launch_shrink_train(sh, p->n_titems, p->r_max, s)) != hipSuccess) return DSV_ERR_DEVICE;
+    sh.part = at<float>(workspace, ws.h_part);
+    sh.part_n = p->T_t;
+    sh.r_max = p->r_max;
+    sh.split_items = p->n_shrink;  // the forward shrink's split: the same sums
+    if ((e = launch_shrink_train(sh, p->n_titems, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
     hs = hrec;
     ldhs = ldh;
   }
@@ -614,14 +632,14 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   ta.part = part_a;
   ta.keep = keep;  // dA contracts the masked input
   ta.keep_words = keep_words;
-  if ((e = launch_token_reduce(tb, ta, p->n_chunks, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  if ((e = launch_token_reduce(tb, ta, p->n_chunks, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 4. fixed-order sums into dB (scaled by s_a) and dA.
   const int32_t* tad_ptr = p->dptr(L.tad_chunk_ptr);
   const int32_t* tad_chunks = p->dptr(L.tad_chunks);
   const ReduceOutArgs ob{part_b, N, scales, 0, dB, 1.f};
   const ReduceOutArgs oa{part_a, K, nullptr, 1, dA, dropping ? ds.scale : 1.f};
-  if ((e = launch_reduce_out(ob, oa, p->r_max, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks, accumulate, s)) !=
+  if ((e = launch_reduce_out(ob, oa, p->r_max, p->r_train, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks, accumulate, s)) !=
       hipSuccess)
     return DSV_ERR_DEVICE;
 
@@ -873,13 +891,17 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     sk.out2 = p->T_t > 0 ? static_cast<uint16_t*>(q.H_save) : nullptr;
     sk.ld2 = p->r_max;
     sk.row_train = p->dptr(L.row_train);
+    sk.part = at<float>(wsb + base[i], w[i].rk_part);
+    sk.part_n = p->T;
+    sk.r_max = p->r_max;
+    sk.split_items = p->n_shrink;
     if (dropping) {
       sk.keep = at<uint32_t>(wsb + base[i], w[i].keep);
       sk.keep_words = (q.K + 31) / 32;
       sk.drop_scale = ds[i].scale;
     }
   }
-  if (launch_shrink_group(sg, p->n_shrink, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
+  if (launch_shrink_group(sg, p->n_shrink, p->r_used, s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2. gathered rows of every projection in one launch
   if (p->n_gather > 0) {
@@ -1020,8 +1042,12 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     sk.C = q.N;
     sk.out1 = gm[i];
     sk.ld1 = ldh;
+    sk.part = at<float>(wsb + base[i], w[i].g_part);
+    sk.part_n = p->T_t;
+    sk.r_max = p->r_max;
+    sk.split_items = p->n_titems;
   }
-  if (launch_gmat_group(gg, p->n_titems, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
+  if (launch_gmat_group(gg, p->n_titems, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 2b. h of the training rows for projections whose forward kept no H_save
   const uint16_t* hs[DSV_MAX_GROUP];
@@ -1049,10 +1075,14 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     sh.keep = keep[i];
     sh.keep_words = (q.K + 31) / 32;
     sh.drop_scale = ds[i].scale;
+    sh.part = at<float>(wsb + base[i], w[i].h_part);
+    sh.part_n = p->T_t;
+    sh.r_max = p->r_max;
+    sh.split_items = p->n_shrink;  // the forward shrink's split: the same sums
     hs[i] = hrec;
     ldhs[i] = ldh;
   }
-  if (rg.n > 0 && launch_shrink_train_group(rg, p->n_titems, p->r_max, s) != hipSuccess) return DSV_ERR_DEVICE;
+  if (rg.n > 0 && launch_shrink_train_group(rg, p->n_titems, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 3. chunk partials of dy^T h (dB) and x^T g (dA), every projection
   TokenReduceGroup trg{};
@@ -1082,7 +1112,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     ta.keep_words = (q.K + 31) / 32;
   }
   for (int k = 0; k < trg.n; ++k) trg.yoff[k + 1] = trg.yoff[k] + token_col_blocks(trg.a[k].C);
-  if (launch_token_reduce_group(trg, p->n_chunks, s) != hipSuccess) return DSV_ERR_DEVICE;
+  if (launch_token_reduce_group(trg, p->n_chunks, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 4. fixed-order sums into dB (scaled by s_a) and dA, every projection
   ReduceOutGroup og{};
@@ -1092,7 +1122,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     og.a[2 * i + 1] = ReduceOutArgs{trg.a[2 * i + 1].part, projs[i].K, nullptr, 1, projs[i].dA,
                                     dropping ? ds[i].scale : 1.f};
   }
-  if (launch_reduce_out_group(og, p->r_max, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr), p->dptr(L.tad_chunks),
+  if (launch_reduce_out_group(og, p->r_max, p->r_train, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr), p->dptr(L.tad_chunks),
                               ranks, accumulate, s) != hipSuccess)
     return DSV_ERR_DEVICE;
 

@@ -73,7 +73,51 @@ struct SkinnyArgs {
   const uint32_t* keep;
   int32_t keep_words;
   float drop_scale;
+  // Contraction split (skinny_split): with more than one piece, piece q
+  // sums chunks [q * cpp, (q + 1) * cpp) and writes the fp32 sum of element
+  // (begin + row, j) of the item list to part[(q * part_n + begin + row) *
+  // r_max + j]; a second kernel adds the pieces in order and stores the result.
+  float* part;           // [pieces][part_n][r_max] (unused with one piece)
+  int32_t part_n;        // length of the item list (rows grouped by item)
+  int32_t r_max;
+  int32_t split_items;   // the plan's item count that sets the split
+  int32_t pieces, cpp;   // set by the launcher
 };
+
+// Contraction split of the rank-r contractions: a launch whose items alone
+// cannot cover the CUs (fewer than kSkinnySplitBelow items of one projection)
+// splits each item's contraction (chunks of 256 columns) into up to
+// kMaxSkinnyPieces pieces of at least kSkinnyMinChunks chunks, aiming at
+// kSkinnySplitTarget workgroups; with more items the bandwidth is already
+// shared by enough workgroups and a split only adds the second pass.  The
+// split depends on C and on the plan's item count (split_items), not on the
+// launch: the forward shrink and the backward's recomputed h take the shrink's
+// item count, so both sum every row in the same order.
+constexpr int kSkinnySplitBelow = 160;
+constexpr int kSkinnySplitTarget = 384;
+constexpr int kSkinnyMinChunks = 4;
+constexpr int kMaxSkinnyPieces = 8;
+inline void skinny_split(int32_t C, int32_t split_items, int32_t* pieces, int32_t* cpp) {
+  const int32_t nch = (C + 255) / 256;
+  int32_t p = 1;
+  if (split_items > 0 && split_items < kSkinnySplitBelow) {
+    p = (kSkinnySplitTarget + split_items - 1) / split_items;
+    p = p > nch / kSkinnyMinChunks ? nch / kSkinnyMinChunks : p;
+    p = p > kMaxSkinnyPieces ? kMaxSkinnyPieces : p;
+    p = p < 1 ? 1 : p;
+  }
+  int32_t c = (nch + p - 1) / p;
+  c = c < 1 ? 1 : c;
+  *cpp = c;
+  *pieces = nch > 0 ? (nch + c - 1) / c : 1;
+}
+// fp32 partial bytes a rank-r contraction over C needs for an item list of n
+// elements (0 when it is not split).
+inline size_t skinny_part_bytes(int32_t C, int32_t split_items, int64_t n, int32_t r_max) {
+  int32_t pieces, cpp;
+  skinny_split(C, split_items, &pieces, &cpp);
+  return pieces > 1 ? (size_t)pieces * (size_t)n * (size_t)r_max * 4 : 0;
+}
 
 // Per-chunk fp32 partial sums over training tokens:
 //   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Q[t][j]
@@ -102,6 +146,9 @@ inline int32_t token_col_blocks(int32_t C) { return (C + kTokenCols - 1) / kToke
 struct SkinnyGroup {
   SkinnyArgs a[kMaxGroup];
   int32_t n;
+  // set by the launcher: workgroup row y runs piece slot_piece[y] of a[slot_proj[y]]
+  int32_t slot_proj[kMaxGroup * kMaxSkinnyPieces];
+  int32_t slot_piece[kMaxGroup * kMaxSkinnyPieces];
 };
 struct GatherArgs {           // gathered low-rank term of one projection
   const uint16_t* H;          // h of every row [T][ldh]
@@ -142,17 +189,21 @@ struct GemmGroup {
 // supported for 256x256 only.
 hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);
 hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
-hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
-hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
+// Rank-r contractions: r_sel bounds the rank of every item's adapter (it sizes
+// the rank tiles); the partials of a split contraction have stride a.r_max.
+hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_sel, hipStream_t s);
+hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_sel, hipStream_t s);
 // shrink over items of <= 16 rows (the training items): recomputes h for the backward
-hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s);
+hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_sel, hipStream_t s);
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
                                 int32_t r_max, const int32_t* items, int32_t n_items,
                                 const int32_t* gather_rows, const int32_t* ranks,
                                 const float* scales, float* delta, hipStream_t s);
 // Both token reductions of a backward (dB partials, dA partials) in one launch.
+// r_sel: the largest rank of a training adapter (sizes the rank tiles; the
+// partials keep the r_max stride).
 hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
-                               hipStream_t s);
+                               int32_t r_sel, hipStream_t s);
 // Fixed-order sum of one reduction's chunk partials into its output.
 struct ReduceOutArgs {
   const float* part;
@@ -167,22 +218,22 @@ struct ReduceOutGroup {
   int32_t n;
 };
 // Both final sums of a backward in one launch.
-hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
+hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max, int32_t r_sel,
                              const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
                              const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s);
 hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
                               int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
 
 // Grouped forms (n >= 1 entries filled).
-hipError_t launch_shrink_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s);
-hipError_t launch_gmat_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s);
-hipError_t launch_shrink_train_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s);
+hipError_t launch_shrink_group(const SkinnyGroup& g, int32_t n_items, int32_t r_sel, hipStream_t s);
+hipError_t launch_gmat_group(const SkinnyGroup& g, int32_t n_items, int32_t r_sel, hipStream_t s);
+hipError_t launch_shrink_train_group(const SkinnyGroup& g, int32_t n_items, int32_t r_sel, hipStream_t s);
 hipError_t launch_gather_group(const GatherGroup& g, int64_t ldh, int32_t r_max, const int32_t* items,
                                int32_t n_items, const int32_t* gather_rows, const int32_t* ranks,
                                const float* scales, hipStream_t s);
 // entries 2p and 2p+1: the dB and dA reductions of projection p (all with one r_max)
-hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s);
-hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, const int32_t* train_ads,
+hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s);
+hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, int32_t r_sel, const int32_t* train_ads,
                                    int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
                                    const int32_t* ranks, int32_t accumulate, hipStream_t s);
 hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const int32_t* train_ads,

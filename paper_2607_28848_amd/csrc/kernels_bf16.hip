@@ -705,7 +705,8 @@ __device__ __forceinline__ void skinny_store(const SkinnyArgs& g, int a, int beg
 // (a mask byte per 8 columns, applied to the fragment as it is read).
 template <int MODE, int NJ, int ROWS, bool DROP>  // MODE 0: shrink (h -> H_all, H_save), 1: g (-> G)
 __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
-  const SkinnyArgs g = G.a[blockIdx.y];  // the projection's arguments (a copy: scalar registers)
+  const SkinnyArgs g = G.a[G.slot_proj[blockIdx.y]];  // the projection's arguments (scalar registers)
+  const int piece = G.slot_piece[blockIdx.y];
   constexpr int RT = ROWS / 16;           // 16-row tiles per item
   constexpr int SR = ROWS + 16 * NJ;      // LDS rows of a chunk: input rows, then adapter rows
   constexpr int RB = SK_CK * 2;           // bytes per LDS row
@@ -765,7 +766,9 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
     }
   }
   const int lc = 4 * wave + (lane >> 4);  // logical 16-byte chunk of the lane's fragments
-  const int nch = (g.C + SK_CK - 1) / SK_CK;
+  // this workgroup's chunks of the contraction: [c_beg, nch)
+  const int c_beg = piece * g.cpp;
+  const int nch = min((g.C + SK_CK - 1) / SK_CK, c_beg + g.cpp);
   f32x4 acc[RT][NJ];
 #pragma unroll
   for (int t = 0; t < RT; ++t)
@@ -782,9 +785,9 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
   auto chunk = [&](int c, const uint32_t (&mu)[RT], uint32_t (&ml)[RT]) {
     vmem_wait_all();
     __syncthreads();  // chunk c is in; every wave is done with chunk c - 1's buffer
-    if (c + 1 < nch) issue(c + 1, (c + 1) & 1);
+    if (c + 1 < nch) issue(c + 1, (c + 1 - c_beg) & 1);
     if constexpr (DROP) load_mask(min(c + 1, nch - 1), ml);  // unconditional: no merge to wait on
-    const char* sb = smem + (c & 1) * STAGE;
+    const char* sb = smem + ((c - c_beg) & 1) * STAGE;
     bf16x8 xf[RT], qf[NJ];
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
@@ -805,11 +808,11 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
         acc[t][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xf[t], qf[jt], acc[t][jt], 0, 0, 0);
   };
   uint32_t m0[RT] = {}, m1[RT] = {};
-  if (nch > 0) {
-    issue(0, 0);
-    if constexpr (DROP) load_mask(0, m0);
+  if (c_beg < nch) {
+    issue(c_beg, 0);
+    if constexpr (DROP) load_mask(c_beg, m0);
   }
-  for (int c = 0; c < nch; c += 2) {
+  for (int c = c_beg; c < nch; c += 2) {
     chunk(c, m0, m1);
     if (c + 1 < nch) chunk(c + 1, m1, m0);
   }
@@ -833,8 +836,27 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
       float sum = 0.f;
 #pragma unroll
       for (int w = 0; w < SW; ++w) sum += red[(w * ROWS + row) * RW + j];
-      skinny_store<MODE>(g, a, begin, row, j, sum);
+      if (g.pieces == 1)
+        skinny_store<MODE>(g, a, begin, row, j, sum);
+      else
+        g.part[((int64_t)piece * g.part_n + begin + row) * g.r_max + j] = sum;
     }
+  }
+}
+
+// Sum of the pieces of a split rank-r contraction, in piece order, and the
+// store of the result: one workgroup per (item, split projection).
+template <int MODE>
+__global__ __launch_bounds__(256) void skinny_finish_kernel(SkinnyGroup G) {
+  const SkinnyArgs& g = G.a[G.slot_proj[blockIdx.y]];
+  const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
+  const int a = it[0], begin = it[1], cnt = it[2];
+  const int r = g.ranks[a];
+  for (int idx = threadIdx.x; idx < cnt * r; idx += 256) {
+    const int row = idx / r, j = idx - row * r;
+    float sum = 0.f;
+    for (int q = 0; q < g.pieces; ++q) sum += g.part[((int64_t)q * g.part_n + begin + row) * g.r_max + j];
+    skinny_store<MODE>(g, a, begin, row, j, sum);
   }
 }
 
@@ -860,6 +882,9 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
   const int row = (i < cnt) ? gather_rows[sbeg + i] : -1;
   const uint16_t* Ba = B + (int64_t)a * N * r_max;
   const int nb = by * 256 + wave * 64;
+  // B rows start 16-byte aligned when r_max is a multiple of 8: a lane's 8
+  // ranks are then one 16-byte load (else 8 element loads)
+  const bool b16 = (r_max & 7) == 0;
   f32x4 acc[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -875,7 +900,10 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
     for (int ct = 0; ct < 4; ++ct) {
       const int n = nb + 16 * ct + (lane & 15);
       u32x4 bv = zero4();
-      if (n < N && nv > 0) bv = ld8_masked(Ba + (int64_t)n * r_max + jb, 1, nv);
+      if (n < N && nv > 0) {
+        const uint16_t* p = Ba + (int64_t)n * r_max + jb;
+        bv = (b16 && nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
+      }
       acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av), as_bf(bv), acc[ct], 0, 0, 0);
     }
   }
@@ -1055,7 +1083,7 @@ __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
 // Every final sum of a (grouped) backward in one launch: blockIdx.y = which *
 // n_tads + training adapter (which: dB, dA of the first projection, then the
 // next projection's).
-__global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32_t r_max,
+__global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32_t r_max, int32_t r_sel,
                                                          const int32_t* __restrict__ train_ads, int32_t n_tads,
                                                          const int32_t* __restrict__ tad_ptr,
                                                          const int32_t* __restrict__ tad_chunks,
@@ -1066,10 +1094,11 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32
   const int C = g.C;
   const int a = train_ads[ta], r = ranks[a];
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)C * r_max) return;
+  if (idx >= (int64_t)C * r_sel) return;
   // j fastest, the partials' layout: the reads are coalesced in both output
-  // layouts (the partials outweigh the output by the number of chunks)
-  const int c = (int)(idx / r_max), j = (int)(idx % r_max);
+  // layouts (the partials outweigh the output by the number of chunks); the
+  // threads cover the ranks below r_sel (>= every training adapter's rank)
+  const int c = (int)(idx / r_sel), j = (int)(idx % r_sel);
   if (c >= C || j >= r) return;
   float sum = 0.f;
   for (int p = tad_ptr[ta]; p < tad_ptr[ta + 1]; ++p)
@@ -1142,35 +1171,52 @@ hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
 
 namespace {
 template <int MODE, int NJ, int ROWS, bool DROP>
-void launch_skinny_kernel(const SkinnyGroup& g, int32_t n_items, hipStream_t s) {
-  hipLaunchKernelGGL((skinny_kernel<MODE, NJ, ROWS, DROP>), dim3(n_items, g.n), dim3(64 * SW), 0, s, g);
+void launch_skinny_kernel(const SkinnyGroup& g, int32_t n_items, int32_t ny, hipStream_t s) {
+  hipLaunchKernelGGL((skinny_kernel<MODE, NJ, ROWS, DROP>), dim3(n_items, ny), dim3(64 * SW), 0, s, g);
 }
 
 template <int MODE, int ROWS, bool DROP>
-void launch_skinny_nj(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
-  if (r_max <= 16) launch_skinny_kernel<MODE, 1, ROWS, DROP>(g, n_items, s);
-  else if (r_max <= 32) launch_skinny_kernel<MODE, 2, ROWS, DROP>(g, n_items, s);
-  else launch_skinny_kernel<MODE, 4, ROWS, DROP>(g, n_items, s);
+void launch_skinny_nj(const SkinnyGroup& g, int32_t n_items, int32_t ny, int32_t r_max, hipStream_t s) {
+  if (r_max <= 16) launch_skinny_kernel<MODE, 1, ROWS, DROP>(g, n_items, ny, s);
+  else if (r_max <= 32) launch_skinny_kernel<MODE, 2, ROWS, DROP>(g, n_items, ny, s);
+  else launch_skinny_kernel<MODE, 4, ROWS, DROP>(g, n_items, ny, s);
 }
 
-// Every projection of a group takes the dropout path or none does.  The
-// projections are launched longest contraction first (workgroups are
-// dispatched projection by projection), so the long items start first and the
-// short ones fill in behind them.
+// Every projection of a group takes the dropout path or none does.  Each
+// projection's contraction may be split into pieces (skinny_split); the pieces
+// are launched longest first (workgroups are dispatched row by row of the
+// grid), so the long ones start first and the short ones fill in behind them.
+// Split projections need their partial buffer (part, part_n, r_max); a second
+// launch sums their pieces.
 template <int MODE, int ROWS>
 hipError_t launch_skinny(const SkinnyGroup& g0, int32_t n_items, int32_t r_max, hipStream_t s) {
   if (n_items <= 0 || g0.n <= 0) return hipSuccess;
-  if (g0.n > kMaxGroup) return hipErrorInvalidValue;
+  if (g0.n > kMaxGroup || r_max < 1 || r_max > 64) return hipErrorInvalidValue;
   for (int p = 1; p < g0.n; ++p)
     if ((g0.a[p].keep != nullptr) != (g0.a[0].keep != nullptr)) return hipErrorInvalidValue;
   SkinnyGroup g = g0;
-  std::stable_sort(g.a, g.a + g.n, [](const SkinnyArgs& x, const SkinnyArgs& y) { return x.C > y.C; });
-  if constexpr (MODE == 0) {
-    if (g.a[0].keep != nullptr) launch_skinny_nj<MODE, ROWS, true>(g, n_items, r_max, s);
-    else launch_skinny_nj<MODE, ROWS, false>(g, n_items, r_max, s);
-  } else {
-    launch_skinny_nj<MODE, ROWS, false>(g, n_items, r_max, s);
+  for (int p = 0; p < g.n; ++p) {
+    skinny_split(g.a[p].C, g.a[p].split_items, &g.a[p].pieces, &g.a[p].cpp);
+    if (g.a[p].pieces > 1 && (g.a[p].part == nullptr || g.a[p].part_n < 0 || g.a[p].r_max < r_max))
+      return hipErrorInvalidValue;
   }
+  std::stable_sort(g.a, g.a + g.n, [](const SkinnyArgs& x, const SkinnyArgs& y) { return x.cpp > y.cpp; });
+  int ny = 0;
+  for (int p = 0; p < g.n; ++p)
+    for (int q = 0; q < g.a[p].pieces; ++q) {
+      g.slot_proj[ny] = p;
+      g.slot_piece[ny++] = q;
+    }
+  if constexpr (MODE == 0) {
+    if (g.a[0].keep != nullptr) launch_skinny_nj<MODE, ROWS, true>(g, n_items, ny, r_max, s);
+    else launch_skinny_nj<MODE, ROWS, false>(g, n_items, ny, r_max, s);
+  } else {
+    launch_skinny_nj<MODE, ROWS, false>(g, n_items, ny, r_max, s);
+  }
+  int nf = 0;
+  for (int p = 0; p < g.n; ++p)
+    if (g.a[p].pieces > 1) g.slot_proj[nf++] = p;
+  if (nf > 0) hipLaunchKernelGGL((skinny_finish_kernel<MODE>), dim3(n_items, nf), dim3(256), 0, s, g);
   return hipGetLastError();
 }
 
@@ -1242,11 +1288,11 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
 }
 
 template <bool DROP>
-void launch_token_reduce_nj(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s) {
+void launch_token_reduce_nj(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s) {
   const dim3 grid(n_chunks, g.yoff[g.n]);
-  if (g.a[0].r_max <= 16)
+  if (r_sel <= 16)
     hipLaunchKernelGGL((token_reduce_kernel<1, DROP>), grid, dim3(512), 0, s, g);
-  else if (g.a[0].r_max <= 32)
+  else if (r_sel <= 32)
     hipLaunchKernelGGL((token_reduce_kernel<2, DROP>), grid, dim3(512), 0, s, g);
   else
     hipLaunchKernelGGL((token_reduce_kernel<4, DROP>), grid, dim3(512), 0, s, g);
@@ -1254,52 +1300,52 @@ void launch_token_reduce_nj(const TokenReduceGroup& g, int32_t n_chunks, hipStre
 
 // A launch whose reductions include a masked one runs the kernel with the
 // masking code; it masks the reductions that carry a mask.
-hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, hipStream_t s) {
+hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s) {
   if (n_chunks <= 0 || g.n <= 0) return hipSuccess;
-  if (g.n > 2 * kMaxGroup || g.yoff[0] != 0) return hipErrorInvalidValue;
+  if (g.n > 2 * kMaxGroup || g.yoff[0] != 0 || r_sel < 1 || r_sel > g.a[0].r_max) return hipErrorInvalidValue;
   bool any_keep = false;
   for (int k = 0; k < g.n; ++k) {
     if (g.a[k].r_max != g.a[0].r_max || g.yoff[k + 1] - g.yoff[k] != token_col_blocks(g.a[k].C))
       return hipErrorInvalidValue;
     any_keep |= g.a[k].keep != nullptr;
   }
-  if (any_keep) launch_token_reduce_nj<true>(g, n_chunks, s);
-  else launch_token_reduce_nj<false>(g, n_chunks, s);
+  if (any_keep) launch_token_reduce_nj<true>(g, n_chunks, r_sel, s);
+  else launch_token_reduce_nj<false>(g, n_chunks, r_sel, s);
   return hipGetLastError();
 }
 
 hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
-                               hipStream_t s) {
+                               int32_t r_sel, hipStream_t s) {
   TokenReduceGroup g{};
   g.a[0] = a0;
   g.a[1] = a1;
   g.yoff[1] = token_col_blocks(a0.C);
   g.yoff[2] = g.yoff[1] + token_col_blocks(a1.C);
   g.n = 2;
-  return launch_token_reduce_group(g, n_chunks, s);
+  return launch_token_reduce_group(g, n_chunks, r_sel, s);
 }
 
-hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, const int32_t* train_ads,
+hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, int32_t r_sel, const int32_t* train_ads,
                                    int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
                                    const int32_t* ranks, int32_t accumulate, hipStream_t s) {
   if (n_tads <= 0 || g.n <= 0) return hipSuccess;
-  if (g.n > 2 * kMaxGroup) return hipErrorInvalidValue;
+  if (g.n > 2 * kMaxGroup || r_sel < 1 || r_sel > r_max) return hipErrorInvalidValue;
   int64_t cmax = 0;
   for (int k = 0; k < g.n; ++k) cmax = g.a[k].C > cmax ? g.a[k].C : cmax;
-  const int64_t total = cmax * r_max;
+  const int64_t total = cmax * r_sel;
   hipLaunchKernelGGL(reduce_out_kernel, dim3((unsigned)((total + 255) / 256), g.n * n_tads), dim3(256), 0, s, g,
-                     r_max, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate);
+                     r_max, r_sel, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate);
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max,
+hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max, int32_t r_sel,
                              const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
                              const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s) {
   ReduceOutGroup g{};
   g.a[0] = o0;
   g.a[1] = o1;
   g.n = 2;
-  return launch_reduce_out_group(g, r_max, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate, s);
+  return launch_reduce_out_group(g, r_max, r_sel, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate, s);
 }
 
 hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const int32_t* train_ads,

@@ -241,6 +241,9 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
     for (int32_t b = r.lo; b < r.hi; b += kItemRows)
       train_items.insert(train_items.end(), {r.adapter, b, std::min(kItemRows, r.hi - b), 0});
   const int32_t n_tads = (int32_t)train_ads.size();
+  p.r_used = p.r_train = 0;
+  for (int32_t t = 0; t < T; ++t) p.r_used = std::max(p.r_used, p.ranks[row_adapter[t]]);
+  for (int32_t a : train_ads) p.r_train = std::max(p.r_train, p.ranks[a]);
   std::vector<int32_t> tad_ptr(n_tads + 1, 0), tad_chunks;
   p.tad_max_chunks.assign(n_tads, 0);
   for (int32_t s = 0; s < n_tads; ++s) {

@@ -67,6 +67,9 @@ struct MetaLayout {
 
 struct dsv_plan {
   int32_t T = 0, n_ad = 0, r_max = 0, T_t = 0;
+  // largest rank among the adapters with rows / with training rows: the rank-r
+  // kernels size their rank tiles for these rather than for r_max
+  int32_t r_used = 0, r_train = 0;
   int32_t n_ftiles = 0, n_shrink = 0, n_gather = 0, n_gitems = 0, n_btiles = 0,
           n_chunks = 0, n_tads = 0, n_titems = 0, n_ftiles128 = 0, n_btiles128 = 0;
   std::vector<int32_t> ranks;

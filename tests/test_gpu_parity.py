@@ -110,7 +110,8 @@ def test_split_tiles_ragged():
                dx_rows=dx_rows.astype(np.int32))
 
 
-@pytest.mark.parametrize("dtype,K,N", [("bf16", 520, 776), ("f32", 520, 776), ("bf16", 4096, 4096)])
+@pytest.mark.parametrize("dtype,K,N", [("bf16", 520, 776), ("f32", 520, 776), ("bf16", 4096, 4096),
+                                       ("bf16", 4104, 2056)])
 def test_residual_only_retention_recomputes_h_bit_exact(dtype, K, N):
     """A forward that keeps no H_save (the caller keeps X) and a backward that
     recomputes h from X and A give bit-identical Y, dA, dB and dX to keeping H_save
@@ -130,12 +131,14 @@ def test_residual_only_retention_recomputes_h_bit_exact(dtype, K, N):
         assert torch.equal(bits(a), bits(b))
 
 
-def test_split_contraction_rank_kernels():
-    """K = N = 4096 with r_max 16: the shrink (over K) and g (over N) split their
-    contraction into chunks summed by a second kernel; Y and dX on sampled rows,
-    H_save, dA and dB in full."""
+@pytest.mark.parametrize("K,N", [(4096, 4096), (4104, 2056)])
+def test_split_contraction_rank_kernels(K, N):
+    """Contractions of 8+ chunks of 256 columns: the shrink (over K) and g (over N)
+    split them into pieces (K = 4096: 2 of 8 chunks; K = 4104: 3 pieces of 6, 6 and 5
+    chunks, the last one 8 columns wide; N = 2056: 5 + 4 chunks) whose fp32 sums a
+    second kernel adds in order; Y and dX on sampled rows, H_save, dA and dB in full."""
     ranks = [16, 8, 16, 12, 5]
-    w = wl.custom(MIXED, ranks, K=4096, N=4096, r_max=16, name="split_rank")
+    w = wl.custom(MIXED, ranks, K=K, N=N, r_max=16, name="split_rank")
     run = Run(w, pad=np.nan)
     Y, H = run.fwd()
     dA, dB, dX = run.bwd(H)
