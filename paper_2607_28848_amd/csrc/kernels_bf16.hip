@@ -888,24 +888,34 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
   f32x4 acc[4];
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct) acc[ct] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int j0 = 0; j0 < r; j0 += 32) {
-    const int jb = j0 + 8 * (lane >> 4);
+  // both 32-rank steps (r <= 64) are loaded before the first MFMA: one round
+  // trip to memory per workgroup instead of one per step
+  u32x4 av[2], bv[2][4];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int jb = 32 * s + 8 * (lane >> 4);
     const int nv = min(8, r - jb);
-    u32x4 av = zero4();
+    av[s] = zero4();
     if (row >= 0 && nv > 0) {
       const uint16_t* p = H + (int64_t)row * ldh + jb;
-      av = (nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
+      av[s] = (nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
     }
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct) {
       const int n = nb + 16 * ct + (lane & 15);
-      u32x4 bv = zero4();
+      bv[s][ct] = zero4();
       if (n < N && nv > 0) {
         const uint16_t* p = Ba + (int64_t)n * r_max + jb;
-        bv = (b16 && nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
+        bv[s][ct] = (b16 && nv == 8) ? ld16(p) : ld8_masked(p, 1, nv);
       }
-      acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av), as_bf(bv), acc[ct], 0, 0, 0);
     }
+  }
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    if (32 * s >= r) break;
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+      acc[ct] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av[s]), as_bf(bv[s][ct]), acc[ct], 0, 0, 0);
   }
   const float s = scales[a];
 #pragma unroll
