@@ -583,8 +583,11 @@ __device__ __forceinline__ void gemm_piece(const GemmArgs& g, char* smem, int ti
       const uint2 lo = *reinterpret_cast<const uint2*>(slice + rr * SRS + 16 * ch);
       const uint2 hi = *reinterpret_cast<const uint2*>(slice + rr * SRS + 16 * ch + 8);
       const int orow = wm * WM + 32 * i + rr, ocol = n0 + wn * WN + 8 * ch;
+      // streaming stores: the output is not read again by this launch, so its
+      // lines should not displace the operand panels the XCD's tiles share in L2
       if (orow < nrows && ocol < g.Nout)
-        *reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + orow) * g.ldo + ocol) = u32x4{lo.x, lo.y, hi.x, hi.y};
+        __builtin_nontemporal_store(u32x4{lo.x, lo.y, hi.x, hi.y},
+                                    reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + orow) * g.ldo + ocol));
     }
     asm volatile("" ::: "memory");  // the slice is read before the next rows overwrite it
   }
