@@ -2,7 +2,8 @@
 """Throughput of the co-batched multi-LoRA layer (forward + LoRA backward) on one MI355X.
 
 One step = one pass of the whole path over one synthetic batch: pack the segment
-table (dsv_segments_build, host + one copy to the device), then for every
+table (dsv_segments_build, host + one copy to the device, on a side stream so that it
+overlaps the previous step's kernels, double-buffered), then for every
 projection of the workload the co-batched forward (shrink, gathered low-rank
 terms, base GEMM with the low-rank prologue, training-row h saved) and the LoRA
 backward of the training rows (g, dB, dA, dX).  Inputs are resident in HBM
@@ -184,6 +185,9 @@ def main():
                          "then transposes W in the kernel)")
     ap.add_argument("--dropout", type=float, default=0.0, metavar="P",
                     help="LoRA dropout P on the training rows in the timed step (fresh mask per step)")
+    ap.add_argument("--upload", default="side", choices=("side", "inorder"),
+                    help="side: each step's plan metadata is uploaded on a side stream into alternating "
+                         "buffers, overlapping the previous step; inorder: on the compute stream")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run 3 plain device copies of MIB MiB (reference for HBM byte counters)")
     args = ap.parse_args()
@@ -257,6 +261,15 @@ def main():
     meta_bytes = ctypes.c_size_t(probe.meta_bytes)
     metas = [torch.empty(max(probe.meta_bytes, 256), dtype=torch.uint8, device=dev) for _ in range(2)]
     sh = ctypes.c_void_p(int(stream.cuda_stream))
+    # A step's plan is uploaded on a side stream (default priority), so the copy of
+    # step i's metadata overlaps step i-1's kernels instead of sitting between them.
+    # The metadata is double-buffered: buffer b is rewritten only after the step that
+    # last read it has finished (meta_free[b], recorded on the compute stream), and the
+    # compute stream waits for the upload (meta_ready[b]) before its first kernel.
+    up_stream = torch.cuda.Stream(dev)
+    uh = ctypes.c_void_p(int(up_stream.cuda_stream))
+    meta_free = [torch.cuda.Event() for _ in range(2)]
+    meta_ready = [torch.cuda.Event() for _ in range(2)]
     ptr = lambda t: ctypes.c_void_p(int(t.data_ptr()))  # noqa: E731
     plan_ms = []
     def make_step(launch, use_wt=not args.no_wt):
@@ -280,14 +293,21 @@ def main():
 
         def step(i):
             h = ctypes.c_void_p()
+            b = i & 1
+            side = args.upload == "side"
+            if side:
+                up_stream.wait_event(meta_free[b])
             tp = time.perf_counter()
             rc = lib.dsv_segments_build(seg.ctypes.data_as(i32p), seg.shape[0], w.n_tokens,
                                         ranks.ctypes.data_as(i32p), scales.ctypes.data_as(f32p),
-                                        ranks.shape[0], w.r_max, ptr(metas[i & 1]), ctypes.byref(meta_bytes),
-                                        sh, ctypes.byref(h))
+                                        ranks.shape[0], w.r_max, ptr(metas[b]), ctypes.byref(meta_bytes),
+                                        uh if side else sh, ctypes.byref(h))
             plan_ms.append((time.perf_counter() - tp) * 1e3)
             if rc != 0:
                 raise RuntimeError("dsv_segments_build failed: %d" % rc)
+            if side:
+                meta_ready[b].record(up_stream)
+                stream.wait_event(meta_ready[b])
             if groups is not None:
                 drs = None
                 if args.dropout > 0:  # one mask stream per projection and step
@@ -311,6 +331,8 @@ def main():
                                                               ptr(gws_b[gi]), gws_b[gi].numel(), sh)
                     if rc != 0:
                         raise RuntimeError("dsv_lora_bwd_grouped failed: %d" % rc)
+                if side:
+                    meta_free[b].record(stream)
                 lib.dsv_plan_free(h)
                 return
             for p, proj in enumerate(w.projections):
@@ -337,7 +359,9 @@ def main():
                                           0, ptr(d["wsb"]), d["wsb"].numel(), sh)
                 if rc != 0:
                     raise RuntimeError("dsv_lora_bwd failed: %d" % rc)
-            lib.dsv_plan_free(h)  # the blob's copy was issued; the device metadata stays valid
+            if side:
+                meta_free[b].record(stream)
+            lib.dsv_plan_free(h)  # waits for the blob's upload; the device metadata stays valid
         return step, groups
 
     step, groups = make_step(args.launch)
@@ -351,6 +375,8 @@ def main():
     torch.cuda.synchronize()
     log("warmup done (%d steps)" % args.warmup)
     plan_ms.clear()
+    # The library times every GEMM launch of the timed steps with HIP events that
+    # ride the launches' own dispatches (no packets between kernels).
     dsv.timing_enable(True)
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
@@ -364,8 +390,8 @@ def main():
     wall = time.perf_counter() - wall0
     dsv.timing_enable(False)
     plan_med = round(float(np.median(plan_ms)), 4) if plan_ms else None
-    fwd_ms, fwd_n, bwd_ms, bwd_n = dsv.timing_read()
     gpu_ms = ev0.elapsed_time(ev1)
+    fwd_ms, fwd_n, bwd_ms, bwd_n = dsv.timing_read()
     elapsed_s = max(wall, gpu_ms / 1e3)
     ms_per_step = elapsed_s * 1e3 / args.steps
 
@@ -602,6 +628,7 @@ def main():
             "algorithmic_gflop_per_step": round(step_flops / 1e9, 2),
             "plan_build_ms": plan_med,
             "lora_dropout": args.dropout,
+            "metadata_upload": args.upload,
             "launch": args.launch,
             "dx_weight": "W transposed (kept once, like W)" if groups is not None and not args.no_wt else "W",
             "launch_groups": ([[p.name for p in w.projections[lo:hi]] for lo, hi in groups] if groups is not None
@@ -619,6 +646,7 @@ def main():
             "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
             "avg_launch_us": round(fwd_avg_ms * 1e3, 2),
             "launches": fwd_n,
+            "launch_timing": "HIP events attached to the GEMM dispatches of the timed steps",
             "dx_gemm_tflops": round(bwd_achieved, 2) if bwd_achieved else None,
             "gemm_launches": gemm_launches,
         },

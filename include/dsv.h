@@ -107,7 +107,12 @@ typedef struct dsv_plan dsv_plan;
  * d_meta != NULL: a 256-byte aligned device buffer of at least *meta_bytes
  *   bytes; the packed metadata is copied into it with one asynchronous copy
  *   on hip_stream, and the returned plan refers to it.  d_meta must stay
- *   allocated while the plan is used.
+ *   allocated while the plan is used.  The copy is ordered on hip_stream
+ *   only: work queued on another stream that still reads an earlier plan in
+ *   the same buffer must finish first, and launches on another stream must
+ *   wait for the copy (an event recorded on hip_stream after this call).
+ *   Uploading on a side stream into alternating buffers lets the copy of the
+ *   next batch's metadata overlap the current batch's kernels.
  * On error *out_plan is set to NULL (when out_plan is not NULL).
  */
 int dsv_segments_build(const dsv_segment* segs, int32_t n_segs, int32_t n_tokens,

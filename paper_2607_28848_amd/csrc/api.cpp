@@ -198,21 +198,28 @@ struct Timing {
 };
 Timing g_timing;
 
-// Records the start event of a timed launch; returns the pair index or -1.
+// Hands the events of a timed launch to the next GEMM launch (they are
+// recorded within its kernels' dispatches); returns the pair index or -1.
 int timing_begin(int kind, hipStream_t s) {
+  (void)s;
   Timing& t = g_timing;
   if (!t.on || t.n >= Timing::kMaxPairs) return -1;
   const int i = t.n;
   for (int k = 0; k < 2; ++k)
     if (!t.ev[i][k] && hipEventCreate(&t.ev[i][k]) != hipSuccess) return -1;
-  if (hipEventRecord(t.ev[i][0], s) != hipSuccess) return -1;
+  set_launch_events(t.ev[i][0], t.ev[i][1]);
   t.kind[i] = kind;
   t.n = i + 1;
   return i;
 }
 
+// A pair whose launch launched nothing (or failed before its last kernel) is
+// dropped: its events were never recorded.
 void timing_end(int i, hipStream_t s) {
-  if (i >= 0) (void)hipEventRecord(g_timing.ev[i][1], s);
+  (void)s;
+  if (i < 0 || !launch_events_pending()) return;
+  set_launch_events(nullptr, nullptr);
+  if (i == g_timing.n - 1) g_timing.n = i;
 }
 
 }  // namespace

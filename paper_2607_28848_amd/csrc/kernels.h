@@ -188,6 +188,12 @@ struct GemmGroup {
 // plan's row-tile list of height tm.  Split tiles (sk_tiles > 0) are
 // supported for 256x256 only.
 hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);
+// Benchmark timing: the next GEMM launch (launch_gemm_nt / _nn / _group_*)
+// records `start` as its first kernel begins and `stop` as its last kernel
+// ends, within the kernels' dispatches.  launch_events_pending() is true while
+// an event has not been handed to a launch (nothing was launched).
+void set_launch_events(hipEvent_t start, hipEvent_t stop);
+bool launch_events_pending();
 hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
 // Rank-r contractions: r_sel bounds the rank of every item's adapter (it sizes
 // the rank tiles); the partials of a split contraction have stride a.r_max.

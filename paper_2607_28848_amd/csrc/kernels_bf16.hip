@@ -16,6 +16,7 @@
 //   token_reduce     fp32 per-chunk partials of dy^T h and x^T g.
 //   reduce_out       fixed-order sum of the partials into dB / dA.
 //   gemm (NN)        dx = dy W + g A_a (prologue adds g A_a).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -1140,6 +1141,23 @@ __global__ __launch_bounds__(256) void transpose_b_kernel(TransposeGroup G, int3
 }  // namespace
 
 namespace {
+// Benchmark timing of the next GEMM launch (set_launch_events): the start
+// event rides the launch's first kernel and the stop event its last one, as
+// part of their dispatches (hipExtLaunchKernelGGL), so the timing adds no
+// packets between kernels.
+hipEvent_t g_ev_start = nullptr, g_ev_stop = nullptr;
+
+template <typename F, typename... Args>
+void launch_timed(F kernel, dim3 grid, dim3 block, hipStream_t s, bool first, bool last, Args... args) {
+  hipEvent_t e0 = first ? g_ev_start : nullptr, e1 = last ? g_ev_stop : nullptr;
+  if (e0 || e1)
+    hipExtLaunchKernelGGL(kernel, grid, block, 0, s, e0, e1, 0, args...);
+  else
+    hipLaunchKernelGGL(kernel, grid, block, 0, s, args...);
+  if (first) g_ev_start = nullptr;
+  if (last) g_ev_stop = nullptr;
+}
+
 // Tile configurations: (TM, TN, wave grid, K-step, pipeline stages); two
 // waves per SIMD in each (8 waves per 256-row workgroup, or two 4-wave
 // 128 x 128 workgroups per CU).
@@ -1157,17 +1175,17 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   }
   const dim3 grid((unsigned)(a.dp_tiles + (int64_t)a.sk_tiles * (a.sk_tiles > 0 ? a.sk_split : 0)));
   if (tm == 256 && tn == 256 && a.sk_tiles > 0) {
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>), grid, dim3(512), 0, s, a);
+    launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>, grid, dim3(512), s, true, false, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL((split_fixup_kernel<NN, 256, 256>), dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)),
-                       dim3(256), 0, s, a);
+    launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)), dim3(256), s,
+                 false, true, a);
   } else if (tm == 256 && tn == 256)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>), grid, dim3(512), 0, s, a);
+    launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>, grid, dim3(512), s, true, true, a);
   else if (tm == 256 && tn == 128)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 256, 128, 4, 2, 64, 2, false>), grid, dim3(512), 0, s, a);
+    launch_timed(gemm_lora_kernel<NN, 256, 128, 4, 2, 64, 2, false>, grid, dim3(512), s, true, true, a);
   else if (tm == 128 && tn == 128)
-    hipLaunchKernelGGL((gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2, false>), grid, dim3(256), 0, s, a);
+    launch_timed(gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2, false>, grid, dim3(256), s, true, true, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -1177,6 +1195,13 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
 hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   return launch_gemm_tiled<false>(a, tm, tn, s);
 }
+
+void set_launch_events(hipEvent_t start, hipEvent_t stop) {
+  g_ev_start = start;
+  g_ev_stop = stop;
+}
+
+bool launch_events_pending() { return g_ev_start != nullptr || g_ev_stop != nullptr; }
 
 hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   return launch_gemm_tiled<true>(a, tm, tn, s);
@@ -1248,7 +1273,7 @@ hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
     if (g.off[p + 1] - g.off[p] != a.n_mtiles * a.n_ntiles || a.sk_tiles != 0) return hipErrorInvalidValue;
   }
   if (g.off[g.n] <= 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_group_kernel<NN>), dim3((unsigned)g.off[g.n]), dim3(512), 0, s, g);
+  launch_timed(gemm_group_kernel<NN>, dim3((unsigned)g.off[g.n]), dim3(512), s, true, true, g);
   return hipGetLastError();
 }
 }  // namespace

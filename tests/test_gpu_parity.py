@@ -271,7 +271,8 @@ def test_accumulate_and_untouched_slices():
 
 def _sampled(w, p, n_rows=24, seed=0):
     """Full-size projection: every output of the HIP path against the reference on
-    sampled rows (Y, dX) and in full (H_save, dA, dB)."""
+    sampled rows (Y, dX) and in full (H_save, dA, dB); a one-projection workload also
+    through the grouped call the bench times (dX on the transposed weight), bit for bit."""
     import torch
     K, N = w.projections[p].K, w.projections[p].N
     _say("case %s/%s T=%d Tt=%d K=%d N=%d" % (w.name, w.projections[p].name, w.n_tokens,
@@ -286,6 +287,20 @@ def _sampled(w, p, n_rows=24, seed=0):
     rows = np.unique(np.concatenate([rng.choice(w.n_tokens, n_rows, replace=False),
                                      rng.choice(firsts, min(n_rows, len(firsts)), replace=False)]))
     Tt = w.train_tokens
+    if len(w.projections) == 1 and Tt:
+        # the bench's launch of a one-projection workload: a group of one whose dX
+        # GEMM reads the transposed weight; same sums, so bit-identical results
+        Wt = run.W.t().contiguous()
+        (Yg, Hg), = run.dsv.cobatch_fwd_grouped(run.plan, [(run.X, run.W, run.A, run.B)])
+        (dAg, dBg, dXg), = run.dsv.lora_bwd_grouped(run.plan, [(run.X, run.W, run.A, run.B, Hg, run.dY)],
+                                                    wts=[Wt])
+        torch.cuda.synchronize()
+        bits = lambda t: t.view(torch.int16) if t.dtype == torch.bfloat16 else t.view(torch.int32)  # noqa: E731
+        for a, b in ((Y, Yg), (dX, dXg), (dA, dAg), (dB, dBg)):
+            assert torch.equal(bits(a), bits(b))
+        r_t = min(r for _, r in train_mask_slices(w))  # columns every H_save row holds
+        assert torch.equal(bits(H[:, :r_t]), bits(Hg[:, :r_t]))
+        del Wt, Yg, Hg, dAg, dBg, dXg
     dx_rows = np.unique(np.concatenate([rng.choice(Tt, n_rows, replace=False), [0, Tt - 1]])) if Tt else None
     return _check_all(w, run, Y, H, dA, dB, dX, TOL_BF16, rows=rows.astype(np.int32),
                       dx_rows=None if dx_rows is None else dx_rows.astype(np.int32))
@@ -316,3 +331,32 @@ def test_llama70b_full_size(p):
 @pytest.mark.parametrize("frac", [0.0, 0.5, 1.0])
 def test_load_sweep_full_size(frac):
     _sampled(wl.load_sweep(frac), 0, n_rows=12)
+
+
+def test_gemm_launch_timing():
+    """dsv_timing_*: the events ride the GEMM launches' dispatches, one pair per launch
+    (forward, dX: a split-tile launch is timed from its tile kernel to its fixup), with
+    positive durations; a backward without training rows launches no GEMM and adds no pair."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    w = wl.custom(MIXED, [16, 8, 16, 12, 5], K=4096, N=4104, r_max=16, name="timing")
+    run = Run(w, pad=np.nan)
+    fc = dsv.gemm_config(run.plan, dsv.BF16, 4096, 4104, 0)
+    bc = dsv.gemm_config(run.plan, dsv.BF16, 4096, 4104, 1)
+    _say("  gemm configs: fwd %s dX %s" % (fc, bc))
+    torch.cuda.synchronize()
+    dsv.timing_read()  # discard anything recorded before
+    dsv.timing_enable(True)
+    try:
+        Y, H = run.fwd()
+        dA, dB, dX = run.bwd(H)
+        inf = dsv.segments_build([(s, l, a, 0) for (s, l, a, _) in w.segments], w.n_tokens, w.ranks, w.scales,
+                                 w.r_max, device="cuda")
+        dsv.lora_bwd(inf, run.X, run.W, run.A, run.B, None, run.dY[:1])
+        torch.cuda.synchronize()
+    finally:
+        dsv.timing_enable(False)
+    fwd_ms, fwd_n, bwd_ms, bwd_n = dsv.timing_read()
+    assert (fwd_n, bwd_n) == (1, 1)
+    assert 0.0 < fwd_ms < 1e3 and 0.0 < bwd_ms < 1e3
+    assert dsv.timing_read()[1] == 0  # a read resets the pairs
