@@ -48,6 +48,17 @@ WORKLOADS = {
 }
 
 
+LAUNCH_NOTES = {
+    "set": ("one grouped call per direction over all projections: their synthetic inputs are independent, "
+            "so this is the same work, but in a model o waits for attention and down for the MLP product; "
+            "an upper bound of a real layer's launches (extras.launch_modes_ms_per_step.layer is the "
+            "realisable grouping)"),
+    "layer": ("grouped calls over the projections a transformer layer can run together: q/k/v, o, "
+              "gate/up, down"),
+    "single": "one call per projection",
+}
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -162,6 +173,76 @@ def cpu_baseline(w, stores, n_fwd_rows, n_dx_rows, seed=0):
     return flops, secs
 
 
+def cpu_model():
+    """The host CPU's model name (first entry of /proc/cpuinfo), or None."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
+
+
+def library_gemm_context(w, P, stream, reps=20):
+    """The same GEMM shapes through torch (hipBLASLt / rocBLAS on ROCm) on the same
+    resident bf16 data, as context for the roofline: each projection's forward base
+    product X W^T ([T][K] x [N][K]^T) and dX product dY W ([T_t][N] x [N][K]), without
+    the low-rank terms.  Timed as whole loops of the 7 + 7 products (the clock settles
+    as it does in the bench's step), then one shape at a time."""
+    import torch
+    import torch.nn.functional as F
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    Tt = w.train_tokens
+    outs = [(torch.empty((w.n_tokens, p.N), dtype=torch.bfloat16, device=P[i]["X"].device),
+             torch.empty((max(Tt, 1), p.K), dtype=torch.bfloat16, device=P[i]["X"].device))
+            for i, p in enumerate(w.projections)]
+
+    def fwd(i):
+        torch.matmul(P[i]["X"], P[i]["W"].t(), out=outs[i][0])
+
+    def dx(i):
+        torch.matmul(P[i]["dY"], P[i]["W"], out=outs[i][1])
+
+    def timed(fn, n):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / n
+
+    ff = [2.0 * w.n_tokens * p.K * p.N for p in w.projections]
+    fb = [2.0 * Tt * p.K * p.N for p in w.projections]
+    n = len(w.projections)
+    out = {"library": str(torch.backends.cuda.preferred_blas_library()),
+           "note": "torch.matmul on the bench's resident bf16 operands, base products only"}
+    t_fwd = timed(lambda: [fwd(i) for i in range(n)], reps)
+    out["fwd_all_us"] = round(t_fwd, 1)
+    out["fwd_all_tflops"] = round(sum(ff) / (t_fwd * 1e-6) / 1e12, 1)
+    if Tt:
+        t_bwd = timed(lambda: [dx(i) for i in range(n)], reps)
+        out["dx_all_us"] = round(t_bwd, 1)
+        out["dx_all_tflops"] = round(sum(fb) / (t_bwd * 1e-6) / 1e12, 1)
+        t_both = timed(lambda: [fwd(i) for i in range(n)] + [dx(i) for i in range(n)], reps)
+        out["fwd_plus_dx_us"] = round(t_both, 1)
+        out["fwd_plus_dx_tflops"] = round((sum(ff) + sum(fb)) / (t_both * 1e-6) / 1e12, 1)
+    per = {}
+    for i, p in enumerate(w.projections):
+        t = timed(lambda: fwd(i), reps)
+        d = {"fwd_us": round(t, 1), "fwd_tflops": round(ff[i] / (t * 1e-6) / 1e12, 1)}
+        if Tt:
+            t = timed(lambda: dx(i), reps)
+            d.update(dx_us=round(t, 1), dx_tflops=round(fb[i] / (t * 1e-6) / 1e12, 1))
+        per["%s %dx%d" % (p.name, p.K, p.N)] = d
+    out["per_projection"] = per
+    del outs
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,8 +255,9 @@ def main():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timings after the main loop (AdamW, recomputed h, dropout, co-batching "
                          "overhead, launch modes)")
-    ap.add_argument("--extras", default="all", choices=("all", "overhead"),
-                    help="overhead: of the timings after the main loop, only the co-batching overhead")
+    ap.add_argument("--extras", default="all", choices=("all", "overhead", "library"),
+                    help="overhead: of the timings after the main loop, only the co-batching overhead; "
+                         "library: only the library-GEMM context")
     ap.add_argument("--launch", default="set", choices=("single", "layer", "set"),
                     help="single: one call per projection; layer: grouped calls over the projections a "
                          "transformer layer can run together (q/k/v, o, gate/up, down); set: one grouped call "
@@ -516,10 +598,15 @@ def main():
             log("step without dropout %.1f us, with dropout 0.05 %.1f us" % (dt_["off"], dt_["p0.05"]))
             del wsf_d, wsb_d
 
+        # The same base products through torch's GEMM library, as context.
+        if args.extras in ("all", "library"):
+            extras["library_gemm"] = library_gemm_context(w, P, stream)
+            log("library GEMMs: %s" % {k: v for k, v in extras["library_gemm"].items() if k != "per_projection"})
+
         # Co-batching overhead: the forward of the batch as it is against the forward of
         # the same segment table with every is_train flag cleared (no H_save rows, no
         # training-row bookkeeping), both in the bench's launch mode.
-        if w.train_tokens > 0:
+        if w.train_tokens > 0 and args.extras in ("all", "overhead"):
             inf_segs = [(s, l, a, 0) for (s, l, a, _) in w.segments]
             plan_inf = dsv.segments_build(inf_segs, w.n_tokens, w.ranks, w.scales, w.r_max, device=dev)
             wsf_o = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
@@ -598,8 +685,9 @@ def main():
         log("cpu baseline: fp64 reference on a sample (%d rows/projection fwd, %d dX rows)"
             % (args.cpu_rows, args.cpu_dx_rows))
         fl, secs = cpu_baseline(w, stores, args.cpu_rows, args.cpu_dx_rows)
-        cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
-        cpu = {"value": fl / secs / 1e12, "unit": "TFLOP/s", "cores": cores, "kind": "oracle",
+        import oracle
+        cpu = {"value": fl / secs / 1e12, "unit": "TFLOP/s", "cores": oracle.threads(), "kind": "oracle",
+               "cpu_model": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0)),
                "sample": "every projection: forward of %d sampled rows, backward g/dA/dB over all %d "
                          "training rows and dX of %d sampled training rows; %.2f GFLOP in %.1f s"
                          % (args.cpu_rows, w.train_tokens, args.cpu_dx_rows, fl / 1e9, secs)}
@@ -630,6 +718,7 @@ def main():
             "lora_dropout": args.dropout,
             "metadata_upload": args.upload,
             "launch": args.launch,
+            "launch_note": LAUNCH_NOTES[args.launch],
             "dx_weight": "W transposed (kept once, like W)" if groups is not None and not args.no_wt else "W",
             "launch_groups": ([[p.name for p in w.projections[lo:hi]] for lo, hi in groups] if groups is not None
                               else [[p.name] for p in w.projections]),

@@ -329,7 +329,10 @@ int dsv_lora_bwd_grouped_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t 
                                  size_t workspace_bytes, void* hip_stream);
 
 /*
- * Kernel timing for benchmarks.  While enabled (on = 1), every
+ * Kernel timing: benchmark instrumentation only, not part of the layer's
+ * computation (the results of every other call are the same with it on or
+ * off).  Its state is process-global: one set of event pairs shared by every
+ * thread, stream and device of the process.  While enabled (on = 1), every
  * dsv_cobatch_fwd / dsv_lora_bwd call records a HIP event pair on its own
  * stream immediately around its matrix-core GEMM launch (forward: the base
  * GEMM with its low-rank prologue; backward: the dX GEMM; in both, when tiles

@@ -57,8 +57,15 @@ def _load():
                                       f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p, f64p,
                                       ci, i32p, f64p]
         lib.dsvo_backward.restype = ci
+        lib.dsvo_threads.argtypes = []
+        lib.dsvo_threads.restype = ci
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the reference's loops run with."""
+    return int(_load().dsvo_threads())
 
 
 def _i32(a):

@@ -11,6 +11,9 @@
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
 
 /* Segment table -> per-row adapter and the ascending list of training rows.
  * The table must tile [0,T): every row is covered exactly once (Sec. 3.2:
@@ -221,4 +224,14 @@ int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
   free(row_adapter);
   free(train_rows);
   return bad ? -1 : 0;
+}
+
+/* Threads the OpenMP loops above run with (1 without OpenMP): reported next to
+ * the reference's measured rate. */
+int dsvo_threads(void) {
+#ifdef _OPENMP
+  return omp_get_max_threads();
+#else
+  return 1;
+#endif
 }

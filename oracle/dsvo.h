@@ -79,6 +79,9 @@ int dsvo_backward(int T, int K, int N, int n_seg, const int32_t* seg,
                   const double* drop, const double* dY, double* G, double* dA, double* dB,
                   int n_dx, const int32_t* dx_rows, double* dX);
 
+/* OpenMP threads of the loops above (1 without OpenMP). */
+int dsvo_threads(void);
+
 #ifdef __cplusplus
 }
 #endif

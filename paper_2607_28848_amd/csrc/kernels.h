@@ -184,7 +184,7 @@ struct GemmGroup {
 };
 
 // Launchers (bf16).  Each returns hipSuccess or the launch error.
-// Tile shapes (tm x tn): 256x256, 256x128 or 128x128; `tiles` must be the
+// Tile shapes (tm x tn): 256x256 or 128x128; `tiles` must be the
 // plan's row-tile list of height tm.  Split tiles (sk_tiles > 0) are
 // supported for 256x256 only.
 hipError_t launch_gemm_nt(const GemmArgs& a, int tm, int tn, hipStream_t s);

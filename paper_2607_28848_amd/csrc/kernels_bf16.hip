@@ -106,9 +106,10 @@ __device__ __forceinline__ void transpose8x8(const u32x4 in[8], u32x4 out[8]) {
 }
 
 // ---------------------------------------------------------------------------
-// GEMM with a low-rank prologue.  TM x TN output tile per workgroup (256x256,
-// 256x128 or 128x128), 4 waves in a 2 x 2 grid, each wave (TM/2) x (TN/2) =
-// FM x FN tiles of v_mfma_f32_32x32x16_bf16.  K-steps of 64.
+// GEMM with a low-rank prologue.  TM x TN output tile per workgroup: 256x256
+// (8 waves in a 2 x 4 grid, each wave 128 x 64) or 128x128 (4 waves in a 2 x 2
+// grid, each 64 x 64), FM x FN tiles of v_mfma_f32_32x32x16_bf16 per wave.
+// K-steps of 64.
 //
 // Operand tiles go from global memory straight into LDS (buffer loads with
 // the LDS destination, 16 bytes per lane, one contiguous KiB per wave
@@ -1182,8 +1183,6 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
                  false, true, a);
   } else if (tm == 256 && tn == 256)
     launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>, grid, dim3(512), s, true, true, a);
-  else if (tm == 256 && tn == 128)
-    launch_timed(gemm_lora_kernel<NN, 256, 128, 4, 2, 64, 2, false>, grid, dim3(512), s, true, true, a);
   else if (tm == 128 && tn == 128)
     launch_timed(gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2, false>, grid, dim3(256), s, true, true, a);
   else

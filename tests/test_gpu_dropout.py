@@ -163,9 +163,9 @@ def test_dropout_split_tiles_ragged():
 
 @pytest.mark.timeout(600)
 def test_dropout_llama8b_full_size():
-    """The Llama-3-8B q projection (K = N = 4096) of the mixed 4096-token batch with
-    dropout 0.05 on its training rows: Y and dX on sampled rows, H_save, dA, dB in
-    full."""
+    """The Llama-3-8B q projection (K = N = 4096) of the mixed batch (6144 rows: 4096
+    inference + 2048 training) with dropout 0.05 on its training rows: Y and dX on
+    sampled rows, H_save, dA, dB in full."""
     import torch
     w = wl.llama8b_mixed()
     K = w.projections[0].K

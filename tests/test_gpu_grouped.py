@@ -139,26 +139,36 @@ def test_grouped_matches_single_calls_and_repeats():
 
 @pytest.mark.timeout(900)
 def test_grouped_llama8b_layer_set_full_size():
-    """The whole Llama-3-8B layer set (q, k, v, o, gate, up, down) of the mixed
-    4096-token batch in one grouped forward and one grouped backward: Y and dX of
-    every projection on sampled rows, H_save, dA, dB in full."""
+    """The launch the benchmark times, at full size: the whole Llama-3-8B layer set
+    (q, k, v, o, gate, up, down) of the mixed batch (T = 6144 rows: 4096 inference
+    + 2048 training) in one grouped forward and one grouped backward whose dX GEMMs
+    read the transposed frozen weights.  Y and dX of every projection on sampled
+    rows, H_save, dA, dB in full, against the fp64 reference; the backward without
+    the transposed weights is bit-identical."""
     import torch
     from paper_2607_28848_amd import dsv
     w = wl.llama8b_mixed()
-    _say("case grouped %s" % w.name)
+    _say("case grouped %s (bench launch: one call per step kind, dX on W transposed)" % w.name)
     plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
     ts, dev = [], []
     for i in range(len(w.projections)):
         t = w.tensors(i)
         ts.append(t)
         dev.append({k: to_dev(t.store[k], "bf16") for k in ("X", "W", "A", "B", "dY")})
+    wts = [d["W"].t().contiguous() for d in dev]
     out = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"]) for d in dev])
-    grads = dsv.lora_bwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"])
-                                        for i, d in enumerate(dev)])
+    bw = [(d["X"], d["W"], d["A"], d["B"], out[i][1], d["dY"]) for i, d in enumerate(dev)]
+    grads = dsv.lora_bwd_grouped(plan, bw, wts=wts)
+    plain = dsv.lora_bwd_grouped(plan, bw)
     torch.cuda.synchronize()
+    for i in range(len(dev)):
+        for a, b in zip(grads[i], plain[i]):
+            assert torch.equal(_bits(a), _bits(b))
+    del plain, wts
     tr = plan.train_rows()
     rng = np.random.default_rng(11)
     Tt = w.train_tokens
+    assert (w.n_tokens, Tt) == (6144, 2048)
     projs = list(w.projections)
     for i, proj in enumerate(projs):
         _say(" projection %s K=%d N=%d" % (proj.name, proj.K, proj.N))

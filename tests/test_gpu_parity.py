@@ -328,8 +328,9 @@ def test_llama70b_full_size(p):
 
 
 @pytest.mark.timeout(600)
-@pytest.mark.parametrize("frac", [0.0, 0.5, 1.0])
+@pytest.mark.parametrize("frac", [0.0, 0.25, 0.5, 0.75, 1.0])
 def test_load_sweep_full_size(frac):
+    """Load sweep on the 4096 x 14336 layer: 16384 tokens, training fraction 0 .. 1."""
     _sampled(wl.load_sweep(frac), 0, n_rows=12)
 
 
