@@ -169,6 +169,34 @@ int dsv_cobatch_fwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
                     void* H_save, void* workspace, size_t workspace_bytes, void* hip_stream);
 
 /*
+ * dsv_cobatch_fwd_noalloc -- dsv_cobatch_fwd for callers that cannot allocate
+ * device memory or pass a workspace: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  It calls no allocating
+ * routine (no hipMalloc / hipFree, no library allocation): its intermediates
+ * (h of every row, the fp32 low-rank terms of the gathered rows, the partial
+ * sums of a split shrink) live in a fixed scratch array in the library's own
+ * device memory, DSV_NOALLOC_SCRATCH_BYTES per device, held from the first
+ * call on a device until the process ends.  The caller still passes inputs and
+ * outputs; arguments, layouts and alignment as dsv_cobatch_fwd.
+ * A batch whose intermediates exceed the scratch (dsv_cobatch_fwd_workspace of
+ * the same plan and shape is an upper bound of what is used) returns
+ * DSV_ERR_SIZE before any launch.  The base GEMM splits no tile along the
+ * contraction (a split keeps a partial tile per piece): where
+ * dsv_cobatch_fwd splits one (dsv_gemm_config pass 0 reports split tiles), Y
+ * may differ from it in the last bit (another summation order); otherwise
+ * Y and H_save are bit-identical to dsv_cobatch_fwd.
+ * Every call on a device uses that device's one scratch array, which keeps
+ * the last call's contents (no call relies on them): calls that overlap on
+ * one device -- on different streams without ordering, or from several
+ * threads -- race on it and give wrong results.  Calls ordered on one stream
+ * are safe.
+ */
+#define DSV_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int dsv_cobatch_fwd_noalloc(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
+                            const void* X, const void* W, const void* A, const void* B, void* Y,
+                            void* H_save, void* hip_stream);
+
+/*
  * dsv_lora_bwd_workspace -- bytes of device workspace dsv_lora_bwd needs
  * (transposed copies of the small operands, g, and the fp32 partial sums of
  * the deterministic reductions over training tokens).

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdsv.so")
-SOURCES = ["plan.cpp", "api.cpp", "kernels_bf16.hip", "kernels_f32.hip", "optim.hip", "dropout.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "kernels_bf16.hip", "kernels_f32.hip", "optim.hip", "dropout.hip", "scratch.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [

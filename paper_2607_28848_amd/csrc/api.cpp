@@ -52,7 +52,7 @@ constexpr int kMinSkIters = 8;
 constexpr double kEff256 = 1.12;
 constexpr double kSplitCost64 = 0.4;
 
-GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C) {
+GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C, bool allow_split = true) {
   GemmPlan best;
   best.n_mtiles = m128;
   best.n_ntiles = (n_out + 127) / 128;
@@ -73,7 +73,7 @@ GemmPlan plan_gemm(int32_t m256, int32_t m128, int32_t n_out, int32_t C) {
   const int64_t full = t256 / cus, r = t256 % cus;
   double cost256 = (double)(full + (r > 0)) * 4.0 / kEff256;
   const int64_t split = r > 0 ? std::min<int64_t>(cus / r, nk / kMinSkIters) : 0;
-  if (split >= 2 && ((full * cus) & 7) == 0) {
+  if (allow_split && split >= 2 && ((full * cus) & 7) == 0) {
     const double cost_split =
         ((double)full + 1.0 / (double)split) * 4.0 / kEff256 + kSplitCost64 * 64.0 / (double)nk;
     if (cost_split < cost256) {
@@ -156,9 +156,9 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
   return w;
 }
 
-GemmPlan fwd_gemm_plan(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
+GemmPlan fwd_gemm_plan(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, bool allow_split = true) {
   if (dt != DSV_BF16 || p.T == 0) return GemmPlan{};
-  return plan_gemm(p.n_ftiles, p.n_ftiles128, N, K);
+  return plan_gemm(p.n_ftiles, p.n_ftiles128, N, K, allow_split);
 }
 GemmPlan bwd_gemm_plan(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N) {
   if (dt != DSV_BF16 || p.T_t == 0) return GemmPlan{};
@@ -355,9 +355,13 @@ bool dropout_spec(const dsv_dropout* d, DropoutSpec* out) {
   return true;
 }
 
+// noalloc: the allocation-free form (dsv_cobatch_fwd_noalloc): the workspace is
+// the library's device scratch, the GEMM plan splits no tile along the
+// contraction (a split needs a partial tile per piece, tens of MB), and no
+// benchmark timing events are created.
 int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
              const void* B, void* Y, void* H_save, const dsv_dropout* drop, void* workspace,
-             size_t workspace_bytes, void* hip_stream) {
+             size_t workspace_bytes, void* hip_stream, bool noalloc = false) {
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
   DropoutSpec ds{};
@@ -367,7 +371,7 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   if (p->T == 0) return DSV_OK;  // empty batch: nothing to read or write
   if (!ptr_ok(X) || !ptr_ok(W) || !ptr_ok(A) || !ptr_ok(B) || !ptr_ok(Y)) return DSV_ERR_ARG;
   if (H_save && !aligned16(H_save)) return DSV_ERR_ARG;
-  const GemmPlan gp = fwd_gemm_plan(*p, dt, K, N);
+  const GemmPlan gp = fwd_gemm_plan(*p, dt, K, N, !noalloc);
   const FwdWs ws = fwd_ws(*p, dt, K, N, gp);
   if (ws.total > 0) {
     if (!workspace || (reinterpret_cast<uintptr_t>(workspace) & 255)) return DSV_ERR_ARG;
@@ -472,7 +476,7 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   g.scales = scales;
   g.delta = delta;
   g.gslot = p->dptr(L.gslot);
-  const int tk = timing_begin(0, s);
+  const int tk = noalloc ? -1 : timing_begin(0, s);
   e = launch_gemm_nt(g, gp.tm, gp.tn, s);
   timing_end(tk, s);
   if (e != hipSuccess) return DSV_ERR_DEVICE;
@@ -693,6 +697,17 @@ extern "C" int dsv_cobatch_fwd(const dsv_plan* p, dsv_dtype dt, int32_t K, int32
                                const void* W, const void* A, const void* B, void* Y, void* H_save,
                                void* workspace, size_t workspace_bytes, void* hip_stream) {
   return fwd_impl(p, dt, K, N, X, W, A, B, Y, H_save, nullptr, workspace, workspace_bytes, hip_stream);
+}
+
+extern "C" int dsv_cobatch_fwd_noalloc(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
+                                       const void* W, const void* A, const void* B, void* Y, void* H_save,
+                                       void* hip_stream) {
+  // the device scratch replaces the workspace: its address on the current
+  // device (looked up on the device's first call), never the array's name
+  void* scratch = nullptr;
+  if (noalloc_scratch(&scratch) != hipSuccess) return DSV_ERR_DEVICE;
+  return fwd_impl(p, dt, K, N, X, W, A, B, Y, H_save, nullptr, scratch, kNoAllocScratchBytes, hip_stream,
+                  /*noalloc=*/true);
 }
 
 extern "C" int dsv_cobatch_fwd_dropout(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,

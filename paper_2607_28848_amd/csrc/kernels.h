@@ -183,6 +183,13 @@ struct GemmGroup {
   int32_t n;
 };
 
+// Device scratch of the allocation-free forward (dsv_cobatch_fwd_noalloc): a
+// file-scope array of kNoAllocScratchBytes in the library's device memory,
+// one copy per device.  noalloc_scratch() returns the current device's address
+// of it (looked up with hipGetSymbolAddress on the device's first call and kept).
+constexpr size_t kNoAllocScratchBytes = size_t(64) << 20;
+hipError_t noalloc_scratch(void** out);
+
 // Launchers (bf16).  Each returns hipSuccess or the launch error.
 // Tile shapes (tm x tn): 256x256 or 128x128; `tiles` must be the
 // plan's row-tile list of height tm.  Split tiles (sk_tiles > 0) are

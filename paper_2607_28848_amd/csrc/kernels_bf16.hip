@@ -1237,7 +1237,14 @@ hipError_t launch_skinny(const SkinnyGroup& g0, int32_t n_items, int32_t r_max, 
     if (g.a[p].pieces > 1 && (g.a[p].part == nullptr || g.a[p].part_n < 0 || g.a[p].r_max < r_max))
       return hipErrorInvalidValue;
   }
-  std::stable_sort(g.a, g.a + g.n, [](const SkinnyArgs& x, const SkinnyArgs& y) { return x.cpp > y.cpp; });
+  // stable insertion sort by chunks per piece, longest first (at most kMaxGroup
+  // entries; no temporary buffer, so the allocation-free forward stays so)
+  for (int p = 1; p < g.n; ++p) {
+    const SkinnyArgs x = g.a[p];
+    int q = p;
+    for (; q > 0 && g.a[q - 1].cpp < x.cpp; --q) g.a[q] = g.a[q - 1];
+    g.a[q] = x;
+  }
   int ny = 0;
   for (int p = 0; p < g.n; ++p)
     for (int q = 0; q < g.a[p].pieces; ++q) {

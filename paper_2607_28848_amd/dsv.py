@@ -61,6 +61,9 @@ _lib.dsv_cobatch_fwd_workspace.restype = ctypes.c_int
 _lib.dsv_cobatch_fwd.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                  _vp, _sz, _vp]
 _lib.dsv_cobatch_fwd.restype = ctypes.c_int
+_lib.dsv_cobatch_fwd_noalloc.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp]
+_lib.dsv_cobatch_fwd_noalloc.restype = ctypes.c_int
+NOALLOC_SCRATCH_BYTES = 64 << 20  # DSV_NOALLOC_SCRATCH_BYTES of include/dsv.h
 _lib.dsv_lora_bwd_workspace.argtypes = [_vp, ctypes.c_int, _i32, _i32, ctypes.POINTER(_sz)]
 _lib.dsv_lora_bwd_workspace.restype = ctypes.c_int
 _lib.dsv_lora_bwd.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp, _vp,
@@ -292,6 +295,19 @@ def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, str
                                             _ptr(Y), _ptr(H_save), ctypes.byref(d), _ptr(ws),
                                             ws.numel() * ws.element_size(), _stream_handle(stream)),
                "dsv_cobatch_fwd_dropout")
+    return Y, H_save
+
+
+def cobatch_fwd_noalloc(plan: Plan, X, W, A, B, Y, H_save=None, stream=None):
+    """dsv_cobatch_fwd_noalloc: the forward with the library's device scratch as
+    workspace (no device allocation in the call).  The caller passes the outputs:
+    Y [T][N] and, when the batch has training rows, H_save [T_t][r_max] (or None
+    to keep nothing).  Returns (Y, H_save)."""
+    dt = _dtype_code(X)
+    K = X.shape[1]
+    N = W.shape[0]
+    _check(_lib.dsv_cobatch_fwd_noalloc(plan.handle, dt, K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y),
+                                        _ptr(H_save), _stream_handle(stream)), "dsv_cobatch_fwd_noalloc")
     return Y, H_save
 
 
