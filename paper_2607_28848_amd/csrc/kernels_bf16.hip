@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "kernels.h"
 #include "plan.h"
@@ -639,6 +640,401 @@ __global__ __launch_bounds__(512) void gemm_group_kernel(GemmGroup G) {
 }
 
 // ---------------------------------------------------------------------------
+// GEMM, 16x16x32 form of the 256 x 256 tile (NT: Q is [Nout][C]): 4 waves in a
+// 2 x 2 grid, one per SIMD, each wave 128 x 128 = 8 x 8 blocks of
+// v_mfma_f32_16x16x32_bf16 with its 256 fp32 accumulators.  Against the 8-wave
+// 32x32x16 tile this reads a third fewer LDS bytes per MFMA (a wave's 16
+// fragments feed 64 MFMAs per 32-wide step) and keeps every per-lane address
+// in registers, so the main loop issues no address arithmetic: fragment reads
+// are a base register plus an immediate, operand loads a base register plus a
+// scalar offset.  Same LDS image (K-contiguous rows, chunk c of row r in slot
+// c ^ swz(r)), direct-to-LDS loads, two-stage pipeline, low-rank prologue
+// semantics and single-rounding epilogue as gemm_piece.
+//
+// Accumulator layout (weight fragment as the first MFMA operand): acc[i][j][v]
+// is output row wm*128 + 16i + lane%16, column wn*128 + 16j + 4(lane/16) + v.
+// ---------------------------------------------------------------------------
+typedef short s16x4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+
+// Four bf16 values p[e * stride], e < n_valid (1 <= n_valid), the rest zero;
+// straight-line loads from clamped addresses.
+__device__ __forceinline__ u32x2v ld4_sel(const uint16_t* p, int64_t stride, int n_valid) {
+  uint32_t w[2] = {0u, 0u};
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const uint32_t x = (uint32_t)p[(int64_t)min(e, n_valid - 1) * stride];
+    w[e >> 1] |= (e < n_valid ? x : 0u) << (16 * (e & 1));
+  }
+  return u32x2v{w[0], w[1]};
+}
+
+// Issue order of the instructions before it in its block: NV pairs (MFMA,
+// vector-memory read), then ND pairs (MFMA, LDS read), then the other MFMAs.
+template <int NV, int ND, int NM>
+__device__ __forceinline__ void sched_interleave() {
+#pragma unroll
+  for (int q = 0; q < NV; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+  }
+#pragma unroll
+  for (int q = 0; q < ND; ++q) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, NM - NV - ND, 0);
+}
+
+template <bool SK>
+__device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int tid, int lin, int t_sk, int piece,
+                                             int kb, int ke, int nk) {
+  constexpr int TM = 256, TN = 256, TK = 64, NW = 4, WM = 128, WN = 128, FM = 8, FN = 8;
+  constexpr int ROWB = TK * 2;                   // bytes per LDS row
+  constexpr int A_BYTES = TM * ROWB, STAGE = A_BYTES + TN * ROWB;
+  constexpr int LOADS = TM * ROWB / 1024 / 4;    // 1 KiB direct loads per wave per operand
+  static_assert(LOADS == 8 && TN == TM, "load split");
+  const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  int mt, nt;
+  tile_coords(g, lin, mt, nt);
+  const int32_t* td = g.tiles + (int64_t)mt * kTileWords;
+  const int m0 = td[0], ngroups = td[1], has_gather = td[2], nrows = td[3];
+  const int n0 = nt * TN;
+  // Both operands are contraction-contiguous rows of the same length (the
+  // launcher checks ldp == ldq), so one set of lane offsets serves both.
+  const int ld = (int)g.ldp;
+  const int64_t a_rows = min((int64_t)TM, (int64_t)g.M - m0);
+  const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
+  // Descriptors over the tile's row panels (rows past the operand read zeros);
+  // a K-step adds 2 k0 bytes to the scalar offset.  A panel is at most 256
+  // rows of 2^20 elements, so every offset fits in 32 bits.
+  const i32x4 ra = make_rsrc(g.P + (int64_t)m0 * ld, (uint64_t)a_rows * ld * 2);
+  const i32x4 rb = make_rsrc(g.Q + (int64_t)n0 * ld, (uint64_t)b_cols * ld * 2);
+
+  // Operand loads: load i of a wave fills LDS rows 8q .. 8q+7 (q = 8 wave + i),
+  // lane ln taking row 8q + ln/8, logical chunk (ln%8) ^ swz(row), which is
+  // (ln%8) ^ (ln/8) ^ i.  The lane parts of the offsets stay in registers; the
+  // row block and the K-step go in the scalar offset.
+  const int lr = lane >> 3;
+  int voff[LOADS];
+#pragma unroll
+  for (int i = 0; i < LOADS; ++i) voff[i] = ((((lane & 7) ^ lr ^ i) << 4)) + lr * ld * 2;
+  // whole K-step kt into `stage` (k0 + TK <= C)
+  auto issue_whole = [&](int kt, int stage) {
+    const int kbytes = kt * TK * 2;
+    char* sa = smem + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int q = wave * LOADS + i;
+      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, voff[i],
+                                      __builtin_amdgcn_readfirstlane(q * 16 * ld + kbytes), 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int q = wave * LOADS + i;
+      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voff[i],
+                                      __builtin_amdgcn_readfirstlane(q * 16 * ld + kbytes), 0, 0);
+    }
+  };
+  // any K-step: chunks past the contraction read nothing (zeros)
+  auto issue = [&](int kt, int stage) {
+    const int k0 = kt * TK;
+    if (k0 + TK <= g.C) {
+      issue_whole(kt, stage);
+      return;
+    }
+    char* sa = smem + stage * STAGE;
+#pragma unroll
+    for (int i = 0; i < LOADS; ++i) {
+      const int q = wave * LOADS + i;
+      const int row = 8 * q + lr;
+      const int c = (lane & 7) ^ swz<TK>(row);
+      const int vo = (k0 + 8 * c < g.C) ? (row * ld + k0 + 8 * c) * 2 : (int)0x7FFFFFF0;
+      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
+      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, vo, 0, 0, 0);
+    }
+  };
+
+#pragma unroll
+  for (int p = 0; p < 2; ++p)
+    if (kb + p < ke) issue(kb + p, p);
+
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // ---- low-rank prologue (the piece that starts the tile's K range) -----
+  // acc += (s_a h) B_a for the rows of each group, with 16x16x16 MFMAs over
+  // steps of 16 ranks (a lane holds 4 ranks of one row / column); s_a h is
+  // split into bf16 hi + lo as in gemm_piece.
+  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
+    const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
+    if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
+    const int r = g.ranks[a];
+    const float sc = g.scales ? g.scales[a] : 1.f;
+    const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
+    const bool full16 = (r & 15) == 0;
+    const bool lq_vec = full16 && g.lq_j == 1 && (g.lq_col & 3) == 0;
+    for (int j0 = 0; j0 < r; j0 += 16) {
+      const int jb = j0 + 4 * (lane >> 4);
+      const int nv = min(4, r - jb);
+      const int jbc = nv > 0 ? jb : 0, nvc = max(nv, 1);
+      s16x4v af_hi[FM], af_lo[FM], bq[FN];
+      bool any_lo = false;
+#pragma unroll
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * WM + 16 * i + (lane & 15);
+        const bool rin = row >= lo && row < hi && nv > 0;
+        const uint16_t* p = g.Lp + (int64_t)(m0 + (rin ? row : lo)) * g.ldl + jbc;
+        u32x2v v = full16 ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, 1, nvc);
+        v = rin ? v : u32x2v{0u, 0u};
+        uint32_t wh[2], wl[2];
+#pragma unroll
+        for (int d = 0; d < 2; ++d) {
+          const float x0 = sc * __uint_as_float(v[d] << 16);
+          const float x1 = sc * __uint_as_float(v[d] & 0xffff0000u);
+          const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+          const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+          wh[d] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+          wl[d] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+          any_lo |= (wl[d] & 0x7fff7fffu) != 0u;
+        }
+        af_hi[i] = __builtin_bit_cast(s16x4v, u32x2v{wh[0], wh[1]});
+        af_lo[i] = __builtin_bit_cast(s16x4v, u32x2v{wl[0], wl[1]});
+      }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + wn * WN + 16 * j + (lane & 15);
+        const bool cin = col < g.Nout && nv > 0;
+        const uint16_t* p = lq + (int64_t)jbc * g.lq_j + (int64_t)min(col, g.Nout - 1) * g.lq_col;
+        u32x2v v = lq_vec ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, g.lq_j, nvc);
+        bq[j] = __builtin_bit_cast(s16x4v, cin ? v : u32x2v{0u, 0u});
+      }
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_hi[i], acc[i][j], 0, 0, 0);
+      if (__builtin_amdgcn_ballot_w64(any_lo) != 0) {
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_lo[i], acc[i][j], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- dropout of the low-rank term (dX under LoRA dropout) --------------
+  // A 16-column block lies inside one 32-column mask word.
+  if (kb == 0 && g.keep != nullptr) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 16 * i + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int c0 = n0 + wn * WN + 16 * j;
+        const int wd = c0 >> 5;
+        const uint32_t x = g.keep[(int64_t)(m0 + min(row, nrows - 1)) * g.keep_words + min(wd, g.keep_words - 1)];
+        const uint32_t mw = x & (0u - (uint32_t)(row < nrows && wd < g.keep_words));
+        const int bit = (c0 & 31) + 4 * (lane >> 4);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[i][j][v] = ((mw >> (bit + v)) & 1u) ? acc[i][j][v] * g.keep_scale : 0.f;
+      }
+    }
+  }
+
+  // ---- main loop ----------------------------------------------------------
+  // Fragment (i, 32-wide step s) of the A tile: row R + lane%16 with R =
+  // wm*128 + 16i, logical chunk 4s + lane/16.  With row%8 = lane%8 and
+  // (row/8)%8 = (2i + lane/8%2)%8 the slot is lanepart ^ (4s ^ 2i%8), so a
+  // fragment is at one of four lane offsets, picked by the constant
+  // 4s ^ 2i%8, plus the immediate R*128.  The B tile is the same with wn, j.
+  const int l15 = lane & 15;
+  const int lanepart = (lane >> 4) ^ (l15 & 7) ^ (l15 >> 3);
+  int off_a[4], off_b[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    off_a[c] = (wm * WM + l15) * ROWB + 16 * (lanepart ^ (2 * c));
+    off_b[c] = A_BYTES + (wn * WN + l15) * ROWB + 16 * (lanepart ^ (2 * c));
+  }
+  auto rd_a = [&](const char* st, int s, int i) {
+    return as_bf(*reinterpret_cast<const u32x4*>(st + off_a[((2 * s) ^ i) & 3] + 16 * i * ROWB));
+  };
+  auto rd_b = [&](const char* st, int s, int j) {
+    return as_bf(*reinterpret_cast<const u32x4*>(st + off_b[((2 * s) ^ j) & 3] + 16 * j * ROWB));
+  };
+
+  // Fragments: two A sets (the current step's and the next one's) and one B
+  // set whose fragment j is replaced by the next step's once the 8 MFMAs of
+  // column block j have been issued.
+  bf16x8 fa0[FM], fa1[FM], fb[FN];
+  if (ke - kb >= 2) __builtin_amdgcn_s_waitcnt(vmcnt_imm(2 * LOADS));  // first K-step landed
+  else vmem_wait_all();
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < FN; ++j) fb[j] = rd_b(smem, 0, j);
+#pragma unroll
+  for (int i = 0; i < FM; ++i) fa0[i] = rd_a(smem, 0, i);
+
+  // Direct loads of whole K-step kl into buffer ls: load n of the wave's 16
+  // (A for n < 8, B after).  A texture unit takes a 1 KiB load in about 16
+  // cycles, so the 64 loads a K-step needs per CU are spread evenly, two per
+  // wave per column block (a block's 8 MFMAs take 128 cycles), over the
+  // second step, after the barrier that frees their buffer.
+  auto load_n = [&](int kl, int ls, int n) {
+    const int i = n & 7;
+    const int q = wave * LOADS + i;
+    llvm_amdgcn_raw_buffer_load_lds(n < 8 ? ra : rb, (lds_u32*)(smem + ls * STAGE + (n < 8 ? 0 : A_BYTES) + q * 1024),
+                                    16, voff[i], __builtin_amdgcn_readfirstlane(q * 16 * ld + kl * TK * 2), 0, 0);
+  };
+  // One 32-wide step with fragments (cur, fb); reads the next step's
+  // fragments (nxt, fb) from buffer `st_next` step s_next, in the order fixed
+  // by scheduling fences, per column block j: its 8 MFMAs, then (when `load`)
+  // loads 2j, 2j+1 of whole K-step kl into buffer ls, then the next B
+  // fragment j (replacing fb[j] once block j's MFMAs are issued) and A
+  // fragments 2j, 2j+1 (blocks 0-3).
+  auto step = [&](bf16x8 (&cur)[FM], bf16x8 (&nxt)[FM], const char* st_next, int s_next, bool load, int kl,
+                  int ls) {
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], cur[i], acc[i][j], 0, 0, 0);
+      if (load) {
+        load_n(kl, ls, 2 * j);
+        load_n(kl, ls, 2 * j + 1);
+      }
+      if (j < 4) {
+        nxt[2 * j] = rd_a(st_next, s_next, 2 * j);
+        nxt[2 * j + 1] = rd_a(st_next, s_next, 2 * j + 1);
+      }
+      fb[j] = rd_b(st_next, s_next, j);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // K-step kt in buffer `stage` with K-step kt+1 to follow: first step, then
+  // the barrier that publishes kt+1 (every wave's loads of it were issued
+  // during the previous K-step's second step) and frees buffer `stage`, then
+  // the second step, which reads kt+1's first fragments and loads whole
+  // K-step kt+2 into buffer `stage` (when `load`).
+  auto kstep = [&](int kt, int stage, bool load) {
+    step(fa0, fa1, smem + stage * STAGE, 1, false, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    vmem_wait_all();  // kt+1 landed (its loads are the only ones in flight)
+    __syncthreads();  // everyone's part of kt+1 is in; buffer `stage` is free
+    __builtin_amdgcn_sched_barrier(0);
+    if (!load && kt + 2 < ke) issue(kt + 2, stage);  // a partial last K-step
+    step(fa1, fa0, smem + (stage ^ 1) * STAGE, 0, load, kt + 2, stage);
+  };
+  int kt = kb, stage = 0;
+  const int main_end = min(ke, g.C / TK) - 2;  // kt < main_end: kt+2 is whole and below ke
+  for (; kt < main_end; ++kt, stage ^= 1) kstep(kt, stage, true);
+  for (; kt + 1 < ke; ++kt, stage ^= 1) kstep(kt, stage, false);
+  // the last K-step: no successor to read
+  step(fa0, fa1, smem + stage * STAGE, 1, false, 0, 0);
+#pragma unroll
+  for (int j = 0; j < FN; ++j)
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fb[j], fa1[i], acc[i][j], 0, 0, 0);
+  const int last_stage = stage;
+
+  // ---- a piece of a split tile: its fp32 partial goes to its slot --------
+  if (SK && !(kb == 0 && ke == nk)) {
+    float* part = g.sk_part + (int64_t)(t_sk * g.sk_split + piece) * (TM * TN);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 16 * i + l15;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = wn * WN + 16 * j + 4 * (lane >> 4);
+        *reinterpret_cast<f32x4*>(part + row * TN + col) = acc[i][j];
+      }
+    }
+    return;
+  }
+
+  // ---- epilogue: one rounding, staged through LDS for 16-byte stores ----
+  // Each wave stages its rows 32 at a time (fragment rows i = 2t, 2t+1) in its
+  // own slice of the buffer the last K-step did not use; a lane writes 4
+  // columns (8 bytes) of a row, then the wave reads the slice back as
+  // 16-byte row chunks and stores 256-byte row segments.  Slice row stride
+  // 272 bytes (68 dwords): the 8-byte writes of 16 rows x 2 column groups of
+  // one half-wave fall on distinct banks.
+  constexpr int SRS = WN * 2 + 16;
+  static_assert(NW * 32 * SRS <= STAGE, "epilogue slices fit the idle pipeline buffer");
+  char* slice = smem + (last_stage ^ 1) * STAGE + wave * 32 * SRS;
+  const bool gathered = has_gather && g.delta != nullptr;
+#pragma unroll
+  for (int t = 0; t < FM / 2; ++t) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const int i = 2 * t + h;
+      const int row = wm * WM + 16 * i + l15;
+      const int gs = (gathered && row < nrows) ? g.gslot[m0 + row] : -1;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = wn * WN + 16 * j + 4 * (lane >> 4);
+        f32x4 x = acc[i][j];
+        if (gathered) {
+          const f32x4 d = *reinterpret_cast<const f32x4*>(g.delta + (int64_t)max(gs, 0) * g.Nout +
+                                                          min(n0 + col, g.Nout - 4));
+          x += (gs >= 0 && n0 + col < g.Nout) ? d : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+        const uint32_t w0 = f2bf2(x[0], x[1]), w1 = f2bf2(x[2], x[3]);
+        *reinterpret_cast<uint2*>(slice + (16 * h + l15) * SRS + 2 * (col - wn * WN)) = make_uint2(w0, w1);
+      }
+    }
+    asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: the slice is complete
+    constexpr int CPR = WN / 8;     // 16-byte chunks per slice row
+#pragma unroll
+    for (int q = 0; q < 32 * CPR / 64; ++q) {
+      const int id = 64 * q + lane;
+      const int rr = id / CPR, ch = id % CPR;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(slice + rr * SRS + 16 * ch);
+      const int orow = wm * WM + 32 * t + rr, ocol = n0 + wn * WN + 8 * ch;
+      if (orow < nrows && ocol < g.Nout)
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + orow) * g.ldo + ocol));
+    }
+    asm volatile("" ::: "memory");  // the slice is read before the next rows overwrite it
+  }
+}
+
+template <bool SK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_kernel(GemmArgs g) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * 256 * 64 * 2];
+  const int nk = (g.C + 63) / 64;
+  int lin, t_sk = -1, piece = 0, kb = 0, ke = nk;
+  if (!SK || (int)blockIdx.x < g.dp_tiles) {
+    lin = xcd_major(blockIdx.x, SK ? g.dp_tiles : gridDim.x);
+  } else {
+    const int q = xcd_major(blockIdx.x - g.dp_tiles, gridDim.x - g.dp_tiles);
+    piece = q / g.sk_tiles;
+    t_sk = q - piece * g.sk_tiles;
+    lin = g.dp_tiles + t_sk;
+    kb = (int)(((int64_t)piece * nk) / g.sk_split);
+    ke = (int)(((int64_t)(piece + 1) * nk) / g.sk_split);
+  }
+  gemm_piece16<SK>(g, smem, threadIdx.x, lin, t_sk, piece, kb, ke, nk);
+}
+
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_group_kernel(GemmGroup G) {
+  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * 256 * 64 * 2];
+  int pj = 0;
+  while (pj + 1 < G.n && (int)blockIdx.x >= G.off[pj + 1]) ++pj;
+  const GemmArgs g = G.a[pj];
+  const int local = (int)blockIdx.x - G.off[pj];
+  const int lin = xcd_major(local, G.off[pj + 1] - G.off[pj]);
+  const int nk = (g.C + 63) / 64;
+  gemm_piece16<false>(g, smem, threadIdx.x, lin, -1, 0, 0, nk, nk);
+}
+
+// ---------------------------------------------------------------------------
 // Split tiles: sum the fp32 partials of a tile's pieces in K order, add the
 // gathered rows' term, round once to bf16 and store -- the GEMM epilogue for
 // the tiles the GEMM left in pieces.  Elementwise: one thread per 4 columns
@@ -1175,15 +1571,38 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
       return hipErrorInvalidValue;
   }
   const dim3 grid((unsigned)(a.dp_tiles + (int64_t)a.sk_tiles * (a.sk_tiles > 0 ? a.sk_split : 0)));
-  if (tm == 256 && tn == 256 && a.sk_tiles > 0) {
-    launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>, grid, dim3(512), s, true, false, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)), dim3(256), s,
-                 false, true, a);
-  } else if (tm == 256 && tn == 256)
-    launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>, grid, dim3(512), s, true, true, a);
-  else if (tm == 128 && tn == 128)
+  if constexpr (!NN) {
+    // 256 x 256 NT tiles: the 16x16x32 form (both operands rows of the
+    // contraction, one row length)
+    if (tm == 256 && tn == 256) {
+      if (a.ldp != a.ldq) return hipErrorInvalidValue;
+      if (a.sk_tiles > 0) {
+        launch_timed(gemm16_kernel<true>, grid, dim3(256), s, true, false, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)), dim3(256),
+                     s, false, true, a);
+      } else {
+        launch_timed(gemm16_kernel<false>, grid, dim3(256), s, true, true, a);
+      }
+      return hipGetLastError();
+    }
+  }
+  if constexpr (NN) {  // 256 x 256 NN tiles (dX reading W transposed in LDS)
+    if (tm == 256 && tn == 256) {
+      if (a.sk_tiles > 0) {
+        launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>, grid, dim3(512), s, true, false, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)),
+                     dim3(256), s, false, true, a);
+      } else {
+        launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, false>, grid, dim3(512), s, true, true, a);
+      }
+      return hipGetLastError();
+    }
+  }
+  if (tm == 128 && tn == 128)
     launch_timed(gemm_lora_kernel<NN, 128, 128, 2, 2, 64, 2, false>, grid, dim3(256), s, true, true, a);
   else
     return hipErrorInvalidValue;
@@ -1279,7 +1698,13 @@ hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
     if (g.off[p + 1] - g.off[p] != a.n_mtiles * a.n_ntiles || a.sk_tiles != 0) return hipErrorInvalidValue;
   }
   if (g.off[g.n] <= 0) return hipSuccess;
-  launch_timed(gemm_group_kernel<NN>, dim3((unsigned)g.off[g.n]), dim3(512), s, true, true, g);
+  if constexpr (!NN) {
+    for (int p = 0; p < g.n; ++p)
+      if (g.a[p].ldp != g.a[p].ldq) return hipErrorInvalidValue;
+    launch_timed(gemm16_group_kernel, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+  } else {
+    launch_timed(gemm_group_kernel<NN>, dim3((unsigned)g.off[g.n]), dim3(512), s, true, true, g);
+  }
   return hipGetLastError();
 }
 }  // namespace
