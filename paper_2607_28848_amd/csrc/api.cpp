@@ -465,6 +465,7 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   g.Nout = N;
   g.C = K;
   g.tiles = p->dptr(gp.tm == 256 ? L.fwd_tiles : L.fwd_tiles128);
+  g.uniform_rows = gp.tm == 256;
   set_split(g, gp, workspace, ws.sk_part);
   g.Lp = h_all;
   g.ldl = ldh;
@@ -669,6 +670,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     g.Nout = K;
     g.C = N;
     g.tiles = p->dptr(gp.tm == 256 ? L.bwd_tiles : L.bwd_tiles128);
+    g.uniform_rows = gp.tm == 256 && p->btiles_uniform;
     set_split(g, gp, workspace, ws.sk_part);
     g.Lp = gm;
     g.ldl = ldh;
@@ -959,6 +961,7 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     g.Nout = q.N;
     g.C = q.K;
     g.tiles = p->dptr(L.fwd_tiles);
+    g.uniform_rows = 1;
     set_split(g, whole256(p->n_ftiles, q.N), nullptr, 0);
     g.Lp = sg.a[i].out1;
     g.ldl = ldh;
@@ -1170,6 +1173,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
       g.Nout = q.K;
       g.C = q.N;
       g.tiles = p->dptr(L.bwd_tiles);
+      g.uniform_rows = p->btiles_uniform;
       set_split(g, whole256(p->n_btiles, q.K), nullptr, 0);
       g.Lp = gm[i];
       g.ldl = ldh;

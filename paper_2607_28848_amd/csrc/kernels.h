@@ -24,6 +24,7 @@ struct GemmArgs {
   int32_t M;             // rows of P (bounds of the operand loads)
   int32_t Nout, C;
   const int32_t* tiles;  // row tiles, kTileWords words each
+  int32_t uniform_rows;  // 256-row tile mt is rows [256 mt, min(M, 256 mt + 256)): no descriptor read needed
   int32_t n_mtiles, n_ntiles;
   const uint16_t* Lp;
   int64_t ldl;

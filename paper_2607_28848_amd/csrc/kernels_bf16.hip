@@ -686,7 +686,9 @@ __device__ __forceinline__ void sched_interleave() {
   __builtin_amdgcn_sched_group_barrier(0x008, NM - NV - ND, 0);
 }
 
-template <bool SK>
+// DROP: the instantiation that masks the low-rank term (dX under LoRA
+// dropout); the others carry no masking code.
+template <bool SK, bool DROP>
 __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int tid, int lin, int t_sk, int piece,
                                              int kb, int ke, int nk) {
   constexpr int TM = 256, TN = 256, TK = 64, NW = 4, WM = 128, WN = 128, FM = 8, FN = 8;
@@ -700,8 +702,18 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   int mt, nt;
   tile_coords(g, lin, mt, nt);
   const int32_t* td = g.tiles + (int64_t)mt * kTileWords;
-  const int m0 = td[0], ngroups = td[1], has_gather = td[2], nrows = td[3];
+  // uniform rows: the first loads need not wait for the tile descriptor
+  const int m0 = g.uniform_rows ? mt * TM : td[0];
+  const int nrows = g.uniform_rows ? min(TM, g.M - m0) : td[3];
   const int n0 = nt * TN;
+  // Everything the first low-rank group needs is read here, before the first
+  // direct load: past those loads a read of kernel-visible memory can no
+  // longer be a scalar load, and a vector load would wait for every load
+  // issued before it (vector-memory operations complete in order).
+  const int ngroups = td[1], has_gather = td[2];
+  const int g0_a = td[4], g0_lo = td[5], g0_hi = td[6];  // zeros when the tile has no group
+  const int g0_r = g.ranks[g0_a];
+  const float g0_sc = g.scales ? g.scales[g0_a] : 1.f;
   // Both operands are contraction-contiguous rows of the same length (the
   // launcher checks ldp == ldq), so one set of lane offsets serves both.
   const int ld = (int)g.ldp;
@@ -757,9 +769,33 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
     }
   };
 
+  issue(kb, 0);
+
+  // The first group's first 16 ranks are loaded between the first two
+  // K-steps, so the wait for them is the wait for the first K-step alone
+  // (vector-memory operations complete in order) rather than for both.  This
+  // covers the forward form (h and B rows with contiguous ranks, r a multiple
+  // of 16) for a wave that has rows in the group; anything else loads below.
+  const bool pre = kb == 0 && ngroups > 0 && g.lq_j == 1 && (g.lq_col & 3) == 0 && (g0_r & 15) == 0 &&
+                   g0_hi > wm * WM && g0_lo < wm * WM + WM;
+  u32x2v pre_h[FM], pre_b[FN];
+  if (pre) {
+    const int a = g0_a, lo = g0_lo, hi = g0_hi;
+    const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
+    const int jb = 4 * (lane >> 4);
 #pragma unroll
-  for (int p = 0; p < 2; ++p)
-    if (kb + p < ke) issue(kb + p, p);
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 16 * i + (lane & 15);
+      const int rr = (row >= lo && row < hi) ? row : lo;
+      pre_h[i] = *reinterpret_cast<const u32x2v*>(g.Lp + (int64_t)(m0 + rr) * g.ldl + jb);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int col = n0 + wn * WN + 16 * j + (lane & 15);
+      pre_b[j] = *reinterpret_cast<const u32x2v*>(lq + jb + (int64_t)min(col, g.Nout - 1) * g.lq_col);
+    }
+  }
+  if (kb + 1 < ke) issue(kb + 1, 1);
 
   f32x4 acc[FM][FN];
 #pragma unroll
@@ -771,67 +807,82 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   // acc += (s_a h) B_a for the rows of each group, with 16x16x16 MFMAs over
   // steps of 16 ranks (a lane holds 4 ranks of one row / column); s_a h is
   // split into bf16 hi + lo as in gemm_piece.
-  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
-    const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
-    if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
-    const int r = g.ranks[a];
-    const float sc = g.scales ? g.scales[a] : 1.f;
-    const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
-    const bool full16 = (r & 15) == 0;
-    const bool lq_vec = full16 && g.lq_j == 1 && (g.lq_col & 3) == 0;
-    for (int j0 = 0; j0 < r; j0 += 16) {
-      const int jb = j0 + 4 * (lane >> 4);
-      const int nv = min(4, r - jb);
-      const int jbc = nv > 0 ? jb : 0, nvc = max(nv, 1);
-      s16x4v af_hi[FM], af_lo[FM], bq[FN];
-      bool any_lo = false;
+  auto lr_mfma = [&](const u32x2v (&hv)[FM], const u32x2v (&bv)[FN], int lo, int hi, int nv, float sc) {
+    s16x4v af_hi[FM], af_lo[FM], bq[FN];
+    bool any_lo = false;
 #pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int row = wm * WM + 16 * i + (lane & 15);
-        const bool rin = row >= lo && row < hi && nv > 0;
-        const uint16_t* p = g.Lp + (int64_t)(m0 + (rin ? row : lo)) * g.ldl + jbc;
-        u32x2v v = full16 ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, 1, nvc);
-        v = rin ? v : u32x2v{0u, 0u};
-        uint32_t wh[2], wl[2];
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 16 * i + (lane & 15);
+      const bool rin = row >= lo && row < hi && nv > 0;
+      const u32x2v v = rin ? hv[i] : u32x2v{0u, 0u};
+      uint32_t wh[2], wl[2];
 #pragma unroll
-        for (int d = 0; d < 2; ++d) {
-          const float x0 = sc * __uint_as_float(v[d] << 16);
-          const float x1 = sc * __uint_as_float(v[d] & 0xffff0000u);
-          const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
-          const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
-          wh[d] = (uint32_t)h0 | ((uint32_t)h1 << 16);
-          wl[d] = (uint32_t)l0 | ((uint32_t)l1 << 16);
-          any_lo |= (wl[d] & 0x7fff7fffu) != 0u;
-        }
-        af_hi[i] = __builtin_bit_cast(s16x4v, u32x2v{wh[0], wh[1]});
-        af_lo[i] = __builtin_bit_cast(s16x4v, u32x2v{wl[0], wl[1]});
+      for (int d = 0; d < 2; ++d) {
+        const float x0 = sc * __uint_as_float(v[d] << 16);
+        const float x1 = sc * __uint_as_float(v[d] & 0xffff0000u);
+        const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+        const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+        wh[d] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        wl[d] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        any_lo |= (wl[d] & 0x7fff7fffu) != 0u;
       }
+      af_hi[i] = __builtin_bit_cast(s16x4v, u32x2v{wh[0], wh[1]});
+      af_lo[i] = __builtin_bit_cast(s16x4v, u32x2v{wl[0], wl[1]});
+    }
 #pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = n0 + wn * WN + 16 * j + (lane & 15);
-        const bool cin = col < g.Nout && nv > 0;
-        const uint16_t* p = lq + (int64_t)jbc * g.lq_j + (int64_t)min(col, g.Nout - 1) * g.lq_col;
-        u32x2v v = lq_vec ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, g.lq_j, nvc);
-        bq[j] = __builtin_bit_cast(s16x4v, cin ? v : u32x2v{0u, 0u});
-      }
+    for (int j = 0; j < FN; ++j) {
+      const int col = n0 + wn * WN + 16 * j + (lane & 15);
+      bq[j] = __builtin_bit_cast(s16x4v, (col < g.Nout && nv > 0) ? bv[j] : u32x2v{0u, 0u});
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_hi[i], acc[i][j], 0, 0, 0);
+    if (__builtin_amdgcn_ballot_w64(any_lo) != 0) {
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_hi[i], acc[i][j], 0, 0, 0);
-      if (__builtin_amdgcn_ballot_w64(any_lo) != 0) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_lo[i], acc[i][j], 0, 0, 0);
+    }
+  };
+  // the prefetched step: its data arrive with the first K-step
+  if (pre) lr_mfma(pre_h, pre_b, g0_lo, g0_hi, 4, g0_sc);
+  // every other (group, 16-rank step) of the tile
+  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
+    const int a = gi == 0 ? g0_a : td[4 + 3 * gi], lo = gi == 0 ? g0_lo : td[5 + 3 * gi];
+    const int hi = gi == 0 ? g0_hi : td[6 + 3 * gi];
+    if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
+    const int r = gi == 0 ? g0_r : g.ranks[a];
+    const float sc = gi == 0 ? g0_sc : (g.scales ? g.scales[a] : 1.f);
+    const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
+    const bool full16 = (r & 15) == 0;
+    const bool lq_vec = full16 && g.lq_j == 1 && (g.lq_col & 3) == 0;
+    for (int j0 = (gi == 0 && pre) ? 16 : 0; j0 < r; j0 += 16) {
+      const int jb = j0 + 4 * (lane >> 4);
+      const int nv = min(4, r - jb);
+      const int jbc = nv > 0 ? jb : 0, nvc = max(nv, 1);
+      u32x2v hv[FM], bv[FN];
 #pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_lo[i], acc[i][j], 0, 0, 0);
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * WM + 16 * i + (lane & 15);
+        const uint16_t* p = g.Lp + (int64_t)(m0 + ((row >= lo && row < hi) ? row : lo)) * g.ldl + jbc;
+        hv[i] = full16 ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, 1, nvc);
       }
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + wn * WN + 16 * j + (lane & 15);
+        const uint16_t* p = lq + (int64_t)jbc * g.lq_j + (int64_t)min(col, g.Nout - 1) * g.lq_col;
+        bv[j] = lq_vec ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, g.lq_j, nvc);
+      }
+      lr_mfma(hv, bv, lo, hi, nv, sc);
     }
   }
 
   // ---- dropout of the low-rank term (dX under LoRA dropout) --------------
   // A 16-column block lies inside one 32-column mask word.
-  if (kb == 0 && g.keep != nullptr) {
+  if (DROP && kb == 0 && g.keep != nullptr) {
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       const int row = wm * WM + 16 * i + (lane & 15);
@@ -1005,7 +1056,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   }
 }
 
-template <bool SK>
+template <bool SK, bool DROP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_kernel(GemmArgs g) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * 256 * 64 * 2];
   const int nk = (g.C + 63) / 64;
@@ -1020,9 +1071,10 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     kb = (int)(((int64_t)piece * nk) / g.sk_split);
     ke = (int)(((int64_t)(piece + 1) * nk) / g.sk_split);
   }
-  gemm_piece16<SK>(g, smem, threadIdx.x, lin, t_sk, piece, kb, ke, nk);
+  gemm_piece16<SK, DROP>(g, smem, threadIdx.x, lin, t_sk, piece, kb, ke, nk);
 }
 
+template <bool DROP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_group_kernel(GemmGroup G) {
   __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * 256 * 64 * 2];
   int pj = 0;
@@ -1031,7 +1083,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   const int local = (int)blockIdx.x - G.off[pj];
   const int lin = xcd_major(local, G.off[pj + 1] - G.off[pj]);
   const int nk = (g.C + 63) / 64;
-  gemm_piece16<false>(g, smem, threadIdx.x, lin, -1, 0, 0, nk, nk);
+  gemm_piece16<false, DROP>(g, smem, threadIdx.x, lin, -1, 0, 0, nk, nk);
 }
 
 // ---------------------------------------------------------------------------
@@ -1576,14 +1628,18 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
     // contraction, one row length)
     if (tm == 256 && tn == 256) {
       if (a.ldp != a.ldq) return hipErrorInvalidValue;
+      const bool drop = a.keep != nullptr;
       if (a.sk_tiles > 0) {
-        launch_timed(gemm16_kernel<true>, grid, dim3(256), s, true, false, a);
+        if (drop) launch_timed(gemm16_kernel<true, true>, grid, dim3(256), s, true, false, a);
+        else launch_timed(gemm16_kernel<true, false>, grid, dim3(256), s, true, false, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)), dim3(256),
                      s, false, true, a);
+      } else if (drop) {
+        launch_timed(gemm16_kernel<false, true>, grid, dim3(256), s, true, true, a);
       } else {
-        launch_timed(gemm16_kernel<false>, grid, dim3(256), s, true, true, a);
+        launch_timed(gemm16_kernel<false, false>, grid, dim3(256), s, true, true, a);
       }
       return hipGetLastError();
     }
@@ -1701,7 +1757,10 @@ hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
   if constexpr (!NN) {
     for (int p = 0; p < g.n; ++p)
       if (g.a[p].ldp != g.a[p].ldq) return hipErrorInvalidValue;
-    launch_timed(gemm16_group_kernel, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+    bool drop = false;
+    for (int p = 0; p < g.n; ++p) drop = drop || g.a[p].keep != nullptr;
+    if (drop) launch_timed(gemm16_group_kernel<true>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+    else launch_timed(gemm16_group_kernel<false>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
   } else {
     launch_timed(gemm_group_kernel<NN>, dim3((unsigned)g.off[g.n]), dim3(512), s, true, true, g);
   }

@@ -219,6 +219,11 @@ int build(const dsv_segment* segs, int32_t n_segs, int32_t T, const int32_t* ran
     return out;
   };
   std::vector<int32_t> bwd_tiles = bwd_tiles_of(kTileM);
+  p.btiles_uniform = true;
+  for (size_t t = 0; t * kTileWords < bwd_tiles.size(); ++t) {
+    const int32_t r0 = bwd_tiles[t * kTileWords], n = bwd_tiles[t * kTileWords + 3];
+    if (r0 != (int32_t)t * kTileM || n != std::min<int32_t>(kTileM, Tt - r0)) p.btiles_uniform = false;
+  }
   std::vector<int32_t> bwd_tiles128 = bwd_tiles_of(kBlockM);
 
   // Adapters owning training rows, and single-adapter chunks of the compact

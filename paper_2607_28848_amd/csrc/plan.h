@@ -72,6 +72,9 @@ struct dsv_plan {
   int32_t r_used = 0, r_train = 0;
   int32_t n_ftiles = 0, n_shrink = 0, n_gather = 0, n_gitems = 0, n_btiles = 0,
           n_chunks = 0, n_tads = 0, n_titems = 0, n_ftiles128 = 0, n_btiles128 = 0;
+  // every 256-row backward tile t covers compact rows [256 t, min(T_t, 256 t + 256))
+  // (no tile ends early at the adapter-run limit), as every forward tile does
+  bool btiles_uniform = false;
   std::vector<int32_t> ranks;
   std::vector<float> scales;
   std::vector<int32_t> train_rows;     // host copy, compact order
