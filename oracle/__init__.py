@@ -25,6 +25,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "dsvo.c")
 _LIB = os.path.join(_HERE, "libdsvo.so")
+_ASAN_LIB = os.path.join(_HERE, "_build", "libdsvo_asan.so")
 _lib = None
 
 
@@ -39,12 +40,28 @@ def build(force: bool = True) -> str:
     return _LIB
 
 
+def build_asan() -> str:
+    """Compile dsvo.c with AddressSanitizer + UBSan into _build/libdsvo_asan.so,
+    for host-sanitizer runs of the oracle's tests (DSVO_LIBRARY names it)."""
+    os.makedirs(os.path.dirname(_ASAN_LIB), exist_ok=True)
+    tmp = _ASAN_LIB + ".tmp%d" % os.getpid()
+    subprocess.check_call(
+        ["gcc", "-O1", "-g", "-fopenmp", "-shared", "-fPIC", "-std=c99", "-Wall",
+         "-fsanitize=address,undefined", "-fno-sanitize-recover=undefined", "-fno-omit-frame-pointer",
+         "-o", tmp, _SRC, "-lm"], cwd=_HERE)
+    os.replace(tmp, _ASAN_LIB)
+    return _ASAN_LIB
+
+
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
-            build(force=True)
-        lib = ctypes.CDLL(_LIB)
+        path = os.environ.get("DSVO_LIBRARY")
+        if not path:
+            path = _LIB
+            if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+                build(force=True)
+        lib = ctypes.CDLL(path)
         i32p = ctypes.POINTER(ctypes.c_int32)
         f64p = ctypes.POINTER(ctypes.c_double)
         ci = ctypes.c_int

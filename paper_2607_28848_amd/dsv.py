@@ -18,11 +18,13 @@ from typing import Optional, Sequence
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libdsv.so")
+# DSV_LIBRARY may name another build of the same library (the host-sanitized
+# variant of build.py); it must exist, there is no fallback either way.
+LIB_PATH = os.environ.get("DSV_LIBRARY") or os.path.join(_HERE, "libdsv.so")
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError("libdsv.so is not built: run `python -m paper_2607_28848_amd.build` "
-                      "(there is no fallback implementation)")
+    raise ImportError("%s is not built: run `python -m paper_2607_28848_amd.build` "
+                      "(there is no fallback implementation)" % LIB_PATH)
 
 # torch ships its own HIP runtime (same SONAME as /opt/rocm's).  Load it first so
 # that libdsv.so binds to that one runtime: device pointers and streams handed

@@ -211,6 +211,95 @@ def test_blob_matches_independent_packer(name, segs, ranks, r_max):
     np.testing.assert_array_equal(dsv.segments_build(perm, T, ranks, scales, r_max).meta_words(), got)
 
 
+def _random_table(rng):
+    """A random valid table: T in [0, 1200], pieces of 1..300 rows (mostly short),
+    random adapters, ranks and training flags, in random table order, with a few
+    zero-length entries mixed in."""
+    n_ad = int(rng.integers(1, 12))
+    r_max = int(rng.choice([1, 4, 8, 16, 33, 64]))
+    ranks = [int(x) for x in rng.integers(1, r_max + 1, n_ad)]
+    T_target = int(rng.integers(1, 1201)) if rng.random() > 0.08 else 0   # some empty batches
+    segs, s = [], 0
+    while s < T_target:
+        ln = int(min(T_target - s, rng.choice([1, 2, 3, 5, 16, 40, 127, 300])))
+        segs.append((s, ln, int(rng.integers(0, n_ad)), int(rng.random() < 0.4)))
+        s += ln
+    for _ in range(int(rng.integers(0, 3))):
+        segs.append((int(rng.integers(0, s + 1)), 0, int(rng.integers(0, n_ad)), int(rng.integers(0, 2))))
+    segs = [segs[i] for i in rng.permutation(len(segs))]
+    return segs, s, ranks, r_max
+
+
+def _corrupt(rng, segs, T, ranks, r_max):
+    """Apply one defect; returns (segs, T, ranks, r_max, expected status name)."""
+    nz = [i for i, x in enumerate(segs) if x[1] > 0]
+    kind = int(rng.integers(0, 8))
+    segs = list(segs)
+    ranks = list(ranks)
+    if kind == 0 and nz:                       # drop a non-empty entry: gap, or short of T
+        del segs[nz[int(rng.integers(0, len(nz)))]]
+        return segs, T, ranks, r_max, "ERR_LAYOUT"
+    if kind == 1 and nz:                       # lengthen one entry: overlap, or past T
+        i = nz[int(rng.integers(0, len(nz)))]
+        st, ln, a, tr = segs[i]
+        segs[i] = (st, ln + int(rng.integers(1, 4)), a, tr)
+        return segs, T, ranks, r_max, "ERR_LAYOUT"
+    if kind == 2 and segs:                     # adapter id out of range
+        i = int(rng.integers(0, len(segs)))
+        st, ln, a, tr = segs[i]
+        segs[i] = (st, ln, int(rng.choice([-1, len(ranks), len(ranks) + 7])), tr)
+        return segs, T, ranks, r_max, "ERR_RANGE"
+    if kind == 3 and segs:                     # training flag not 0/1
+        i = int(rng.integers(0, len(segs)))
+        st, ln, a, tr = segs[i]
+        segs[i] = (st, ln, a, int(rng.choice([-1, 2, 255])))
+        return segs, T, ranks, r_max, "ERR_RANGE"
+    if kind == 4:                              # one rank outside [1, r_max]
+        ranks[int(rng.integers(0, len(ranks)))] = int(rng.choice([0, -3, r_max + 1]))
+        return segs, T, ranks, r_max, "ERR_RANGE"
+    if kind == 5:                              # r_max outside [1, 64]
+        return segs, T, ranks, int(rng.choice([0, -1, 65, 1 << 30])), "ERR_RANGE"
+    if kind == 6 and nz:                       # negative start or length
+        i = nz[int(rng.integers(0, len(nz)))]
+        st, ln, a, tr = segs[i]
+        segs[i] = (-1 - st, ln, a, tr) if rng.random() < 0.5 else (st, -ln, a, tr)
+        return segs, T, ranks, r_max, "ERR_LAYOUT"
+    return segs, T, ranks, r_max, "OK"
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_tables_valid_and_defective(seed):
+    """Random tables, half of them with one defect: a valid table packs to the
+    independent packer's blob and answers every query consistently; a defective
+    one returns its status and builds no plan.  (Also the workload of the
+    host-sanitizer run of this file.)"""
+    dsv = _dsv()
+    rng = np.random.default_rng(1000 + seed)
+    segs, T, ranks, r_max = _random_table(rng)
+    scales = [float(x) for x in rng.uniform(-4, 4, len(ranks)).astype(np.float32)]
+    if seed % 2:
+        segs, T, ranks, r_max, status = _corrupt(rng, segs, T, ranks, r_max)
+    else:
+        status = "OK"
+    if status != "OK":
+        with pytest.raises(dsv.DsvError) as e:
+            dsv.segments_build(segs, T, ranks, scales, r_max)
+        assert e.value.status == getattr(dsv, status)
+        return
+    plan = dsv.segments_build(segs, T, ranks, scales, r_max)
+    np.testing.assert_array_equal(plan.meta_words(), py_pack(segs, T, ranks, scales))
+    tr = sorted(t for (st, l, a, x) in segs if x for t in range(st, st + l))
+    np.testing.assert_array_equal(plan.train_rows(), tr)
+    c = plan.counts()
+    g = plan.gathered_rows()
+    assert c["gathered_rows"] == len(g) and len(set(g.tolist())) == len(g)
+    assert all(0 <= t < T for t in g.tolist())
+    for dt in (dsv.BF16, dsv.F32):
+        for K, N in ((8, 8), (4096, 14336), (14336, 4096)):
+            assert dsv.fwd_workspace_bytes(plan, dt, K, N) >= 0
+            assert dsv.bwd_workspace_bytes(plan, dt, K, N) >= 0
+
+
 def test_zero_length_segments_are_ignored():
     dsv = _dsv()
     segs = [(0, 5, 0, 0), (5, 0, 1, 1), (5, 3, 1, 1), (8, 0, 0, 0)]
