@@ -409,6 +409,35 @@ int dsv_adamw_step(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N, 
                    float* B_master, float* A_m, float* A_v, float* B_m, float* B_v, void* A,
                    void* B, void* hip_stream);
 
+/*
+ * dsv_adamw_step_grouped -- the same AdamW step for the adapters of up to
+ * DSV_MAX_GROUP projections of one layer (q, k, v, o, gate, up, down share
+ * the batch's training adapters but have their own K x N), in one launch.
+ * projs[n_proj] holds each projection's shape and the buffers dsv_adamw_step
+ * takes (same layouts, ownership and NULL rules).  Every element is computed
+ * exactly as dsv_adamw_step computes it, so a group and the single calls give
+ * bit-identical results.  Returns DSV_ERR_RANGE for n_proj outside
+ * [1, DSV_MAX_GROUP], DSV_ERR_ARG for a NULL projs, else as dsv_adamw_step
+ * (any bad entry fails the whole call before anything is launched).
+ */
+typedef struct {
+  int32_t K, N;
+  const float* dA;        /* [n_ad][r_max][K] */
+  const float* dB;        /* [n_ad][N][r_max] */
+  float* A_master;        /* [n_ad][r_max][K] fp32 */
+  float* B_master;        /* [n_ad][N][r_max] fp32 */
+  float* A_m;
+  float* A_v;
+  float* B_m;
+  float* B_v;
+  void* A;                /* parameter copy (bf16 or fp32), or NULL */
+  void* B;
+} dsv_adamw_proj;
+
+int dsv_adamw_step_grouped(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,
+                           const dsv_adamw_proj* projs, int32_t step, const dsv_adamw_hparams* hp,
+                           void* hip_stream);
+
 /* GEMM launch configuration that dsv_cobatch_fwd (pass 0) or dsv_lora_bwd
  * (pass 1, the dX GEMM) uses for this plan, dtype and K x N on the current
  * device, for benchmarks and tests.  out[6] receives: tile rows, tile

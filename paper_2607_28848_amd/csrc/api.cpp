@@ -251,27 +251,42 @@ extern "C" int dsv_timing_read(double* fwd_ms, int32_t* fwd_n, double* bwd_ms, i
   return rc;
 }
 
-extern "C" int dsv_adamw_step(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, int32_t step,
-                              const dsv_adamw_hparams* hp, const float* dA, const float* dB, float* A_master,
-                              float* B_master, float* A_m, float* A_v, float* B_m, float* B_v, void* A,
-                              void* B, void* hip_stream) {
-  int rc = check_common(p, dt, K, N);
-  if (rc != DSV_OK) return rc;
+namespace {
+
+// AdamW of up to DSV_MAX_GROUP projections in one launch (dsv_adamw_step is a
+// group of one): validation first, nothing launched on any error.
+int adamw_impl(const dsv_plan* p, dsv_dtype dt, int32_t n, const dsv_adamw_proj* projs, int32_t step,
+               const dsv_adamw_hparams* hp, hipStream_t stream) {
+  if (!p) return DSV_ERR_ARG;
+  if (n < 1 || n > DSV_MAX_GROUP) return DSV_ERR_RANGE;
+  if (!projs) return DSV_ERR_ARG;
+  for (int32_t i = 0; i < n; ++i) {
+    const int rc = check_common(p, dt, projs[i].K, projs[i].N);
+    if (rc != DSV_OK) return rc;
+  }
   if (!p->d_meta || !hp) return DSV_ERR_ARG;
   if (step < 1 || !std::isfinite(hp->lr) || hp->lr < 0.0 || !std::isfinite(hp->weight_decay) ||
       hp->weight_decay < 0.0 || !(hp->beta1 >= 0.0 && hp->beta1 < 1.0) ||
       !(hp->beta2 >= 0.0 && hp->beta2 < 1.0) || !(hp->eps > 0.0) || !std::isfinite(hp->eps))
     return DSV_ERR_RANGE;
-  if (!ptr_ok(dA) || !ptr_ok(dB) || !ptr_ok(A_master) || !ptr_ok(B_master) || !ptr_ok(A_m) ||
-      !ptr_ok(A_v) || !ptr_ok(B_m) || !ptr_ok(B_v) || (A && !aligned16(A)) || (B && !aligned16(B)))
-    return DSV_ERR_ARG;
+  for (int32_t i = 0; i < n; ++i) {
+    const dsv_adamw_proj& q = projs[i];
+    if (!ptr_ok(q.dA) || !ptr_ok(q.dB) || !ptr_ok(q.A_master) || !ptr_ok(q.B_master) || !ptr_ok(q.A_m) ||
+        !ptr_ok(q.A_v) || !ptr_ok(q.B_m) || !ptr_ok(q.B_v) || (q.A && !aligned16(q.A)) ||
+        (q.B && !aligned16(q.B)))
+      return DSV_ERR_ARG;
+  }
   if (p->n_tads == 0) return DSV_OK;
   AdamWArgs a{};
-  a.K = K;
-  a.N = N;
   a.r_max = p->r_max;
+  a.n_proj = n;
+  a.bf16 = dt == DSV_BF16;
   a.train_ads = p->dptr(p->lay.train_ads);
   a.ranks = p->dptr(p->lay.ranks);
+  // B in float4 units when every training rank and the rank stride are multiples of 4
+  bool bvec = (p->r_max & 3) == 0;
+  for (int32_t s = 0; s < p->n_tads; ++s) bvec = bvec && (p->ranks[p->meta[p->lay.train_ads + s]] & 3) == 0;
+  a.bvec = bvec ? 1 : 0;
   // factors formed in double on the host, rounded once to fp32
   const double bc1 = 1.0 - std::pow(hp->beta1, (double)step);
   const double bc2 = 1.0 - std::pow(hp->beta2, (double)step);
@@ -283,19 +298,49 @@ extern "C" int dsv_adamw_step(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_
   a.eps = (float)hp->eps;
   a.step_size = (float)(hp->lr / bc1);
   a.sqrt_bc2 = (float)std::sqrt(bc2);
-  a.dA = dA;
-  a.dB = dB;
-  a.pA = A_master;
-  a.pB = B_master;
-  a.mA = A_m;
-  a.vA = A_v;
-  a.mB = B_m;
-  a.vB = B_v;
-  a.A = A;
-  a.B = B;
-  a.bf16 = dt == DSV_BF16;
-  return launch_adamw(a, p->n_tads, static_cast<hipStream_t>(hip_stream)) == hipSuccess ? DSV_OK
-                                                                                       : DSV_ERR_DEVICE;
+  int64_t blocks = 0;
+  for (int32_t i = 0; i < n; ++i) {
+    const dsv_adamw_proj& q = projs[i];
+    // units of the largest training rank; smaller ranks leave threads idle
+    const int64_t r = p->r_train;
+    const int64_t units = r * q.K / 4 + (bvec ? (int64_t)q.N * r / 4 : (int64_t)q.N * r);
+    const int64_t bpa = (units + 255) / 256;
+    if (bpa * 256 > INT32_MAX) return DSV_ERR_SIZE;  // the kernel indexes units in 32 bits
+    AdamWProj& d = a.proj[i];
+    d.K = q.K;
+    d.N = q.N;
+    d.blk_begin = (int32_t)blocks;
+    d.bpa = (int32_t)bpa;
+    d.dA = q.dA;
+    d.dB = q.dB;
+    d.pA = q.A_master;
+    d.pB = q.B_master;
+    d.mA = q.A_m;
+    d.vA = q.A_v;
+    d.mB = q.B_m;
+    d.vB = q.B_v;
+    d.A = q.A;
+    d.B = q.B;
+    blocks += bpa * p->n_tads;
+    if (blocks > INT32_MAX) return DSV_ERR_SIZE;
+  }
+  return launch_adamw(a, blocks, stream) == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
+}
+
+}  // namespace
+
+extern "C" int dsv_adamw_step(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, int32_t step,
+                              const dsv_adamw_hparams* hp, const float* dA, const float* dB, float* A_master,
+                              float* B_master, float* A_m, float* A_v, float* B_m, float* B_v, void* A,
+                              void* B, void* hip_stream) {
+  const dsv_adamw_proj one{K, N, dA, dB, A_master, B_master, A_m, A_v, B_m, B_v, A, B};
+  return adamw_impl(p, dt, 1, &one, step, hp, static_cast<hipStream_t>(hip_stream));
+}
+
+extern "C" int dsv_adamw_step_grouped(const dsv_plan* p, dsv_dtype dt, int32_t n_proj,
+                                      const dsv_adamw_proj* projs, int32_t step, const dsv_adamw_hparams* hp,
+                                      void* hip_stream) {
+  return adamw_impl(p, dt, n_proj, projs, step, hp, static_cast<hipStream_t>(hip_stream));
 }
 
 extern "C" int dsv_gemm_config(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, int32_t pass,

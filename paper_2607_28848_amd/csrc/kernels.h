@@ -255,23 +255,31 @@ hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const 
 hipError_t launch_gemm_group_nt(const GemmGroup& g, hipStream_t s);
 hipError_t launch_gemm_group_nn(const GemmGroup& g, hipStream_t s);
 
-// Fused AdamW step of the training adapters' A and B slices (fp32 master
-// weights and moments in the A / B layouts; the parameter copy A / B is bf16
-// when bf16 != 0, fp32 otherwise, or not written when nullptr).
+// Fused AdamW step of the training adapters' A and B slices of up to
+// kMaxGroup projections in one launch (fp32 master weights and moments in
+// the A / B layouts; the parameter copy A / B is bf16 when bf16 != 0, fp32
+// otherwise, or not written when nullptr).  Projection p owns blocks
+// [blk_begin, blk_begin + n_tads * bpa): bpa blocks per training adapter, over
+// the adapter's A slice (float4 units) and then its B slice (float4 units of
+// four rank entries when bvec, single entries otherwise).
+struct AdamWProj {
+  int32_t K, N;
+  int32_t blk_begin, bpa;
+  const float *dA, *dB;
+  float *pA, *pB, *mA, *vA, *mB, *vB;
+  void *A, *B;
+};
 struct AdamWArgs {
-  int32_t K, N, r_max;
+  int32_t r_max, n_proj, bvec, bf16;
   const int32_t* train_ads;  // training adapters (device)
   const int32_t* ranks;
   float decay;               // 1 - lr * wd
   float b1, b2, c1, c2, eps; // beta1, beta2, 1 - beta1, 1 - beta2
   float step_size;           // lr / (1 - b1^t)
   float sqrt_bc2;            // sqrt(1 - b2^t)
-  const float *dA, *dB;
-  float *pA, *pB, *mA, *vA, *mB, *vB;
-  void *A, *B;
-  int32_t bf16;
+  AdamWProj proj[kMaxGroup];
 };
-hipError_t launch_adamw(const AdamWArgs& a, int32_t n_tads, hipStream_t s);
+hipError_t launch_adamw(const AdamWArgs& a, int64_t n_blocks, hipStream_t s);
 
 // LoRA dropout of the training rows: mask parameters (thr = floor(p 2^32),
 // scale = 1 / (1 - p)) and the bitmask kernel.

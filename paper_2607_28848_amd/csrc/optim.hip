@@ -31,54 +31,83 @@ __device__ __forceinline__ void adamw_one(const AdamWArgs& a, float g, float& p,
   p -= a.step_size * m / (sqrtf(v) / a.sqrt_bc2 + a.eps);
 }
 
-// blockIdx.y: training adapter; x: 256-thread blocks over the adapter's A part
-// (r_a rows of K, contiguous: 4 elements per thread) then its B part (N rows of
-// r_a entries with stride r_max: 1 element per thread).
+__device__ __forceinline__ void adamw4(const AdamWArgs& a, float4 g, float4& p, float4& m, float4& v) {
+  adamw_one(a, g.x, p.x, m.x, v.x);
+  adamw_one(a, g.y, p.y, m.y, v.y);
+  adamw_one(a, g.z, p.z, m.z, v.z);
+  adamw_one(a, g.w, p.w, m.w, v.w);
+}
+
+// One float4 unit at element e of a slice: gradient, master and moments read,
+// master and moments written, the rounded copy written (if any).
+__device__ __forceinline__ void unit4(const AdamWArgs& a, int64_t e, const float* dg, float* pm, float* mm,
+                                      float* vm, void* copy) {
+  const float4 g = *reinterpret_cast<const float4*>(dg + e);
+  float4 p = *reinterpret_cast<const float4*>(pm + e);
+  float4 m = *reinterpret_cast<const float4*>(mm + e);
+  float4 v = *reinterpret_cast<const float4*>(vm + e);
+  adamw4(a, g, p, m, v);
+  *reinterpret_cast<float4*>(pm + e) = p;
+  *reinterpret_cast<float4*>(mm + e) = m;
+  *reinterpret_cast<float4*>(vm + e) = v;
+  if (copy && a.bf16) {
+    const uint32_t lo = (uint32_t)f2bf_rne(p.x) | ((uint32_t)f2bf_rne(p.y) << 16);
+    const uint32_t hi = (uint32_t)f2bf_rne(p.z) | ((uint32_t)f2bf_rne(p.w) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(copy) + e) = make_uint2(lo, hi);
+  } else if (copy) {
+    *reinterpret_cast<float4*>(static_cast<float*>(copy) + e) = p;
+  }
+}
+
+// One block: 256 units of one (projection, training adapter) pair.  The
+// projection is found from the block index (blk_begin ascending), then the
+// adapter slot and the block's place inside the adapter's A-then-B units.
 __global__ __launch_bounds__(256) void adamw_kernel(AdamWArgs a) {
-  const int ad = a.train_ads[blockIdx.y];
-  const int r = a.ranks[ad];
-  const int64_t nA4 = (int64_t)r * a.K / 4, nB = (int64_t)a.N * r;
-  const int64_t u = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int32_t bid = (int32_t)blockIdx.x;
+  int p = 0;
+#pragma unroll
+  for (int q = 1; q < kMaxGroup; ++q)
+    if (q < a.n_proj && bid >= a.proj[q].blk_begin) p = q;
+  const AdamWProj& P = a.proj[p];
+  // the host keeps every per-adapter unit count below 2^31: 32-bit index math
+  const uint32_t local = (uint32_t)(bid - P.blk_begin);
+  const uint32_t slot = local / (uint32_t)P.bpa;
+  const int ad = a.train_ads[slot];
+  const uint32_t r = (uint32_t)a.ranks[ad];
+  const uint32_t nA4 = r * ((uint32_t)P.K / 4u);
+  const uint32_t u = (local - slot * (uint32_t)P.bpa) * 256u + threadIdx.x;
   if (u < nA4) {
-    const int64_t e = (int64_t)ad * a.r_max * a.K + 4 * u;  // rows j < r are contiguous
-    const float4 g = *reinterpret_cast<const float4*>(a.dA + e);
-    float4 p = *reinterpret_cast<const float4*>(a.pA + e);
-    float4 m = *reinterpret_cast<const float4*>(a.mA + e);
-    float4 v = *reinterpret_cast<const float4*>(a.vA + e);
-    adamw_one(a, g.x, p.x, m.x, v.x);
-    adamw_one(a, g.y, p.y, m.y, v.y);
-    adamw_one(a, g.z, p.z, m.z, v.z);
-    adamw_one(a, g.w, p.w, m.w, v.w);
-    *reinterpret_cast<float4*>(a.pA + e) = p;
-    *reinterpret_cast<float4*>(a.mA + e) = m;
-    *reinterpret_cast<float4*>(a.vA + e) = v;
-    if (a.A && a.bf16) {
-      const uint32_t lo = (uint32_t)f2bf_rne(p.x) | ((uint32_t)f2bf_rne(p.y) << 16);
-      const uint32_t hi = (uint32_t)f2bf_rne(p.z) | ((uint32_t)f2bf_rne(p.w) << 16);
-      *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.A) + e) = make_uint2(lo, hi);
-    } else if (a.A) {
-      *reinterpret_cast<float4*>(static_cast<float*>(a.A) + e) = p;
+    // rows j < r of the adapter's A slice are contiguous
+    unit4(a, (int64_t)ad * a.r_max * P.K + 4 * (int64_t)u, P.dA, P.pA, P.mA, P.vA, P.A);
+    return;
+  }
+  const uint32_t q = u - nA4;
+  const int64_t base = (int64_t)ad * P.N * a.r_max;
+  if (a.bvec) {
+    // B row n holds entries j < r at n * r_max + j; r and r_max multiples of 4
+    const uint32_t r4 = r >> 2;
+    if (q < (uint32_t)P.N * r4) {
+      const uint32_t n = q / r4, j4 = q - n * r4;
+      unit4(a, base + (int64_t)n * a.r_max + 4 * j4, P.dB, P.pB, P.mB, P.vB, P.B);
     }
-  } else if (u - nA4 < nB) {
-    const int64_t q = u - nA4, n = q / r, j = q - n * r;
-    const int64_t e = (int64_t)ad * a.N * a.r_max + n * a.r_max + j;
-    float p = a.pB[e], m = a.mB[e], v = a.vB[e];
-    adamw_one(a, a.dB[e], p, m, v);
-    a.pB[e] = p;
-    a.mB[e] = m;
-    a.vB[e] = v;
-    if (a.B && a.bf16) static_cast<uint16_t*>(a.B)[e] = f2bf_rne(p);
-    else if (a.B) static_cast<float*>(a.B)[e] = p;
+  } else if (q < (uint32_t)P.N * r) {
+    const uint32_t n = q / r, j = q - n * r;
+    const int64_t e = base + (int64_t)n * a.r_max + j;
+    float pv = P.pB[e], m = P.mB[e], v = P.vB[e];
+    adamw_one(a, P.dB[e], pv, m, v);
+    P.pB[e] = pv;
+    P.mB[e] = m;
+    P.vB[e] = v;
+    if (P.B && a.bf16) static_cast<uint16_t*>(P.B)[e] = f2bf_rne(pv);
+    else if (P.B) static_cast<float*>(P.B)[e] = pv;
   }
 }
 
 }  // namespace
 
-hipError_t launch_adamw(const AdamWArgs& a, int32_t n_tads, hipStream_t s) {
-  if (n_tads <= 0) return hipSuccess;
-  // blocks enough for the largest rank (r_max); threads past an adapter's count exit
-  const int64_t units = (int64_t)a.r_max * a.K / 4 + (int64_t)a.N * a.r_max;
-  hipLaunchKernelGGL(adamw_kernel, dim3((unsigned)((units + 255) / 256), (unsigned)n_tads), dim3(256), 0, s, a);
+hipError_t launch_adamw(const AdamWArgs& a, int64_t n_blocks, hipStream_t s) {
+  if (n_blocks <= 0) return hipSuccess;
+  hipLaunchKernelGGL(adamw_kernel, dim3((unsigned)n_blocks), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

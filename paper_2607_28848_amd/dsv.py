@@ -122,6 +122,16 @@ class AdamWHparams(ctypes.Structure):
 
 _lib.dsv_adamw_step.argtypes = [_vp, ctypes.c_int, _i32, _i32, _i32, ctypes.POINTER(AdamWHparams)] + [_vp] * 11
 _lib.dsv_adamw_step.restype = ctypes.c_int
+
+
+class AdamWProj(ctypes.Structure):
+    _fields_ = [("K", _i32), ("N", _i32)] + [(n, _vp) for n in (
+        "dA", "dB", "A_master", "B_master", "A_m", "A_v", "B_m", "B_v", "A", "B")]
+
+
+_lib.dsv_adamw_step_grouped.argtypes = [_vp, ctypes.c_int, _i32, ctypes.POINTER(AdamWProj), _i32,
+                                        ctypes.POINTER(AdamWHparams), _vp]
+_lib.dsv_adamw_step_grouped.restype = ctypes.c_int
 _lib.dsv_gemm_config.argtypes = [_vp, ctypes.c_int, _i32, _i32, _i32, _i32p]
 _lib.dsv_gemm_config.restype = ctypes.c_int
 _lib.dsv_status_string.argtypes = [ctypes.c_int]
@@ -467,6 +477,39 @@ def adamw_step(plan: Plan, step: int, dA, dB, A_master, B_master, A_m, A_v, B_m,
                                ptr(A_master), ptr(B_master), ptr(A_m), ptr(A_v), ptr(B_m), ptr(B_v),
                                ptr(A), ptr(B), _stream_handle(stream)),
            "dsv_adamw_step")
+
+
+def adamw_step_grouped(plan: Plan, step: int, items, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                       weight_decay=0.01, stream=None):
+    """The AdamW step of several projections in one launch (dsv_adamw_step_grouped).
+    items: [(dA, dB, A_master, B_master, A_m, A_v, B_m, B_v, A, B)], A / B may be None."""
+    adamw_grouped_prepared(plan, items, lr, beta1, beta2, eps, weight_decay, stream)(step)
+
+
+def adamw_grouped_prepared(plan: Plan, items, lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8,
+                           weight_decay=0.01, stream=None):
+    """Marshal the arguments of dsv_adamw_step_grouped once; returns step(t), which
+    only makes the call (for loops that repeat it over the same buffers)."""
+    import torch
+    arr = (AdamWProj * len(items))()
+    code = None
+    ptr = lambda t: None if t is None else ctypes.c_void_p(t.data_ptr())  # noqa: E731
+    for i, it in enumerate(items):
+        dA, dB, Am, Bm, mA, vA, mB, vB, A, B = it
+        ref = A if A is not None else Am
+        c = BF16 if ref.dtype == torch.bfloat16 else F32
+        if code is None:
+            code = c
+        elif c != code:
+            raise ValueError("adamw_step_grouped: parameter copies of one dtype")
+        arr[i] = AdamWProj(Am.shape[2], Bm.shape[1], *[ptr(t) for t in (dA, dB, Am, Bm, mA, vA, mB, vB, A, B)])
+    hp = AdamWHparams(lr, beta1, beta2, eps, weight_decay)
+    args = (plan.handle, code if code is not None else BF16, len(items), arr)
+    tail = (ctypes.byref(hp), _stream_handle(stream))
+
+    def step(t: int) -> None:
+        _check(_lib.dsv_adamw_step_grouped(*args, t, *tail), "dsv_adamw_step_grouped")
+    return step
 
 
 GEMM_CONFIG_NAMES = ("tile_m", "tile_n", "row_tiles", "col_tiles", "split_tiles", "split_ways")

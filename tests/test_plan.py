@@ -450,3 +450,27 @@ def test_grouped_argument_checks_on_host():
             dsv.fwd_workspace_bytes(plan, dt, 64, 64) for _ in shapes)
         assert dsv.bwd_grouped_workspace_bytes(plan, dt, shapes) >= sum(
             dsv.bwd_workspace_bytes(plan, dt, K, 64) for K, _ in shapes) // 2
+
+
+def test_adamw_grouped_argument_checks_on_host():
+    """dsv_adamw_step_grouped rejects a bad group size (ERR_RANGE), a NULL array
+    (ERR_ARG), a bad shape in any entry (ERR_SIZE), bad hyper-parameters
+    (ERR_RANGE) and a host-only plan (ERR_ARG) before touching the device."""
+    import ctypes
+    dsv = _dsv()
+    lib = dsv.lib_handle()
+    plan = dsv.segments_build([(0, 16, 0, 1)], 16, [4], [2.0], 4)
+    fake = ctypes.c_void_p(4096)
+    arr = (dsv.AdamWProj * 9)()
+    for i in range(9):
+        arr[i] = dsv.AdamWProj(64, 64, *([fake] * 10))
+    hp = dsv.AdamWHparams(1e-3, 0.9, 0.999, 1e-8, 0.01)
+    for n in (0, -1, 9):
+        assert lib.dsv_adamw_step_grouped(plan.handle, dsv.BF16, n, arr, 1, ctypes.byref(hp), None) == dsv.ERR_RANGE
+    assert lib.dsv_adamw_step_grouped(plan.handle, dsv.BF16, 2, None, 1, ctypes.byref(hp), None) == dsv.ERR_ARG
+    arr[1].N = 60
+    assert lib.dsv_adamw_step_grouped(plan.handle, dsv.BF16, 2, arr, 1, ctypes.byref(hp), None) == dsv.ERR_SIZE
+    arr[1].N = 64
+    assert lib.dsv_adamw_step_grouped(plan.handle, dsv.BF16, 2, arr, 1, ctypes.byref(hp), None) == dsv.ERR_ARG
+    assert lib.dsv_adamw_step_grouped(None, dsv.BF16, 2, arr, 1, ctypes.byref(hp), None) == dsv.ERR_ARG
+    assert lib.dsv_adamw_step(plan.handle, dsv.BF16, 64, 64, 1, ctypes.byref(hp), *([fake] * 10), None) == dsv.ERR_ARG
