@@ -662,8 +662,8 @@ def main():
     gemm_launches = {proj.name: {"fwd": cfg_str(dsv.gemm_config(probe, code, proj.K, proj.N, 0)),
                                  "dx": cfg_str(dsv.gemm_config(probe, code, proj.K, proj.N, 1))}
                      for proj in w.projections}
-    roof_kernel = ("gemm_lora_kernel<NT> + split_fixup_kernel<NT> (forward base GEMM with the low-rank "
-                   "prologue; the fixup sums contraction-split tiles)")
+    roof_kernel = ("gemm16_kernel (256x256 tiles; gemm_lora_kernel for 128x128) + split_fixup_kernel<NT> "
+                   "(forward base GEMM with the low-rank prologue; the fixup sums contraction-split tiles)")
     if groups is not None and any(hi - lo > 1 for lo, hi in groups):
         pc = probe.counts()
         for lo, hi in groups:
@@ -675,7 +675,7 @@ def main():
                 "dx": "256x256 tiles, %d in one launch" % sum(pc["bwd_tiles"] * ((p.K + 255) // 256) for p in ps)}
             for p in ps:
                 gemm_launches.pop(p.name, None)
-        roof_kernel = ("gemm_group_kernel<NT> (the forward base GEMMs with their low-rank prologues, every "
+        roof_kernel = ("gemm16_group_kernel<false> (the forward base GEMMs with their low-rank prologues, every "
                        "projection of a group in one launch; with --launch set, one launch per step)")
 
     cpu = None

@@ -90,7 +90,7 @@ struct FwdWs {
   size_t h_all, delta, keep, sk_part, rk_part, total;
 };
 struct BwdWs {
-  size_t bt, g, hrec, part_b, part_a, keep, sk_part, g_part, h_part, total;
+  size_t g, hrec, part_b, part_a, keep, sk_part, g_part, h_part, total;
 };
 
 // Dropout bitmask of the training rows: ceil(K / 32) words per row.
@@ -129,8 +129,6 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
   BwdWs w{};
   size_t off = 0;
   if (dt == DSV_BF16) {
-    w.bt = off;
-    off = align256(off + (size_t)p.n_tads * p.r_max * N * 2);
     w.g = off;
     off = align256(off + (size_t)p.T_t * ld_rank(p.r_max) * 2);
     w.hrec = off;  // h of the training rows, recomputed when H_save is not kept
@@ -140,8 +138,8 @@ BwdWs bwd_ws(const dsv_plan& p, dsv_dtype dt, int32_t K, int32_t N, const GemmPl
     w.part_a = off;
     off = align256(off + (size_t)p.n_chunks * K * p.r_max * 4);
     off = carve_sk(gp, off, &w.sk_part);
-    w.g_part = off;  // pieces of a split g contraction
-    off = align256(off + skinny_part_bytes(N, p.n_titems, p.T_t, p.r_max));
+    w.g_part = off;  // g's partials, one per 256-column block of N
+    off = align256(off + (size_t)token_col_blocks(N) * p.T_t * p.r_max * 4);
     w.h_part = off;  // pieces of a split recomputed h
     off = align256(off + skinny_part_bytes(K, p.n_shrink, p.T_t, p.r_max));
   } else {
@@ -600,41 +598,13 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   }
 
   const int64_t ldh = ld_rank(p->r_max);
-  uint16_t* bt = at<uint16_t>(workspace, ws.bt);
   uint16_t* gm = at<uint16_t>(workspace, ws.g);
   float* part_b = at<float>(workspace, ws.part_b);
   float* part_a = at<float>(workspace, ws.part_a);
   const int32_t* train_ads = p->dptr(L.train_ads);
 
-  // 1. transposed copies of the training adapters' B ([r_max][N] per adapter).
-  if ((e = launch_transpose_b(static_cast<const uint16_t*>(B), N, p->r_max, train_ads, p->n_tads, ranks,
-                              bt, s)) != hipSuccess)
-    return DSV_ERR_DEVICE;
-
-  // 2. g = s_a dy B_a (contraction over N) -> G [T_t][ldh].
-  SkinnyArgs sk{};
-  sk.P = static_cast<const uint16_t*>(dY);
-  sk.ldp = N;
-  sk.rows = nullptr;
-  sk.items = p->dptr(L.train_items);
-  sk.Q = bt;
-  sk.q_ad = (int64_t)p->r_max * N;
-  sk.ldq = N;
-  sk.qsel = p->dptr(L.ad_slot);
-  sk.ranks = ranks;
-  sk.scales = scales;
-  sk.C = N;
-  sk.out1 = gm;
-  sk.ld1 = ldh;
-  sk.out2 = nullptr;
-  sk.part = at<float>(workspace, ws.g_part);
-  sk.part_n = p->T_t;
-  sk.r_max = p->r_max;
-  sk.split_items = p->n_titems;
-  if ((e = launch_gmat(sk, p->n_titems, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
-
-  // 2b. H_save not kept (residual-only retention): recompute h of the training
-  //     rows from X with the forward's shrink (same values, bit for bit).
+  // 1. H_save not kept (residual-only retention): recompute h of the training
+  //    rows from X with the forward's shrink (same values, bit for bit).
   const uint16_t* hs = static_cast<const uint16_t*>(H_save);
   int64_t ldhs = p->r_max;
   if (!hs) {
@@ -667,31 +637,62 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     ldhs = ldh;
   }
 
-  // 3. per-chunk fp32 partials of dy^T h (-> dB) and x^T g (-> dA).
-  TokenReduceArgs tb{};
-  tb.P = static_cast<const uint16_t*>(dY);
-  tb.ldp = N;
-  tb.prow = nullptr;
-  tb.Q = hs;
-  tb.ldq = ldhs;
-  tb.chunks = p->dptr(L.chunks);
-  tb.ranks = ranks;
-  tb.C = N;
-  tb.r_max = p->r_max;
-  tb.part = part_b;
-  TokenReduceArgs ta = tb;
-  ta.P = static_cast<const uint16_t*>(X);
-  ta.ldp = K;
-  ta.prow = p->dptr(L.train_rows);
-  ta.Q = gm;
-  ta.ldq = ldh;
-  ta.C = K;
-  ta.part = part_a;
-  ta.keep = keep;  // dA contracts the masked input
-  ta.keep_words = keep_words;
-  if ((e = launch_token_reduce(tb, ta, p->n_chunks, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  // 2. per-chunk fp32 partials of dy^T h (-> dB); the same pass writes the
+  //    per-column-block partials of dy B_a (-> g), reading dy once.
+  TokenReduceGroup tb{};
+  tb.n = 1;
+  TokenReduceArgs& rb = tb.a[0];
+  rb.P = static_cast<const uint16_t*>(dY);
+  rb.ldp = N;
+  rb.prow = nullptr;
+  rb.Q = hs;
+  rb.ldq = ldhs;
+  rb.chunks = p->dptr(L.chunks);
+  rb.ranks = ranks;
+  rb.C = N;
+  rb.r_max = p->r_max;
+  rb.part = part_b;
+  rb.B = static_cast<const uint16_t*>(B);
+  rb.gpart = at<float>(workspace, ws.g_part);
+  rb.gpart_n = p->T_t;
+  tb.yoff[1] = token_col_blocks(N);
+  if ((e = launch_token_reduce_group(tb, p->n_chunks, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
-  // 4. fixed-order sums into dB (scaled by s_a) and dA.
+  // 3. g = s_a dy B_a: the block partials summed in order, rounded once -> G [T_t][ldh]
+  SkinnyGroup gf{};
+  gf.n = 1;
+  SkinnyArgs& sk = gf.a[0];
+  sk.items = p->dptr(L.train_items);
+  sk.ranks = ranks;
+  sk.scales = scales;
+  sk.out1 = gm;
+  sk.ld1 = ldh;
+  sk.part = rb.gpart;
+  sk.part_n = p->T_t;
+  sk.r_max = p->r_max;
+  sk.pieces = token_col_blocks(N);
+  if ((e = launch_g_finish_group(gf, p->n_titems, s)) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 4. per-chunk fp32 partials of x^T g (-> dA)
+  TokenReduceGroup ta{};
+  ta.n = 1;
+  TokenReduceArgs& ra = ta.a[0];
+  ra.P = static_cast<const uint16_t*>(X);
+  ra.ldp = K;
+  ra.prow = p->dptr(L.train_rows);
+  ra.Q = gm;
+  ra.ldq = ldh;
+  ra.chunks = p->dptr(L.chunks);
+  ra.ranks = ranks;
+  ra.C = K;
+  ra.r_max = p->r_max;
+  ra.part = part_a;
+  ra.keep = keep;  // dA contracts the masked input
+  ra.keep_words = keep_words;
+  ta.yoff[1] = token_col_blocks(K);
+  if ((e = launch_token_reduce_group(ta, p->n_chunks, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 5. fixed-order sums into dB (scaled by s_a) and dA.
   const int32_t* tad_ptr = p->dptr(L.tad_chunk_ptr);
   const int32_t* tad_chunks = p->dptr(L.tad_chunks);
   const ReduceOutArgs ob{part_b, N, scales, 0, dB, 1.f};
@@ -700,7 +701,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
       hipSuccess)
     return DSV_ERR_DEVICE;
 
-  // 5. dx = dy W + g A_a on the matrix cores (W read with a transposing load).
+  // 6. dx = dy W + g A_a on the matrix cores (W read with a transposing load).
   //    Under dropout g A_a passes through the input's mask (in the accumulators,
   //    between the low-rank prologue and the main loop).
   if (dX) {
@@ -1074,11 +1075,9 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   const int64_t ldh = ld_rank(p->r_max);
   const int32_t* train_ads = p->dptr(L.train_ads);
-  uint16_t* bt[DSV_MAX_GROUP];
   uint16_t* gm[DSV_MAX_GROUP];
   uint32_t* keep[DSV_MAX_GROUP];
   for (int i = 0; i < n_proj; ++i) {
-    bt[i] = at<uint16_t>(wsb + base[i], w[i].bt);
     gm[i] = at<uint16_t>(wsb + base[i], w[i].g);
     keep[i] = dropping ? at<uint32_t>(wsb + base[i], w[i].keep) : nullptr;
   }
@@ -1088,38 +1087,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     for (int i = 0; i < n_proj; ++i)
       if (launch_dropout_mask(keep[i], p->T_t, projs[i].K, ds[i], s) != hipSuccess) return DSV_ERR_DEVICE;
 
-  // 1. transposed B of the training adapters, every projection
-  TransposeGroup tg{};
-  tg.n = n_proj;
-  for (int i = 0; i < n_proj; ++i) tg.a[i] = TransposeArgs{static_cast<const uint16_t*>(projs[i].B), projs[i].N, bt[i]};
-  if (launch_transpose_group(tg, p->r_max, train_ads, p->n_tads, ranks, s) != hipSuccess) return DSV_ERR_DEVICE;
-
-  // 2. g = s_a dy B_a, every projection
-  SkinnyGroup gg{};
-  gg.n = n_proj;
-  for (int i = 0; i < n_proj; ++i) {
-    const dsv_bwd_proj& q = projs[i];
-    SkinnyArgs& sk = gg.a[i];
-    sk.P = static_cast<const uint16_t*>(q.dY);
-    sk.ldp = q.N;
-    sk.items = p->dptr(L.train_items);
-    sk.Q = bt[i];
-    sk.q_ad = (int64_t)p->r_max * q.N;
-    sk.ldq = q.N;
-    sk.qsel = p->dptr(L.ad_slot);
-    sk.ranks = ranks;
-    sk.scales = scales;
-    sk.C = q.N;
-    sk.out1 = gm[i];
-    sk.ld1 = ldh;
-    sk.part = at<float>(wsb + base[i], w[i].g_part);
-    sk.part_n = p->T_t;
-    sk.r_max = p->r_max;
-    sk.split_items = p->n_titems;
-  }
-  if (launch_gmat_group(gg, p->n_titems, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
-
-  // 2b. h of the training rows for projections whose forward kept no H_save
+  // 1. h of the training rows for projections whose forward kept no H_save
   const uint16_t* hs[DSV_MAX_GROUP];
   int64_t ldhs[DSV_MAX_GROUP];
   SkinnyGroup rg{};
@@ -1154,12 +1122,13 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   }
   if (rg.n > 0 && launch_shrink_train_group(rg, p->n_titems, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
 
-  // 3. chunk partials of dy^T h (dB) and x^T g (dA), every projection
-  TokenReduceGroup trg{};
-  trg.n = 2 * n_proj;
+  // 2. chunk partials of dy^T h (dB), every projection; the same pass writes
+  //    the column-block partials of dy B_a (g), reading dy once
+  TokenReduceGroup tbg{};
+  tbg.n = n_proj;
   for (int i = 0; i < n_proj; ++i) {
     const dsv_bwd_proj& q = projs[i];
-    TokenReduceArgs& tb = trg.a[2 * i];
+    TokenReduceArgs& tb = tbg.a[i];
     tb.P = static_cast<const uint16_t*>(q.dY);
     tb.ldp = q.N;
     tb.Q = hs[i];
@@ -1169,34 +1138,65 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     tb.C = q.N;
     tb.r_max = p->r_max;
     tb.part = at<float>(wsb + base[i], w[i].part_b);
-    TokenReduceArgs& ta = trg.a[2 * i + 1];
-    ta = tb;
+    tb.B = static_cast<const uint16_t*>(q.B);
+    tb.gpart = at<float>(wsb + base[i], w[i].g_part);
+    tb.gpart_n = p->T_t;
+    tbg.yoff[i + 1] = tbg.yoff[i] + token_col_blocks(q.N);
+  }
+  if (launch_token_reduce_group(tbg, p->n_chunks, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 3. g = s_a dy B_a of every projection: block partials summed in order, rounded once
+  SkinnyGroup gf{};
+  gf.n = n_proj;
+  for (int i = 0; i < n_proj; ++i) {
+    SkinnyArgs& sk = gf.a[i];
+    sk.items = p->dptr(L.train_items);
+    sk.ranks = ranks;
+    sk.scales = scales;
+    sk.out1 = gm[i];
+    sk.ld1 = ldh;
+    sk.part = tbg.a[i].gpart;
+    sk.part_n = p->T_t;
+    sk.r_max = p->r_max;
+    sk.pieces = token_col_blocks(projs[i].N);
+  }
+  if (launch_g_finish_group(gf, p->n_titems, s) != hipSuccess) return DSV_ERR_DEVICE;
+
+  // 4. chunk partials of x^T g (dA), every projection
+  TokenReduceGroup tag{};
+  tag.n = n_proj;
+  for (int i = 0; i < n_proj; ++i) {
+    const dsv_bwd_proj& q = projs[i];
+    TokenReduceArgs& ta = tag.a[i];
     ta.P = static_cast<const uint16_t*>(q.X);
     ta.ldp = q.K;
     ta.prow = p->dptr(L.train_rows);
     ta.Q = gm[i];
     ta.ldq = ldh;
+    ta.chunks = p->dptr(L.chunks);
+    ta.ranks = ranks;
     ta.C = q.K;
+    ta.r_max = p->r_max;
     ta.part = at<float>(wsb + base[i], w[i].part_a);
     ta.keep = keep[i];  // dA contracts the masked input
     ta.keep_words = (q.K + 31) / 32;
+    tag.yoff[i + 1] = tag.yoff[i] + token_col_blocks(q.K);
   }
-  for (int k = 0; k < trg.n; ++k) trg.yoff[k + 1] = trg.yoff[k] + token_col_blocks(trg.a[k].C);
-  if (launch_token_reduce_group(trg, p->n_chunks, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
+  if (launch_token_reduce_group(tag, p->n_chunks, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
 
-  // 4. fixed-order sums into dB (scaled by s_a) and dA, every projection
+  // 5. fixed-order sums into dB (scaled by s_a) and dA, every projection
   ReduceOutGroup og{};
   og.n = 2 * n_proj;
   for (int i = 0; i < n_proj; ++i) {
-    og.a[2 * i] = ReduceOutArgs{trg.a[2 * i].part, projs[i].N, scales, 0, projs[i].dB, 1.f};
-    og.a[2 * i + 1] = ReduceOutArgs{trg.a[2 * i + 1].part, projs[i].K, nullptr, 1, projs[i].dA,
+    og.a[2 * i] = ReduceOutArgs{tbg.a[i].part, projs[i].N, scales, 0, projs[i].dB, 1.f};
+    og.a[2 * i + 1] = ReduceOutArgs{tag.a[i].part, projs[i].K, nullptr, 1, projs[i].dA,
                                     dropping ? ds[i].scale : 1.f};
   }
   if (launch_reduce_out_group(og, p->r_max, p->r_train, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr), p->dptr(L.tad_chunks),
                               ranks, accumulate, s) != hipSuccess)
     return DSV_ERR_DEVICE;
 
-  // 5. every dX GEMM in one launch, longest contraction first (projections with a
+  // 6. every dX GEMM in one launch, longest contraction first (projections with a
   //    transposed weight in one NT launch, the others in one NN launch)
   int32_t Cs[DSV_MAX_GROUP], order[DSV_MAX_GROUP];
   for (int i = 0; i < n_proj; ++i) Cs[i] = projs[i].N;

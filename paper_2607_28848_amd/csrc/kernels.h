@@ -122,6 +122,10 @@ inline size_t skinny_part_bytes(int32_t C, int32_t split_items, int64_t n, int32
 
 // Per-chunk fp32 partial sums over training tokens:
 //   part[chunk][c][j] = sum_{t in chunk} P[prow(t)][c] Q[t][j]
+// With B (the g launch, P = dY), the same workgroup also contracts the P rows
+// it stages with the adapter's B over its 256-column block cb:
+//   gpart[cb][t][j] = sum_{c in block cb} P[t][c] B_a[c][j]
+// (g = s_a dy B_a once the blocks are summed in order, by launch_g_finish_group).
 struct TokenReduceArgs {
   const uint16_t* P;
   int64_t ldp;
@@ -134,6 +138,9 @@ struct TokenReduceArgs {
   float* part;
   const uint32_t* keep;  // dropout mask of P's elements (compact rows), nullptr: none
   int32_t keep_words;
+  const uint16_t* B;     // g launch: adapter stacks [n_ad][C][r_max]
+  float* gpart;          // g launch: [token_col_blocks(C)][gpart_n][r_max]
+  int32_t gpart_n;       // T_t
 };
 
 // Grouped launches: one kernel runs the same step of up to kMaxGroup
@@ -167,15 +174,6 @@ struct TokenReduceGroup {
   int32_t yoff[2 * kMaxGroup + 1];  // prefix of the kTokenCols-column blocks
   int32_t n;
 };
-struct TransposeArgs {
-  const uint16_t* B;  // [n_ad][N][r_max]
-  int32_t N;
-  uint16_t* Bt;       // [n_tads][r_max][N]
-};
-struct TransposeGroup {
-  TransposeArgs a[kMaxGroup];
-  int32_t n;
-};
 // GEMM group: whole 256x256 tiles, workgroups [off[p], off[p+1]) take the
 // tiles of projection a[p] (XCD-major within the projection).
 struct GemmGroup {
@@ -206,18 +204,12 @@ hipError_t launch_gemm_nn(const GemmArgs& a, int tm, int tn, hipStream_t s);
 // Rank-r contractions: r_sel bounds the rank of every item's adapter (it sizes
 // the rank tiles); the partials of a split contraction have stride a.r_max.
 hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_sel, hipStream_t s);
-hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_sel, hipStream_t s);
 // shrink over items of <= 16 rows (the training items): recomputes h for the backward
 hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_sel, hipStream_t s);
 hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* B, int32_t N,
                                 int32_t r_max, const int32_t* items, int32_t n_items,
                                 const int32_t* gather_rows, const int32_t* ranks,
                                 const float* scales, float* delta, hipStream_t s);
-// Both token reductions of a backward (dB partials, dA partials) in one launch.
-// r_sel: the largest rank of a training adapter (sizes the rank tiles; the
-// partials keep the r_max stride).
-hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
-                               int32_t r_sel, hipStream_t s);
 // Fixed-order sum of one reduction's chunk partials into its output.
 struct ReduceOutArgs {
   const float* part;
@@ -235,23 +227,26 @@ struct ReduceOutGroup {
 hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, int32_t r_max, int32_t r_sel,
                              const int32_t* train_ads, int32_t n_tads, const int32_t* tad_ptr,
                              const int32_t* tad_chunks, const int32_t* ranks, int32_t accumulate, hipStream_t s);
-hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
-                              int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s);
-
 // Grouped forms (n >= 1 entries filled).
 hipError_t launch_shrink_group(const SkinnyGroup& g, int32_t n_items, int32_t r_sel, hipStream_t s);
-hipError_t launch_gmat_group(const SkinnyGroup& g, int32_t n_items, int32_t r_sel, hipStream_t s);
 hipError_t launch_shrink_train_group(const SkinnyGroup& g, int32_t n_items, int32_t r_sel, hipStream_t s);
 hipError_t launch_gather_group(const GatherGroup& g, int64_t ldh, int32_t r_max, const int32_t* items,
                                int32_t n_items, const int32_t* gather_rows, const int32_t* ranks,
                                const float* scales, hipStream_t s);
-// entries 2p and 2p+1: the dB and dA reductions of projection p (all with one r_max)
+// Token reductions of a backward, every entry with one r_max.  r_sel: the
+// largest rank of a training adapter (sizes the rank tiles; the partials keep
+// the r_max stride).  Either every entry carries B (the dB reductions, which
+// also write the g partials of their column blocks; no dropout mask) or none
+// does (the dA reductions).
 hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s);
+// g = s_a * (sum of the column blocks' partials, in block order), rounded once
+// to bf16, for every projection of the group: entry p sums a[p].pieces
+// partials of a[p].part ([pieces][part_n][r_max]) over the items (compact
+// training rows of one adapter) and stores a[p].out1[row][j], j < r_a.
+hipError_t launch_g_finish_group(const SkinnyGroup& g, int32_t n_items, hipStream_t s);
 hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, int32_t r_sel, const int32_t* train_ads,
                                    int32_t n_tads, const int32_t* tad_ptr, const int32_t* tad_chunks,
                                    const int32_t* ranks, int32_t accumulate, hipStream_t s);
-hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const int32_t* train_ads,
-                                  int32_t n_tads, const int32_t* ranks, hipStream_t s);
 hipError_t launch_gemm_group_nt(const GemmGroup& g, hipStream_t s);
 hipError_t launch_gemm_group_nn(const GemmGroup& g, hipStream_t s);
 

@@ -11,11 +11,13 @@
 //                    groups add s_a h B_a^T in the prologue, gathered rows add
 //                    their fp32 term; one rounding to bf16 at the end.
 // Backward (Sec. 3.2 backward of the training rows):
-//   transpose_b/h    small transposed copies of B_a and H_save.
-//   gmat             g = s_a dy B_a (contraction over N).
-//   token_reduce     fp32 per-chunk partials of dy^T h and x^T g.
+//   token_reduce     fp32 per-chunk partials of dy^T h (dB) that also
+//                    contract the dy rows they stage with B_a: per-block
+//                    partials of g = s_a dy B_a, so dy is read once for both.
+//   g finish         fixed-order sum of g's block partials, rounded once.
+//   token_reduce     fp32 per-chunk partials of x^T g (dA).
 //   reduce_out       fixed-order sum of the partials into dB / dA.
-//   gemm (NN)        dx = dy W + g A_a (prologue adds g A_a).
+//   gemm (NT / NN)   dx = dy W + g A_a (prologue adds g A_a).
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
@@ -1307,8 +1309,19 @@ __global__ __launch_bounds__(256) void skinny_finish_kernel(SkinnyGroup G) {
   const int r = g.ranks[a];
   for (int idx = threadIdx.x; idx < cnt * r; idx += 256) {
     const int row = idx / r, j = idx - row * r;
+    const float* src = g.part + (int64_t)(begin + row) * g.r_max + j;
+    const int64_t stride = (int64_t)g.part_n * g.r_max;
+    // eight loads in flight, added in piece order (the same sum as one at a time)
     float sum = 0.f;
-    for (int q = 0; q < g.pieces; ++q) sum += g.part[((int64_t)q * g.part_n + begin + row) * g.r_max + j];
+    int q = 0;
+    for (; q + 8 <= g.pieces; q += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = src[(q + u) * stride];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += v[u];
+    }
+    for (; q < g.pieces; ++q) sum += src[q * stride];
     skinny_store<MODE>(g, a, begin, row, j, sum);
   }
 }
@@ -1399,15 +1412,23 @@ __global__ __launch_bounds__(256) void gather_expand_kernel(
 // ---------------------------------------------------------------------------
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-template <int NJ, bool DROP>
+// GP (the dB reductions, P = dY): the workgroup also writes the g partial of
+// its column block.  The adapter's B rows of the block sit in LDS rank-major
+// (bts[j][c], kBtRow-byte rows), loaded once; in every step waves 0 and 1
+// take the step's tokens 0-15 and 16-31 as MFMA A-operands (rows read from the
+// staged P image as they are, 16 bytes = 8 columns per lane) against B's
+// columns, 8 contractions of 32 columns, and store the [16][r] partial.
+constexpr int kBtRow = kTokenCols * 2 + 16;
+
+template <int NJ, bool DROP, bool GP>
 __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
   constexpr int TS = 32;                     // tokens per step
   constexpr int STAGE = TS * kTokenCols * 2;  // P bytes per stage
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE + (GP ? 16 * NJ * kBtRow : 0)];
   int k = 0;  // the reduction: blockIdx.y runs over every reduction's column blocks
   while (k + 1 < G.n && (int)blockIdx.y >= G.yoff[k + 1]) ++k;
   const TokenReduceArgs g = G.a[k];
-  const int cbase = ((int)blockIdx.y - G.yoff[k]) * kTokenCols;
+  const int cb = (int)blockIdx.y - G.yoff[k], cbase = cb * kTokenCols;
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
   const int a = ck[0], begin = ck[1], cnt = ck[2];
@@ -1463,6 +1484,25 @@ __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
       m[e] = g.keep[(int64_t)(begin + t) * g.keep_words + kw];
     }
   };
+  if constexpr (GP) {
+    // B_a[c][j] of the block's columns into bts[j][c]; zero past the rank and
+    // past C (published by the first step's barrier)
+    char* bts = smem + 2 * STAGE;
+    const uint16_t* Ba = g.B + (int64_t)a * g.C * g.r_max;
+    const bool b16 = (g.r_max & 7) == 0;  // a rank octet is one aligned 16-byte load
+    for (int idx = tid; idx < kTokenCols * 2 * NJ; idx += 512) {
+      const int cl = idx % kTokenCols, jo = idx / kTokenCols;  // column, rank octet
+      const int c = cbase + cl, nv = min(8, r - 8 * jo);
+      u32x4 v = zero4();
+      if (c < g.C && nv > 0) {
+        const uint16_t* src = Ba + (int64_t)c * g.r_max + 8 * jo;
+        v = (b16 && nv == 8) ? ld16(src) : ld8_masked(src, 1, nv);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        *reinterpret_cast<uint16_t*>(bts + (8 * jo + e) * kBtRow + 2 * cl) = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    }
+  }
   auto tr_read = [&](const char* p) -> u32x2 {
     const s16x4 h = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
     return u32x2{(uint32_t)(uint16_t)h[0] | ((uint32_t)(uint16_t)h[1] << 16),
@@ -1511,6 +1551,34 @@ __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
 #pragma unroll
       for (int jt = 0; jt < NJ; ++jt)
         acc[ct][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(x[ct]), as_bf(qu[jt]), acc[ct][jt], 0, 0, 0);
+    }
+    if constexpr (GP) {
+      if (wave < 2) {
+        const char* bts = smem + 2 * STAGE;
+        const int t = 16 * wave + lam;  // the lane's token row of the step (A-operand row)
+        f32x4 ga[NJ];
+#pragma unroll
+        for (int jt = 0; jt < NJ; ++jt) ga[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll 2
+        for (int kc = 0; kc < kTokenCols / 32; ++kc) {
+          const int c8 = 4 * kc + gq;  // the lane's 16-byte column chunk
+          const u32x4 av = *reinterpret_cast<const u32x4*>(sb + t * (kTokenCols * 2) + 16 * (c8 ^ (2 * (t & 3))));
+#pragma unroll
+          for (int jt = 0; jt < NJ; ++jt) {
+            const u32x4 bv = *reinterpret_cast<const u32x4*>(bts + (16 * jt + lam) * kBtRow + 16 * c8);
+            ga[jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av), as_bf(bv), ga[jt], 0, 0, 0);
+          }
+        }
+        // ga[jt][v]: token 16 wave + 4 gq + v of the step, rank 16 jt + lam
+        float* gp = g.gpart + ((int64_t)cb * g.gpart_n + begin) * g.r_max;
+#pragma unroll
+        for (int jt = 0; jt < NJ; ++jt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int tok = step * TS + 16 * wave + 4 * gq + v, j = 16 * jt + lam;
+            if (tok < cnt && j < r) gp[(int64_t)tok * g.r_max + j] = ga[jt][v];
+          }
+      }
     }
   };
   u32x4 q0[NJ], q1[NJ];
@@ -1563,28 +1631,25 @@ __global__ __launch_bounds__(256) void reduce_out_kernel(ReduceOutGroup G, int32
   // threads cover the ranks below r_sel (>= every training adapter's rank)
   const int c = (int)(idx / r_sel), j = (int)(idx % r_sel);
   if (c >= C || j >= r) return;
+  // eight chunk partials in flight, added in chunk order (the same sum as one
+  // at a time); the chunk ids are the same for the whole workgroup
+  const float* src = g.part + (int64_t)c * r_max + j;
+  const int64_t cs = (int64_t)C * r_max;
+  const int p1 = tad_ptr[ta + 1];
   float sum = 0.f;
-  for (int p = tad_ptr[ta]; p < tad_ptr[ta + 1]; ++p)
-    sum += g.part[((int64_t)tad_chunks[p] * C + c) * r_max + j];
+  int p = tad_ptr[ta];
+  for (; p + 8 <= p1; p += 8) {
+    float v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) v[u] = src[tad_chunks[p + u] * cs];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) sum += v[u];
+  }
+  for (; p < p1; ++p) sum += src[tad_chunks[p] * cs];
   if (g.scales) sum *= g.scales[a];
   sum *= g.post;
   float* o = g.a_layout ? g.out + ((int64_t)a * r_max + j) * C + c : g.out + ((int64_t)a * C + c) * r_max + j;
   *o = accumulate ? *o + sum : sum;
-}
-
-// Bt[slot][j][n] = B[a][n][j]  (j < r_a; other rows zero).
-__global__ __launch_bounds__(256) void transpose_b_kernel(TransposeGroup G, int32_t r_max,
-                                                          const int32_t* __restrict__ train_ads, int32_t n_tads,
-                                                          const int32_t* __restrict__ ranks) {
-  const int pj = (int)blockIdx.z / n_tads, slot = (int)blockIdx.z - pj * n_tads, j = blockIdx.y;
-  const uint16_t* __restrict__ B = G.a[pj].B;
-  uint16_t* __restrict__ Bt = G.a[pj].Bt;
-  const int32_t N = G.a[pj].N;
-  const int n = blockIdx.x * 256 + threadIdx.x;
-  if (n >= N) return;
-  const int a = train_ads[slot];
-  const uint16_t v = (j < ranks[a]) ? B[((int64_t)a * N + n) * r_max + j] : (uint16_t)0;
-  Bt[((int64_t)slot * r_max + j) * N + n] = v;
 }
 
 }  // namespace
@@ -1772,20 +1837,12 @@ hipError_t launch_shrink(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hi
   return launch_skinny<0, kRankItemRows>(one(a), n_items, r_max, s);
 }
 
-hipError_t launch_gmat(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
-  return launch_skinny<1, kItemRows>(one(a), n_items, r_max, s);
-}
-
 hipError_t launch_shrink_train(const SkinnyArgs& a, int32_t n_items, int32_t r_max, hipStream_t s) {
   return launch_skinny<0, kItemRows>(one(a), n_items, r_max, s);
 }
 
 hipError_t launch_shrink_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
   return launch_skinny<0, kRankItemRows>(g, n_items, r_max, s);
-}
-
-hipError_t launch_gmat_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
-  return launch_skinny<1, kItemRows>(g, n_items, r_max, s);
 }
 
 hipError_t launch_shrink_train_group(const SkinnyGroup& g, int32_t n_items, int32_t r_max, hipStream_t s) {
@@ -1815,42 +1872,51 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
   return launch_gather_group(g, ldh, r_max, items, n_items, gather_rows, ranks, scales, s);
 }
 
-template <bool DROP>
+template <bool DROP, bool GP>
 void launch_token_reduce_nj(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s) {
   const dim3 grid(n_chunks, g.yoff[g.n]);
   if (r_sel <= 16)
-    hipLaunchKernelGGL((token_reduce_kernel<1, DROP>), grid, dim3(512), 0, s, g);
+    hipLaunchKernelGGL((token_reduce_kernel<1, DROP, GP>), grid, dim3(512), 0, s, g);
   else if (r_sel <= 32)
-    hipLaunchKernelGGL((token_reduce_kernel<2, DROP>), grid, dim3(512), 0, s, g);
+    hipLaunchKernelGGL((token_reduce_kernel<2, DROP, GP>), grid, dim3(512), 0, s, g);
   else
-    hipLaunchKernelGGL((token_reduce_kernel<4, DROP>), grid, dim3(512), 0, s, g);
+    hipLaunchKernelGGL((token_reduce_kernel<4, DROP, GP>), grid, dim3(512), 0, s, g);
 }
 
 // A launch whose reductions include a masked one runs the kernel with the
-// masking code; it masks the reductions that carry a mask.
+// masking code; it masks the reductions that carry a mask.  A launch of
+// reductions that carry B (the dB side) also writes the g partials.
 hipError_t launch_token_reduce_group(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s) {
   if (n_chunks <= 0 || g.n <= 0) return hipSuccess;
   if (g.n > 2 * kMaxGroup || g.yoff[0] != 0 || r_sel < 1 || r_sel > g.a[0].r_max) return hipErrorInvalidValue;
   bool any_keep = false;
+  int n_b = 0;
   for (int k = 0; k < g.n; ++k) {
     if (g.a[k].r_max != g.a[0].r_max || g.yoff[k + 1] - g.yoff[k] != token_col_blocks(g.a[k].C))
       return hipErrorInvalidValue;
     any_keep |= g.a[k].keep != nullptr;
+    if (g.a[k].B != nullptr) {
+      if (g.a[k].gpart == nullptr || g.a[k].gpart_n < 1) return hipErrorInvalidValue;
+      ++n_b;
+    }
   }
-  if (any_keep) launch_token_reduce_nj<true>(g, n_chunks, r_sel, s);
-  else launch_token_reduce_nj<false>(g, n_chunks, r_sel, s);
+  if (n_b != 0 && (n_b != g.n || any_keep)) return hipErrorInvalidValue;
+  if (n_b) launch_token_reduce_nj<false, true>(g, n_chunks, r_sel, s);
+  else if (any_keep) launch_token_reduce_nj<true, false>(g, n_chunks, r_sel, s);
+  else launch_token_reduce_nj<false, false>(g, n_chunks, r_sel, s);
   return hipGetLastError();
 }
 
-hipError_t launch_token_reduce(const TokenReduceArgs& a0, const TokenReduceArgs& a1, int32_t n_chunks,
-                               int32_t r_sel, hipStream_t s) {
-  TokenReduceGroup g{};
-  g.a[0] = a0;
-  g.a[1] = a1;
-  g.yoff[1] = token_col_blocks(a0.C);
-  g.yoff[2] = g.yoff[1] + token_col_blocks(a1.C);
-  g.n = 2;
-  return launch_token_reduce_group(g, n_chunks, r_sel, s);
+hipError_t launch_g_finish_group(const SkinnyGroup& g0, int32_t n_items, hipStream_t s) {
+  if (n_items <= 0 || g0.n <= 0) return hipSuccess;
+  if (g0.n > kMaxGroup) return hipErrorInvalidValue;
+  SkinnyGroup g = g0;
+  for (int p = 0; p < g.n; ++p) {
+    if (g.a[p].part == nullptr || g.a[p].pieces < 1 || g.a[p].out1 == nullptr) return hipErrorInvalidValue;
+    g.slot_proj[p] = p;
+  }
+  hipLaunchKernelGGL((skinny_finish_kernel<1>), dim3(n_items, g.n), dim3(256), 0, s, g);
+  return hipGetLastError();
 }
 
 hipError_t launch_reduce_out_group(const ReduceOutGroup& g, int32_t r_max, int32_t r_sel, const int32_t* train_ads,
@@ -1874,25 +1940,6 @@ hipError_t launch_reduce_out(const ReduceOutArgs& o0, const ReduceOutArgs& o1, i
   g.a[1] = o1;
   g.n = 2;
   return launch_reduce_out_group(g, r_max, r_sel, train_ads, n_tads, tad_ptr, tad_chunks, ranks, accumulate, s);
-}
-
-hipError_t launch_transpose_group(const TransposeGroup& g, int32_t r_max, const int32_t* train_ads,
-                                  int32_t n_tads, const int32_t* ranks, hipStream_t s) {
-  if (n_tads <= 0 || g.n <= 0) return hipSuccess;
-  if (g.n > kMaxGroup) return hipErrorInvalidValue;
-  int32_t nmax = 0;
-  for (int p = 0; p < g.n; ++p) nmax = g.a[p].N > nmax ? g.a[p].N : nmax;
-  hipLaunchKernelGGL(transpose_b_kernel, dim3((nmax + 255) / 256, r_max, n_tads * g.n), dim3(256), 0, s, g, r_max,
-                     train_ads, n_tads, ranks);
-  return hipGetLastError();
-}
-
-hipError_t launch_transpose_b(const uint16_t* B, int32_t N, int32_t r_max, const int32_t* train_ads,
-                              int32_t n_tads, const int32_t* ranks, uint16_t* Bt, hipStream_t s) {
-  TransposeGroup g{};
-  g.a[0] = TransposeArgs{B, N, Bt};
-  g.n = 1;
-  return launch_transpose_group(g, r_max, train_ads, n_tads, ranks, s);
 }
 
 hipError_t launch_gemm_group_nt(const GemmGroup& g, hipStream_t s) { return launch_gemm_group<false>(g, s); }
