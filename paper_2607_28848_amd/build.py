@@ -21,7 +21,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdsv.so")
-SOURCES = ["plan.cpp", "api.cpp", "kernels_bf16.hip", "kernels_f32.hip", "optim.hip", "dropout.hip", "scratch.hip"]
+SOURCES = ["plan.cpp", "api.cpp", "gemm_bf16.hip", "kernels_bf16.hip", "kernels_f32.hip", "optim.hip", "dropout.hip", "scratch.hip"]
 HOST_SOURCES = [s for s in SOURCES if s.endswith(".cpp")]
 ASAN_DIR = os.path.join(PKG, "_build", "host_asan")
 ASAN_LIB = os.path.join(ASAN_DIR, "libdsv.so")
