@@ -329,6 +329,8 @@ def main():
         d["wsf"] = torch.empty(max(dsv.fwd_workspace_bytes(probe, code, K, N), 256), dtype=torch.uint8, device=dev)
         d["wsb"] = torch.empty(max(dsv.bwd_workspace_bytes(probe, code, K, N, dropout=args.dropout > 0), 256),
                                dtype=torch.uint8, device=dev)
+        # the dropout mask of the step, drawn by the forward and read by the backward
+        d["mask"] = torch.empty(max(dsv.dropout_mask_words(probe, K), 1), dtype=torch.int32, device=dev)
         P.append(d)
     torch.cuda.synchronize()
     log("inputs resident on %s" % torch.cuda.get_device_name(dev))
@@ -393,7 +395,8 @@ def main():
             if groups is not None:
                 drs = None
                 if args.dropout > 0:  # one mask stream per projection and step
-                    drs = [(dsv.Dropout * (hi - lo))(*[dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p)
+                    drs = [(dsv.Dropout * (hi - lo))(*[dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p,
+                                                                   ptr(P[p]["mask"]))
                                                         for p in range(lo, hi)]) for lo, hi in groups]
                 for gi, (lo, hi) in enumerate(groups):
                     if drs is None:
@@ -422,7 +425,7 @@ def main():
                 K, N = proj.K, proj.N
                 if args.dropout > 0:
                     # one mask stream per projection and step: offset = step * projections + p
-                    dr = ctypes.byref(dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p))
+                    dr = ctypes.byref(dsv.Dropout(args.dropout, 1234, i * len(w.projections) + p, ptr(d["mask"])))
                     rc = lib.dsv_cobatch_fwd_dropout(h, code, K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]),
                                                      ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]), dr, ptr(d["wsf"]),
                                                      d["wsf"].numel(), sh)
@@ -560,7 +563,7 @@ def main():
 
             # LoRA dropout 0.05 on the training rows (the fine-tuning setting of Sec. 4.1):
             # the whole step (forward + backward of every projection, in the bench's launch
-            # mode) with and without it.
+            # mode) with and without it; the backward reads the mask the forward drew.
             wsf_d = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
                                  dtype=torch.uint8, device=dev) for lo, hi in gl]
             wsb_d = [torch.empty(max(dsv.bwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
@@ -569,12 +572,12 @@ def main():
             def step_all(drop):
                 for gi, (lo, hi) in enumerate(gl):
                     ds = [P[p] for p in range(lo, hi)]
-                    drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
+                    drops = None if drop is None else [(drop, 1234, p, P[p]["mask"]) for p in range(lo, hi)]
                     dsv.cobatch_fwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["Y"], d["H"]) for d in ds],
                                             workspace=wsf_d[gi], stream=stream, dropouts=drops)
                 for gi, (lo, hi) in enumerate(gl):
                     ds = [P[p] for p in range(lo, hi)]
-                    drops = None if drop is None else [(drop, 1234, p) for p in range(lo, hi)]
+                    drops = None if drop is None else [(drop, 1234, p, P[p]["mask"]) for p in range(lo, hi)]
                     dsv.lora_bwd_grouped(probe_dev, [(d["X"], d["W"], d["A"], d["B"], d["H"], d["dY"], d["dA"], d["dB"],
                                                       d["dX"]) for d in ds],
                                          workspace=wsb_d[gi], stream=stream, dropouts=drops,

@@ -398,6 +398,14 @@ bool dropout_spec(const dsv_dropout* d, DropoutSpec* out) {
   return true;
 }
 
+// The caller's mask buffer must hold 32-bit words.
+bool mask_aligned(const dsv_dropout* d) { return !d || !d->mask || (reinterpret_cast<uintptr_t>(d->mask) & 3) == 0; }
+
+// Where a projection's mask lives: the caller's buffer, else the workspace.
+uint32_t* mask_buffer(const dsv_dropout* d, void* ws_keep) {
+  return d && d->mask ? d->mask : static_cast<uint32_t*>(ws_keep);
+}
+
 // noalloc: the allocation-free form (dsv_cobatch_fwd_noalloc): the workspace is
 // the library's device scratch, the GEMM plan splits no tile along the
 // contraction (a split needs a partial tile per piece, tens of MB), and no
@@ -409,6 +417,7 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   if (rc != DSV_OK) return rc;
   DropoutSpec ds{};
   if (drop && !dropout_spec(drop, &ds)) return DSV_ERR_RANGE;
+  if (!mask_aligned(drop)) return DSV_ERR_ARG;
   const bool dropping = drop && drop->p > 0.0 && p->T_t > 0;
   if (!p->d_meta) return DSV_ERR_ARG;
   if (p->T == 0) return DSV_OK;  // empty batch: nothing to read or write
@@ -426,11 +435,12 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   hipError_t e = hipSuccess;
 
-  // 0. dropout mask of the training rows' adapter input.
-  const uint32_t* keep = dropping ? at<uint32_t>(workspace, ws.keep) : nullptr;
+  // 0. dropout mask of the training rows' adapter input (into the caller's
+  //    buffer when one is given, for the backward to read).
+  uint32_t* keep_w = dropping ? mask_buffer(drop, at<uint32_t>(workspace, ws.keep)) : nullptr;
+  const uint32_t* keep = keep_w;
   const int32_t keep_words = (K + 31) / 32;
-  if (dropping && (e = launch_dropout_mask(at<uint32_t>(workspace, ws.keep), p->T_t, K, ds, s)) != hipSuccess)
-    return DSV_ERR_DEVICE;
+  if (dropping && (e = launch_dropout_mask(keep_w, p->T_t, K, ds, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   if (dt == DSV_F32) {
     F32Args a{};
@@ -537,6 +547,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   if (rc != DSV_OK) return rc;
   DropoutSpec ds{};
   if (drop && !dropout_spec(drop, &ds)) return DSV_ERR_RANGE;
+  if (!mask_aligned(drop)) return DSV_ERR_ARG;
   const bool dropping = drop && drop->p > 0.0;
   if (accumulate != 0 && accumulate != 1) return DSV_ERR_RANGE;
   if (!p->d_meta) return DSV_ERR_ARG;
@@ -557,10 +568,12 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   hipError_t e = hipSuccess;
 
-  // 0. the forward's dropout mask, regenerated from the same seed and offset.
-  uint32_t* keep = dropping ? at<uint32_t>(workspace, ws.keep) : nullptr;
+  // 0. the forward's dropout mask: the caller's buffer, or regenerated from
+  //    the same seed and offset.
+  uint32_t* keep = dropping ? mask_buffer(drop, at<uint32_t>(workspace, ws.keep)) : nullptr;
   const int32_t keep_words = (K + 31) / 32;
-  if (dropping && (e = launch_dropout_mask(keep, p->T_t, K, ds, s)) != hipSuccess) return DSV_ERR_DEVICE;
+  if (dropping && !drop->mask && (e = launch_dropout_mask(keep, p->T_t, K, ds, s)) != hipSuccess)
+    return DSV_ERR_DEVICE;
 
   if (dt == DSV_F32) {
     F32Args a{};
@@ -883,6 +896,7 @@ int group_dropout(const dsv_dropout* drops, int32_t n, int32_t T_t, DropoutSpec*
   if (!drops) return DSV_OK;
   for (int i = 0; i < n; ++i) {
     if (!dropout_spec(&drops[i], &ds[i])) return DSV_ERR_RANGE;
+    if (!mask_aligned(&drops[i])) return DSV_ERR_ARG;
     if (drops[i].p > 0.0 && T_t > 0) *any = true;
   }
   return DSV_OK;
@@ -935,11 +949,20 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   const float* scales = reinterpret_cast<const float*>(p->dptr(L.scales));
   const int64_t ldh = ld_rank(p->r_max);
 
-  // 0. dropout masks of the training rows' adapter input
-  if (dropping)
-    for (int i = 0; i < n_proj; ++i)
-      if (launch_dropout_mask(at<uint32_t>(wsb + base[i], w[i].keep), p->T_t, projs[i].K, ds[i], s) != hipSuccess)
-        return DSV_ERR_DEVICE;
+  // 0. dropout masks of the training rows' adapter input, every projection in
+  //    one launch (into the caller's buffers where given)
+  uint32_t* keepg[DSV_MAX_GROUP] = {};
+  if (dropping) {
+    DropoutMaskGroup mg{};
+    mg.n = n_proj;
+    for (int i = 0; i < n_proj; ++i) {
+      keepg[i] = mask_buffer(&drops[i], at<uint32_t>(wsb + base[i], w[i].keep));
+      mg.bits[i] = keepg[i];
+      mg.K[i] = projs[i].K;
+      mg.d[i] = ds[i];
+    }
+    if (launch_dropout_mask_group(mg, p->T_t, s) != hipSuccess) return DSV_ERR_DEVICE;
+  }
 
   // 1. shrink of every projection in one launch
   SkinnyGroup sg{};
@@ -966,7 +989,7 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     sk.r_max = p->r_max;
     sk.split_items = p->n_shrink;
     if (dropping) {
-      sk.keep = at<uint32_t>(wsb + base[i], w[i].keep);
+      sk.keep = keepg[i];
       sk.keep_words = (q.K + 31) / 32;
       sk.drop_scale = ds[i].scale;
     }
@@ -1079,13 +1102,21 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   uint32_t* keep[DSV_MAX_GROUP];
   for (int i = 0; i < n_proj; ++i) {
     gm[i] = at<uint16_t>(wsb + base[i], w[i].g);
-    keep[i] = dropping ? at<uint32_t>(wsb + base[i], w[i].keep) : nullptr;
+    keep[i] = dropping ? mask_buffer(&drops[i], at<uint32_t>(wsb + base[i], w[i].keep)) : nullptr;
   }
 
-  // 0. the forward's dropout masks, regenerated from the same seeds and offsets
-  if (dropping)
-    for (int i = 0; i < n_proj; ++i)
-      if (launch_dropout_mask(keep[i], p->T_t, projs[i].K, ds[i], s) != hipSuccess) return DSV_ERR_DEVICE;
+  // 0. the forward's dropout masks: the caller's buffers, or regenerated from
+  //    the same seeds and offsets (one launch for those)
+  if (dropping) {
+    DropoutMaskGroup mg{};
+    mg.n = n_proj;
+    for (int i = 0; i < n_proj; ++i) {
+      mg.bits[i] = drops[i].mask ? nullptr : keep[i];
+      mg.K[i] = projs[i].K;
+      mg.d[i] = ds[i];
+    }
+    if (launch_dropout_mask_group(mg, p->T_t, s) != hipSuccess) return DSV_ERR_DEVICE;
+  }
 
   // 1. h of the training rows for projections whose forward kept no H_save
   const uint16_t* hs[DSV_MAX_GROUP];

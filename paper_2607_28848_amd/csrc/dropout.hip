@@ -38,34 +38,69 @@ __device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint32_t k0, uint32
 }
 
 // One 32-bit word of the kept-element bitmask per thread: bit b of word w of
-// row i keeps column 32 w + b.
-__global__ __launch_bounds__(256) void dropout_mask_kernel(uint32_t* __restrict__ bits, int32_t Tt,
-                                                           int32_t words, uint32_t thr, uint32_t s0, uint32_t s1,
-                                                           uint32_t o0, uint32_t o1) {
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= (int64_t)Tt * words) return;
-  const uint32_t i = (uint32_t)(idx / words), w = (uint32_t)(idx % words);
+// row i keeps column 32 w + b.  The grid covers every projection of the group
+// back to back, each in whole workgroups (entry p owns workgroups
+// [blk[p], blk[p + 1])), so the entry is the same for a whole workgroup.
+struct MaskLaunch {
+  uint32_t* bits[kMaxGroup];
+  int32_t words[kMaxGroup];
+  uint32_t thr[kMaxGroup], s0[kMaxGroup], s1[kMaxGroup], o0[kMaxGroup], o1[kMaxGroup];
+  int64_t total[kMaxGroup];  // Tt * words
+  int32_t blk[kMaxGroup + 1];
+  int32_t n;
+};
+
+__global__ __launch_bounds__(256) void dropout_mask_kernel(MaskLaunch L) {
+  int p = 0;
+  while (p + 1 < L.n && (int32_t)blockIdx.x >= L.blk[p + 1]) ++p;
+  const int64_t loc = (int64_t)((int32_t)blockIdx.x - L.blk[p]) * 256 + threadIdx.x;
+  if (loc >= L.total[p]) return;
+  const uint32_t words = (uint32_t)L.words[p];
+  const uint32_t i = (uint32_t)(loc / words), w = (uint32_t)(loc % words);
   uint32_t m = 0;
 #pragma unroll
   for (int q = 0; q < 8; ++q) {
-    uint32_t c[4] = {8u * w + (uint32_t)q, i, o0, o1};
-    philox4x32_10(c, s0, s1);
+    uint32_t c[4] = {8u * w + (uint32_t)q, i, L.o0[p], L.o1[p]};
+    philox4x32_10(c, L.s0[p], L.s1[p]);
 #pragma unroll
-    for (int e = 0; e < 4; ++e) m |= (c[e] >= thr ? 1u : 0u) << (4 * q + e);
+    for (int e = 0; e < 4; ++e) m |= (c[e] >= L.thr[p] ? 1u : 0u) << (4 * q + e);
   }
-  bits[idx] = m;
+  L.bits[p][loc] = m;
 }
 
 }  // namespace
 
-hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const DropoutSpec& d, hipStream_t s) {
-  if (Tt <= 0) return hipSuccess;
-  const int32_t words = (K + 31) / 32;
-  const int64_t n = (int64_t)Tt * words;
-  hipLaunchKernelGGL(dropout_mask_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, bits, Tt, words,
-                     d.thr, (uint32_t)d.seed, (uint32_t)(d.seed >> 32), (uint32_t)d.offset,
-                     (uint32_t)(d.offset >> 32));
+hipError_t launch_dropout_mask_group(const DropoutMaskGroup& g, int32_t Tt, hipStream_t s) {
+  if (Tt <= 0 || g.n <= 0) return hipSuccess;
+  if (g.n > kMaxGroup) return hipErrorInvalidValue;
+  MaskLaunch L{};
+  for (int p = 0; p < g.n; ++p) {
+    if (!g.bits[p]) continue;
+    const int q = L.n++;
+    L.bits[q] = g.bits[p];
+    L.words[q] = (g.K[p] + 31) / 32;
+    L.thr[q] = g.d[p].thr;
+    L.s0[q] = (uint32_t)g.d[p].seed;
+    L.s1[q] = (uint32_t)(g.d[p].seed >> 32);
+    L.o0[q] = (uint32_t)g.d[p].offset;
+    L.o1[q] = (uint32_t)(g.d[p].offset >> 32);
+    L.total[q] = (int64_t)Tt * L.words[q];
+    const int64_t end = L.blk[q] + (L.total[q] + 255) / 256;
+    if (end > INT32_MAX) return hipErrorInvalidValue;
+    L.blk[q + 1] = (int32_t)end;
+  }
+  if (L.n == 0 || L.blk[L.n] == 0) return hipSuccess;
+  hipLaunchKernelGGL(dropout_mask_kernel, dim3((unsigned)L.blk[L.n]), dim3(256), 0, s, L);
   return hipGetLastError();
+}
+
+hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const DropoutSpec& d, hipStream_t s) {
+  DropoutMaskGroup g{};
+  g.bits[0] = bits;
+  g.K[0] = K;
+  g.d[0] = d;
+  g.n = 1;
+  return launch_dropout_mask_group(g, Tt, s);
 }
 
 }  // namespace dsv

@@ -667,7 +667,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   // (vector-memory operations complete in order) rather than for both.  This
   // covers the forward form (h and B rows with contiguous ranks, r a multiple
   // of 16) for a wave that has rows in the group; anything else loads below.
-  const bool pre = kb == 0 && ngroups > 0 && g.lq_j == 1 && (g.lq_col & 3) == 0 && (g0_r & 15) == 0 &&
+  const bool pre = !DROP && kb == 0 && ngroups > 0 && g.lq_j == 1 && (g.lq_col & 3) == 0 && (g0_r & 15) == 0 &&
                    g0_hi > wm * WM && g0_lo < wm * WM + WM;
   u32x2v pre_h[FM], pre_b[FN];
   if (pre) {
@@ -738,10 +738,14 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
           acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq[j], af_lo[i], acc[i][j], 0, 0, 0);
     }
   };
+  // Under dropout (the DROP instantiation, launched only with a mask) the
+  // low-rank term is masked per element: it is built one 16-row block at a
+  // time in ordinary registers (below), masked there and added to the block's
+  // accumulators, which are still zero.
   // the prefetched step: its data arrive with the first K-step
   if (pre) lr_mfma(pre_h, pre_b, g0_lo, g0_hi, 4, g0_sc);
   // every other (group, 16-rank step) of the tile
-  for (int gi = 0; kb == 0 && gi < ngroups; ++gi) {
+  for (int gi = 0; !DROP && kb == 0 && gi < ngroups; ++gi) {
     const int a = gi == 0 ? g0_a : td[4 + 3 * gi], lo = gi == 0 ? g0_lo : td[5 + 3 * gi];
     const int hi = gi == 0 ? g0_hi : td[6 + 3 * gi];
     if (hi <= wm * WM || lo >= wm * WM + WM) continue;  // no row of this wave
@@ -772,21 +776,128 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   }
 
   // ---- dropout of the low-rank term (dX under LoRA dropout) --------------
-  // A 16-column block lies inside one 32-column mask word.
-  if (DROP && kb == 0 && g.keep != nullptr) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int row = wm * WM + 16 * i + (lane & 15);
+  // Row block i (rows wm*WM + 16i ..): t[j] = the unmasked term of its 8
+  // column blocks, the same MFMA sequence per element as the plain prologue
+  // (groups in order, 16-rank steps, bf16 hi then lo parts of s_a h); then
+  // element (row, col) keeps t * keep_scale where its mask bit is set, else 0.
+  // Column blocks 2h and 2h+1 of a wave share mask word (n0 + wn*WN)/32 + h
+  // (n0 and wn*WN are multiples of 32).  The next row block's h and mask
+  // words load while the current one is computed; a tile whose rows form one
+  // group of rank <= 16 loads its adapter's B fragments once.  The barrier per
+  // row block keeps the compiler from interleaving row blocks (and their
+  // registers).
+  if (DROP && kb == 0) {
+    const int bit0 = 4 * (lane >> 4);
+    const int wd0 = (n0 + wn * WN) >> 5;
+    const int jb0 = 4 * (lane >> 4);
+    const bool one = ngroups == 1 && g0_r <= 16;  // one group, one 16-rank step
+    auto load_b = [&](const uint16_t* lq, int jbc, int nvc, bool lq_vec, u32x2v (&bv)[FN]) {
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
-        const int c0 = n0 + wn * WN + 16 * j;
-        const int wd = c0 >> 5;
-        const uint32_t x = g.keep[(int64_t)(m0 + min(row, nrows - 1)) * g.keep_words + min(wd, g.keep_words - 1)];
-        const uint32_t mw = x & (0u - (uint32_t)(row < nrows && wd < g.keep_words));
-        const int bit = (c0 & 31) + 4 * (lane >> 4);
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[i][j][v] = ((mw >> (bit + v)) & 1u) ? acc[i][j][v] * g.keep_scale : 0.f;
+        const int col = n0 + wn * WN + 16 * j + (lane & 15);
+        const uint16_t* p = lq + (int64_t)jbc * g.lq_j + (int64_t)min(col, g.Nout - 1) * g.lq_col;
+        bv[j] = lq_vec ? *reinterpret_cast<const u32x2v*>(p) : ld4_sel(p, g.lq_j, nvc);
       }
+    };
+    u32x2v b1[FN];  // the single group's B fragments (one)
+    if (one) {
+      const int nv = min(4, g0_r - jb0);
+      load_b(g.Lq + (int64_t)g0_a * g.lq_ad, nv > 0 ? jb0 : 0, max(nv, 1),
+             (g0_r & 15) == 0 && g.lq_j == 1 && (g.lq_col & 3) == 0, b1);
+    }
+    // h of the single group's row and the mask words of row block i
+    auto load_row = [&](int i, u32x2v& hv, uint32_t (&mw)[FN / 2]) {
+      const int row = wm * WM + 16 * i + (lane & 15);
+      const int nv = min(4, g0_r - jb0);
+      const bool rin = row >= g0_lo && row < g0_hi;
+      const uint16_t* hp = g.Lp + (int64_t)(m0 + (rin ? row : g0_lo)) * g.ldl + (nv > 0 ? jb0 : 0);
+      hv = ((g0_r & 15) == 0) ? *reinterpret_cast<const u32x2v*>(hp) : ld4_sel(hp, 1, max(nv, 1));
+      const uint32_t* kr = g.keep + (int64_t)(m0 + min(row, nrows - 1)) * g.keep_words;
+#pragma unroll
+      for (int h = 0; h < FN / 2; ++h) mw[h] = kr[min(wd0 + h, g.keep_words - 1)];
+    };
+    u32x2v hv_n = u32x2v{0u, 0u};
+    uint32_t mw_n[FN / 2] = {0u, 0u, 0u, 0u};
+    load_row(0, hv_n, mw_n);
+    // t[j] += (s h) B for one (group, 16-rank step); rows outside [lo, hi) add zeros
+    auto lr_row = [&](f32x4 (&t)[FN], u32x2v hv, const u32x2v (&bv)[FN], int row, int lo, int hi, int nv,
+                      float sc) {
+      const u32x2v v = (row >= lo && row < hi && nv > 0) ? hv : u32x2v{0u, 0u};
+      uint32_t wh[2], wl[2];
+      bool any_lo = false;
+#pragma unroll
+      for (int d = 0; d < 2; ++d) {
+        const float x0 = sc * __uint_as_float(v[d] << 16);
+        const float x1 = sc * __uint_as_float(v[d] & 0xffff0000u);
+        const uint16_t h0 = f2bf(x0), h1 = f2bf(x1);
+        const uint16_t l0 = f2bf(x0 - bf2f(h0)), l1 = f2bf(x1 - bf2f(h1));
+        wh[d] = (uint32_t)h0 | ((uint32_t)h1 << 16);
+        wl[d] = (uint32_t)l0 | ((uint32_t)l1 << 16);
+        any_lo |= (wl[d] & 0x7fff7fffu) != 0u;
+      }
+      const s16x4v af_hi = __builtin_bit_cast(s16x4v, u32x2v{wh[0], wh[1]});
+      const s16x4v af_lo = __builtin_bit_cast(s16x4v, u32x2v{wl[0], wl[1]});
+      const bool lo_pass = __builtin_amdgcn_ballot_w64(any_lo) != 0;
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = n0 + wn * WN + 16 * j + (lane & 15);
+        const s16x4v bq = __builtin_bit_cast(s16x4v, (col < g.Nout && nv > 0) ? bv[j] : u32x2v{0u, 0u});
+        t[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq, af_hi, t[j], 0, 0, 0);
+        if (lo_pass) t[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(bq, af_lo, t[j], 0, 0, 0);
+      }
+    };
+    float sel[4];
+#pragma unroll
+    for (int v = 0; v < 4; ++v) sel[v] = (lane & 15) == 4 * (lane >> 4) + v ? 1.f : 0.f;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int rb0 = wm * WM + 16 * i;
+      const int row = rb0 + (lane & 15);
+      const u32x2v hv1 = hv_n;
+      uint32_t mw[FN / 2];
+#pragma unroll
+      for (int h = 0; h < FN / 2; ++h) mw[h] = (row < nrows && wd0 + h < g.keep_words) ? mw_n[h] : 0u;
+      if (i + 1 < FM) load_row(i + 1, hv_n, mw_n);
+      f32x4 t[FN];
+#pragma unroll
+      for (int j = 0; j < FN; ++j) t[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+      if (one) {
+        if (g0_hi > rb0 && g0_lo < rb0 + 16) lr_row(t, hv1, b1, row, g0_lo, g0_hi, min(4, g0_r - jb0), g0_sc);
+      } else {
+        for (int gi = 0; gi < ngroups; ++gi) {
+          const int a = td[4 + 3 * gi], lo = td[5 + 3 * gi], hi = td[6 + 3 * gi];
+          if (hi <= rb0 || lo >= rb0 + 16) continue;  // no row of this block
+          const int r = g.ranks[a];
+          const float sc = g.scales ? g.scales[a] : 1.f;
+          const uint16_t* lq = g.Lq + (int64_t)a * g.lq_ad;
+          const bool full16 = (r & 15) == 0;
+          const bool lq_vec = full16 && g.lq_j == 1 && (g.lq_col & 3) == 0;
+          const bool rin = row >= lo && row < hi;
+          for (int j0 = 0; j0 < r; j0 += 16) {
+            const int jb = j0 + jb0;
+            const int nv = min(4, r - jb);
+            const int jbc = nv > 0 ? jb : 0, nvc = max(nv, 1);
+            const uint16_t* hp = g.Lp + (int64_t)(m0 + (rin ? row : lo)) * g.ldl + jbc;
+            const u32x2v hv = full16 ? *reinterpret_cast<const u32x2v*>(hp) : ld4_sel(hp, 1, nvc);
+            u32x2v bv[FN];
+            load_b(lq, jbc, nvc, lq_vec, bv);
+            lr_row(t, hv, bv, row, lo, hi, nv, sc);
+          }
+        }
+      }
+      // The masked term enters the (zero) accumulators as matrix-core
+      // products, so they stay where the main loop keeps them: fp32 MFMA step
+      // s (16x16x4) multiplies a 0/1 selector (lane holds A[lane%16][lane/16] =
+      // [lane%16 == 4(lane/16) + s]) by the lane's own value v = s, which lands
+      // each value, exactly, in its own accumulator entry.
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const float m = ((mw[j >> 1] >> (16 * (j & 1) + bit0 + v)) & 1u) ? t[j][v] * g.keep_scale : 0.f;
+          acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(sel[v], m, acc[i][j], 0, 0, 0);
+        }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
@@ -1114,8 +1225,11 @@ hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
   if constexpr (!NN) {
     for (int p = 0; p < g.n; ++p)
       if (g.a[p].ldp != g.a[p].ldq) return hipErrorInvalidValue;
-    bool drop = false;
-    for (int p = 0; p < g.n; ++p) drop = drop || g.a[p].keep != nullptr;
+    // the masked instantiation serves launches whose projections all carry a mask
+    int n_keep = 0;
+    for (int p = 0; p < g.n; ++p) n_keep += g.a[p].keep != nullptr;
+    if (n_keep != 0 && n_keep != g.n) return hipErrorInvalidValue;
+    const bool drop = n_keep > 0;
     if (drop) launch_timed(gemm16_group_kernel<true>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
     else launch_timed(gemm16_group_kernel<false>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
   } else {

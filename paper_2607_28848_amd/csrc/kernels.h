@@ -284,6 +284,15 @@ struct DropoutSpec {
   uint64_t seed, offset;
 };
 // bits: [Tt][ceil(K / 32)] words, bit b of word w keeps column 32 w + b.
+// The masks of up to kMaxGroup projections (same Tt) in one launch; entries
+// with bits == nullptr are skipped.
+struct DropoutMaskGroup {
+  uint32_t* bits[kMaxGroup];
+  int32_t K[kMaxGroup];
+  DropoutSpec d[kMaxGroup];
+  int32_t n;
+};
+hipError_t launch_dropout_mask_group(const DropoutMaskGroup& g, int32_t Tt, hipStream_t s);
 hipError_t launch_dropout_mask(uint32_t* bits, int32_t Tt, int32_t K, const DropoutSpec& d, hipStream_t s);
 
 

@@ -72,7 +72,7 @@ _lib.dsv_lora_bwd.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp,
                               _vp, _vp, _i32, _vp, _sz, _vp]
 _lib.dsv_lora_bwd.restype = ctypes.c_int
 class Dropout(ctypes.Structure):
-    _fields_ = [("p", ctypes.c_double), ("seed", ctypes.c_uint64), ("offset", ctypes.c_uint64)]
+    _fields_ = [("p", ctypes.c_double), ("seed", ctypes.c_uint64), ("offset", ctypes.c_uint64), ("mask", _vp)]
 
 
 _lib.dsv_cobatch_fwd_dropout.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
@@ -268,11 +268,19 @@ def bwd_workspace_bytes(plan: Plan, dtype_code: int, K: int, N: int, dropout: bo
 
 
 def _dropout(dropout):
-    """(p, seed, offset) -> the C struct (None stays None)."""
+    """(p, seed, offset) or (p, seed, offset, mask) -> the C struct (None stays None).
+    mask: a device int32 tensor of T_t * ceil(K / 32) words the forward fills and the
+    backward reads (dsv_dropout.mask), or None."""
     if dropout is None:
         return None
-    p, seed, offset = dropout
-    return Dropout(float(p), int(seed), int(offset))
+    p, seed, offset = dropout[:3]
+    mask = dropout[3] if len(dropout) > 3 else None
+    return Dropout(float(p), int(seed), int(offset), None if mask is None else ctypes.c_void_p(mask.data_ptr()))
+
+
+def dropout_mask_words(plan: "Plan", K: int) -> int:
+    """32-bit words of a projection's dropout mask buffer (T_t * ceil(K / 32))."""
+    return plan.train_tokens * ((K + 31) // 32)
 
 
 def _workspace(nbytes, device, given):

@@ -183,3 +183,106 @@ def test_dropout_llama8b_full_size():
     drop = oracle.dropout_multipliers(Tt, K, 0.05, SEED, OFFSET)
     _check(w, run, drop, Y, H, dA, dB, dX, TOL_BF16, rows=rows.astype(np.int32),
            dx_rows=dx_rows.astype(np.int32))
+
+
+def _unpack(buf, Tt, K):
+    """[Tt * ceil(K/32)] mask words -> [Tt][K] keep flags (bit b of word w: column 32 w + b)."""
+    wds = buf.cpu().numpy().view(np.uint32).reshape(Tt, (K + 31) // 32)
+    bits = (wds[:, :, None] >> np.arange(32, dtype=np.uint32)[None, None, :]) & 1
+    return bits.reshape(Tt, -1)[:, :K].astype(bool)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_dropout_mask_buffer_single(dtype):
+    """dsv_dropout.mask: the forward draws the generator's mask into the caller's
+    buffer (bit-exact against the reference generator) and its results do not
+    change; a backward given the buffer matches the one that redraws bit for bit;
+    a backward given a buffer drawn at another offset computes that offset's
+    gradients (it reads the buffer, it does not redraw)."""
+    import torch
+    _say("case dropout mask buffer %s" % dtype)
+    K, N, p = 520, 776, 0.05
+    w = wl.custom(MIXED, MIXED_RANKS, K=K, N=N, dtype=dtype, r_max=64, name="dropout_buf")
+    run = Run(w)
+    ds = run.dsv
+    Tt = w.train_tokens
+    nw = ds.dropout_mask_words(run.plan, K)
+    buf = torch.zeros(nw, dtype=torch.int32, device="cuda")
+    other = torch.zeros(nw, dtype=torch.int32, device="cuda")
+    d = (p, SEED, OFFSET)
+
+    def hbuf():  # H_save with its rank padding cleared (the path never writes it)
+        return torch.zeros((Tt, w.r_max), dtype=run.X.dtype, device=run.X.device)
+
+    Y0, H0 = ds.cobatch_fwd(run.plan, run.X, run.W, run.A, run.B, H_save=hbuf(), dropout=d)
+    Y1, H1 = ds.cobatch_fwd(run.plan, run.X, run.W, run.A, run.B, H_save=hbuf(), dropout=d + (buf,))
+    ds.cobatch_fwd(run.plan, run.X, run.W, run.A, run.B, H_save=hbuf(), dropout=(p, SEED, OFFSET + 1, other))
+    g0 = ds.lora_bwd(run.plan, run.X, run.W, run.A, run.B, H0, run.dY, dropout=d)
+    g1 = ds.lora_bwd(run.plan, run.X, run.W, run.A, run.B, H0, run.dY, dropout=d + (buf,))
+    g2 = ds.lora_bwd(run.plan, run.X, run.W, run.A, run.B, None, run.dY, dropout=d + (buf,))
+    g0b = ds.lora_bwd(run.plan, run.X, run.W, run.A, run.B, None, run.dY, dropout=d)
+    # the offset's mask through the buffer, against the redrawn one of that offset
+    g_o = ds.lora_bwd(run.plan, run.X, run.W, run.A, run.B, None, run.dY, dropout=(p, SEED, OFFSET, other))
+    g_r = ds.lora_bwd(run.plan, run.X, run.W, run.A, run.B, None, run.dY, dropout=(p, SEED, OFFSET + 1))
+    torch.cuda.synchronize()
+    assert np.array_equal(_unpack(buf, Tt, K), oracle.dropout_keep(Tt, K, p, SEED, OFFSET))
+    assert np.array_equal(_unpack(other, Tt, K), oracle.dropout_keep(Tt, K, p, SEED, OFFSET + 1))
+    for a, b in [(Y0, Y1), (H0, H1)] + list(zip(g0, g1)) + list(zip(g0b, g2)) + list(zip(g_o, g_r)):
+        assert torch.equal(_bits(a), _bits(b))
+    assert not torch.equal(_bits(g_o[2]), _bits(g0b[2]))
+
+
+def test_dropout_mask_buffer_grouped():
+    """The grouped calls with per-projection mask buffers (one projection given a
+    buffer in the backward, the other redrawn): every output bit-identical to the
+    grouped calls without buffers, and each buffer the generator's mask."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    _say("case dropout mask buffer grouped")
+    shapes = [(520, 776), (136, 264)]
+    runs = [Run(wl.custom(MIXED, MIXED_RANKS, K=K, N=N, dtype="bf16", r_max=64, name="dbg%d" % i))
+            for i, (K, N) in enumerate(shapes)]
+    plan = runs[0].plan
+    Tt = runs[0].w.train_tokens
+    bufs = [torch.zeros(dsv.dropout_mask_words(plan, K), dtype=torch.int32, device="cuda") for K, _ in shapes]
+    drops = [(0.05, SEED + i, OFFSET) for i in range(2)]
+    def outs():  # Y and H_save, H_save's rank padding cleared (the path never writes it)
+        return [(r.X, r.W, r.A, r.B, torch.empty((r.w.n_tokens, N), dtype=r.X.dtype, device="cuda"),
+                 torch.zeros((Tt, r.w.r_max), dtype=r.X.dtype, device="cuda")) for r, (_, N) in zip(runs, shapes)]
+
+    out0 = dsv.cobatch_fwd_grouped(plan, outs(), dropouts=drops)
+    out1 = dsv.cobatch_fwd_grouped(plan, outs(), dropouts=[d + (b,) for d, b in zip(drops, bufs)])
+    bwd_in = [(r.X, r.W, r.A, r.B, o[1], r.dY) for r, o in zip(runs, out0)]
+    gb0 = dsv.lora_bwd_grouped(plan, bwd_in, dropouts=drops)
+    gb1 = dsv.lora_bwd_grouped(plan, bwd_in, dropouts=[drops[0] + (bufs[0],), drops[1]])
+    torch.cuda.synchronize()
+    for (K, _), b, d in zip(shapes, bufs, drops):
+        assert np.array_equal(_unpack(b, Tt, K), oracle.dropout_keep(Tt, K, 0.05, d[1], OFFSET))
+    for o0, o1 in zip(out0, out1):
+        for a, b in zip(o0, o1):
+            assert torch.equal(_bits(a), _bits(b))
+    for x0, x1 in zip(gb0, gb1):
+        for a, b in zip(x0, x1):
+            assert torch.equal(_bits(a), _bits(b))
+
+
+@pytest.mark.parametrize("K,N", [(520, 776), (4096, 2000)])
+def test_dropout_dx_transposed_weight_bit_exact(K, N):
+    """Under dropout the dX GEMM on the transposed weight (NT) and on W itself (NN)
+    give bit-identical dX, dA and dB (single and grouped calls)."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    _say("case dropout Wt K=%d N=%d" % (K, N))
+    w = wl.custom(SPLIT if K == 4096 else MIXED, SPLIT_RANKS if K == 4096 else MIXED_RANKS, K=K, N=N,
+                  r_max=64, name="dropout_wt")
+    run = Run(w)
+    d = (0.05, SEED, OFFSET)
+    Y, H = run.dsv.cobatch_fwd(run.plan, run.X, run.W, run.A, run.B, dropout=d)
+    Wt = run.W.t().contiguous()
+    args = [(run.X, run.W, run.A, run.B, H, run.dY)]
+    g_nn = dsv.lora_bwd_grouped(run.plan, args + args, dropouts=[d, d])
+    g_nt = dsv.lora_bwd_grouped(run.plan, args + args, dropouts=[d, d], wts=[Wt, Wt])
+    torch.cuda.synchronize()
+    for a, b in zip(g_nn, g_nt):
+        for x, y in zip(a, b):
+            assert torch.equal(_bits(x), _bits(y))

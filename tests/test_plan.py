@@ -407,6 +407,12 @@ def test_dropout_argument_checks_on_host():
                                        None) == dsv.ERR_ARG
     assert lib.dsv_lora_bwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, fake, fake, fake, 0, None,
                                     fake, 1 << 20, None) == dsv.ERR_ARG
+    # a mask buffer that is not 4-byte aligned
+    d = dsv.Dropout(0.05, 1, 0, ctypes.c_void_p(4098))
+    assert lib.dsv_cobatch_fwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, ctypes.byref(d), fake,
+                                       1 << 20, None) == dsv.ERR_ARG
+    assert lib.dsv_lora_bwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, fake, fake, fake, 0,
+                                    ctypes.byref(d), fake, 1 << 20, None) == dsv.ERR_ARG
     d = dsv.Dropout(0.05, 1, 0)  # valid: the host-only plan is what is rejected
     assert lib.dsv_cobatch_fwd_dropout(plan.handle, dsv.BF16, 64, 64, *args, fake, fake, ctypes.byref(d), fake,
                                        1 << 20, None) == dsv.ERR_ARG
