@@ -1023,22 +1023,48 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   static_assert(NW * 32 * SRS <= STAGE, "epilogue slices fit the idle pipeline buffer");
   char* slice = smem + (last_stage ^ 1) * STAGE + wave * 32 * SRS;
   const bool gathered = has_gather && g.delta != nullptr;
+  // Gathered rows add their fp32 term: the wave's row slots are read once and
+  // each slice's terms are loaded while the slice before it is processed.
+  int gsv[FM];
+  f32x4 dn[2][FN];
+  auto load_terms = [&](int t) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int col = wn * WN + 16 * j + 4 * (lane >> 4);
+        const int gs = gsv[2 * t + h];
+        const f32x4 d = *reinterpret_cast<const f32x4*>(g.delta + (int64_t)max(gs, 0) * g.Nout +
+                                                        min(n0 + col, g.Nout - 4));
+        dn[h][j] = (gs >= 0 && n0 + col < g.Nout) ? d : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+  };
+  if (gathered) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int row = wm * WM + 16 * i + l15;
+      gsv[i] = row < nrows ? g.gslot[m0 + row] : -1;
+    }
+    load_terms(0);
+  }
 #pragma unroll
   for (int t = 0; t < FM / 2; ++t) {
+    f32x4 dc[2][FN];
+    if (gathered) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) dc[h][j] = dn[h][j];
+      if (t + 1 < FM / 2) load_terms(t + 1);
+    }
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
       const int i = 2 * t + h;
-      const int row = wm * WM + 16 * i + l15;
-      const int gs = (gathered && row < nrows) ? g.gslot[m0 + row] : -1;
 #pragma unroll
       for (int j = 0; j < FN; ++j) {
         const int col = wn * WN + 16 * j + 4 * (lane >> 4);
         f32x4 x = acc[i][j];
-        if (gathered) {
-          const f32x4 d = *reinterpret_cast<const f32x4*>(g.delta + (int64_t)max(gs, 0) * g.Nout +
-                                                          min(n0 + col, g.Nout - 4));
-          x += (gs >= 0 && n0 + col < g.Nout) ? d : f32x4{0.f, 0.f, 0.f, 0.f};
-        }
+        if (gathered) x += dc[h][j];
         const uint32_t w0 = f2bf2(x[0], x[1]), w1 = f2bf2(x[2], x[3]);
         *reinterpret_cast<uint2*>(slice + (16 * h + l15) * SRS + 2 * (col - wn * WN)) = make_uint2(w0, w1);
       }
