@@ -579,8 +579,9 @@ __device__ __forceinline__ u32x2v ld4_sel(const uint16_t* p, int64_t stride, int
 
 // DROP: the instantiation that masks the low-rank term (dX under LoRA
 // dropout); the others carry no masking code.
-template <bool SK, bool DROP>
-__device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int tid, int lin, int t_sk, int piece,
+template <bool SK, bool DROP, bool NN>
+__device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, char* smem1, int tid, int lin, int t_sk,
+                                             int piece,
                                              int kb, int ke, int nk) {
   constexpr int TM = 256, TN = 256, TK = 64, NW = 4, WM = 128, WN = 128, FM = 8, FN = 8;
   constexpr int ROWB = TK * 2;                   // bytes per LDS row
@@ -589,6 +590,11 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   static_assert(LOADS == 8 && TN == TM, "load split");
   const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave >> 1, wn = wave & 1;
+  // The two pipeline buffers are two LDS arrays: with the buffer index a
+  // constant at a use (the main loop runs K-steps in pairs), the compiler sees
+  // that an LDS read and the direct loads in flight into the other buffer are
+  // disjoint, and makes no read wait for those loads.
+  auto buf = [&](int stage) { return stage ? smem1 : smem0; };
 
   int mt, nt;
   tile_coords(g, lin, mt, nt);
@@ -605,16 +611,22 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   const int g0_a = td[4], g0_lo = td[5], g0_hi = td[6];  // zeros when the tile has no group
   const int g0_r = g.ranks[g0_a];
   const float g0_sc = g.scales ? g.scales[g0_a] : 1.f;
-  // Both operands are contraction-contiguous rows of the same length (the
-  // launcher checks ldp == ldq), so one set of lane offsets serves both.
+  // NT: both operands are contraction-contiguous rows of the same length
+  // (the launcher checks ldp == ldq), so one set of lane offsets serves both.
+  // NN: the weight is [C][Nout] (rows of the contraction, W itself); its tile
+  // of a K-step is TK rows of TN columns, and the launcher checks that the
+  // whole weight's byte offsets fit in 31 bits.
   const int ld = (int)g.ldp;
+  const int ldq = (int)g.ldq;
   const int64_t a_rows = min((int64_t)TM, (int64_t)g.M - m0);
   const int64_t b_cols = min((int64_t)TN, (int64_t)g.Nout - n0);
   // Descriptors over the tile's row panels (rows past the operand read zeros);
   // a K-step adds 2 k0 bytes to the scalar offset.  A panel is at most 256
-  // rows of 2^20 elements, so every offset fits in 32 bits.
+  // rows of 2^20 elements, so every offset fits in 32 bits.  NN: over the
+  // weight from the tile's first column (rows past the contraction read zeros).
   const i32x4 ra = make_rsrc(g.P + (int64_t)m0 * ld, (uint64_t)a_rows * ld * 2);
-  const i32x4 rb = make_rsrc(g.Q + (int64_t)n0 * ld, (uint64_t)b_cols * ld * 2);
+  const i32x4 rb = NN ? make_rsrc(g.Q + n0, ((uint64_t)g.C * ldq - n0) * 2)
+                      : make_rsrc(g.Q + (int64_t)n0 * ld, (uint64_t)b_cols * ld * 2);
 
   // Operand loads: load i of a wave fills LDS rows 8q .. 8q+7 (q = 8 wave + i),
   // lane ln taking row 8q + ln/8, logical chunk (ln%8) ^ swz(row), which is
@@ -624,10 +636,28 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   int voff[LOADS];
 #pragma unroll
   for (int i = 0; i < LOADS; ++i) voff[i] = ((((lane & 7) ^ lr ^ i) << 4)) + lr * ld * 2;
+  // NN weight loads: load i fills tile rows 2q, 2q+1 (q = 8 wave + i, 512
+  // bytes each), lane ln taking row 2q + ln/32, slot ln%32, which holds the
+  // row's 16-byte chunk (ln%32) ^ nn_swz(row); nn_swz(row) depends on i%2 only.
+  int voffb[2];
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const int n_in = 2 * par + (lane >> 5);
+    voffb[par] = ((lane >> 5) * ldq + 8 * ((lane & 31) ^ nn_swz(n_in))) * 2;
+  }
+  auto load_b = [&](int kt, char* sa, int i) {
+    const int q = wave * LOADS + i;
+    if constexpr (NN)
+      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voffb[i & 1],
+                                      __builtin_amdgcn_readfirstlane((kt * TK + 2 * q) * ldq * 2), 0, 0);
+    else
+      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voff[i],
+                                      __builtin_amdgcn_readfirstlane(q * 16 * ld + kt * TK * 2), 0, 0);
+  };
   // whole K-step kt into `stage` (k0 + TK <= C)
   auto issue_whole = [&](int kt, int stage) {
     const int kbytes = kt * TK * 2;
-    char* sa = smem + stage * STAGE;
+    char* sa = buf(stage);
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int q = wave * LOADS + i;
@@ -635,11 +665,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
                                       __builtin_amdgcn_readfirstlane(q * 16 * ld + kbytes), 0, 0);
     }
 #pragma unroll
-    for (int i = 0; i < LOADS; ++i) {
-      const int q = wave * LOADS + i;
-      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voff[i],
-                                      __builtin_amdgcn_readfirstlane(q * 16 * ld + kbytes), 0, 0);
-    }
+    for (int i = 0; i < LOADS; ++i) load_b(kt, sa, i);
   };
   // any K-step: chunks past the contraction read nothing (zeros)
   auto issue = [&](int kt, int stage) {
@@ -648,7 +674,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
       issue_whole(kt, stage);
       return;
     }
-    char* sa = smem + stage * STAGE;
+    char* sa = buf(stage);
 #pragma unroll
     for (int i = 0; i < LOADS; ++i) {
       const int q = wave * LOADS + i;
@@ -656,7 +682,8 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
       const int c = (lane & 7) ^ swz<TK>(row);
       const int vo = (k0 + 8 * c < g.C) ? (row * ld + k0 + 8 * c) * 2 : (int)0x7FFFFFF0;
       llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
-      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, vo, 0, 0, 0);
+      if constexpr (NN) load_b(kt, sa, i);  // rows past the contraction lie past the descriptor
+      else llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, vo, 0, 0, 0);
     }
   };
 
@@ -918,8 +945,26 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   auto rd_a = [&](const char* st, int s, int i) {
     return as_bf(*reinterpret_cast<const u32x4*>(st + off_a[((2 * s) ^ i) & 3] + 16 * i * ROWB));
   };
+  // NN: weight fragment j of step s = output column wn*128 + 16j + lane%16 and
+  // contraction rows 32s + 8(lane/16) .. +7, as two transposing reads of four
+  // rows each: read hh of lane (g4 = lane/16, l = lane%16) addresses row
+  // 32s + 8 g4 + 4 hh + l/4, column wn*128 + 16j + 4(l%4), whose chunk
+  // (c/8) ^ nn_swz(row) is wn*16 + 2((j%4) ^ (l/4)) + 8(j/4) + (l%4)/2.
+  int off_bn[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c)
+    off_bn[c] = A_BYTES + (8 * (lane >> 4) + (l15 >> 2)) * (TN * 2) + 256 * wn + 32 * (c ^ (l15 >> 2)) +
+                16 * ((l15 & 3) >> 1) + 8 * (l15 & 1);
   auto rd_b = [&](const char* st, int s, int j) {
-    return as_bf(*reinterpret_cast<const u32x4*>(st + off_b[((2 * s) ^ j) & 3] + 16 * j * ROWB));
+    if constexpr (NN) {
+      const char* p = st + off_bn[j & 3] + 128 * (j >> 2) + s * 32 * (TN * 2);
+      const s16x4 h0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+      const s16x4 h1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(p + 4 * (TN * 2)));
+      const u32x2v a0 = __builtin_bit_cast(u32x2v, h0), a1 = __builtin_bit_cast(u32x2v, h1);
+      return as_bf(u32x4{a0[0], a0[1], a1[0], a1[1]});
+    } else {
+      return as_bf(*reinterpret_cast<const u32x4*>(st + off_b[((2 * s) ^ j) & 3] + 16 * j * ROWB));
+    }
   };
 
   // Fragments: two A sets (the current step's and the next one's) and one B
@@ -930,9 +975,9 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   else vmem_wait_all();
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < FN; ++j) fb[j] = rd_b(smem, 0, j);
+  for (int j = 0; j < FN; ++j) fb[j] = rd_b(smem0, 0, j);
 #pragma unroll
-  for (int i = 0; i < FM; ++i) fa0[i] = rd_a(smem, 0, i);
+  for (int i = 0; i < FM; ++i) fa0[i] = rd_a(smem0, 0, i);
 
   // Direct loads of whole K-step kl into buffer ls: load n of the wave's 16
   // (A for n < 8, B after).  A texture unit takes a 1 KiB load in about 16
@@ -942,8 +987,12 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   auto load_n = [&](int kl, int ls, int n) {
     const int i = n & 7;
     const int q = wave * LOADS + i;
-    llvm_amdgcn_raw_buffer_load_lds(n < 8 ? ra : rb, (lds_u32*)(smem + ls * STAGE + (n < 8 ? 0 : A_BYTES) + q * 1024),
-                                    16, voff[i], __builtin_amdgcn_readfirstlane(q * 16 * ld + kl * TK * 2), 0, 0);
+    if (NN && n >= 8)
+      load_b(kl, buf(ls), i);
+    else
+      llvm_amdgcn_raw_buffer_load_lds(n < 8 ? ra : rb,
+                                      (lds_u32*)(buf(ls) + (n < 8 ? 0 : A_BYTES) + q * 1024), 16, voff[i],
+                                      __builtin_amdgcn_readfirstlane(q * 16 * ld + kl * TK * 2), 0, 0);
   };
   // One 32-wide step with fragments (cur, fb); reads the next step's
   // fragments (nxt, fb) from buffer `st_next` step s_next, in the order fixed
@@ -976,20 +1025,32 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   // the second step, which reads kt+1's first fragments and loads whole
   // K-step kt+2 into buffer `stage` (when `load`).
   auto kstep = [&](int kt, int stage, bool load) {
-    step(fa0, fa1, smem + stage * STAGE, 1, false, 0, 0);
+    step(fa0, fa1, buf(stage), 1, false, 0, 0);
     __builtin_amdgcn_sched_barrier(0);
     vmem_wait_all();  // kt+1 landed (its loads are the only ones in flight)
     __syncthreads();  // everyone's part of kt+1 is in; buffer `stage` is free
     __builtin_amdgcn_sched_barrier(0);
     if (!load && kt + 2 < ke) issue(kt + 2, stage);  // a partial last K-step
-    step(fa1, fa0, smem + (stage ^ 1) * STAGE, 0, load, kt + 2, stage);
+    step(fa1, fa0, buf(stage ^ 1), 0, load, kt + 2, stage);
   };
   int kt = kb, stage = 0;
   const int main_end = min(ke, g.C / TK) - 2;  // kt < main_end: kt+2 is whole and below ke
-  for (; kt < main_end; ++kt, stage ^= 1) kstep(kt, stage, true);
+  if constexpr (NN) {
+    for (; kt + 1 < main_end; kt += 2) {  // pairs: buffers 0 then 1, constant at every use
+      kstep(kt, 0, true);
+      kstep(kt + 1, 1, true);
+    }
+    if (kt < main_end) {
+      kstep(kt, 0, true);
+      ++kt;
+      stage = 1;
+    }
+  } else {
+    for (; kt < main_end; ++kt, stage ^= 1) kstep(kt, stage, true);
+  }
   for (; kt + 1 < ke; ++kt, stage ^= 1) kstep(kt, stage, false);
   // the last K-step: no successor to read
-  step(fa0, fa1, smem + stage * STAGE, 1, false, 0, 0);
+  step(fa0, fa1, buf(stage), 1, false, 0, 0);
 #pragma unroll
   for (int j = 0; j < FN; ++j)
 #pragma unroll
@@ -1021,7 +1082,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   // one half-wave fall on distinct banks.
   constexpr int SRS = WN * 2 + 16;
   static_assert(NW * 32 * SRS <= STAGE, "epilogue slices fit the idle pipeline buffer");
-  char* slice = smem + (last_stage ^ 1) * STAGE + wave * 32 * SRS;
+  char* slice = buf(last_stage ^ 1) + wave * 32 * SRS;
   const bool gathered = has_gather && g.delta != nullptr;
   // Gathered rows add their fp32 term: the wave's row slots are read once and
   // each slice's terms are loaded while the slice before it is processed.
@@ -1084,9 +1145,10 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem, int 
   }
 }
 
-template <bool SK, bool DROP>
+template <bool SK, bool DROP, bool NN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_kernel(GemmArgs g) {
-  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * 256 * 64 * 2];
+  __shared__ __attribute__((aligned(1024))) char smem0[2 * 256 * 64 * 2];
+  __shared__ __attribute__((aligned(1024))) char smem1[2 * 256 * 64 * 2];
   const int nk = (g.C + 63) / 64;
   int lin, t_sk = -1, piece = 0, kb = 0, ke = nk;
   if (!SK || (int)blockIdx.x < g.dp_tiles) {
@@ -1099,19 +1161,20 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
     kb = (int)(((int64_t)piece * nk) / g.sk_split);
     ke = (int)(((int64_t)(piece + 1) * nk) / g.sk_split);
   }
-  gemm_piece16<SK, DROP>(g, smem, threadIdx.x, lin, t_sk, piece, kb, ke, nk);
+  gemm_piece16<SK, DROP, NN>(g, smem0, smem1, threadIdx.x, lin, t_sk, piece, kb, ke, nk);
 }
 
-template <bool DROP>
+template <bool DROP, bool NN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_group_kernel(GemmGroup G) {
-  __shared__ __attribute__((aligned(1024))) char smem[2 * 2 * 256 * 64 * 2];
+  __shared__ __attribute__((aligned(1024))) char smem0[2 * 256 * 64 * 2];
+  __shared__ __attribute__((aligned(1024))) char smem1[2 * 256 * 64 * 2];
   int pj = 0;
   while (pj + 1 < G.n && (int)blockIdx.x >= G.off[pj + 1]) ++pj;
   const GemmArgs g = G.a[pj];
   const int local = (int)blockIdx.x - G.off[pj];
   const int lin = xcd_major(local, G.off[pj + 1] - G.off[pj]);
   const int nk = (g.C + 63) / 64;
-  gemm_piece16<false, DROP>(g, smem, threadIdx.x, lin, -1, 0, 0, nk, nk);
+  gemm_piece16<false, DROP, NN>(g, smem0, smem1, threadIdx.x, lin, -1, 0, 0, nk, nk);
 }
 
 // ---------------------------------------------------------------------------
@@ -1168,6 +1231,10 @@ void launch_timed(F kernel, dim3 grid, dim3 block, hipStream_t s, bool first, bo
 // Tile configurations: (TM, TN, wave grid, K-step, pipeline stages); two
 // waves per SIMD in each (8 waves per 256-row workgroup, or two 4-wave
 // 128 x 128 workgroups per CU).
+// The 16x16x32 NN form addresses the weight with 32-bit byte offsets from the
+// tile's first column, one K-step past the contraction at most.
+bool nn16_fits(const GemmArgs& a) { return ((int64_t)a.C + 64) * a.ldq * 2 < ((int64_t)1 << 31); }
+
 template <bool NN>
 hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   if (a.n_mtiles <= 0 || a.n_ntiles <= 0) return hipSuccess;
@@ -1188,22 +1255,38 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
       if (a.ldp != a.ldq) return hipErrorInvalidValue;
       const bool drop = a.keep != nullptr;
       if (a.sk_tiles > 0) {
-        if (drop) launch_timed(gemm16_kernel<true, true>, grid, dim3(256), s, true, false, a);
-        else launch_timed(gemm16_kernel<true, false>, grid, dim3(256), s, true, false, a);
+        if (drop) launch_timed(gemm16_kernel<true, true, false>, grid, dim3(256), s, true, false, a);
+        else launch_timed(gemm16_kernel<true, false, false>, grid, dim3(256), s, true, false, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
         launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)), dim3(256),
                      s, false, true, a);
       } else if (drop) {
-        launch_timed(gemm16_kernel<false, true>, grid, dim3(256), s, true, true, a);
+        launch_timed(gemm16_kernel<false, true, false>, grid, dim3(256), s, true, true, a);
       } else {
-        launch_timed(gemm16_kernel<false, false>, grid, dim3(256), s, true, true, a);
+        launch_timed(gemm16_kernel<false, false, false>, grid, dim3(256), s, true, true, a);
       }
       return hipGetLastError();
     }
   }
-  if constexpr (NN) {  // 256 x 256 NN tiles (dX reading W transposed in LDS)
-    if (tm == 256 && tn == 256) {
+  if constexpr (NN) {  // 256 x 256 NN tiles (dX reading W through transposing LDS reads)
+    if (tm == 256 && tn == 256 && nn16_fits(a)) {
+      const bool drop = a.keep != nullptr;
+      if (a.sk_tiles > 0) {
+        if (drop) launch_timed(gemm16_kernel<true, true, true>, grid, dim3(256), s, true, false, a);
+        else launch_timed(gemm16_kernel<true, false, true>, grid, dim3(256), s, true, false, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        launch_timed(split_fixup_kernel<NN, 256, 256>, dim3((unsigned)a.sk_tiles * (256 * 256 / 4 / 256)), dim3(256),
+                     s, false, true, a);
+      } else if (drop) {
+        launch_timed(gemm16_kernel<false, true, true>, grid, dim3(256), s, true, true, a);
+      } else {
+        launch_timed(gemm16_kernel<false, false, true>, grid, dim3(256), s, true, true, a);
+      }
+      return hipGetLastError();
+    }
+    if (tm == 256 && tn == 256) {  // the 8-wave form, for weights past 2^31 bytes
       if (a.sk_tiles > 0) {
         launch_timed(gemm_lora_kernel<NN, 256, 256, 2, 4, 64, 2, true>, grid, dim3(512), s, true, false, a);
         hipError_t e = hipGetLastError();
@@ -1256,10 +1339,23 @@ hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
     for (int p = 0; p < g.n; ++p) n_keep += g.a[p].keep != nullptr;
     if (n_keep != 0 && n_keep != g.n) return hipErrorInvalidValue;
     const bool drop = n_keep > 0;
-    if (drop) launch_timed(gemm16_group_kernel<true>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
-    else launch_timed(gemm16_group_kernel<false>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+    if (drop) launch_timed(gemm16_group_kernel<true, false>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+    else launch_timed(gemm16_group_kernel<false, false>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
   } else {
-    launch_timed(gemm_group_kernel<NN>, dim3((unsigned)g.off[g.n]), dim3(512), s, true, true, g);
+    bool fits = true, drop = false;
+    int n_keep = 0;
+    for (int p = 0; p < g.n; ++p) {
+      fits = fits && nn16_fits(g.a[p]);
+      n_keep += g.a[p].keep != nullptr;
+    }
+    if (n_keep != 0 && n_keep != g.n) return hipErrorInvalidValue;
+    drop = n_keep > 0;
+    if (fits && drop)
+      launch_timed(gemm16_group_kernel<true, true>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+    else if (fits)
+      launch_timed(gemm16_group_kernel<false, true>, dim3((unsigned)g.off[g.n]), dim3(256), s, true, true, g);
+    else
+      launch_timed(gemm_group_kernel<NN>, dim3((unsigned)g.off[g.n]), dim3(512), s, true, true, g);
   }
   return hipGetLastError();
 }
