@@ -111,6 +111,34 @@ def measured_traffic():
     return float(doc["traffic_bytes_per_launch"])
 
 
+def strided_rows(t, code):
+    """t with its rows at the stride dsv_row_stride recommends: t itself when that is
+    its row length, else the [R][C] view of a [R][stride] buffer holding t's values."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    R, C = t.shape
+    st = dsv.row_stride(C, code)
+    if st == C:
+        return t
+    buf = torch.zeros((R, st), dtype=t.dtype, device=t.device)
+    buf[:, :C] = t
+    return buf[:, :C]
+
+
+def layout_note(w, code, layout):
+    """The caller buffers' row strides of the timed step."""
+    if layout == "dense":
+        return "dense: every row exactly K or N elements"
+    from paper_2607_28848_amd import dsv
+    lens = sorted({n for p in w.projections for n in (p.K, p.N) if dsv.row_stride(n, code) != n})
+    if not lens:
+        return "strided (dsv_row_stride): every recommended stride is the row length, so dense"
+    return ("strided: rows of %s elements (X, W, Y, dY, dX, W transposed) stored %s elements apart "
+            "(dsv_row_stride), all other rows dense; the same values and FLOPs "
+            "(extras.launch_modes_ms_per_step.set_dense is the same step on dense buffers)"
+            % ("/".join(map(str, lens)), "/".join(str(dsv.row_stride(n, code)) for n in lens)))
+
+
 def launch_groups(w, launch, dropout):
     """[(lo, hi)] ranges of w.projections run by one grouped call each, or None for
     one call per projection.  `layer` groups the projections whose inputs exist at
@@ -262,6 +290,11 @@ def main():
                     help="single: one call per projection; layer: grouped calls over the projections a "
                          "transformer layer can run together (q/k/v, o, gate/up, down); set: one grouped call "
                          "over the whole set")
+    ap.add_argument("--layout", default="strided", choices=("strided", "dense"),
+                    help="strided: the grouped calls' caller buffers (X, W, Y, dY, dX, the transposed weight) "
+                         "hold their rows at the stride dsv_row_stride recommends (rows of 14336 bf16 elements "
+                         "64 elements apart more); dense: rows of exactly K or N elements.  The single-projection "
+                         "calls (--launch single) take dense buffers")
     ap.add_argument("--no-wt", action="store_true",
                     help="grouped backward without the transposed copy of the frozen weights (the dX GEMM "
                          "then transposes W in the kernel)")
@@ -331,6 +364,8 @@ def main():
                                dtype=torch.uint8, device=dev)
         # the dropout mask of the step, drawn by the forward and read by the backward
         d["mask"] = torch.empty(max(dsv.dropout_mask_words(probe, K), 1), dtype=torch.int32, device=dev)
+        # the same values in rows of the recommended stride (the grouped calls' strided layout)
+        d["s"] = {k: strided_rows(d[k], code) for k in ("X", "W", "Y", "dY", "dX", "Wt")}
         P.append(d)
     torch.cuda.synchronize()
     log("inputs resident on %s" % torch.cuda.get_device_name(dev))
@@ -355,8 +390,9 @@ def main():
     meta_free = [torch.cuda.Event() for _ in range(2)]
     meta_ready = [torch.cuda.Event() for _ in range(2)]
     ptr = lambda t: ctypes.c_void_p(int(t.data_ptr()))  # noqa: E731
+    ld = lambda t: 0 if t.is_contiguous() else int(t.stride(0))  # noqa: E731
     plan_ms = []
-    def make_step(launch, use_wt=not args.no_wt):
+    def make_step(launch, use_wt=not args.no_wt, layout=args.layout):
         """The step function of one launch mode, and its projection groups."""
         groups = launch_groups(w, launch, args.dropout)
         if groups is not None:
@@ -365,9 +401,12 @@ def main():
             bproj = (dsv.BwdProj * len(P))()
             for p, (K, N) in enumerate(shapes):
                 d = P[p]
-                fproj[p] = dsv.FwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["Y"]), ptr(d["H"]))
-                bproj[p] = dsv.BwdProj(K, N, ptr(d["X"]), ptr(d["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["H"]), ptr(d["dY"]),
-                                       ptr(d["dA"]), ptr(d["dB"]), ptr(d["dX"]), ptr(d["Wt"]) if use_wt else None)
+                o = d["s"] if layout == "strided" else d
+                fproj[p] = dsv.FwdProj(K, N, ptr(o["X"]), ptr(o["W"]), ptr(d["A"]), ptr(d["B"]), ptr(o["Y"]), ptr(d["H"]),
+                                       ld(o["X"]), ld(o["W"]), ld(o["Y"]))
+                bproj[p] = dsv.BwdProj(K, N, ptr(o["X"]), ptr(o["W"]), ptr(d["A"]), ptr(d["B"]), ptr(d["H"]), ptr(o["dY"]),
+                                       ptr(d["dA"]), ptr(d["dB"]), ptr(o["dX"]), ptr(o["Wt"]) if use_wt else None,
+                                       ld(o["X"]), ld(o["W"]), ld(o["dY"]), ld(o["dX"]), ld(o["Wt"]) if use_wt else 0)
             fgroup = [(dsv.FwdProj * (hi - lo))(*fproj[lo:hi]) for lo, hi in groups]
             bgroup = [(dsv.BwdProj * (hi - lo))(*bproj[lo:hi]) for lo, hi in groups]
             gws_f = [torch.empty(max(dsv.fwd_grouped_workspace_bytes(probe, code, shapes[lo:hi]), 256),
@@ -639,10 +678,12 @@ def main():
             # The same step in the other launch modes (10 timed steps each); "<mode>_no_wt":
             # the grouped backward without the transposed weights.
             modes = {args.launch + ("_no_wt" if args.no_wt else ""): round(ms_per_step, 4)}
-            for m in ("single", "layer", "set", "layer_no_wt", "set_no_wt"):
+            other = "dense" if args.layout == "strided" else "strided"
+            for m in ("single", "layer", "set", "layer_no_wt", "set_no_wt", "set_" + other):
                 if m in modes or (m == args.launch and not args.no_wt):
                     continue
-                st, _ = make_step(m.replace("_no_wt", ""), use_wt=not m.endswith("_no_wt"))
+                st, _ = make_step(m.split("_")[0], use_wt=not m.endswith("_no_wt"),
+                                  layout=other if m.endswith("_" + other) else args.layout)
                 for i in range(3):
                     st(i)
                 torch.cuda.synchronize()
@@ -721,6 +762,7 @@ def main():
             "launch": args.launch,
             "launch_note": LAUNCH_NOTES[args.launch],
             "dx_weight": "W transposed (kept once, like W)" if groups is not None and not args.no_wt else "W",
+            "layout": layout_note(w, code, args.layout if groups is not None else "dense"),
             "launch_groups": ([[p.name for p in w.projections[lo:hi]] for lo, hi in groups] if groups is not None
                               else [[p.name] for p in w.projections]),
         },

@@ -321,8 +321,29 @@ int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32
  * forward reads W, instead of transposing W inside the kernel (about 20%
  * faster on the Llama-3-8B set on MI355X); the results are bit-identical
  * either way.  Ignored for fp32; NULL reads W.
+ *
+ * Row strides (ldx, ldw, ldy; ldx, ldw, lddy, lddx, ldwt), in elements: the
+ * distance between consecutive rows of that caller buffer.  0 means dense,
+ * the row length (K for X, W and dX; N for Y, dY and Wt).  A non-zero stride
+ * must be at least the row length, a multiple of 8 (rows stay 16-byte
+ * aligned) and at most 2^20, else DSV_ERR_SIZE before any launch.  Only the
+ * first K (or N) elements of a row are read or written; the elements between
+ * rows are never touched, and the results are bit-identical to those on dense
+ * buffers holding the same values.  Strides matter for speed where the dense
+ * row length makes the rows of a GEMM tile collide in the memory system:
+ * dsv_row_stride gives the stride the library recommends.
  */
 #define DSV_MAX_GROUP 8
+
+/*
+ * dsv_row_stride -- the row stride (elements) recommended for caller buffers
+ * whose rows hold n elements of dtype: n + 64 for bf16 rows of more than 8192
+ * elements whose byte length is a multiple of 4096, else n.  (On MI355X the
+ * base GEMM's contraction loop ran about 18% slower over dense bf16 rows of
+ * 14336 elements than over rows 64 elements longer, with the same tile order
+ * and data.)  Returns 0 for n <= 0 or an unknown dtype.
+ */
+int32_t dsv_row_stride(int32_t n, dsv_dtype dtype);
 
 typedef struct {
   int32_t K, N;           /* in / out features of this projection */
@@ -332,6 +353,7 @@ typedef struct {
   const void* B;          /* [n_ad][N][r_max] */
   void* Y;                /* [T][N] out */
   void* H_save;           /* [T_t][r_max] out, or NULL (residual-only retention) */
+  int32_t ldx, ldw, ldy;  /* row strides of X, W, Y (elements; 0: dense) */
 } dsv_fwd_proj;
 
 typedef struct {
@@ -346,6 +368,9 @@ typedef struct {
   float* dB;              /* [n_ad][N][r_max] fp32 */
   void* dX;               /* [T_t][K], or NULL: not computed */
   const void* Wt;         /* optional, bf16: W transposed, [K][N] row-major (see below), or NULL */
+  int32_t ldx, ldw;       /* row strides of X, W (elements; 0: dense) */
+  int32_t lddy, lddx;     /* row strides of dY, dX */
+  int32_t ldwt;           /* row stride of Wt */
 } dsv_bwd_proj;
 
 int dsv_cobatch_fwd_grouped_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t n_proj,

@@ -172,6 +172,41 @@ int check_common(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N) {
 
 int ptr_ok(const void* p) { return p && aligned16(p); }
 
+// Row strides (elements) of one projection's caller buffers: X [T][x],
+// W [N][w], Y [T][y], dY [T_t][dy], dX [T_t][dx], Wt [K][wt].
+struct Strides {
+  int64_t x, w, y, dy, dx, wt;
+};
+Strides dense_strides(int32_t K, int32_t N) { return Strides{K, K, N, N, K, N}; }
+// A caller's stride: 0 is the dense row length; any other value must hold a
+// row (>= len), keep rows 16-byte aligned (a multiple of 8 elements) and
+// stay within the kernels' 32-bit panel offsets (<= kMaxDim).
+int row_stride(int32_t given, int32_t len, int64_t* out) {
+  if (given == 0) {
+    *out = len;
+    return DSV_OK;
+  }
+  if (given < len || (given & 7) || given > kMaxDim) return DSV_ERR_SIZE;
+  *out = given;
+  return DSV_OK;
+}
+int fwd_strides(const dsv_fwd_proj& q, Strides* st) {
+  *st = dense_strides(q.K, q.N);
+  int rc = row_stride(q.ldx, q.K, &st->x);
+  if (rc == DSV_OK) rc = row_stride(q.ldw, q.K, &st->w);
+  if (rc == DSV_OK) rc = row_stride(q.ldy, q.N, &st->y);
+  return rc;
+}
+int bwd_strides(const dsv_bwd_proj& q, Strides* st) {
+  *st = dense_strides(q.K, q.N);
+  int rc = row_stride(q.ldx, q.K, &st->x);
+  if (rc == DSV_OK) rc = row_stride(q.ldw, q.K, &st->w);
+  if (rc == DSV_OK) rc = row_stride(q.lddy, q.N, &st->dy);
+  if (rc == DSV_OK) rc = row_stride(q.lddx, q.K, &st->dx);
+  if (rc == DSV_OK) rc = row_stride(q.ldwt, q.N, &st->wt);
+  return rc;
+}
+
 template <typename T>
 T* at(void* base, size_t off) {
   return reinterpret_cast<T*>(static_cast<char*>(base) + off);
@@ -412,9 +447,10 @@ uint32_t* mask_buffer(const dsv_dropout* d, void* ws_keep) {
 // benchmark timing events are created.
 int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
              const void* B, void* Y, void* H_save, const dsv_dropout* drop, void* workspace,
-             size_t workspace_bytes, void* hip_stream, bool noalloc = false) {
+             size_t workspace_bytes, void* hip_stream, const Strides* lds = nullptr, bool noalloc = false) {
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
+  const Strides ld = lds ? *lds : dense_strides(K, N);
   DropoutSpec ds{};
   if (drop && !dropout_spec(drop, &ds)) return DSV_ERR_RANGE;
   if (!mask_aligned(drop)) return DSV_ERR_ARG;
@@ -461,6 +497,9 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     a.A = static_cast<const float*>(A);
     a.B = static_cast<const float*>(B);
     a.Y = static_cast<float*>(Y);
+    a.ldx = ld.x;
+    a.ldw = ld.w;
+    a.ldy = ld.y;
     a.Hsave = p->T_t > 0 ? static_cast<float*>(H_save) : nullptr;
     a.Hall = at<float>(workspace, ws.h_all);
     e = launch_f32_fwd(a, s);
@@ -474,7 +513,7 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   // 1. shrink: h of every row, grouped by adapter.
   SkinnyArgs sk{};
   sk.P = static_cast<const uint16_t*>(X);
-  sk.ldp = K;
+  sk.ldp = ld.x;
   sk.rows = p->dptr(L.shrink_rows);
   sk.items = p->dptr(L.shrink_items);
   sk.Q = static_cast<const uint16_t*>(A);
@@ -509,11 +548,11 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   // 3. base GEMM with the low-rank prologue, one rounding.
   GemmArgs g{};
   g.P = static_cast<const uint16_t*>(X);
-  g.ldp = K;
+  g.ldp = ld.x;
   g.Q = static_cast<const uint16_t*>(W);
-  g.ldq = K;
+  g.ldq = ld.w;
   g.out = static_cast<uint16_t*>(Y);
-  g.ldo = N;
+  g.ldo = ld.y;
   g.M = p->T;
   g.Nout = N;
   g.C = K;
@@ -542,9 +581,10 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
 int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
              const void* B, const void* H_save, const void* dY, float* dA, float* dB, void* dX,
              int32_t accumulate, const dsv_dropout* drop, const void* Wt, void* workspace,
-             size_t workspace_bytes, void* hip_stream) {
+             size_t workspace_bytes, void* hip_stream, const Strides* lds = nullptr) {
   int rc = check_common(p, dt, K, N);
   if (rc != DSV_OK) return rc;
+  const Strides ld = lds ? *lds : dense_strides(K, N);
   DropoutSpec ds{};
   if (drop && !dropout_spec(drop, &ds)) return DSV_ERR_RANGE;
   if (!mask_aligned(drop)) return DSV_ERR_ARG;
@@ -605,6 +645,10 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     a.dA = dA;
     a.dB = dB;
     a.dX = static_cast<float*>(dX);
+    a.ldx = ld.x;
+    a.ldw = ld.w;
+    a.lddy = ld.dy;
+    a.lddx = ld.dx;
     a.accumulate = accumulate;
     e = launch_f32_bwd(a, s);
     return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
@@ -624,7 +668,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     uint16_t* hrec = at<uint16_t>(workspace, ws.hrec);
     SkinnyArgs sh{};
     sh.P = static_cast<const uint16_t*>(X);
-    sh.ldp = K;
+    sh.ldp = ld.x;
     sh.rows = p->dptr(L.train_rows);
     sh.items = p->dptr(L.train_items);
     sh.Q = static_cast<const uint16_t*>(A);
@@ -656,7 +700,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   tb.n = 1;
   TokenReduceArgs& rb = tb.a[0];
   rb.P = static_cast<const uint16_t*>(dY);
-  rb.ldp = N;
+  rb.ldp = ld.dy;
   rb.prow = nullptr;
   rb.Q = hs;
   rb.ldq = ldhs;
@@ -691,7 +735,7 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   ta.n = 1;
   TokenReduceArgs& ra = ta.a[0];
   ra.P = static_cast<const uint16_t*>(X);
-  ra.ldp = K;
+  ra.ldp = ld.x;
   ra.prow = p->dptr(L.train_rows);
   ra.Q = gm;
   ra.ldq = ldh;
@@ -720,11 +764,11 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   if (dX) {
     GemmArgs g{};
     g.P = static_cast<const uint16_t*>(dY);
-    g.ldp = N;
+    g.ldp = ld.dy;
     g.Q = static_cast<const uint16_t*>(Wt ? Wt : W);
-    g.ldq = Wt ? N : K;
+    g.ldq = Wt ? ld.wt : ld.w;
     g.out = static_cast<uint16_t*>(dX);
-    g.ldo = K;
+    g.ldo = ld.dx;
     g.M = p->T_t;
     g.Nout = K;
     g.C = N;
@@ -768,7 +812,7 @@ extern "C" int dsv_cobatch_fwd_noalloc(const dsv_plan* p, dsv_dtype dt, int32_t 
   void* scratch = nullptr;
   if (noalloc_scratch(&scratch) != hipSuccess) return DSV_ERR_DEVICE;
   return fwd_impl(p, dt, K, N, X, W, A, B, Y, H_save, nullptr, scratch, kNoAllocScratchBytes, hip_stream,
-                  /*noalloc=*/true);
+                  /*lds=*/nullptr, /*noalloc=*/true);
 }
 
 extern "C" int dsv_cobatch_fwd_dropout(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X,
@@ -857,6 +901,12 @@ void by_contraction(int32_t n, const int32_t* C, int32_t* order) {
 
 }  // namespace
 
+extern "C" int32_t dsv_row_stride(int32_t n, dsv_dtype dt) {
+  if (n <= 0 || (dt != DSV_BF16 && dt != DSV_F32)) return 0;
+  if (dt == DSV_BF16 && n > 8192 && ((int64_t)n * 2) % 4096 == 0) return n + 64;
+  return n;
+}
+
 extern "C" int dsv_cobatch_fwd_grouped_workspace(const dsv_plan* p, dsv_dtype dt, int32_t n_proj,
                                                  const dsv_fwd_proj* projs, size_t* bytes) {
   int rc = check_group(p, dt, n_proj, projs);
@@ -906,15 +956,18 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
                      const dsv_dropout* drops, void* workspace, size_t workspace_bytes, void* hip_stream) {
   int rc = check_group(p, dt, n_proj, projs);
   if (rc != DSV_OK) return rc;
+  Strides st[DSV_MAX_GROUP];
   if (n_proj == 1) {
     const dsv_fwd_proj& q = projs[0];
+    if ((rc = check_common(p, dt, q.K, q.N)) != DSV_OK || (rc = fwd_strides(q, &st[0])) != DSV_OK) return rc;
     return fwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, drops, workspace, workspace_bytes,
-                    hip_stream);
+                    hip_stream, &st[0]);
   }
   // every check before any launch
   for (int i = 0; i < n_proj; ++i) {
     const dsv_fwd_proj& q = projs[i];
     if ((rc = check_common(p, dt, q.K, q.N)) != DSV_OK) return rc;
+    if ((rc = fwd_strides(q, &st[i])) != DSV_OK) return rc;
   }
   DropoutSpec ds[DSV_MAX_GROUP];
   bool dropping = false;
@@ -938,7 +991,7 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     for (int i = 0; i < n_proj; ++i) {
       const dsv_fwd_proj& q = projs[i];
       rc = fwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.Y, q.H_save, drops ? &drops[i] : nullptr, wsb + base[i],
-                    w[i].total, hip_stream);
+                    w[i].total, hip_stream, &st[i]);
       if (rc != DSV_OK) return rc;
     }
     return DSV_OK;
@@ -971,7 +1024,7 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     const dsv_fwd_proj& q = projs[i];
     SkinnyArgs& sk = sg.a[i];
     sk.P = static_cast<const uint16_t*>(q.X);
-    sk.ldp = q.K;
+    sk.ldp = st[i].x;
     sk.rows = p->dptr(L.shrink_rows);
     sk.items = p->dptr(L.shrink_items);
     sk.Q = static_cast<const uint16_t*>(q.A);
@@ -1021,11 +1074,11 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     const dsv_fwd_proj& q = projs[i];
     GemmArgs& g = G.a[k];
     g.P = static_cast<const uint16_t*>(q.X);
-    g.ldp = q.K;
+    g.ldp = st[i].x;
     g.Q = static_cast<const uint16_t*>(q.W);
-    g.ldq = q.K;
+    g.ldq = st[i].w;
     g.out = static_cast<uint16_t*>(q.Y);
-    g.ldo = q.N;
+    g.ldo = st[i].y;
     g.M = p->T;
     g.Nout = q.N;
     g.C = q.K;
@@ -1054,13 +1107,17 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
                      const dsv_dropout* drops, void* workspace, size_t workspace_bytes, void* hip_stream) {
   int rc = check_group(p, dt, n_proj, projs);
   if (rc != DSV_OK) return rc;
+  Strides st[DSV_MAX_GROUP];
   if (n_proj == 1) {
     const dsv_bwd_proj& q = projs[0];
+    if ((rc = check_common(p, dt, q.K, q.N)) != DSV_OK || (rc = bwd_strides(q, &st[0])) != DSV_OK) return rc;
     return bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate, drops, q.Wt,
-                    workspace, workspace_bytes, hip_stream);
+                    workspace, workspace_bytes, hip_stream, &st[0]);
   }
-  for (int i = 0; i < n_proj; ++i)
+  for (int i = 0; i < n_proj; ++i) {
     if ((rc = check_common(p, dt, projs[i].K, projs[i].N)) != DSV_OK) return rc;
+    if ((rc = bwd_strides(projs[i], &st[i])) != DSV_OK) return rc;
+  }
   DropoutSpec ds[DSV_MAX_GROUP];
   bool dropping = false;
   if ((rc = group_dropout(drops, n_proj, p->T_t, ds, &dropping)) != DSV_OK) return rc;
@@ -1087,7 +1144,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     for (int i = 0; i < n_proj; ++i) {
       const dsv_bwd_proj& q = projs[i];
       rc = bwd_impl(p, dt, q.K, q.N, q.X, q.W, q.A, q.B, q.H_save, q.dY, q.dA, q.dB, q.dX, accumulate,
-                    drops ? &drops[i] : nullptr, q.Wt, wsb + base[i], w[i].total, hip_stream);
+                    drops ? &drops[i] : nullptr, q.Wt, wsb + base[i], w[i].total, hip_stream, &st[i]);
       if (rc != DSV_OK) return rc;
     }
     return DSV_OK;
@@ -1130,7 +1187,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     uint16_t* hrec = at<uint16_t>(wsb + base[i], w[i].hrec);
     SkinnyArgs& sh = rg.a[rg.n++];
     sh.P = static_cast<const uint16_t*>(q.X);
-    sh.ldp = q.K;
+    sh.ldp = st[i].x;
     sh.rows = p->dptr(L.train_rows);
     sh.items = p->dptr(L.train_items);
     sh.Q = static_cast<const uint16_t*>(q.A);
@@ -1161,7 +1218,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     const dsv_bwd_proj& q = projs[i];
     TokenReduceArgs& tb = tbg.a[i];
     tb.P = static_cast<const uint16_t*>(q.dY);
-    tb.ldp = q.N;
+    tb.ldp = st[i].dy;
     tb.Q = hs[i];
     tb.ldq = ldhs[i];
     tb.chunks = p->dptr(L.chunks);
@@ -1200,7 +1257,7 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     const dsv_bwd_proj& q = projs[i];
     TokenReduceArgs& ta = tag.a[i];
     ta.P = static_cast<const uint16_t*>(q.X);
-    ta.ldp = q.K;
+    ta.ldp = st[i].x;
     ta.prow = p->dptr(L.train_rows);
     ta.Q = gm[i];
     ta.ldq = ldh;
@@ -1240,11 +1297,11 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
       if (!q.dX || (q.Wt != nullptr) != (nt == 1)) continue;
       GemmArgs& g = G.a[G.n];
       g.P = static_cast<const uint16_t*>(q.dY);
-      g.ldp = q.N;
+      g.ldp = st[i].dy;
       g.Q = static_cast<const uint16_t*>(nt ? q.Wt : q.W);
-      g.ldq = nt ? q.N : q.K;
+      g.ldq = nt ? st[i].wt : st[i].w;
       g.out = static_cast<uint16_t*>(q.dX);
-      g.ldo = q.K;
+      g.ldo = st[i].dx;
       g.M = p->T_t;
       g.Nout = q.K;
       g.C = q.N;

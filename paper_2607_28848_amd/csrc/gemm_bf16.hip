@@ -611,8 +611,9 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
   const int g0_a = td[4], g0_lo = td[5], g0_hi = td[6];  // zeros when the tile has no group
   const int g0_r = g.ranks[g0_a];
   const float g0_sc = g.scales ? g.scales[g0_a] : 1.f;
-  // NT: both operands are contraction-contiguous rows of the same length
-  // (the launcher checks ldp == ldq), so one set of lane offsets serves both.
+  // NT: both operands are contraction-contiguous rows; the lane offsets are
+  // computed for the A rows' stride and shifted by lr (ldq - ldp) elements for
+  // the B rows (zero when the strides agree).
   // NN: the weight is [C][Nout] (rows of the contraction, W itself); its tile
   // of a K-step is TK rows of TN columns, and the launcher checks that the
   // whole weight's byte offsets fit in 31 bits.
@@ -626,7 +627,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
   // weight from the tile's first column (rows past the contraction read zeros).
   const i32x4 ra = make_rsrc(g.P + (int64_t)m0 * ld, (uint64_t)a_rows * ld * 2);
   const i32x4 rb = NN ? make_rsrc(g.Q + n0, ((uint64_t)g.C * ldq - n0) * 2)
-                      : make_rsrc(g.Q + (int64_t)n0 * ld, (uint64_t)b_cols * ld * 2);
+                      : make_rsrc(g.Q + (int64_t)n0 * ldq, (uint64_t)b_cols * ldq * 2);
 
   // Operand loads: load i of a wave fills LDS rows 8q .. 8q+7 (q = 8 wave + i),
   // lane ln taking row 8q + ln/8, logical chunk (ln%8) ^ swz(row), which is
@@ -639,6 +640,7 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
   // NN weight loads: load i fills tile rows 2q, 2q+1 (q = 8 wave + i, 512
   // bytes each), lane ln taking row 2q + ln/32, slot ln%32, which holds the
   // row's 16-byte chunk (ln%32) ^ nn_swz(row); nn_swz(row) depends on i%2 only.
+  const int dq_lane = lr * (ldq - ld) * 2;  // NT: B row offset minus A row offset
   int voffb[2];
 #pragma unroll
   for (int par = 0; par < 2; ++par) {
@@ -651,8 +653,8 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
       llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voffb[i & 1],
                                       __builtin_amdgcn_readfirstlane((kt * TK + 2 * q) * ldq * 2), 0, 0);
     else
-      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voff[i],
-                                      __builtin_amdgcn_readfirstlane(q * 16 * ld + kt * TK * 2), 0, 0);
+      llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, voff[i] + dq_lane,
+                                      __builtin_amdgcn_readfirstlane(q * 16 * ldq + kt * TK * 2), 0, 0);
   };
   // whole K-step kt into `stage` (k0 + TK <= C)
   auto issue_whole = [&](int kt, int stage) {
@@ -680,10 +682,15 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
       const int q = wave * LOADS + i;
       const int row = 8 * q + lr;
       const int c = (lane & 7) ^ swz<TK>(row);
-      const int vo = (k0 + 8 * c < g.C) ? (row * ld + k0 + 8 * c) * 2 : (int)0x7FFFFFF0;
+      const bool in_c = k0 + 8 * c < g.C;
+      const int vo = in_c ? (row * ld + k0 + 8 * c) * 2 : (int)0x7FFFFFF0;
       llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(sa + q * 1024), 16, vo, 0, 0, 0);
-      if constexpr (NN) load_b(kt, sa, i);  // rows past the contraction lie past the descriptor
-      else llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, vo, 0, 0, 0);
+      if constexpr (NN) {
+        load_b(kt, sa, i);  // rows past the contraction lie past the descriptor
+      } else {
+        const int vb = in_c ? (row * ldq + k0 + 8 * c) * 2 : (int)0x7FFFFFF0;
+        llvm_amdgcn_raw_buffer_load_lds(rb, (lds_u32*)(sa + A_BYTES + q * 1024), 16, vb, 0, 0, 0);
+      }
     }
   };
 
@@ -987,11 +994,10 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
   auto load_n = [&](int kl, int ls, int n) {
     const int i = n & 7;
     const int q = wave * LOADS + i;
-    if (NN && n >= 8)
+    if (n >= 8)
       load_b(kl, buf(ls), i);
     else
-      llvm_amdgcn_raw_buffer_load_lds(n < 8 ? ra : rb,
-                                      (lds_u32*)(buf(ls) + (n < 8 ? 0 : A_BYTES) + q * 1024), 16, voff[i],
+      llvm_amdgcn_raw_buffer_load_lds(ra, (lds_u32*)(buf(ls) + q * 1024), 16, voff[i],
                                       __builtin_amdgcn_readfirstlane(q * 16 * ld + kl * TK * 2), 0, 0);
   };
   // One 32-wide step with fragments (cur, fb); reads the next step's
@@ -1250,9 +1256,8 @@ hipError_t launch_gemm_tiled(const GemmArgs& a, int tm, int tn, hipStream_t s) {
   const dim3 grid((unsigned)(a.dp_tiles + (int64_t)a.sk_tiles * (a.sk_tiles > 0 ? a.sk_split : 0)));
   if constexpr (!NN) {
     // 256 x 256 NT tiles: the 16x16x32 form (both operands rows of the
-    // contraction, one row length)
+    // contraction, each with its own row stride)
     if (tm == 256 && tn == 256) {
-      if (a.ldp != a.ldq) return hipErrorInvalidValue;
       const bool drop = a.keep != nullptr;
       if (a.sk_tiles > 0) {
         if (drop) launch_timed(gemm16_kernel<true, true, false>, grid, dim3(256), s, true, false, a);
@@ -1332,8 +1337,6 @@ hipError_t launch_gemm_group(const GemmGroup& g, hipStream_t s) {
   }
   if (g.off[g.n] <= 0) return hipSuccess;
   if constexpr (!NN) {
-    for (int p = 0; p < g.n; ++p)
-      if (g.a[p].ldp != g.a[p].ldq) return hipErrorInvalidValue;
     // the masked instantiation serves launches whose projections all carry a mask
     int n_keep = 0;
     for (int p = 0; p < g.n; ++p) n_keep += g.a[p].keep != nullptr;

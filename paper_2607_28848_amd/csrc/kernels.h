@@ -312,6 +312,7 @@ struct F32Args {
   const float* scales;
   const float *X, *W, *A, *B, *Hs, *dY;
   float *Y, *Hsave, *Hall, *G, *dA, *dB, *dX;
+  int64_t ldx, ldw, ldy, lddy, lddx;  // row strides of X, W, Y, dY, dX
   float* Hrec;   // backward with Hs == nullptr: h of the training rows recomputed here
   const uint32_t* keep;  // dropout mask of the training rows (nullptr: none)
   int32_t keep_words;

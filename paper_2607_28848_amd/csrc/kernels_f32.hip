@@ -22,7 +22,7 @@ __global__ void f32_shrink(F32Args g) {
   if (t >= g.T) return;
   const int a = g.row_adapter[t];
   if (j >= g.ranks[a]) return;
-  const float* x = g.X + (int64_t)t * g.K;
+  const float* x = g.X + (int64_t)t * g.ldx;
   const float* Aj = g.A + ((int64_t)a * g.r_max + j) * g.K;
   const int tr = g.row_train[t];
   const bool drop = g.keep && tr >= 0;  // dropout on a training row's low-rank input
@@ -41,7 +41,7 @@ __global__ void f32_hrec(F32Args g) {
   if (i >= g.Tt) return;
   const int a = g.train_adapter[i];
   if (j >= g.ranks[a]) return;
-  const float* x = g.X + (int64_t)g.train_rows[i] * g.K;
+  const float* x = g.X + (int64_t)g.train_rows[i] * g.ldx;
   const float* Aj = g.A + ((int64_t)a * g.r_max + j) * g.K;
   const bool drop = g.keep != nullptr;
   float acc = 0.f;
@@ -56,15 +56,15 @@ __global__ void f32_out(F32Args g) {
   const int t = (int)(idx / g.N), n = (int)(idx % g.N);
   if (t >= g.T) return;
   const int a = g.row_adapter[t], r = g.ranks[a];
-  const float* x = g.X + (int64_t)t * g.K;
-  const float* w = g.W + (int64_t)n * g.K;
+  const float* x = g.X + (int64_t)t * g.ldx;
+  const float* w = g.W + (int64_t)n * g.ldw;
   float low = 0.f;
   const float* h = g.Hall + (int64_t)t * g.r_max;
   const float* b = g.B + ((int64_t)a * g.N + n) * g.r_max;
   for (int j = 0; j < r; ++j) low = fmaf(h[j], b[j], low);
   float acc = g.scales[a] * low;
   for (int k = 0; k < g.K; ++k) acc = fmaf(x[k], w[k], acc);
-  g.Y[(int64_t)t * g.N + n] = acc;
+  g.Y[(int64_t)t * g.ldy + n] = acc;
 }
 
 // g = s_a dy B_a for every training row.
@@ -74,7 +74,7 @@ __global__ void f32_gmat(F32Args g) {
   if (i >= g.Tt) return;
   const int a = g.train_adapter[i];
   if (j >= g.ranks[a]) return;
-  const float* dy = g.dY + (int64_t)i * g.N;
+  const float* dy = g.dY + (int64_t)i * g.lddy;
   const float* b = g.B + (int64_t)a * g.N * g.r_max + j;
   float acc = 0.f;
   for (int n = 0; n < g.N; ++n) acc = fmaf(dy[n], b[(int64_t)n * g.r_max], acc);
@@ -94,7 +94,7 @@ __global__ void f32_db(F32Args g) {
   for (int p = g.tad_ptr[slot]; p < g.tad_ptr[slot + 1]; ++p) {
     const int32_t* ck = g.chunks + (int64_t)g.tad_chunks[p] * kItemWords;
     for (int i = ck[1]; i < ck[1] + ck[2]; ++i)
-      acc = fmaf(g.Hs[(int64_t)i * g.r_max + j], g.dY[(int64_t)i * g.N + n], acc);
+      acc = fmaf(g.Hs[(int64_t)i * g.r_max + j], g.dY[(int64_t)i * g.lddy + n], acc);
   }
   float* o = g.dB + ((int64_t)a * g.N + n) * g.r_max + j;
   const float v = g.scales[a] * acc;
@@ -113,7 +113,7 @@ __global__ void f32_da(F32Args g) {
   for (int p = g.tad_ptr[slot]; p < g.tad_ptr[slot + 1]; ++p) {
     const int32_t* ck = g.chunks + (int64_t)g.tad_chunks[p] * kItemWords;
     for (int i = ck[1]; i < ck[1] + ck[2]; ++i) {
-      const float x = g.X[(int64_t)g.train_rows[i] * g.K + k];
+      const float x = g.X[(int64_t)g.train_rows[i] * g.ldx + k];
       acc = fmaf(g.G[(int64_t)i * g.r_max + j], (g.keep && !kept(g, i, k)) ? 0.f : x, acc);
     }
   }
@@ -133,9 +133,9 @@ __global__ void f32_dx(F32Args g) {
   const float* Aa = g.A + (int64_t)a * g.r_max * g.K + k;
   for (int j = 0; j < r; ++j) acc = fmaf(gi[j], Aa[(int64_t)j * g.K], acc);
   if (g.keep) acc = kept(g, i, k) ? acc * g.drop_scale : 0.f;  // through the dropout mask
-  const float* dy = g.dY + (int64_t)i * g.N;
-  for (int n = 0; n < g.N; ++n) acc = fmaf(dy[n], g.W[(int64_t)n * g.K + k], acc);
-  g.dX[(int64_t)i * g.K + k] = acc;
+  const float* dy = g.dY + (int64_t)i * g.lddy;
+  for (int n = 0; n < g.N; ++n) acc = fmaf(dy[n], g.W[(int64_t)n * g.ldw + k], acc);
+  g.dX[(int64_t)i * g.lddx + k] = acc;
 }
 
 unsigned blocks(int64_t n) { return (unsigned)((n + 255) / 256); }

@@ -85,12 +85,17 @@ _lib.dsv_lora_bwd_dropout.argtypes = [_vp, ctypes.c_int, _i32, _i32, _vp, _vp, _
 _lib.dsv_lora_bwd_dropout.restype = ctypes.c_int
 class FwdProj(ctypes.Structure):
     _fields_ = [("K", _i32), ("N", _i32), ("X", _vp), ("W", _vp), ("A", _vp), ("B", _vp), ("Y", _vp),
-                ("H_save", _vp)]
+                ("H_save", _vp), ("ldx", _i32), ("ldw", _i32), ("ldy", _i32)]
 
 
 class BwdProj(ctypes.Structure):
     _fields_ = [("K", _i32), ("N", _i32), ("X", _vp), ("W", _vp), ("A", _vp), ("B", _vp), ("H_save", _vp),
-                ("dY", _vp), ("dA", _vp), ("dB", _vp), ("dX", _vp), ("Wt", _vp)]
+                ("dY", _vp), ("dA", _vp), ("dB", _vp), ("dX", _vp), ("Wt", _vp), ("ldx", _i32), ("ldw", _i32),
+                ("lddy", _i32), ("lddx", _i32), ("ldwt", _i32)]
+
+
+_lib.dsv_row_stride.argtypes = [_i32, ctypes.c_int]
+_lib.dsv_row_stride.restype = _i32
 
 
 MAX_GROUP = 8
@@ -165,6 +170,29 @@ def _stream_handle(stream):
 
 def _ptr(t) -> ctypes.c_void_p:
     return ctypes.c_void_p(0 if t is None else int(t.data_ptr()))
+
+
+def row_stride(n: int, dtype_code: int = 0) -> int:
+    """dsv_row_stride: the row stride (elements) recommended for buffers with rows of n elements."""
+    return int(_lib.dsv_row_stride(int(n), int(dtype_code)))
+
+
+def _ld(t, row_len: int) -> int:
+    """The row stride a grouped call passes for tensor t: 0 when t is dense, else t.stride(0).
+    The elements of a row must be contiguous."""
+    if t is None or t.is_contiguous():
+        return 0
+    if t.dim() != 2 or t.shape[1] != row_len or t.stride(1) != 1:
+        raise ValueError("a strided operand must be 2-D with contiguous rows of %d elements" % row_len)
+    return int(t.stride(0))
+
+
+def _dense(*ts):
+    """The single-projection calls take dense buffers only (the grouped calls take row strides)."""
+    for t in ts:
+        if t is not None and not t.is_contiguous():
+            raise ValueError("non-contiguous operand: the single-projection calls take dense buffers; "
+                             "pass row-strided operands to the grouped calls")
 
 
 class Plan:
@@ -297,6 +325,7 @@ def cobatch_fwd(plan: Plan, X, W, A, B, Y=None, H_save=None, workspace=None, str
     dropout=(p, seed, offset): LoRA dropout on the training rows' adapter input
     (dsv_cobatch_fwd_dropout)."""
     import torch
+    _dense(X, W, A, B, Y, H_save)
     dt = _dtype_code(X)
     T, K = X.shape
     N = W.shape[0]
@@ -323,6 +352,7 @@ def cobatch_fwd_noalloc(plan: Plan, X, W, A, B, Y, H_save=None, stream=None):
     workspace (no device allocation in the call).  The caller passes the outputs:
     Y [T][N] and, when the batch has training rows, H_save [T_t][r_max] (or None
     to keep nothing).  Returns (Y, H_save)."""
+    _dense(X, W, A, B, Y, H_save)
     dt = _dtype_code(X)
     K = X.shape[1]
     N = W.shape[0]
@@ -336,6 +366,7 @@ def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want
     """LoRA gradients of the training rows: dA, dB (fp32) and dX.  dropout=(p, seed,
     offset) must repeat the forward's (dsv_lora_bwd_dropout)."""
     import torch
+    _dense(X, W, A, B, H_save, dY, dA, dB, dX)
     dt = _dtype_code(X)
     T, K = X.shape
     N = W.shape[0]
@@ -365,7 +396,10 @@ def lora_bwd(plan: Plan, X, W, A, B, H_save, dY, dA=None, dB=None, dX=None, want
 def _fwd_projs(items):
     arr = (FwdProj * len(items))()
     for i, (X, W, A, B, Y, H) in enumerate(items):
-        arr[i] = FwdProj(X.shape[1], W.shape[0], _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y), _ptr(H))
+        K, N = X.shape[1], W.shape[0]
+        _dense(A, B, H)
+        arr[i] = FwdProj(K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(Y), _ptr(H), _ld(X, K), _ld(W, K),
+                         _ld(Y, N))
     return arr
 
 
@@ -456,8 +490,10 @@ def lora_bwd_grouped(plan: Plan, projs, accumulate: bool = False, want_dx: bool 
     arr = (BwdProj * len(items))()
     for i, (X, W, A, B, H, dY, dA, dB, dX) in enumerate(items):
         Wt = wts[i] if wts is not None else None
-        arr[i] = BwdProj(X.shape[1], W.shape[0], _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H), _ptr(dY), _ptr(dA),
-                         _ptr(dB), _ptr(dX), _ptr(Wt))
+        K, N = X.shape[1], W.shape[0]
+        _dense(A, B, H, dA, dB)
+        arr[i] = BwdProj(K, N, _ptr(X), _ptr(W), _ptr(A), _ptr(B), _ptr(H), _ptr(dY), _ptr(dA), _ptr(dB), _ptr(dX),
+                         _ptr(Wt), _ld(X, K), _ld(W, K), _ld(dY, N), _ld(dX, K), _ld(Wt, N))
     dr = _dropouts(dropouts, len(items))
     if dr is None:
         _check(_lib.dsv_lora_bwd_grouped(plan.handle, dt, len(items), arr, 1 if accumulate else 0, _ptr(ws),

@@ -144,7 +144,8 @@ def test_grouped_llama8b_layer_set_full_size():
     + 2048 training) in one grouped forward and one grouped backward whose dX GEMMs
     read the transposed frozen weights.  Y and dX of every projection on sampled
     rows, H_save, dA, dB in full, against the fp64 reference; the backward without
-    the transposed weights is bit-identical."""
+    the transposed weights, and both calls on the benchmark's row-strided buffers,
+    are bit-identical."""
     import torch
     from paper_2607_28848_amd import dsv
     w = wl.llama8b_mixed()
@@ -164,7 +165,30 @@ def test_grouped_llama8b_layer_set_full_size():
     for i in range(len(dev)):
         for a, b in zip(grads[i], plain[i]):
             assert torch.equal(_bits(a), _bits(b))
-    del plain, wts
+    del plain
+
+    # the benchmark's default layout: rows of the recommended stride (gate/up/down
+    # rows of 14336 elements 14400 apart), bit-identical to the dense buffers
+    def srow(t):
+        st = dsv.row_stride(t.shape[1], dsv.BF16)
+        if st == t.shape[1]:
+            return t
+        buf = torch.zeros((t.shape[0], st), dtype=t.dtype, device=t.device)
+        buf[:, :t.shape[1]] = t
+        return buf[:, :t.shape[1]]
+
+    assert any(dsv.row_stride(n, dsv.BF16) != n for p in w.projections for n in (p.K, p.N))
+    sdev = [{k: srow(d[k]) for k in ("X", "W", "dY")} for d in dev]
+    out_s = dsv.cobatch_fwd_grouped(plan, [(s["X"], s["W"], d["A"], d["B"], srow(torch.zeros_like(out[i][0])),
+                                            torch.zeros_like(out[i][1])) for i, (s, d) in enumerate(zip(sdev, dev))])
+    grads_s = dsv.lora_bwd_grouped(plan, [(s["X"], s["W"], d["A"], d["B"], out_s[i][1], s["dY"], None, None,
+                                           srow(torch.zeros_like(grads[i][2])))
+                                          for i, (s, d) in enumerate(zip(sdev, dev))], wts=[srow(t) for t in wts])
+    torch.cuda.synchronize()
+    for i in range(len(dev)):
+        for a, b in list(zip(out_s[i], out[i])) + list(zip(grads_s[i], grads[i])):
+            assert torch.equal(_bits(a.contiguous()), _bits(b))
+    del sdev, out_s, grads_s, wts
     tr = plan.train_rows()
     rng = np.random.default_rng(11)
     Tt = w.train_tokens

@@ -458,6 +458,70 @@ def test_grouped_argument_checks_on_host():
             dsv.bwd_workspace_bytes(plan, dt, K, 64) for K, _ in shapes) // 2
 
 
+def test_row_strides_checked_on_host():
+    """Row strides of the grouped calls: 0 (dense) and any multiple of 8 from the row
+    length up to 2^20 pass the checks (the host-only plan then fails with ERR_ARG);
+    a stride shorter than a row, not a multiple of 8, above 2^20 or negative fails
+    with ERR_SIZE before anything else, in a group of one and of two, for every
+    strided operand.  dsv_row_stride pads long bf16 rows whose byte length is a
+    multiple of 4096; the binding passes a row-strided view's stride and refuses
+    non-contiguous operands in the single-projection calls."""
+    import ctypes
+    import torch
+    dsv = _dsv()
+    lib = dsv.lib_handle()
+    plan = dsv.segments_build([(0, 16, 0, 1), (16, 300, 1, 0)], 316, [4, 4], [2.0, 2.0], 4)
+    fake = ctypes.c_void_p(4096)
+    K, N = 72, 136
+    lens = {"ldx": K, "ldw": K, "ldy": N, "lddy": N, "lddx": K, "ldwt": N}
+    for n in (1, 2):
+        arr = (dsv.FwdProj * n)()
+        for i in range(n):
+            arr[i] = dsv.FwdProj(K, N, fake, fake, fake, fake, fake, fake)
+        assert lib.dsv_cobatch_fwd_grouped(plan.handle, dsv.BF16, n, arr, fake, 1 << 20, None) == dsv.ERR_ARG
+        for f in ("ldx", "ldw", "ldy"):
+            for v in (lens[f], lens[f] + 8, lens[f] + 64, 1 << 20):
+                setattr(arr[n - 1], f, v)
+                assert lib.dsv_cobatch_fwd_grouped(plan.handle, dsv.BF16, n, arr, fake, 1 << 20, None) == dsv.ERR_ARG
+            for v in (lens[f] - 8, lens[f] + 4, (1 << 20) + 8, -8):
+                setattr(arr[n - 1], f, v)
+                for dt in (dsv.BF16, dsv.F32):
+                    assert lib.dsv_cobatch_fwd_grouped(plan.handle, dt, n, arr, fake, 1 << 20, None) == dsv.ERR_SIZE, (f, v)
+            setattr(arr[n - 1], f, 0)
+        barr = (dsv.BwdProj * n)()
+        for i in range(n):
+            barr[i] = dsv.BwdProj(K, N, fake, fake, fake, fake, fake, fake, fake, fake, fake, fake)
+        assert lib.dsv_lora_bwd_grouped(plan.handle, dsv.BF16, n, barr, 0, fake, 1 << 20, None) == dsv.ERR_ARG
+        for f in ("ldx", "ldw", "lddy", "lddx", "ldwt"):
+            setattr(barr[n - 1], f, lens[f] + 64)
+            assert lib.dsv_lora_bwd_grouped(plan.handle, dsv.BF16, n, barr, 0, fake, 1 << 20, None) == dsv.ERR_ARG
+            for v in (lens[f] - 8, lens[f] + 4, (1 << 20) + 8, -8):
+                setattr(barr[n - 1], f, v)
+                for dt in (dsv.BF16, dsv.F32):
+                    assert lib.dsv_lora_bwd_grouped(plan.handle, dt, n, barr, 0, fake, 1 << 20, None) == dsv.ERR_SIZE, (f, v)
+            setattr(barr[n - 1], f, 0)
+    # the recommended stride
+    assert dsv.row_stride(14336, dsv.BF16) == 14400
+    assert dsv.row_stride(28672, dsv.BF16) == 28736
+    for n in (4096, 8192, 1024, 10000, 14344, 8):
+        assert dsv.row_stride(n, dsv.BF16) == n
+    assert dsv.row_stride(14336, dsv.F32) == 14336
+    assert dsv.row_stride(0, dsv.BF16) == 0 and dsv.row_stride(14336, 7) == 0
+    # binding: the stride of a row-strided view, dense = 0, column-strided refused
+    buf = torch.zeros((10, 88), dtype=torch.bfloat16)
+    assert dsv._ld(buf[:, :72], 72) == 88
+    assert dsv._ld(buf, 88) == 0 and dsv._ld(None, 72) == 0
+    with pytest.raises(ValueError):
+        dsv._ld(buf.t(), 10)
+    with pytest.raises(ValueError):
+        dsv._ld(buf[:, :72:2], 36)
+    X = buf[:, :72]
+    with pytest.raises(ValueError):
+        dsv.cobatch_fwd(plan, X, torch.zeros((8, 72), dtype=torch.bfloat16), None, None)
+    with pytest.raises(ValueError):
+        dsv.lora_bwd(plan, X, torch.zeros((8, 72), dtype=torch.bfloat16), None, None, None, None)
+
+
 def test_adamw_grouped_argument_checks_on_host():
     """dsv_adamw_step_grouped rejects a bad group size (ERR_RANGE), a NULL array
     (ERR_ARG), a bad shape in any entry (ERR_SIZE), bad hyper-parameters
