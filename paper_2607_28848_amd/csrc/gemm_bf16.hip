@@ -77,6 +77,12 @@ struct GemmShape {
 
 // s_waitcnt immediate (gfx9 encoding): wait until at most n vector-memory
 // operations of this wave are outstanding; lgkm and exp counters untouched.
+// A compile-time flag passed as a value (selects a generic lambda's form).
+template <bool B>
+struct bool_c {
+  static constexpr bool value = B;
+};
+
 constexpr int vmcnt_imm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
 // Workgroup id -> logical index.  Consecutive workgroup ids land on different
@@ -1088,67 +1094,86 @@ __device__ __forceinline__ void gemm_piece16(const GemmArgs& g, char* smem0, cha
   // one half-wave fall on distinct banks.
   constexpr int SRS = WN * 2 + 16;
   static_assert(NW * 32 * SRS <= STAGE, "epilogue slices fit the idle pipeline buffer");
+  constexpr int CPR = WN / 8;  // 16-byte chunks per slice row
+  static_assert(CPR == 16, "a slice read step covers 4 rows of 16 chunks");
   char* slice = buf(last_stage ^ 1) + wave * 32 * SRS;
+  // Read-back step q of slice t: lane ln takes chunk ln % 16 of slice row
+  // 4q + ln / 16.  Its output address is a wave-uniform part (row
+  // m0 + wm WM + 32t + 4q, column n0 + wn WN) plus a per-lane offset.
+  const int64_t ldo2 = g.ldo * 2;
+  const uint32_t lane_off = (uint32_t)((lane >> 4) * ldo2 + 16 * (lane & 15));
+  char* const out_w = reinterpret_cast<char*>(g.out) + ((int64_t)(m0 + wm * WM) * g.ldo + n0 + wn * WN) * 2;
+  // The plain form (a whole tile without gathered rows) is compiled apart
+  // from the general one: its stores need no bounds checks and its values no
+  // gathered terms, which would otherwise be selected and added everywhere.
   const bool gathered = has_gather && g.delta != nullptr;
-  // Gathered rows add their fp32 term: the wave's row slots are read once and
-  // each slice's terms are loaded while the slice before it is processed.
-  int gsv[FM];
-  f32x4 dn[2][FN];
-  auto load_terms = [&](int t) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = wn * WN + 16 * j + 4 * (lane >> 4);
-        const int gs = gsv[2 * t + h];
-        const f32x4 d = *reinterpret_cast<const f32x4*>(g.delta + (int64_t)max(gs, 0) * g.Nout +
-                                                        min(n0 + col, g.Nout - 4));
-        dn[h][j] = (gs >= 0 && n0 + col < g.Nout) ? d : f32x4{0.f, 0.f, 0.f, 0.f};
-      }
-  };
-  if (gathered) {
-#pragma unroll
-    for (int i = 0; i < FM; ++i) {
-      const int row = wm * WM + 16 * i + l15;
-      gsv[i] = row < nrows ? g.gslot[m0 + row] : -1;
-    }
-    load_terms(0);
-  }
-#pragma unroll
-  for (int t = 0; t < FM / 2; ++t) {
-    f32x4 dc[2][FN];
-    if (gathered) {
+  auto epilogue = [&](auto plain_c) {
+    constexpr bool PLAIN = decltype(plain_c)::value;
+    // Gathered rows add their fp32 term: the wave's row slots are read once
+    // and each slice's terms are loaded while the slice before it is processed.
+    int gsv[FM];
+    f32x4 dn[2][FN];
+    auto load_terms = [&](int t) {
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int j = 0; j < FN; ++j) dc[h][j] = dn[h][j];
-      if (t + 1 < FM / 2) load_terms(t + 1);
-    }
+        for (int j = 0; j < FN; ++j) {
+          const int col = wn * WN + 16 * j + 4 * (lane >> 4);
+          const int gs = gsv[2 * t + h];
+          const f32x4 d = *reinterpret_cast<const f32x4*>(g.delta + (int64_t)max(gs, 0) * g.Nout +
+                                                          min(n0 + col, g.Nout - 4));
+          dn[h][j] = (gs >= 0 && n0 + col < g.Nout) ? d : f32x4{0.f, 0.f, 0.f, 0.f};
+        }
+    };
+    if (!PLAIN && gathered) {
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      const int i = 2 * t + h;
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int col = wn * WN + 16 * j + 4 * (lane >> 4);
-        f32x4 x = acc[i][j];
-        if (gathered) x += dc[h][j];
-        const uint32_t w0 = f2bf2(x[0], x[1]), w1 = f2bf2(x[2], x[3]);
-        *reinterpret_cast<uint2*>(slice + (16 * h + l15) * SRS + 2 * (col - wn * WN)) = make_uint2(w0, w1);
+      for (int i = 0; i < FM; ++i) {
+        const int row = wm * WM + 16 * i + l15;
+        gsv[i] = row < nrows ? g.gslot[m0 + row] : -1;
       }
+      load_terms(0);
     }
-    asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: the slice is complete
-    constexpr int CPR = WN / 8;     // 16-byte chunks per slice row
 #pragma unroll
-    for (int q = 0; q < 32 * CPR / 64; ++q) {
-      const int id = 64 * q + lane;
-      const int rr = id / CPR, ch = id % CPR;
-      const u32x4 v = *reinterpret_cast<const u32x4*>(slice + rr * SRS + 16 * ch);
-      const int orow = wm * WM + 32 * t + rr, ocol = n0 + wn * WN + 8 * ch;
-      if (orow < nrows && ocol < g.Nout)
-        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(g.out + (int64_t)(m0 + orow) * g.ldo + ocol));
+    for (int t = 0; t < FM / 2; ++t) {
+      f32x4 dc[2][FN];
+      if (!PLAIN && gathered) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+#pragma unroll
+          for (int j = 0; j < FN; ++j) dc[h][j] = dn[h][j];
+        if (t + 1 < FM / 2) load_terms(t + 1);
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int i = 2 * t + h;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = wn * WN + 16 * j + 4 * (lane >> 4);
+          f32x4 x = acc[i][j];
+          if (!PLAIN && gathered) x += dc[h][j];
+          const uint32_t w0 = f2bf2(x[0], x[1]), w1 = f2bf2(x[2], x[3]);
+          *reinterpret_cast<uint2*>(slice + (16 * h + l15) * SRS + 2 * (col - wn * WN)) = make_uint2(w0, w1);
+        }
+      }
+      asm volatile("" ::: "memory");  // a wave's LDS accesses run in order: the slice is complete
+#pragma unroll
+      for (int q = 0; q < 32 * CPR / 64; ++q) {
+        const u32x4 v = *reinterpret_cast<const u32x4*>(slice + (4 * q + (lane >> 4)) * SRS + 16 * (lane & 15));
+        char* const dst = out_w + (int64_t)(32 * t + 4 * q) * ldo2 + lane_off;
+        if constexpr (PLAIN) {
+          __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
+        } else {
+          const int orow = wm * WM + 32 * t + 4 * q + (lane >> 4), ocol = n0 + wn * WN + 8 * (lane & 15);
+          if (orow < nrows && ocol < g.Nout) __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dst));
+        }
+      }
+      asm volatile("" ::: "memory");  // the slice is read before the next rows overwrite it
     }
-    asm volatile("" ::: "memory");  // the slice is read before the next rows overwrite it
-  }
+  };
+  if (!gathered && nrows >= TM && n0 + TN <= g.Nout)
+    epilogue(bool_c<true>{});
+  else
+    epilogue(bool_c<false>{});
 }
 
 template <bool SK, bool DROP, bool NN>
