@@ -75,15 +75,11 @@ struct GemmShape {
   static constexpr int LDS = NS * STAGE;
 };
 
-// s_waitcnt immediate (gfx9 encoding): wait until at most n vector-memory
-// operations of this wave are outstanding; lgkm and exp counters untouched.
 // A compile-time flag passed as a value (selects a generic lambda's form).
 template <bool B>
 struct bool_c {
   static constexpr bool value = B;
 };
-
-constexpr int vmcnt_imm(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
 
 // Workgroup id -> logical index.  Consecutive workgroup ids land on different
 // XCDs (round robin over 8); the renumbering gives each XCD a contiguous
@@ -1199,8 +1195,11 @@ template <bool DROP, bool NN>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void gemm16_group_kernel(GemmGroup G) {
   __shared__ __attribute__((aligned(1024))) char smem0[2 * 256 * 64 * 2];
   __shared__ __attribute__((aligned(1024))) char smem1[2 * 256 * 64 * 2];
+  // the workgroup's projection: every boundary compared at once (one batch
+  // of argument loads instead of one dependent load per projection)
   int pj = 0;
-  while (pj + 1 < G.n && (int)blockIdx.x >= G.off[pj + 1]) ++pj;
+#pragma unroll
+  for (int p = 1; p < kMaxGroup; ++p) pj += (p < G.n && (int)blockIdx.x >= G.off[p]) ? 1 : 0;
   const GemmArgs g = G.a[pj];
   const int local = (int)blockIdx.x - G.off[pj];
   const int lin = xcd_major(local, G.off[pj + 1] - G.off[pj]);

@@ -46,6 +46,11 @@ namespace {
 constexpr int SW = 8;       // waves per rank-contraction workgroup
 constexpr int SK_CK = 256;  // contraction columns per chunk
 
+// Zeros in global memory: a direct-to-LDS load from here writes zeros, so a
+// lane with nothing to load still issues its load and every wave issues the
+// same number of loads per chunk (what a partial vmcnt wait relies on).
+__device__ const u32x4 kZeroRow[64] = {};
+
 typedef __attribute__((address_space(1))) const void global_cv;
 extern "C" __device__ void llvm_amdgcn_global_load_lds(global_cv* src, lds_u32* lds, int size, int offset,
                                                        int aux) __asm("llvm.amdgcn.global.load.lds");
@@ -80,7 +85,11 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
   constexpr int L = SR / 2 / SW;          // 1 KiB load instructions per wave per chunk
   constexpr int STAGE = SR * RB;
   static_assert(L * 2 * SW == SR, "loads per wave");
-  __shared__ __attribute__((aligned(1024))) char smem[2 * STAGE];
+  // Chunks in flight: three buffers (two chunks loading while one is used)
+  // where that keeps two workgroups per CU (72 KB of LDS), else two.  Under
+  // dropout the mask loads share the vector-memory counter, so two.
+  constexpr int NSTG = (!DROP && 3 * STAGE <= 72 * 1024) ? 3 : 2;
+  __shared__ __attribute__((aligned(1024))) char smem[NSTG * STAGE];
   const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int32_t* it = g.items + (int64_t)blockIdx.x * kItemWords;
   const int a = it[0], begin = it[1], cnt = it[2];
@@ -115,10 +124,15 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
     for (int i = 0; i < L; ++i) {
       const int q = wave * L + i;
       const int k = c * SK_CK + 8 * (sl ^ ((2 * q + sub) & 7));
-      if (k < kcap[i])
+      if constexpr (NSTG == 3) {  // every lane loads: L loads per wave per chunk
+        const void* from = k < kcap[i] ? static_cast<const void*>(src[i] + c * SK_CK)
+                                       : static_cast<const void*>(&kZeroRow[lane]);
+        llvm_amdgcn_global_load_lds((global_cv*)from, (lds_u32*)(base + q * 1024), 16, 0, 0);
+      } else if (k < kcap[i]) {
         llvm_amdgcn_global_load_lds((global_cv*)(src[i] + c * SK_CK), (lds_u32*)(base + q * 1024), 16, 0, 0);
-      else
+      } else {
         *reinterpret_cast<u32x4*>(base + q * 1024 + 16 * lane) = zero4();
+      }
     }
   };
   // dropout: compact training index of each fragment row of the lane (-1: none)
@@ -150,11 +164,22 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
     for (int t = 0; t < RT; ++t) m[t] = keep_byte(g.keep, g.keep_words, max(trl[t], 0), col);
   };
   auto chunk = [&](int c, const uint32_t (&mu)[RT], uint32_t (&ml)[RT]) {
-    vmem_wait_all();
-    __syncthreads();  // chunk c is in; every wave is done with chunk c - 1's buffer
-    if (c + 1 < nch) issue(c + 1, (c + 1 - c_beg) & 1);
+    if constexpr (NSTG == 3) {
+      // This wave's loads of chunk c are in (chunk c + 1's L loads may still be
+      // in flight), and after the barrier everyone's are.  A plain barrier: the
+      // fence of __syncthreads would wait for every load in flight.
+      if (c + 1 < nch) __builtin_amdgcn_s_waitcnt(vmcnt_imm(L));
+      else vmem_wait_all();
+      asm volatile("" ::: "memory");
+      __builtin_amdgcn_s_barrier();
+      asm volatile("" ::: "memory");
+    } else {
+      vmem_wait_all();
+      __syncthreads();  // chunk c is in; every wave is done with chunk c - 1's buffer
+    }
+    if (c + NSTG - 1 < nch) issue(c + NSTG - 1, (c + NSTG - 1 - c_beg) % NSTG);
     if constexpr (DROP) load_mask(min(c + 1, nch - 1), ml);  // unconditional: no merge to wait on
-    const char* sb = smem + ((c - c_beg) & 1) * STAGE;
+    const char* sb = smem + ((c - c_beg) % NSTG) * STAGE;
     bf16x8 xf[RT], qf[NJ];
 #pragma unroll
     for (int t = 0; t < RT; ++t) {
@@ -177,6 +202,7 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
   uint32_t m0[RT] = {}, m1[RT] = {};
   if (c_beg < nch) {
     issue(c_beg, 0);
+    if (NSTG == 3 && c_beg + 1 < nch) issue(c_beg + 1, 1);
     if constexpr (DROP) load_mask(c_beg, m0);
   }
   for (int c = c_beg; c < nch; c += 2) {
@@ -185,7 +211,7 @@ __global__ __launch_bounds__(64 * SW) void skinny_kernel(SkinnyGroup G) {
   }
   __syncthreads();  // the stage buffers become the reduction buffer
   constexpr int RW = 16 * NJ + 1;
-  static_assert(SW * ROWS * RW * 4 <= 2 * STAGE, "reduction buffer");
+  static_assert(SW * ROWS * RW * 4 <= NSTG * STAGE, "reduction buffer");
   float* red = reinterpret_cast<float*>(smem);  // [SW][ROWS][RW]
 #pragma unroll
   for (int t = 0; t < RT; ++t)
