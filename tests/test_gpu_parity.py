@@ -110,15 +110,18 @@ def test_split_tiles_ragged():
                dx_rows=dx_rows.astype(np.int32))
 
 
-@pytest.mark.parametrize("dtype,K,N", [("bf16", 520, 776), ("f32", 520, 776), ("bf16", 4096, 4096),
-                                       ("bf16", 4104, 2056)])
-def test_residual_only_retention_recomputes_h_bit_exact(dtype, K, N):
+@pytest.mark.parametrize("dtype,K,N,r_max", [("bf16", 520, 776, 64), ("f32", 520, 776, 64), ("bf16", 4096, 4096, 64),
+                                             ("bf16", 4104, 2056, 64), ("bf16", 4104, 2056, 16),
+                                             ("bf16", 520, 776, 16)])
+def test_residual_only_retention_recomputes_h_bit_exact(dtype, K, N, r_max):
     """A forward that keeps no H_save (the caller keeps X) and a backward that
     recomputes h from X and A give bit-identical Y, dA, dB and dX to keeping H_save
     (the recompute is the forward's own shrink over the training rows; at K = 4096 both
-    split the contraction into chunks)."""
+    split the contraction into chunks).  r_max = 16 runs the rank-16 shrink, whose
+    chunks load three buffers deep."""
     import torch
-    w = wl.custom(MIXED, MIXED_RANKS, K=K, N=N, dtype=dtype, r_max=64, name="recompute")
+    ranks = MIXED_RANKS if r_max == 64 else [16, 8, 16, 12, 5]
+    w = wl.custom(MIXED, ranks, K=K, N=N, dtype=dtype, r_max=r_max, name="recompute")
     run = Run(w)
     Y1, H = run.fwd()
     dA1, dB1, dX1 = run.bwd(H)
