@@ -548,6 +548,218 @@ __global__ __launch_bounds__(512) void token_reduce_kernel(TokenReduceGroup G) {
       }
 }
 
+// ---------------------------------------------------------------------------
+// The same reductions without dropout, pipelined two steps deep, for Q rows
+// that are 16-byte aligned (ldq a multiple of 8).  The step's Q tile (32
+// tokens x 16 ranks per wave below NJ) goes into LDS by direct loads beside
+// the P tile and is read back transposed like it, so no step has to combine
+// scalar loads it just issued.  Two buffers, each a separate array picked by
+// a compile-time number (a read of one buffer then never waits for the
+// direct loads into the other).  Step s waits for its own loads only, every
+// wave reads its fragments (GP: waves 0 and 1 also store the previous step's
+// g partial and compute this step's from the buffer), a second barrier frees
+// the buffer, and the direct loads of step s + 2 go into it before the
+// MFMAs: two steps stay in flight per workgroup.  The direct loads are the
+// last vector-memory operations of a step, and every wave issues three of
+// them in every step, also for the two steps past the end (lanes and waves
+// with nothing to load read a zero row, the spare waves into a scratch tile
+// of the buffer), so the wait at the top of a step is always "all but the
+// last three".  The chunk's P row numbers sit in LDS, loaded once.  Sums,
+// their order and the results are those of token_reduce_kernel.
+// ---------------------------------------------------------------------------
+template <int V>
+struct int_c {
+  static constexpr int value = V;
+};
+
+__device__ __forceinline__ u32x2 tr_read16(const char* p) {
+  const s16x4 h = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)p);
+  return u32x2{(uint32_t)(uint16_t)h[0] | ((uint32_t)(uint16_t)h[1] << 16),
+               (uint32_t)(uint16_t)h[2] | ((uint32_t)(uint16_t)h[3] << 16)};
+}
+
+// Up to 16 ranks: six waves per SIMD, so that three workgroups share a CU
+// (their LDS fits as well).
+template <int NJ, bool GP>
+__global__ __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(NJ == 1 ? 6 : 1))) void token_reduce_pipe_kernel(
+    TokenReduceGroup G) {
+  constexpr int TS = 32;                   // tokens per step
+  constexpr int PB = TS * kTokenCols * 2;  // P bytes per step
+  constexpr int QB = 1024;                 // Q bytes per step and 16 ranks
+  constexpr int NLD = 3;                   // direct loads per wave and step
+  // [P tile][Q tiles][spare tile]
+  __shared__ __attribute__((aligned(256))) char st0[PB + (NJ + 1) * QB];
+  __shared__ __attribute__((aligned(256))) char st1[PB + (NJ + 1) * QB];
+  __shared__ __attribute__((aligned(16))) char bts[GP ? 16 * NJ * kBtRow : 16];
+  __shared__ int32_t prl[kChunkRows];
+  int k = 0;  // the reduction: blockIdx.y runs over every reduction's column blocks
+  while (k + 1 < G.n && (int)blockIdx.y >= G.yoff[k + 1]) ++k;
+  const TokenReduceArgs g = G.a[k];
+  const int cb = (int)blockIdx.y - G.yoff[k], cbase = cb * kTokenCols;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int32_t* ck = g.chunks + (int64_t)blockIdx.x * kItemWords;
+  const int a = ck[0], begin = ck[1], cnt = min(ck[2], kChunkRows);
+  const int r = g.ranks[a];
+  const int nsteps = (cnt + TS - 1) / TS;
+  const int sub = lane >> 5, sl = lane & 31;  // staging: row within the instruction, slot
+  const int gq = lane >> 4, lam = lane & 15;  // fragments: token octet, column / rank
+  for (int i = tid; i < cnt; i += 512) prl[i] = g.prow ? g.prow[begin + i] : begin + i;
+  __syncthreads();
+  // P rows 2q + sub of the step (q = 2 wave + i), slot sl holding the row's
+  // 16-byte chunk sl ^ 2(row % 4); wave w < NJ loads Q[token][16w .. 16w+15]
+  // as [32 tokens][32 bytes], one token half per lane
+  auto issue = [&](int step, char* sb) {
+    const int t0 = step * TS;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int q = 2 * wave + i, row = 2 * q + sub;
+      const int c = cbase + 8 * (sl ^ (2 * (row & 3)));
+      const bool in = t0 + row < cnt && c < g.C;
+      const void* from = in ? static_cast<const void*>(g.P + (int64_t)prl[max(min(t0 + row, cnt - 1), 0)] * g.ldp + c)
+                            : static_cast<const void*>(&kZeroRow[lane]);
+      llvm_amdgcn_global_load_lds((global_cv*)from, (lds_u32*)(sb + (q * 1024)), 16, 0, 0);
+    }
+    const int tq = lane >> 1, j0 = 16 * wave + 8 * (lane & 1);
+    const bool in = wave < NJ && t0 + tq < cnt && j0 < g.ldq;
+    const void* from = in ? static_cast<const void*>(g.Q + (int64_t)(begin + t0 + tq) * g.ldq + j0)
+                          : static_cast<const void*>(&kZeroRow[lane]);
+    llvm_amdgcn_global_load_lds((global_cv*)from, (lds_u32*)(sb + (PB + min(wave, NJ) * QB)), 16, 0, 0);
+  };
+  issue(0, st0);
+  issue(1, st1);
+  if constexpr (GP) {
+    // B_a[c][j] of the block's columns into bts[j][c]; zero past the rank and
+    // past C (published by the first step's barrier)
+    const uint16_t* Ba = g.B + (int64_t)a * g.C * g.r_max;
+    const bool b16 = (g.r_max & 7) == 0;  // a rank octet is one aligned 16-byte load
+    for (int idx = tid; idx < kTokenCols * 2 * NJ; idx += 512) {
+      const int cl = idx % kTokenCols, jo = idx / kTokenCols;  // column, rank octet
+      const int c = cbase + cl, nv = min(8, r - 8 * jo);
+      u32x4 v = zero4();
+      if (c < g.C && nv > 0) {
+        const uint16_t* src = Ba + (int64_t)c * g.r_max + 8 * jo;
+        v = (b16 && nv == 8) ? ld16(src) : ld8_masked(src, 1, nv);
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        *reinterpret_cast<uint16_t*>(bts + (8 * jo + e) * kBtRow + 2 * cl) = (uint16_t)(v[e >> 1] >> (16 * (e & 1)));
+    }
+  }
+  f32x4 acc[2][NJ], ga[NJ];
+#pragma unroll
+  for (int jt = 0; jt < NJ; ++jt) {
+    acc[0][jt] = acc[1][jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    ga[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  // GP: the g partial of a step, ga[jt][v] = token 16 wave + 4 gq + v of the
+  // step, rank 16 jt + lam (waves 0 and 1)
+  auto gp_store = [&](int step) {
+    if (wave < 2) {
+      float* gp = g.gpart + ((int64_t)cb * g.gpart_n + begin) * g.r_max;
+#pragma unroll
+      for (int jt = 0; jt < NJ; ++jt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int tok = step * TS + 16 * wave + 4 * gq + v, j = 16 * jt + lam;
+          if (tok < cnt && j < r) gp[(int64_t)tok * g.r_max + j] = ga[jt][v];
+        }
+    }
+  };
+  // Byte offsets of the lane's fragment reads within a buffer (every LDS
+  // address below is one offset from its array: the compiler then tells the
+  // two buffers apart and waits only for the loads into the one read).  The
+  // token t = 8 gq + 4 hh + lam / 4 has t % 4 = lam / 4 for both halves hh,
+  // so the second half is 4 rows (2048 bytes) further.
+  int off_x[2];
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct) {
+    const int t = 8 * gq + (lam >> 2);
+    const int col = 32 * wave + 16 * ct + 4 * (lam & 3);  // within the block
+    off_x[ct] = t * (kTokenCols * 2) + 16 * ((col >> 3) ^ (2 * (t & 3))) + 2 * (col & 7);
+  }
+  const int off_q = PB + (8 * gq + (lam >> 2)) * 32 + 8 * (lam & 3);
+  // GP: row t = 16 wave + lam, chunk (4 kc + gq) ^ 2(t % 4) = 8(kc / 2) + ((4(kc % 2) + gq) ^ 2(t % 4))
+  int off_av[2], off_bt[NJ];
+#pragma unroll
+  for (int b = 0; b < 2; ++b) {
+    const int t = 16 * wave + lam;
+    off_av[b] = t * (kTokenCols * 2) + 16 * ((4 * b + gq) ^ (2 * (t & 3)));
+  }
+#pragma unroll
+  for (int jt = 0; jt < NJ; ++jt) off_bt[jt] = (16 * jt + lam) * kBtRow + 16 * gq;
+  auto step_fn = [&](int step, auto bsel) {
+    char* sb = decltype(bsel)::value ? st1 : st0;
+    __builtin_amdgcn_s_waitcnt(vmcnt_imm(NLD));
+    // every wave's part of the step is in (a plain barrier: a fence would
+    // also wait for the next step's loads)
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    // x[ct]: columns 32 wave + 16 ct + lam, tokens 8 gq + e (the A operand);
+    // xq[jt]: rank 16 jt + lam, the same tokens (the B operand)
+    u32x4 x[2], xq[NJ];
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct) {
+      const u32x2 h0 = tr_read16(sb + off_x[ct]), h1 = tr_read16(sb + (off_x[ct] + 4 * (kTokenCols * 2)));
+      x[ct] = u32x4{h0[0], h0[1], h1[0], h1[1]};
+    }
+#pragma unroll
+    for (int jt = 0; jt < NJ; ++jt) {
+      const u32x2 h0 = tr_read16(sb + (off_q + jt * QB)), h1 = tr_read16(sb + (off_q + jt * QB + 4 * 32));
+      xq[jt] = (16 * jt + lam < r) ? u32x4{h0[0], h0[1], h1[0], h1[1]} : zero4();
+    }
+    // GP, waves 0 and 1: store the previous step's g partial, then this
+    // step's: the lane's token row 16 wave + lam of the step as it is (16
+    // bytes = 8 columns per chunk) against B's columns, 8 contractions of 32
+    // columns, read from the buffer before it is released
+    if constexpr (GP) {
+      if (step > 0) gp_store(step - 1);
+      if (wave < 2) {
+#pragma unroll
+        for (int jt = 0; jt < NJ; ++jt) ga[jt] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < kTokenCols / 32; ++kc) {
+          const u32x4 av = *reinterpret_cast<const u32x4*>(sb + (off_av[kc & 1] + 128 * (kc >> 1)));
+#pragma unroll
+          for (int jt = 0; jt < NJ; ++jt) {
+            const u32x4 bv = *reinterpret_cast<const u32x4*>(bts + (off_bt[jt] + 64 * kc));
+            ga[jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(av), as_bf(bv), ga[jt], 0, 0, 0);
+          }
+        }
+      }
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");  // the buffer is free
+    issue(step + 2, sb);  // zeros past the chunk
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+      for (int jt = 0; jt < NJ; ++jt)
+        acc[ct][jt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf(x[ct]), as_bf(xq[jt]), acc[ct][jt], 0, 0, 0);
+  };
+  // pairs of steps, then a last even one: every path into a step has the
+  // other buffer's loads issued after this buffer's
+  int step = 0;
+  for (; step + 1 < nsteps; step += 2) {
+    step_fn(step, int_c<0>{});
+    step_fn(step + 1, int_c<1>{});
+  }
+  if (step < nsteps) step_fn(step, int_c<0>{});
+  vmem_wait_all();  // the loads of the two steps past the end are in before the LDS is released
+  if constexpr (GP) {
+    if (nsteps > 0) gp_store(nsteps - 1);
+  }
+  // acc[ct][jt][v]: column 32 wave + 16 ct + 4 gq + v of the block, rank 16 jt + lam
+  float* out = g.part + (int64_t)blockIdx.x * g.C * g.r_max;
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+    for (int jt = 0; jt < NJ; ++jt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int c = cbase + 32 * wave + 16 * ct + 4 * gq + v;
+        const int j = 16 * jt + lam;
+        if (j < r && c < g.C) out[(int64_t)c * g.r_max + j] = acc[ct][jt][v];
+      }
+}
+
 // Fixed-order sum of one training adapter's chunk partials.
 // Every final sum of a (grouped) backward in one launch: blockIdx.y = which *
 // n_tads + training adapter (which: dB, dA of the first projection, then the
@@ -700,6 +912,19 @@ hipError_t launch_gather_expand(const uint16_t* H, int64_t ldh, const uint16_t* 
 template <bool DROP, bool GP>
 void launch_token_reduce_nj(const TokenReduceGroup& g, int32_t n_chunks, int32_t r_sel, hipStream_t s) {
   const dim3 grid(n_chunks, g.yoff[g.n]);
+  // the pipelined kernel when every reduction's Q rows are 16-byte aligned
+  bool q16 = !DROP;
+  for (int k = 0; k < g.n; ++k)
+    q16 = q16 && (g.a[k].ldq & 7) == 0 && (reinterpret_cast<uintptr_t>(g.a[k].Q) & 15) == 0;
+  if (q16) {
+    if (r_sel <= 16)
+      hipLaunchKernelGGL((token_reduce_pipe_kernel<1, GP>), grid, dim3(512), 0, s, g);
+    else if (r_sel <= 32)
+      hipLaunchKernelGGL((token_reduce_pipe_kernel<2, GP>), grid, dim3(512), 0, s, g);
+    else
+      hipLaunchKernelGGL((token_reduce_pipe_kernel<4, GP>), grid, dim3(512), 0, s, g);
+    return;
+  }
   if (r_sel <= 16)
     hipLaunchKernelGGL((token_reduce_kernel<1, DROP, GP>), grid, dim3(512), 0, s, g);
   else if (r_sel <= 32)
