@@ -112,15 +112,18 @@ def test_split_tiles_ragged():
 
 @pytest.mark.parametrize("dtype,K,N,r_max", [("bf16", 520, 776, 64), ("f32", 520, 776, 64), ("bf16", 4096, 4096, 64),
                                              ("bf16", 4104, 2056, 64), ("bf16", 4104, 2056, 16),
-                                             ("bf16", 520, 776, 16)])
+                                             ("bf16", 520, 776, 16), ("bf16", 520, 776, 12)])
 def test_residual_only_retention_recomputes_h_bit_exact(dtype, K, N, r_max):
     """A forward that keeps no H_save (the caller keeps X) and a backward that
     recomputes h from X and A give bit-identical Y, dA, dB and dX to keeping H_save
     (the recompute is the forward's own shrink over the training rows; at K = 4096 both
     split the contraction into chunks).  r_max = 16 runs the rank-16 shrink, whose
-    chunks load three buffers deep."""
+    chunks load three buffers deep.  r_max = 12 gives the kept H_save rows of 24
+    bytes: the dB reduction then reads h element by element (the two-buffer token
+    reduction), while the recomputed h (rows of 16 entries) goes through the
+    pipelined one that stages h in LDS; both sum in the same order."""
     import torch
-    ranks = MIXED_RANKS if r_max == 64 else [16, 8, 16, 12, 5]
+    ranks = MIXED_RANKS if r_max == 64 else [min(x, r_max) for x in (16, 8, 16, 12, 5)]
     w = wl.custom(MIXED, ranks, K=K, N=N, dtype=dtype, r_max=r_max, name="recompute")
     run = Run(w)
     Y1, H = run.fwd()
