@@ -77,6 +77,19 @@ def test_mixed_bf16_ragged():
     _full(w)
 
 
+WIDE = [(0, 70, 1, 0), (70, 300, 2, 1), (370, 3, 0, 0), (373, 45, 2, 1), (418, 290, 0, 1), (708, 1, 1, 0)]
+
+
+@pytest.mark.parametrize("train_rank", [32, 64])
+def test_wide_training_ranks(train_rank):
+    """A training adapter of rank 32 or 64 (the token reductions then run two or
+    four 16-rank tiles) beside one of rank 16, with training segments of 300, 45
+    and 290 tokens (several 256-token chunks, ragged against the 32-token steps)
+    and inference rows between them: Y, H_save, dA, dB and dX against the oracle."""
+    w = wl.custom(WIDE, [16, 8, train_rank], K=520, N=776, r_max=64, name="wide_rank%d" % train_rank)
+    _full(w)
+
+
 SPLIT = ([(0, 180, 1, 0)] + [(180 + i, 1, 2 + i % 3, 0) for i in range(20)] +
          [(200, 300, 0, 1), (500, 200, 3, 0)])
 SPLIT_RANKS = [16, 8, 32, 64, 5]
