@@ -315,6 +315,19 @@ int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32
  * compute for each entry; they return DSV_ERR_ARG for a NULL dropouts and
  * DSV_ERR_RANGE for any p outside [0, 1), and use the same workspace sizes.
  *
+ * Streams (bf16 backward of two or more projections): dX needs g only, so
+ * the dA reductions and the final sums of dA and dB run beside the dX GEMMs
+ * on a second stream of the current device that the library creates on first
+ * use (default priority, non-blocking, kept until the process ends).  That
+ * work is forked from hip_stream after g is complete and joined back into
+ * hip_stream by an event wait before the call returns: everything the call
+ * writes is complete in hip_stream order, as with one stream, and the results
+ * are the same bits.  The fork and join are enqueued under a library lock, so
+ * calls from several host threads stay correct; their side work queues up on
+ * the one side stream.  Under stream capture the second stream joins the
+ * capture through the fork event.  If the second stream cannot be created the
+ * call runs everything on hip_stream.
+ *
  * dsv_bwd_proj.Wt: the frozen weight is never updated, so a caller may keep it
  * a second time, transposed ([K][N], 16-byte aligned, the same bf16 values).
  * With it the dX GEMM reads its weight tile contraction-contiguous, as the

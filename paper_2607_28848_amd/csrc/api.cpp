@@ -5,6 +5,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 
 #include "kernels.h"
 #include "plan.h"
@@ -1103,6 +1104,41 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
 }
 
+// A second stream of the current device (default priority, non-blocking)
+// and two events, created on first use: the grouped backward runs its dA
+// reduction and final sums there, beside the dX GEMM on the caller's stream,
+// which needs neither.  The fork and join are enqueued under a lock, so calls
+// from several host threads do not interleave on the shared events; the side
+// work of successive calls queues up on the one side stream.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+SideStream g_side[64];
+
+// The current device's side stream (created if needed), or nullptr.
+SideStream* side_stream() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  SideStream& sd = g_side[dev];
+  if (!sd.s) {
+    hipStream_t st = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e0, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess) {
+      if (e0) (void)hipEventDestroy(e0);
+      (void)hipStreamDestroy(st);
+      return nullptr;
+    }
+    sd.fork = e0;
+    sd.join = e1;
+    sd.s = st;
+  }
+  return &sd;
+}
+
 int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_bwd_proj* projs, int32_t accumulate,
                      const dsv_dropout* drops, void* workspace, size_t workspace_bytes, void* hip_stream) {
   int rc = check_group(p, dt, n_proj, projs);
@@ -1270,7 +1306,6 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     ta.keep_words = (q.K + 31) / 32;
     tag.yoff[i + 1] = tag.yoff[i] + token_col_blocks(q.K);
   }
-  if (launch_token_reduce_group(tag, p->n_chunks, p->r_train, s) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 5. fixed-order sums into dB (scaled by s_a) and dA, every projection
   ReduceOutGroup og{};
@@ -1280,55 +1315,78 @@ int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
     og.a[2 * i + 1] = ReduceOutArgs{tag.a[i].part, projs[i].K, nullptr, 1, projs[i].dA,
                                     dropping ? ds[i].scale : 1.f};
   }
-  if (launch_reduce_out_group(og, p->r_max, p->r_train, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr), p->dptr(L.tad_chunks),
-                              ranks, accumulate, s) != hipSuccess)
-    return DSV_ERR_DEVICE;
+  auto dA_and_sums = [&](hipStream_t sx) -> int {
+    if (launch_token_reduce_group(tag, p->n_chunks, p->r_train, sx) != hipSuccess) return DSV_ERR_DEVICE;
+    if (launch_reduce_out_group(og, p->r_max, p->r_train, train_ads, p->n_tads, p->dptr(L.tad_chunk_ptr),
+                                p->dptr(L.tad_chunks), ranks, accumulate, sx) != hipSuccess)
+      return DSV_ERR_DEVICE;
+    return DSV_OK;
+  };
 
   // 6. every dX GEMM in one launch, longest contraction first (projections with a
   //    transposed weight in one NT launch, the others in one NN launch)
-  int32_t Cs[DSV_MAX_GROUP], order[DSV_MAX_GROUP];
-  for (int i = 0; i < n_proj; ++i) Cs[i] = projs[i].N;
-  by_contraction(n_proj, Cs, order);
-  for (int nt = 1; nt >= 0; --nt) {
-    GemmGroup G{};
-    for (int k = 0; k < n_proj; ++k) {
-      const int i = order[k];
-      const dsv_bwd_proj& q = projs[i];
-      if (!q.dX || (q.Wt != nullptr) != (nt == 1)) continue;
-      GemmArgs& g = G.a[G.n];
-      g.P = static_cast<const uint16_t*>(q.dY);
-      g.ldp = st[i].dy;
-      g.Q = static_cast<const uint16_t*>(nt ? q.Wt : q.W);
-      g.ldq = nt ? st[i].wt : st[i].w;
-      g.out = static_cast<uint16_t*>(q.dX);
-      g.ldo = st[i].dx;
-      g.M = p->T_t;
-      g.Nout = q.K;
-      g.C = q.N;
-      g.tiles = p->dptr(L.bwd_tiles);
-      g.uniform_rows = p->btiles_uniform;
-      set_split(g, whole256(p->n_btiles, q.K), nullptr, 0);
-      g.Lp = gm[i];
-      g.ldl = ldh;
-      g.Lq = static_cast<const uint16_t*>(q.A);
-      g.lq_ad = (int64_t)p->r_max * q.K;
-      g.lq_j = q.K;
-      g.lq_col = 1;
-      g.ranks = ranks;
-      g.keep = keep[i];  // dropout: g A_a through the input's mask
-      g.keep_words = (q.K + 31) / 32;
-      g.keep_scale = ds[i].scale;
-      G.off[G.n + 1] = G.off[G.n] + g.n_mtiles * g.n_ntiles;
-      ++G.n;
+  auto dx_all = [&](hipStream_t s) -> int {
+    int32_t Cs[DSV_MAX_GROUP], order[DSV_MAX_GROUP];
+    for (int i = 0; i < n_proj; ++i) Cs[i] = projs[i].N;
+    by_contraction(n_proj, Cs, order);
+    for (int nt = 1; nt >= 0; --nt) {
+      GemmGroup G{};
+      for (int k = 0; k < n_proj; ++k) {
+        const int i = order[k];
+        const dsv_bwd_proj& q = projs[i];
+        if (!q.dX || (q.Wt != nullptr) != (nt == 1)) continue;
+        GemmArgs& g = G.a[G.n];
+        g.P = static_cast<const uint16_t*>(q.dY);
+        g.ldp = st[i].dy;
+        g.Q = static_cast<const uint16_t*>(nt ? q.Wt : q.W);
+        g.ldq = nt ? st[i].wt : st[i].w;
+        g.out = static_cast<uint16_t*>(q.dX);
+        g.ldo = st[i].dx;
+        g.M = p->T_t;
+        g.Nout = q.K;
+        g.C = q.N;
+        g.tiles = p->dptr(L.bwd_tiles);
+        g.uniform_rows = p->btiles_uniform;
+        set_split(g, whole256(p->n_btiles, q.K), nullptr, 0);
+        g.Lp = gm[i];
+        g.ldl = ldh;
+        g.Lq = static_cast<const uint16_t*>(q.A);
+        g.lq_ad = (int64_t)p->r_max * q.K;
+        g.lq_j = q.K;
+        g.lq_col = 1;
+        g.ranks = ranks;
+        g.keep = keep[i];  // dropout: g A_a through the input's mask
+        g.keep_words = (q.K + 31) / 32;
+        g.keep_scale = ds[i].scale;
+        G.off[G.n + 1] = G.off[G.n] + g.n_mtiles * g.n_ntiles;
+        ++G.n;
+      }
+      if (G.n > 0) {
+        const int tk = timing_begin(1, s);
+        const hipError_t e = nt ? launch_gemm_group_nt(G, s) : launch_gemm_group_nn(G, s);
+        timing_end(tk, s);
+        if (e != hipSuccess) return DSV_ERR_DEVICE;
+      }
     }
-    if (G.n > 0) {
-      const int tk = timing_begin(1, s);
-      const hipError_t e = nt ? launch_gemm_group_nt(G, s) : launch_gemm_group_nn(G, s);
-      timing_end(tk, s);
-      if (e != hipSuccess) return DSV_ERR_DEVICE;
+    return DSV_OK;
+  };
+
+  // dX needs g only: the dA reduction and the final sums run beside it on the
+  // side stream (joined back into the caller's stream before the call returns)
+  {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    if (SideStream* sd = side_stream()) {
+      if (hipEventRecord(sd->fork, s) != hipSuccess) return DSV_ERR_DEVICE;
+      if ((rc = dx_all(s)) != DSV_OK) return rc;
+      if (hipStreamWaitEvent(sd->s, sd->fork, 0) != hipSuccess) return DSV_ERR_DEVICE;
+      if ((rc = dA_and_sums(sd->s)) != DSV_OK) return rc;
+      if (hipEventRecord(sd->join, sd->s) != hipSuccess || hipStreamWaitEvent(s, sd->join, 0) != hipSuccess)
+        return DSV_ERR_DEVICE;
+      return DSV_OK;
     }
   }
-  return DSV_OK;
+  if ((rc = dA_and_sums(s)) != DSV_OK) return rc;
+  return dx_all(s);
 }
 
 }  // namespace
