@@ -579,6 +579,41 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
 
 // Wt (optional, bf16): the frozen weight transposed, [K][N]; the dX GEMM then
 // reads it K-contiguous like the forward's W instead of transposing W on the fly.
+// A second stream of the current device (default priority, non-blocking)
+// and two events, created on first use: the bf16 backward runs its dA
+// reduction and final sums there, beside the dX GEMM on the caller's stream,
+// which needs neither.  The fork and join are enqueued under a lock, so calls
+// from several host threads do not interleave on the shared events; the side
+// work of successive calls queues up on the one side stream.
+struct SideStream {
+  hipStream_t s = nullptr;
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+SideStream g_side[64];
+
+// The current device's side stream (created if needed), or nullptr.
+SideStream* side_stream() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  SideStream& sd = g_side[dev];
+  if (!sd.s) {
+    hipStream_t st = nullptr;
+    hipEvent_t e0 = nullptr, e1 = nullptr;
+    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
+    if (hipEventCreateWithFlags(&e0, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess) {
+      if (e0) (void)hipEventDestroy(e0);
+      (void)hipStreamDestroy(st);
+      return nullptr;
+    }
+    sd.fork = e0;
+    sd.join = e1;
+    sd.s = st;
+  }
+  return &sd;
+}
+
 int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* X, const void* W, const void* A,
              const void* B, const void* H_save, const void* dY, float* dA, float* dB, void* dX,
              int32_t accumulate, const dsv_dropout* drop, const void* Wt, void* workspace,
@@ -748,21 +783,25 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
   ra.keep = keep;  // dA contracts the masked input
   ra.keep_words = keep_words;
   ta.yoff[1] = token_col_blocks(K);
-  if ((e = launch_token_reduce_group(ta, p->n_chunks, p->r_train, s)) != hipSuccess) return DSV_ERR_DEVICE;
 
   // 5. fixed-order sums into dB (scaled by s_a) and dA.
   const int32_t* tad_ptr = p->dptr(L.tad_chunk_ptr);
   const int32_t* tad_chunks = p->dptr(L.tad_chunks);
   const ReduceOutArgs ob{part_b, N, scales, 0, dB, 1.f};
   const ReduceOutArgs oa{part_a, K, nullptr, 1, dA, dropping ? ds.scale : 1.f};
-  if ((e = launch_reduce_out(ob, oa, p->r_max, p->r_train, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks, accumulate, s)) !=
-      hipSuccess)
-    return DSV_ERR_DEVICE;
+  auto dA_and_sums = [&](hipStream_t sx) -> int {
+    if (launch_token_reduce_group(ta, p->n_chunks, p->r_train, sx) != hipSuccess) return DSV_ERR_DEVICE;
+    if (launch_reduce_out(ob, oa, p->r_max, p->r_train, train_ads, p->n_tads, tad_ptr, tad_chunks, ranks, accumulate,
+                          sx) != hipSuccess)
+      return DSV_ERR_DEVICE;
+    return DSV_OK;
+  };
+  if (!dX) return dA_and_sums(s);
 
   // 6. dx = dy W + g A_a on the matrix cores (W read with a transposing load).
   //    Under dropout g A_a passes through the input's mask (in the accumulators,
   //    between the low-rank prologue and the main loop).
-  if (dX) {
+  auto dx_gemm = [&](hipStream_t s) -> int {
     GemmArgs g{};
     g.P = static_cast<const uint16_t*>(dY);
     g.ldp = ld.dy;
@@ -790,11 +829,27 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     g.keep_words = keep_words;
     g.keep_scale = ds.scale;
     const int tk = timing_begin(1, s);
-    e = Wt ? launch_gemm_nt(g, gp.tm, gp.tn, s) : launch_gemm_nn(g, gp.tm, gp.tn, s);
+    const hipError_t e = Wt ? launch_gemm_nt(g, gp.tm, gp.tn, s) : launch_gemm_nn(g, gp.tm, gp.tn, s);
     timing_end(tk, s);
-    if (e != hipSuccess) return DSV_ERR_DEVICE;
+    return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
+  };
+
+  // dX needs g only: the dA reduction and the final sums run beside it on the
+  // side stream (joined back into the caller's stream before the call returns)
+  {
+    std::lock_guard<std::mutex> lk(g_side_mu);
+    if (SideStream* sd = side_stream()) {
+      if (hipEventRecord(sd->fork, s) != hipSuccess) return DSV_ERR_DEVICE;
+      if ((rc = dx_gemm(s)) != DSV_OK) return rc;
+      if (hipStreamWaitEvent(sd->s, sd->fork, 0) != hipSuccess) return DSV_ERR_DEVICE;
+      if ((rc = dA_and_sums(sd->s)) != DSV_OK) return rc;
+      if (hipEventRecord(sd->join, sd->s) != hipSuccess || hipStreamWaitEvent(s, sd->join, 0) != hipSuccess)
+        return DSV_ERR_DEVICE;
+      return DSV_OK;
+    }
   }
-  return DSV_OK;
+  if ((rc = dA_and_sums(s)) != DSV_OK) return rc;
+  return dx_gemm(s);
 }
 
 }  // namespace
@@ -1102,41 +1157,6 @@ int fwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_
   const hipError_t e = launch_gemm_group_nt(G, s);
   timing_end(tk, s);
   return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
-}
-
-// A second stream of the current device (default priority, non-blocking)
-// and two events, created on first use: the grouped backward runs its dA
-// reduction and final sums there, beside the dX GEMM on the caller's stream,
-// which needs neither.  The fork and join are enqueued under a lock, so calls
-// from several host threads do not interleave on the shared events; the side
-// work of successive calls queues up on the one side stream.
-struct SideStream {
-  hipStream_t s = nullptr;
-  hipEvent_t fork = nullptr, join = nullptr;
-};
-std::mutex g_side_mu;
-SideStream g_side[64];
-
-// The current device's side stream (created if needed), or nullptr.
-SideStream* side_stream() {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  SideStream& sd = g_side[dev];
-  if (!sd.s) {
-    hipStream_t st = nullptr;
-    hipEvent_t e0 = nullptr, e1 = nullptr;
-    if (hipStreamCreateWithFlags(&st, hipStreamNonBlocking) != hipSuccess) return nullptr;
-    if (hipEventCreateWithFlags(&e0, hipEventDisableTiming) != hipSuccess ||
-        hipEventCreateWithFlags(&e1, hipEventDisableTiming) != hipSuccess) {
-      if (e0) (void)hipEventDestroy(e0);
-      (void)hipStreamDestroy(st);
-      return nullptr;
-    }
-    sd.fork = e0;
-    sd.join = e1;
-    sd.s = st;
-  }
-  return &sd;
 }
 
 int bwd_grouped_impl(const dsv_plan* p, dsv_dtype dt, int32_t n_proj, const dsv_bwd_proj* projs, int32_t accumulate,
