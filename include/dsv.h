@@ -216,10 +216,7 @@ int dsv_lora_bwd_workspace(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int
  * give bit-identical results.  H_save == NULL recomputes h of the training
  * rows from X and A first (the forward's own shrink, so the same values bit
  * for bit; 2 T_t K r FLOP and one read of X's training rows), for a forward
- * that kept no H_save.  With no training rows the call is a no-op.  In bf16
- * with dX, the dA reduction and the final sums run on a second stream of the
- * device beside the dX GEMM, joined back into hip_stream before the call
- * returns (see "Streams" under the grouped calls).
+ * that kept no H_save.  With no training rows the call is a no-op.
  */
 int dsv_lora_bwd(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32_t N,
                  const void* X, const void* W, const void* A, const void* B,
@@ -318,8 +315,8 @@ int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32
  * compute for each entry; they return DSV_ERR_ARG for a NULL dropouts and
  * DSV_ERR_RANGE for any p outside [0, 1), and use the same workspace sizes.
  *
- * Streams (the bf16 backward, grouped or single, with dX): dX needs g only,
- * so the dA reductions and the final sums of dA and dB run beside the dX GEMMs
+ * Streams (the grouped bf16 backward of two or more projections): dX needs g
+ * only, so the dA reductions and the final sums of dA and dB run beside the dX GEMMs
  * on a second stream of the current device that the library creates on first
  * use (default priority, non-blocking, kept until the process ends).  That
  * work is forked from hip_stream after g is complete and joined back into

@@ -580,9 +580,9 @@ int fwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
 // Wt (optional, bf16): the frozen weight transposed, [K][N]; the dX GEMM then
 // reads it K-contiguous like the forward's W instead of transposing W on the fly.
 // A second stream of the current device (default priority, non-blocking)
-// and two events, created on first use: the bf16 backward runs its dA
-// reduction and final sums there, beside the dX GEMM on the caller's stream,
-// which needs neither.  The fork and join are enqueued under a lock, so calls
+// and two events, created on first use: the grouped bf16 backward runs its
+// dA reductions and final sums there, beside the dX GEMMs on the caller's
+// stream, which need neither.  The fork and join are enqueued under a lock, so calls
 // from several host threads do not interleave on the shared events; the side
 // work of successive calls queues up on the one side stream.
 struct SideStream {
@@ -833,21 +833,8 @@ int bwd_impl(const dsv_plan* p, dsv_dtype dt, int32_t K, int32_t N, const void* 
     timing_end(tk, s);
     return e == hipSuccess ? DSV_OK : DSV_ERR_DEVICE;
   };
-
-  // dX needs g only: the dA reduction and the final sums run beside it on the
-  // side stream (joined back into the caller's stream before the call returns)
-  {
-    std::lock_guard<std::mutex> lk(g_side_mu);
-    if (SideStream* sd = side_stream()) {
-      if (hipEventRecord(sd->fork, s) != hipSuccess) return DSV_ERR_DEVICE;
-      if ((rc = dx_gemm(s)) != DSV_OK) return rc;
-      if (hipStreamWaitEvent(sd->s, sd->fork, 0) != hipSuccess) return DSV_ERR_DEVICE;
-      if ((rc = dA_and_sums(sd->s)) != DSV_OK) return rc;
-      if (hipEventRecord(sd->join, sd->s) != hipSuccess || hipStreamWaitEvent(s, sd->join, 0) != hipSuccess)
-        return DSV_ERR_DEVICE;
-      return DSV_OK;
-    }
-  }
+  // One projection's dA work is too small to pay for a fork to the side
+  // stream (the grouped call forks): everything on the caller's stream.
   if ((rc = dA_and_sums(s)) != DSV_OK) return rc;
   return dx_gemm(s);
 }
