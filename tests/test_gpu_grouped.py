@@ -331,3 +331,52 @@ def test_grouped_inference_only_training_only_and_empty():
     out = dsv.cobatch_fwd_grouped(plan, [(X, W, A, B), (X, W, A, B)])
     torch.cuda.synchronize()
     assert out[0][0].shape == (0, 64)
+
+
+def test_grouped_backward_graph_replay():
+    """The grouped backward, whose dA reductions and final sums fork to the
+    library's side stream and join back, captured in a graph on torch's capture
+    stream and replayed three times with eager work (clearing the outputs)
+    between replays: every replay's dA, dB and dX bit-identical to the eager
+    call's."""
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(520, 776), (136, 1040), (1040, 264)]
+    _say("case graph replay of the grouped backward %s" % shapes)
+    w, ts, dev = _layer("bf16", shapes)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    Tt = plan.train_tokens
+    fw = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], None,
+                                         torch.zeros((Tt, w.r_max), dtype=torch.bfloat16, device="cuda"))
+                                        for d in dev])
+    n_ad = len(w.ranks)
+    outs = [(torch.zeros((n_ad, w.r_max, K), dtype=torch.float32, device="cuda"),
+             torch.zeros((n_ad, N, w.r_max), dtype=torch.float32, device="cuda"),
+             torch.zeros((Tt, K), dtype=torch.bfloat16, device="cuda")) for K, N in shapes]
+    bw = [(d["X"], d["W"], d["A"], d["B"], fw[i][1], d["dY"], *outs[i]) for i, d in enumerate(dev)]
+    ws = torch.empty(max(dsv.bwd_grouped_workspace_bytes(plan, dsv.BF16, shapes), 256), dtype=torch.uint8,
+                     device="cuda")
+    dsv.lora_bwd_grouped(plan, bw, workspace=ws)
+    torch.cuda.synchronize()
+    ref = [tuple(t.clone() for t in o) for o in outs]
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        dsv.lora_bwd_grouped(plan, bw, workspace=ws)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        dsv.lora_bwd_grouped(plan, bw, workspace=ws)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for o in outs:
+            for t in o:
+                t.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        _say(" replay %d" % rep)
+        for o, r in zip(outs, ref):
+            for a, b in zip(o, r):
+                assert torch.equal(_bits(a), _bits(b))
