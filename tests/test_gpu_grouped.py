@@ -380,3 +380,78 @@ def test_grouped_backward_graph_replay():
         for o, r in zip(outs, ref):
             for a, b in zip(o, r):
                 assert torch.equal(_bits(a), _bits(b))
+
+
+def test_grouped_backward_accumulate_and_threads():
+    """The grouped backward's final sums run on the library's side stream.
+    accumulate=1 there adds exactly what an overwriting call writes (checked bit
+    for bit against the overwriting call plus the prior values, where that sum is
+    exact: the prior values are zeros, then the call's own result), and slices of
+    adapters without training rows keep their bits.  Two host threads running the
+    grouped backward at once on two streams (the side stream and its events are
+    shared) give the single-threaded results bit for bit."""
+    import threading
+
+    import torch
+    from paper_2607_28848_amd import dsv
+    shapes = [(520, 776), (136, 1040), (1040, 264)]
+    _say("case grouped accumulate and threads %s" % shapes)
+    w, ts, dev = _layer("bf16", shapes)
+    plan = dsv.segments_build(w.segments, w.n_tokens, w.ranks, w.scales, w.r_max, device="cuda")
+    Tt = plan.train_tokens
+    fw = dsv.cobatch_fwd_grouped(plan, [(d["X"], d["W"], d["A"], d["B"], None,
+                                         torch.zeros((Tt, w.r_max), dtype=torch.bfloat16, device="cuda"))
+                                        for d in dev])
+    n_ad = len(w.ranks)
+
+    def outputs(fill=0.0):
+        return [(torch.full((n_ad, w.r_max, K), fill, dtype=torch.float32, device="cuda"),
+                 torch.full((n_ad, N, w.r_max), fill, dtype=torch.float32, device="cuda"),
+                 torch.zeros((Tt, K), dtype=torch.bfloat16, device="cuda")) for K, N in shapes]
+
+    def bwd(outs, accumulate=False, stream=None):
+        bw = [(d["X"], d["W"], d["A"], d["B"], fw[i][1], d["dY"], *outs[i]) for i, d in enumerate(dev)]
+        dsv.lora_bwd_grouped(plan, bw, accumulate=accumulate, stream=stream)
+
+    ref = outputs()
+    bwd(ref)
+    torch.cuda.synchronize()
+    # accumulate onto zeros, then onto the result itself: x + 0 = x and x + x = 2x exactly
+    acc = outputs()
+    bwd(acc, accumulate=True)
+    torch.cuda.synchronize()
+    for o, r in zip(acc, ref):
+        assert torch.equal(_bits(o[0]), _bits(r[0])) and torch.equal(_bits(o[1]), _bits(r[1]))
+    bwd(acc, accumulate=True)
+    torch.cuda.synchronize()
+    owners = dict(train_mask_slices(w))
+    for o, r in zip(acc, ref):
+        for a in range(n_ad):
+            if a in owners:
+                assert torch.equal(_bits(o[0][a]), _bits(2 * r[0][a])) and torch.equal(_bits(o[1][a]), _bits(2 * r[1][a]))
+            else:
+                assert torch.equal(_bits(o[0][a]), _bits(r[0][a])) and torch.equal(_bits(o[1][a]), _bits(r[1][a]))
+    # two threads, two streams, several calls each
+    outs = [outputs(), outputs()]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    errors = []
+
+    def worker(k):
+        try:
+            with torch.cuda.stream(streams[k]):
+                for _ in range(4):
+                    bwd(outs[k], stream=streams[k])
+        except Exception as exc:  # noqa: BLE001
+            errors.append(exc)
+
+    th = [threading.Thread(target=worker, args=(k,)) for k in range(2)]
+    for t in th:
+        t.start()
+    for t in th:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    for k in range(2):
+        for o, r in zip(outs[k], ref):
+            for a, b in zip(o, r):
+                assert torch.equal(_bits(a), _bits(b))
