@@ -318,7 +318,8 @@ int dsv_lora_bwd_dropout(const dsv_plan* plan, dsv_dtype dtype, int32_t K, int32
  * Streams (the grouped bf16 backward of two or more projections): dX needs g
  * only, so the dA reductions and the final sums of dA and dB run beside the dX GEMMs
  * on a second stream of the current device that the library creates on first
- * use (default priority, non-blocking, kept until the process ends).  That
+ * use (default priority, non-blocking, kept until the process ends), so
+ * hip_stream must belong to the current device.  That
  * work is forked from hip_stream after g is complete and joined back into
  * hip_stream by an event wait before the call returns: everything the call
  * writes is complete in hip_stream order, as with one stream, and the results
